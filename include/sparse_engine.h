@@ -1,0 +1,229 @@
+/*
+ * sparse_engine.h — C-ABI of the sparse-first decode hot path on MI355X (gfx950).
+ *
+ * The library implements the per-step work of two sparse-attention methods over
+ * a paged, per-KV-head KV cache, following the SparseEngine paper's statement of
+ * the problem:
+ *   - the cache manager owns layout, position mapping and write/update/release
+ *     (Section 3.1, "Method-Customized CacheManager");
+ *   - attention reads a view of the cache: o = Attention(q, BuildView(C, I))
+ *     (Section 3.1, eq. attention-view), whose payload pairs the physical KV with
+ *     context lengths and page-table coordinates (Appendix B, "Attention View
+ *     Payloads");
+ *   - H2O grows accumulated scores and evicts to a budget with a protected recent
+ *     window (Appendix A.3, eqs. background-h2o-score, background-h2o-retention);
+ *   - Quest ranks pages by a min/max upper bound of the logits and reads the best
+ *     pages (Appendix A.3, eqs. background-quest-summary, background-quest-score).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  Units.   A unit is one (request, KV head) of one layer: unit = req * Hkv + h.
+ *           Units are independent.  A multi-layer cache is one view per layer
+ *           (each with its own block_table and lengths rows; pools may be shared).
+ *  GQA.     Query head a reads KV head floor(a / G), G = q_per_kv (Appendix A.1,
+ *           "MHA, MQA, and GQA"), so a unit's G query rows are contiguous.
+ *  Layout.  Slot s of a unit lives in physical page block_table[unit][s / 16] at
+ *           row s % 16 (Appendix A.2, "Logical Positions and Physical Blocks", in
+ *           0-based form).  A page holds its 16 keys, then its 16 values.
+ *  Memory.  Every pointer argument is a DEVICE pointer owned by the caller, except
+ *           `kv` (the view struct itself, host memory, read during the call) and
+ *           the `host_out` of se_read_device_errors.  The library allocates no
+ *           memory and keeps no state between calls; calls on different streams
+ *           may run concurrently when their buffers do not overlap.
+ *  Streams. Every compute call only enqueues work on `stream` and returns without
+ *           waiting (so a sequence of calls can be captured in a hipGraph).  Only
+ *           se_read_device_errors synchronises.
+ *  Errors.  The host checks only scalars and pointer presence and returns a status
+ *           before enqueuing anything.  Problems that can only be seen on the device
+ *           (a bad page id, a full unit, a length above max_len) set bits in the
+ *           int32 word *dev_err (atomic OR) and the affected unit is left unchanged;
+ *           read and clear the word with se_read_device_errors.
+ *  Numbers. K/V/q are bf16; logits, softmax and accumulation are fp32; outputs fp32.
+ *  Limits.  page_size must be 16; head_dim 64 or 128; q_per_kv 1, 2, 4 or 8.
+ */
+#ifndef SPARSE_ENGINE_H
+#define SPARSE_ENGINE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum se_status {
+  SE_OK = 0,
+  SE_ERR_INVALID_ARGUMENT = 1, /* a NULL required pointer, a negative size, ...     */
+  SE_ERR_UNSUPPORTED = 2,      /* a size the kernels are not built for               */
+  SE_ERR_WORKSPACE = 3,        /* ws is NULL or smaller than se_workspace_bytes()    */
+  SE_ERR_HIP = 4               /* a HIP launch error                                  */
+} se_status;
+
+/* Bits of the device error word. */
+#define SE_DEVERR_BAD_PAGE      1u  /* a block-table entry outside [0, num_pages)          */
+#define SE_DEVERR_CAPACITY      2u  /* an append past max_pages * page_size                */
+#define SE_DEVERR_BAD_LENGTH    4u  /* lengths[unit] < 0, or above max_len / capacity     */
+#define SE_DEVERR_BAD_SELECTION 8u  /* a sel_pages entry outside the unit's pages          */
+#define SE_DEVERR_BAD_POSITIONS 16u /* eviction found repeated positions (retained != B)  */
+
+/* Flags of se_decode_attend. */
+#define SE_ATTEND_ACCUMULATE 1u /* fused H2O score update (eq. background-h2o-score)   */
+
+/* Flags of se_quest_select. */
+#define SE_QUEST_SCORES_GIVEN 1u /* skip the bound; select from page_scores (input)   */
+
+/* Operation ids for se_workspace_bytes. */
+#define SE_OP_DECODE_ATTEND 1
+#define SE_OP_QUEST_SELECT  2
+
+/* The cache view (Section 3.1, eq. attention-view; Appendix B, "Attention View
+ * Payloads").  Only the pointers an operation needs must be non-NULL. */
+typedef struct se_kv_view {
+  void*          kv_pool;     /* bf16 [num_pages][2][page_size][head_dim]: K block, V block */
+  int32_t*       pos_pool;    /* int32 [num_pages][page_size]: logical position per slot    */
+  float*         score_pool;  /* fp32 [num_pages][page_size]: H2O accumulated score, or NULL */
+  void*          meta_pool;   /* bf16 [num_pages][2][head_dim]: Quest per-page min, max, or NULL */
+  const int32_t* block_table; /* int32 [num_units][max_pages]: physical page of each logical page */
+  int32_t*       lengths;     /* int32 [num_units]: resident slots, updated on the device   */
+  int64_t        num_pages;   /* pages in the pools (bounds for block-table entries)        */
+  int32_t        num_units;   /* requests * num_kv_heads                                    */
+  int32_t        num_kv_heads;
+  int32_t        max_pages;   /* block-table row length; a unit holds <= max_pages*16 slots */
+  int32_t        page_size;   /* must be 16                                                 */
+  int32_t        head_dim;    /* 64 or 128                                                  */
+} se_kv_view;
+
+/*
+ * se_decode_attend — append the decode token, then attention over the view.
+ *
+ * Per unit, with L the value of lengths[unit] on entry:
+ *  1. Append (when k_new and v_new are both non-NULL): the new token's key and value
+ *     go to slot L, pos_pool gets new_pos[req], score_pool (if non-NULL) gets 0,
+ *     meta_pool (if non-NULL) folds the key into its page's min/max (a fresh page
+ *     starts from the key), and lengths[unit] becomes L + 1 (Appendix A.3: the
+ *     available set is the retained set plus the new token, which starts with
+ *     score zero; Quest: a new key updates its page's extrema).
+ *  2. Attention (Appendix A.1, eq. background-selected-attention) for each of the
+ *     G query rows of the unit over its read set S:
+ *       sel_pages == NULL: S = every resident slot (H2O: the whole available set);
+ *       otherwise S = the slots of the logical pages sel_pages[unit][0..top_k)
+ *       (entries < 0 are skipped) plus the current page, floor(L'/16) with L' the
+ *       length after the append minus 1, read up to the newest slot (Quest).
+ *     z_j = scale * <q, k_j>, out = sum_j softmax_S(z)_j v_j, lse = log sum_j e^{z_j}.
+ *  3. With SE_ATTEND_ACCUMULATE (needs score_pool): every slot of S gets its weight
+ *     summed over the unit's G query heads added to its score (eq.
+ *     background-h2o-score; GQA reading: sum over the group).
+ *
+ *  q        bf16 [num_req][num_kv_heads * q_per_kv][head_dim]
+ *  k_new,
+ *  v_new    bf16 [num_req][num_kv_heads][head_dim], or both NULL (no append)
+ *  new_pos  int32 [num_req], needed with an append
+ *  sel_pages int32 [num_units][top_k] logical page ids, or NULL
+ *  scale    logit scale, normally 1/sqrt(head_dim) rounded to float32
+ *  max_len  upper bound on the resident slots of any unit after the append; sizes
+ *           the launch.  A unit above it sets SE_DEVERR_BAD_LENGTH and is skipped.
+ *  out      fp32 [num_req][num_kv_heads * q_per_kv][head_dim]
+ *  lse      fp32 [num_req][num_kv_heads * q_per_kv], or NULL
+ *  logits   fp32 [num_units][q_per_kv][logits_stride] (z per slot), or NULL; only
+ *           with sel_pages == NULL; logits_stride >= max_len
+ *  ws       device workspace of se_workspace_bytes(SE_OP_DECODE_ATTEND, ...) bytes,
+ *           zero-filled before its first use; every call leaves it zero-filled again
+ *           where it must be (counters).  Not shared between concurrent calls.
+ *  dev_err  int32 device word (see SE_DEVERR_*), never NULL
+ */
+se_status se_decode_attend(const se_kv_view* kv, int32_t q_per_kv, const void* q,
+                           const void* k_new, const void* v_new, const int32_t* new_pos,
+                           const int32_t* sel_pages, int32_t top_k, float scale,
+                           int32_t max_len, uint32_t flags, float* out, float* lse,
+                           float* logits, int32_t logits_stride, void* ws, size_t ws_bytes,
+                           int32_t* dev_err, hipStream_t stream);
+
+/*
+ * se_accumulate_scores — the H2O score update as its own pass (eq.
+ * background-h2o-score): for every unit and every resident slot j < lengths[unit],
+ *   score(j) += sum over the unit's G query heads a of exp(logits[unit][a][j] - lse[a]).
+ * logits and lse are those se_decode_attend wrote in the same step (all-slots mode).
+ *  logits fp32 [num_units][q_per_kv][logits_stride]; lse fp32 [num_req][Hq]
+ *  max_len upper bound on lengths[unit]; a unit above it sets SE_DEVERR_BAD_LENGTH.
+ */
+se_status se_accumulate_scores(const se_kv_view* kv, int32_t q_per_kv, const float* logits,
+                               int32_t logits_stride, const float* lse, int32_t max_len,
+                               int32_t* dev_err, hipStream_t stream);
+
+/*
+ * se_evict_compact — H2O retention and in-place compaction (Appendix A.3, eq.
+ * background-h2o-retention; Section 3.1: eviction updates the retained-slot mapping
+ * and the context length, then releases the discarded slots).
+ * Per unit with L = lengths[unit] > budget (otherwise nothing changes):
+ *   W = the min(recent, budget) slots with the largest positions;
+ *   keep W plus the best budget - |W| other slots by (score desc, position asc);
+ *   holes = evicted slots below budget (ascending), movers = kept slots at or above
+ *   budget (ascending); the k-th mover's key, value, position and score move into
+ *   the k-th hole; lengths[unit] = budget.
+ *  freed_pages int32 [num_units][freed_stride] or NULL: receives the physical ids of
+ *              the unit's pages that hold no slot afterwards, i.e. logical pages
+ *              ceil(budget/16) .. ceil(L/16)-1 in order; freed_count[unit] (int32,
+ *              may be NULL) their number (0 when nothing was evicted).  The block
+ *              table is not modified: a caller that hands these pages to another
+ *              owner must install a fresh page before a later append reaches them.
+ *  budget  1 .. 8192; recent >= 0; max_len an upper bound on lengths[unit].
+ */
+se_status se_evict_compact(const se_kv_view* kv, int32_t budget, int32_t recent,
+                           int32_t max_len, int32_t* freed_pages, int32_t freed_stride,
+                           int32_t* freed_count, int32_t* dev_err, hipStream_t stream);
+
+/*
+ * se_quest_summarize — per-page key min/max for every resident page (Appendix A.3,
+ * eq. background-quest-summary): for each unit and logical page b < ceil(L/16),
+ * meta_pool[page][0][c] = min and [1][c] = max of k[c] over the page's slots < L.
+ * Used once after prefill; se_decode_attend maintains the summaries afterwards.
+ */
+se_status se_quest_summarize(const se_kv_view* kv, int32_t max_len, int32_t* dev_err,
+                             hipStream_t stream);
+
+/*
+ * se_quest_select — Quest page selection (Appendix A.3, eq. background-quest-score).
+ * Called before the step's se_decode_attend, with the current decode query.  With
+ * L = lengths[unit], the token about to be appended opens or continues page
+ * floor(L/16), the current page, which is always read; the candidates are the pages
+ * [0, floor(L/16)).  For candidate b and query row a of the group:
+ *   zhat_a(b) = scale * sum_c max(q_a[c] * min_b[c], q_a[c] * max_b[c]),
+ * the page score is max over the group's rows (GQA reading), and sel_pages[unit]
+ * receives the top_k candidates by (score desc, page index asc), in ascending page
+ * order, padded with -1 when there are fewer candidates than top_k.
+ *  q           bf16 [num_req][num_kv_heads * q_per_kv][head_dim]
+ *  sel_pages   int32 [num_units][top_k] (output)
+ *  page_scores fp32 [num_units][scores_stride], or NULL: receives the page scores of
+ *              the candidates; with SE_QUEST_SCORES_GIVEN it is the input instead and
+ *              the bound is not computed (q may then be NULL).
+ *  top_k       1 .. 4096; max_len an upper bound on lengths[unit];
+ *              scores_stride >= max_pages.
+ *  ws          se_workspace_bytes(SE_OP_QUEST_SELECT, ...) bytes (no zero-fill needed)
+ */
+se_status se_quest_select(const se_kv_view* kv, int32_t q_per_kv, const void* q, float scale,
+                          int32_t top_k, int32_t max_len, uint32_t flags, int32_t* sel_pages,
+                          float* page_scores, int32_t scores_stride, void* ws, size_t ws_bytes,
+                          int32_t* dev_err, hipStream_t stream);
+
+/* Workspace bytes an operation needs for these sizes (0 if none).  op is one of
+ * SE_OP_*; max_len as passed to the call; top_k only for SE_OP_DECODE_ATTEND with a
+ * selection (0 otherwise). */
+size_t se_workspace_bytes(int32_t op, int32_t num_units, int32_t max_len, int32_t max_pages,
+                          int32_t q_per_kv, int32_t head_dim, int32_t top_k);
+
+/* Waits for `stream`, copies the device error word to *host_out and clears it. */
+se_status se_read_device_errors(int32_t* dev_err, int32_t* host_out, hipStream_t stream);
+
+/* A static string naming a status. */
+const char* se_status_string(se_status status);
+
+/* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
+int32_t se_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPARSE_ENGINE_H */

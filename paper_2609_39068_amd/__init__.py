@@ -1,0 +1,14 @@
+"""Sparse-first decode hot path on MI355X (gfx950): H2O eviction and Quest page
+selection around paged GQA decode attention, as HIP kernels behind a C-ABI
+(include/sparse_engine.h).  This package holds the HIP sources (csrc/), their
+build script, the ctypes binding and the decode-step driver."""
+
+from ._binding import (  # noqa: F401
+    EXPORTED, KVView, SparseEngineError, se_accumulate_scores, se_decode_attend,
+    se_evict_compact, se_quest_select, se_quest_summarize, se_read_device_errors,
+    se_version, se_workspace_bytes, status_string,
+    SE_ATTEND_ACCUMULATE, SE_QUEST_SCORES_GIVEN, SE_OP_DECODE_ATTEND, SE_OP_QUEST_SELECT,
+    SE_DEVERR_BAD_PAGE, SE_DEVERR_CAPACITY, SE_DEVERR_BAD_LENGTH, SE_DEVERR_BAD_SELECTION,
+    SE_DEVERR_BAD_POSITIONS,
+)
+from .decode import H2ODecoder, QuestDecoder  # noqa: F401

@@ -1,0 +1,83 @@
+"""Decode-step drivers: the order in which one layer's step calls the C-ABI.
+
+The paper's lifecycle (Section 3.1, "Fine-Grained Lifecycle Hooks") runs
+Quest's query-dependent page selection in build_decode_selection, before
+attention, and H2O's score update plus online eviction in finish_step, after
+it.  These drivers issue exactly that sequence of library calls on the
+current stream, with workspaces allocated once up front; they never wait for
+the device.
+"""
+
+import torch
+
+from . import _binding as se
+
+
+class H2ODecoder:
+    """One layer's H2O decode step: append + attention + fused score update
+    (se_decode_attend), then retention and compaction (se_evict_compact)."""
+
+    def __init__(self, view: se.KVView, q_per_kv: int, scale: float, budget: int, recent: int,
+                 max_len: int, device, report_freed: bool = False):
+        self.view, self.G, self.scale = view, q_per_kv, scale
+        self.budget, self.recent, self.max_len = budget, recent, max_len
+        d = view.struct.head_dim
+        nbytes = se.se_workspace_bytes(se.SE_OP_DECODE_ATTEND, view.num_units, max_len,
+                                       view.struct.max_pages, q_per_kv, d, 0)
+        self.ws = torch.zeros(max(nbytes, 1), dtype=torch.uint8, device=device)
+        self.dev_err = torch.zeros(1, dtype=torch.int32, device=device)
+        self.freed = None
+        self.freed_count = None
+        if report_freed:
+            self.freed = torch.zeros((view.num_units, view.struct.max_pages), dtype=torch.int32,
+                                     device=device)
+            self.freed_count = torch.zeros(view.num_units, dtype=torch.int32, device=device)
+
+    def attend(self, q, k_new, v_new, new_pos, out, lse=None, accumulate=True):
+        se.se_decode_attend(self.view, self.G, q, k_new, v_new, new_pos, None, 0, self.scale,
+                            self.max_len, se.SE_ATTEND_ACCUMULATE if accumulate else 0, out, lse,
+                            None, 0, self.ws, self.dev_err)
+
+    def evict(self):
+        se.se_evict_compact(self.view, self.budget, self.recent, self.max_len, self.freed,
+                            0 if self.freed is None else self.freed.shape[1], self.freed_count,
+                            self.dev_err)
+
+    def step(self, q, k_new, v_new, new_pos, out, lse=None):
+        self.attend(q, k_new, v_new, new_pos, out, lse)
+        self.evict()
+
+
+class QuestDecoder:
+    """One layer's Quest decode step: page selection (se_quest_select), then
+    append + attention over the selected pages and the current page
+    (se_decode_attend)."""
+
+    def __init__(self, view: se.KVView, q_per_kv: int, scale: float, top_k: int, max_len: int,
+                 device):
+        self.view, self.G, self.scale, self.top_k, self.max_len = view, q_per_kv, scale, top_k, max_len
+        d = view.struct.head_dim
+        mp = view.struct.max_pages
+        na = se.se_workspace_bytes(se.SE_OP_DECODE_ATTEND, view.num_units, max_len, mp, q_per_kv, d, top_k)
+        nq = se.se_workspace_bytes(se.SE_OP_QUEST_SELECT, view.num_units, max_len, mp, q_per_kv, d, 0)
+        self.ws_attend = torch.zeros(max(na, 1), dtype=torch.uint8, device=device)
+        self.ws_select = torch.zeros(max(nq, 1), dtype=torch.uint8, device=device)
+        self.sel = torch.full((view.num_units, top_k), -1, dtype=torch.int32, device=device)
+        self.dev_err = torch.zeros(1, dtype=torch.int32, device=device)
+
+    def summarize(self):
+        se.se_quest_summarize(self.view, self.max_len, self.dev_err)
+
+    def select(self, q, page_scores=None):
+        se.se_quest_select(self.view, self.G, q, self.scale, self.top_k, self.max_len, 0, self.sel,
+                           page_scores, 0 if page_scores is None else page_scores.shape[1],
+                           self.ws_select, self.dev_err)
+
+    def attend(self, q, k_new, v_new, new_pos, out, lse=None):
+        se.se_decode_attend(self.view, self.G, q, k_new, v_new, new_pos, self.sel, self.top_k,
+                            self.scale, self.max_len, 0, out, lse, None, 0, self.ws_attend,
+                            self.dev_err)
+
+    def step(self, q, k_new, v_new, new_pos, out, lse=None):
+        self.select(q)
+        self.attend(q, k_new, v_new, new_pos, out, lse)

@@ -1,0 +1,104 @@
+"""C-ABI checks that need no GPU: every declared symbol is exported, and the
+host-side argument checks return their documented status before anything is
+enqueued (no device pointer is ever dereferenced on these paths)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_39068_amd import _binding as b
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "sparse_engine.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:se_status|size_t|const char\*|int32_t)\s+(se_\w+)\s*\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) == 9, names
+    lib = b.raw_library()
+    for n in names:
+        assert hasattr(lib, n), f"{n} is declared in sparse_engine.h but not exported"
+    assert set(names) == set(b.EXPORTED)
+
+
+def test_status_strings_and_version():
+    assert b.status_string(0) == "SE_OK"
+    assert b.status_string(3) == "SE_ERR_WORKSPACE"
+    assert b.status_string(99) == "SE_UNKNOWN_STATUS"
+    assert b.se_version() == 100
+
+
+def _view(**kw):
+    fields = dict(kv_pool=0x1000, pos_pool=0x2000, score_pool=0x3000, meta_pool=0x4000,
+                  block_table=0x5000, lengths=0x6000, num_pages=64, num_units=4, num_kv_heads=2,
+                  max_pages=8, page_size=16, head_dim=128)
+    fields.update(kw)
+    return b.se_kv_view(**fields)
+
+
+def _attend(view, G=4, q=0x7000, k=None, v=None, pos=None, sel=None, top_k=0, scale=0.1,
+            max_len=128, flags=0, out=0x8000, ws=0x9000, ws_bytes=1 << 40, err=0xA000):
+    return b.raw_library().se_decode_attend(ctypes.byref(view), G, q, k, v, pos, sel, top_k, scale,
+                                            max_len, flags, out, None, None, 0, ws, ws_bytes, err,
+                                            None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(page_size=8), b.SE_ERR_UNSUPPORTED),
+    (dict(head_dim=96), b.SE_ERR_UNSUPPORTED),
+    (dict(num_units=0), b.SE_ERR_INVALID_ARGUMENT),
+    (dict(num_units=5), b.SE_ERR_INVALID_ARGUMENT),       # not a multiple of num_kv_heads
+    (dict(block_table=None), b.SE_ERR_INVALID_ARGUMENT),
+    (dict(lengths=None), b.SE_ERR_INVALID_ARGUMENT),
+])
+def test_view_checks(kw, status):
+    assert _attend(_view(**kw)) == status
+
+
+def test_attend_argument_checks():
+    v = _view()
+    assert _attend(v, G=3) == b.SE_ERR_UNSUPPORTED
+    assert _attend(v, q=None) == b.SE_ERR_INVALID_ARGUMENT
+    assert _attend(v, k=0x100) == b.SE_ERR_INVALID_ARGUMENT           # k without v
+    assert _attend(v, k=0x100, v=0x200) == b.SE_ERR_INVALID_ARGUMENT  # append without new_pos
+    assert _attend(v, max_len=0) == b.SE_ERR_INVALID_ARGUMENT
+    assert _attend(v, sel=0x300, top_k=0) == b.SE_ERR_INVALID_ARGUMENT
+    assert _attend(v, flags=8) == b.SE_ERR_INVALID_ARGUMENT
+    assert _attend(_view(score_pool=None), flags=b.SE_ATTEND_ACCUMULATE) == b.SE_ERR_INVALID_ARGUMENT
+    assert _attend(v, scale=0.0) == b.SE_ERR_INVALID_ARGUMENT
+    assert _attend(v, ws=None) == b.SE_ERR_WORKSPACE
+    assert _attend(v, ws_bytes=16) == b.SE_ERR_WORKSPACE
+    assert _attend(v, err=None) == b.SE_ERR_INVALID_ARGUMENT
+
+
+def test_evict_and_quest_argument_checks():
+    lib = b.raw_library()
+    v = _view()
+    assert lib.se_evict_compact(ctypes.byref(v), 0, 4, 128, None, 0, None, 0xA000, None) == b.SE_ERR_INVALID_ARGUMENT
+    assert lib.se_evict_compact(ctypes.byref(v), 9000, 4, 128, None, 0, None, 0xA000, None) == b.SE_ERR_UNSUPPORTED
+    assert lib.se_evict_compact(ctypes.byref(v), 64, 4, 128, 0x100, 2, None, 0xA000, None) == b.SE_ERR_INVALID_ARGUMENT
+    nv = _view(score_pool=None)
+    assert lib.se_evict_compact(ctypes.byref(nv), 64, 4, 128, None, 0, None, 0xA000, None) == b.SE_ERR_INVALID_ARGUMENT
+    q = lib.se_quest_select
+    assert q(ctypes.byref(v), 4, 0x7000, 0.1, 0, 128, 0, 0x100, None, 0, 0x9000, 1 << 30, 0xA000, None) == b.SE_ERR_INVALID_ARGUMENT
+    assert q(ctypes.byref(v), 4, 0x7000, 0.1, 8, 128, b.SE_QUEST_SCORES_GIVEN, 0x100, None, 0, None, 0, 0xA000, None) == b.SE_ERR_INVALID_ARGUMENT
+    assert q(ctypes.byref(v), 4, 0x7000, 0.1, 8, 128, 0, 0x100, None, 0, None, 0, 0xA000, None) == b.SE_ERR_WORKSPACE
+    assert q(ctypes.byref(v), 4, 0x7000, 0.1, 8, 128, 0, 0x100, 0x200, 4, None, 0, 0xA000, None) == b.SE_ERR_INVALID_ARGUMENT
+    assert lib.se_quest_summarize(ctypes.byref(_view(meta_pool=None)), 128, 0xA000, None) == b.SE_ERR_INVALID_ARGUMENT
+    assert lib.se_accumulate_scores(ctypes.byref(v), 4, 0x100, 64, 0x200, 128, 0xA000, None) == b.SE_ERR_INVALID_ARGUMENT
+    assert lib.se_read_device_errors(None, None, None) == b.SE_ERR_INVALID_ARGUMENT
+
+
+def test_workspace_sizes():
+    # decode: counters + split partials + per-slot weights + per-page references
+    n = b.se_workspace_bytes(b.SE_OP_DECODE_ATTEND, 512, 2049, 129, 4, 128, 0)
+    assert n >= 512 * 2049 * 4 * 4
+    nq = b.se_workspace_bytes(b.SE_OP_DECODE_ATTEND, 256, 33024, 2064, 4, 128, 64)
+    assert nq >= 256 * 65 * 16 * 4 * 4 and nq < n * 4
+    assert b.se_workspace_bytes(b.SE_OP_QUEST_SELECT, 256, 33024, 2064, 4, 128, 0) >= 256 * 2064 * 4
+    assert b.se_workspace_bytes(99, 1, 1, 1, 1, 64, 0) == 0

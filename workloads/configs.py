@@ -1,0 +1,73 @@
+"""The five synthetic decode workloads and their scaled-down test variants.
+
+These stand in for the paper's long-context decode benchmark (Appendix D,
+"Long-Context Decode Benchmark" and "Serving Performance with 32K-token
+Inputs": 128K and 32K inputs, 16-token pages, retained budgets of 2,048 and
+4,096 tokens), whose models and prompts are not available.  The head shape
+Hq=32, Hkv=8, d=128 is the Llama-3-8B GQA shape.
+
+Nothing here computes any part of the method; it only names sizes.
+"""
+
+from dataclasses import dataclass, replace
+from typing import Optional, Tuple
+
+
+@dataclass(frozen=True)
+class Workload:
+    index: int
+    name: str
+    method: str                      # "h2o" or "quest"
+    num_req: int
+    hq: int
+    hkv: int
+    head_dim: int
+    layers: int
+    steps: int
+    page_size: int = 16
+    ctx: Optional[int] = None        # initial logical context per request (uniform)
+    ctx_log_range: Optional[Tuple[int, int]] = None       # log-uniform context per request
+    retained_range: Optional[Tuple[int, int]] = None      # per-head retained length, uniform
+    initial_resident: Optional[int] = None                # resident slots per head (< ctx)
+    budget: Optional[int] = None     # H2O retained budget B
+    recent: Optional[int] = None     # H2O protected recent window w
+    top_k: Optional[int] = None      # Quest selected pages per KV head
+    hh_rate: float = 0.0             # share of positions whose key gets += hh_shift * u
+    hh_shift: float = 0.0
+    relevant_pages: int = 0          # Quest: pages whose keys all get += relevant_shift * u
+    relevant_shift: float = 0.0
+    seed: int = 0
+
+    @property
+    def q_per_kv(self) -> int:
+        return self.hq // self.hkv
+
+    @property
+    def units_per_layer(self) -> int:
+        return self.num_req * self.hkv
+
+    @property
+    def scale(self) -> float:
+        import numpy as np
+        return float(np.float32(1.0 / np.sqrt(self.head_dim)))
+
+
+CONFIGS = [
+    Workload(0, "tiny-h2o-step", "h2o", num_req=2, hq=8, hkv=2, head_dim=64, layers=1,
+             steps=1, ctx=512, budget=128, recent=64, hh_rate=0.01, hh_shift=4.0, seed=0),
+    Workload(1, "llama3-8b-layer-h2o", "h2o", num_req=64, hq=32, hkv=8, head_dim=128, layers=1,
+             steps=256, ctx=32768, budget=2048, recent=256, hh_rate=0.01, hh_shift=4.0, seed=1),
+    Workload(2, "llama3-8b-layer-quest", "quest", num_req=32, hq=32, hkv=8, head_dim=128, layers=1,
+             steps=256, ctx=32768, top_k=64, relevant_pages=8, relevant_shift=3.0, seed=2),
+    Workload(3, "ragged-continuous-batch-h2o", "h2o", num_req=128, hq=32, hkv=8, head_dim=128,
+             layers=1, steps=128, ctx_log_range=(2048, 131072), retained_range=(1024, 4096),
+             budget=4096, recent=512, hh_rate=0.01, hh_shift=4.0, seed=3),
+    Workload(4, "llama3-8b-32-layer-h2o", "h2o", num_req=256, hq=32, hkv=8, head_dim=128, layers=32,
+             steps=64, ctx=131072, initial_resident=4096, budget=4096, recent=512,
+             hh_rate=0.01, hh_shift=4.0, seed=4),
+]
+
+
+def scaled(w: Workload, **changes) -> Workload:
+    """A variant of a workload with some sizes changed (test cases)."""
+    return replace(w, **changes)
