@@ -1,0 +1,356 @@
+#!/usr/bin/env python3
+"""Decode attention + eviction benchmark on one MI355X.
+
+Default workload: the Llama-3-8B-shaped single layer with H2O (64 requests,
+Hq=32, Hkv=8, d=128, 32768-token contexts, budget 2048 with a 256-token
+window, 256 decode steps).  One timed step is one decode step of the whole
+batch through the hot path: se_decode_attend (append, split-K attention,
+fused score update) then se_evict_compact (retention + compaction).  The
+first step evicts 32769 -> 2048 per head; later steps evict one slot.
+
+Protocol: the state is generated on the device (seeded), warm-up steps run on
+a copy that is then dropped, and the K timed steps start from the generated
+state with every input already resident in HBM.  The timed region is
+bracketed by device synchronisations; per-call HIP events on the launch
+stream give each kernel's duration for the roofline figure.
+
+Prints one JSON line.  `--config N` runs another workload (0..4) for
+measurement; `--gpus N` with N > 1 is refused (single-GPU build).
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode attn+eviction tokens/s/GPU; achieved HBM GB/s vs MI355X peak"
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_attend_llama3-8b-layer-h2o_traffic.txt")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed decode steps (default: the workload's)")
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--config", type=int, default=1, help="workload index 0..4")
+    ap.add_argument("--cpu-baseline", choices=["auto", "skip"], default="auto")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one plain 4 GiB device copy (counter calibration under rocprofv3)")
+    return ap.parse_args()
+
+
+# --------------------------------------------------------------------- CPU oracle baseline
+
+def _oracle_unit_run(i):
+    """One unit's trajectory through the oracle, in a forked worker that only
+    touches NumPy arrays prepared by the parent."""
+    from threadpoolctl import threadpool_limits
+    from oracle import h2o, quest
+    from oracle.state import new_unit
+    job = _SHARED["jobs"][i]
+    w = _SHARED["w"]
+    with threadpool_limits(1):
+        st = new_unit(job["K"], job["V"], job["pos"])
+        if w.method == "quest":
+            quest.attach_summaries(st)
+        t0 = time.perf_counter()
+        for t in range(len(job["p"])):
+            if w.method == "h2o":
+                h2o.decode_step(st, job["q"][t], job["k"][t], job["v"][t], job["p"][t], w.scale,
+                                w.budget, w.recent)
+            else:
+                quest.decode_step(st, job["q"][t], job["k"][t], job["v"][t], job["p"][t], w.scale, w.top_k)
+        return time.perf_counter() - t0
+
+
+_SHARED = {}
+
+
+def cpu_baseline(w, K):
+    """The oracle, untuned, on a bounded sample of the same workload: the
+    first request (all its KV heads, one layer) for the same K steps,
+    one unit per worker process.  Runs before the GPU is touched; the workers
+    are forked after every input has been converted to NumPy."""
+    import multiprocessing as mp
+    import numpy as np
+    import torch
+    from workloads import build_state, build_steps, scaled, unit_slots
+    sample_req = 1
+    ws = scaled(w, num_req=sample_req, layers=1)
+    host = build_state(ws, "cpu")
+    steps = build_steps(ws, host, "cpu", steps=K)
+    G = ws.q_per_kv
+
+    def f64(t):
+        return t.to(torch.float64).numpy()
+
+    jobs = []
+    for u in range(ws.units_per_layer):
+        req, kvh = divmod(u, ws.hkv)
+        Kt, Vt, pos, _ = unit_slots(host, u)
+        jobs.append({"K": f64(Kt), "V": f64(Vt), "pos": pos.numpy().astype(np.int64),
+                     "q": f64(steps.q[:, 0, req, kvh * G:(kvh + 1) * G]),
+                     "k": f64(steps.k_new[:, 0, req, kvh]), "v": f64(steps.v_new[:, 0, req, kvh]),
+                     "p": [int(x) for x in steps.new_pos[:, req]]})
+    _SHARED["jobs"], _SHARED["w"] = jobs, ws
+    workers = min(16, os.cpu_count() or 1, len(jobs))
+    ctx = mp.get_context("fork")
+    t0 = time.perf_counter()
+    with ctx.Pool(workers) as pool:
+        per_unit = pool.map(_oracle_unit_run, range(len(jobs)))
+    wall = time.perf_counter() - t0
+    return {"value": round(sample_req * K / wall, 2), "unit": "tokens/s", "cores": workers, "kind": "oracle",
+            "sample": (f"{sample_req} of {w.num_req} requests ({len(jobs)} KV-head units, 1 layer) of "
+                       f"'{w.name}', {K} decode steps each, NumPy float64, one unit per process"),
+            "cpu_seconds": round(sum(per_unit), 2), "wall_seconds": round(wall, 2)}
+
+
+# --------------------------------------------------------------------- algorithmic bytes
+
+def attend_bytes(lengths_post, G, D, append=True):
+    """Bytes se_decode_attend must move for one call (H2O, every slot read):
+    per slot the K and V rows plus the score read and write; per unit the G
+    query rows (bf16), the G output rows (fp32) and G lse values, and the
+    appended token (k, v read; k, v, position, score written)."""
+    slots = int(lengths_post.sum())
+    units = int(lengths_post.shape[0])
+    per_slot = 2 * D * 2 + 8
+    per_unit = G * D * 2 + G * D * 4 + G * 4 + (2 * D * 2 * 2 + 8 if append else 0)
+    return slots * per_slot + units * per_unit
+
+
+def evict_bytes(lengths_post, budget, D):
+    """Bytes se_evict_compact must move: every resident slot's score and
+    position once, and each moved slot's K and V rows, position and score
+    read and written (the steady state moves at most one slot)."""
+    import numpy as np
+    L = lengths_post
+    over = L > budget
+    reads = int((L[over]).sum()) * 8
+    moved = np.minimum(np.maximum(L - budget, 0), budget)   # upper bound of movers per unit
+    per_move = 2 * (2 * D * 2 + 8)
+    return reads + int(moved[over].sum()) * per_move
+
+
+def select_bytes(n_cand, G, D, top_k):
+    """se_quest_select: every candidate page's min and max rows, its score
+    written and read back, the G query rows, the top_k selected ids."""
+    units = int(n_cand.shape[0])
+    return int(n_cand.sum()) * (2 * D * 2 + 8) + units * (G * D * 2 + top_k * 4)
+
+
+def quest_attend_bytes(visited, G, D, top_k):
+    """se_decode_attend over a selection: the visited slots' K and V rows; per
+    unit the query, output, appended token (with its page's min/max read and
+    written) and the selected page ids."""
+    units = int(visited.shape[0])
+    per_unit = G * D * 2 + G * D * 4 + 2 * D * 2 * 2 + 8 + 2 * (2 * D * 2) + top_k * 4
+    return int(visited.sum()) * (2 * D * 2) + units * per_unit
+
+
+def source_hash():
+    h = hashlib.sha256()
+    for f in ("decode_attend.hip", "se_common.h"):
+        h.update(open(os.path.join(ROOT, "paper_2609_39068_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic():
+    """HBM bytes per decode_attend launch from the committed rocprofv3
+    counter summary, or None when it is missing or the kernel has changed."""
+    if not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    vals = {}
+    for line in open(TRAFFIC_SUMMARY):
+        if "=" in line and not line.lstrip().startswith("#"):
+            k, v = line.split("=", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("source_hash") != source_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+# --------------------------------------------------------------------- GPU run
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on one GPU only; every unit (request, KV head) is independent, "
+              "so N GPUs would each run this same benchmark on their share of the requests. "
+              "Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    from workloads import CONFIGS
+    w = CONFIGS[args.config]
+    K = int(args.steps if args.steps is not None else w.steps)
+    W = int(args.warmup)
+
+    cpu = None
+    if args.cpu_baseline == "auto":
+        cpu = cpu_baseline(w, K)
+        print(f"cpu baseline: {cpu['value']:.1f} tokens/s on {cpu['cores']} processes", file=sys.stderr, flush=True)
+
+    import numpy as np
+    import torch
+    import paper_2609_39068_amd as se
+    from workloads import build_state, build_steps, clone_state
+
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    dev = torch.device("cuda:0")
+    t_gen = time.perf_counter()
+    state = build_state(w, dev)
+    keep_going = w.layers > 1          # too large to copy: warm up on the state itself
+    n_inputs = K + (W if keep_going else max(W, 0))
+    steps = build_steps(w, state, dev, steps=max(n_inputs, 1))
+    torch.cuda.synchronize()
+    print(f"generated '{w.name}' in {time.perf_counter() - t_gen:.1f}s", file=sys.stderr, flush=True)
+
+    U, G, D = w.units_per_layer, w.q_per_kv, w.head_dim
+    max_len = state.max_pages * 16
+    out = torch.empty((w.num_req, w.hq, D), dtype=torch.float32, device=dev)
+
+    def make(st):
+        views = [se.KVView(st.kv_pool, st.pos_pool, st.score_pool, st.meta_pool,
+                           st.block_table[st.layer_rows(l)], st.lengths[st.layer_rows(l)],
+                           num_kv_heads=w.hkv) for l in range(w.layers)]
+        if w.method == "h2o":
+            ws = se.H2ODecoder.workspace(views[0], G, max_len, dev)
+            err = torch.zeros(1, dtype=torch.int32, device=dev)
+            return [se.H2ODecoder(v, G, w.scale, w.budget, w.recent, max_len, dev, ws=ws, dev_err=err)
+                    for v in views]
+        decs = [se.QuestDecoder(v, G, w.scale, w.top_k, max_len, dev) for v in views]
+        for d in decs:
+            d.summarize()
+        return decs
+
+    def run(decs, t0, t1, events=None):
+        for t in range(t0, t1):
+            for l, d in enumerate(decs):
+                q, kn, vn, npos = steps.q[t, l], steps.k_new[t, l], steps.v_new[t, l], steps.new_pos[t]
+                if events is not None:
+                    e = events[t - t0][l]
+                    e[0].record()
+                if w.method == "h2o":
+                    d.attend(q, kn, vn, npos, out)
+                    if events is not None:
+                        e[1].record()
+                    d.evict()
+                else:
+                    d.select(q)
+                    if events is not None:
+                        e[1].record()
+                    d.attend(q, kn, vn, npos, out)
+                if events is not None:
+                    e[2].record()
+
+    # warm-up
+    t_base = 0
+    if W > 0:
+        if keep_going:
+            decs = make(state)
+            run(decs, 0, W)
+            t_base = W
+        else:
+            scratch = clone_state(state)
+            run(make(scratch), 0, W)
+            torch.cuda.synchronize()
+            del scratch
+            torch.cuda.empty_cache()
+            decs = make(state)
+    else:
+        decs = make(state)
+    torch.cuda.synchronize()
+    lengths0 = state.lengths.cpu().numpy().astype(np.int64)
+
+    events = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(w.layers)]
+              for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(decs, t_base, t_base + K, events)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    errs = se.se_read_device_errors(decs[0].dev_err)
+    if errs:
+        raise RuntimeError(f"device error bits {errs:#x} during the timed run")
+
+    # per-call durations and algorithmic bytes (lengths follow the method's rule on the host)
+    first_ms, second_ms = [], []
+    first_bytes, second_bytes = 0, 0
+    L = lengths0.reshape(w.layers, U).copy()
+    for t in range(K):
+        for l in range(w.layers):
+            e = events[t][l]
+            first_ms.append(e[0].elapsed_time(e[1]))
+            second_ms.append(e[1].elapsed_time(e[2]))
+            Lp = L[l] + 1
+            if w.method == "h2o":
+                first_bytes += attend_bytes(Lp, G, D)
+                second_bytes += evict_bytes(Lp, w.budget, D)
+                L[l] = np.minimum(Lp, w.budget)
+            else:
+                n_cand = L[l] // 16
+                visited = np.minimum(n_cand, w.top_k) * 16 + ((Lp - 1) % 16 + 1)
+                first_bytes += select_bytes(n_cand, G, D, w.top_k)
+                second_bytes += quest_attend_bytes(visited, G, D, w.top_k)
+                L[l] = Lp
+    tokens = w.num_req * K
+    value = tokens / elapsed
+    if w.method == "h2o":
+        dom_name, dom_ms, dom_bytes = "decode_attend", sum(first_ms), first_bytes
+        other = {"evict_compact": {"avg_us": 1e3 * sum(second_ms) / len(second_ms),
+                                   "algorithmic_GBps": second_bytes / (sum(second_ms) * 1e-3) / 1e9}}
+    else:
+        dom_name, dom_ms, dom_bytes = "quest_select", sum(first_ms), first_bytes
+        other = {"decode_attend": {"avg_us": 1e3 * sum(second_ms) / len(second_ms),
+                                   "algorithmic_GBps": second_bytes / (sum(second_ms) * 1e-3) / 1e9}}
+    n_launch = K * w.layers
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    traffic = read_traffic() if (w.index == 1 and w.method == "h2o") else None
+    result = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(1e3 * elapsed / K, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "method": w.method, "batch": w.num_req, "hq": w.hq, "hkv": w.hkv,
+                   "head_dim": D, "page_size": w.page_size, "layers": w.layers, "context": w.ctx,
+                   "budget": w.budget, "recent": w.recent, "top_k": w.top_k, "accumulate": "f32",
+                   "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": "hbm", "kernel": dom_name, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "avg_launch_us": round(1e3 * dom_ms / n_launch, 3),
+                     "algorithmic_bytes_per_launch": round(dom_bytes / n_launch)},
+        "step_GBps": round((first_bytes + second_bytes) / elapsed / 1e9, 1),
+        "kernels": other,
+        "cpu_baseline": cpu,
+    }
+    if w.method == "h2o" and w.index == 1 and K > 1:
+        result["phases"] = {"step1_ms": round(first_ms[0] + second_ms[0], 3),
+                            "steady_ms_per_step": round((sum(first_ms[1:]) + sum(second_ms[1:])) / (K - 1), 4)}
+    if args.copy_calibration:
+        n = 4 << 30
+        a = torch.empty(n, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        result["copy_calibration_bytes"] = n
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

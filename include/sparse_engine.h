@@ -109,8 +109,8 @@ typedef struct se_kv_view {
  *     G query rows of the unit over its read set S:
  *       sel_pages == NULL: S = every resident slot (H2O: the whole available set);
  *       otherwise S = the slots of the logical pages sel_pages[unit][0..top_k)
- *       (entries < 0 are skipped) plus the current page, floor(L'/16) with L' the
- *       length after the append minus 1, read up to the newest slot (Quest).
+ *       (entries < 0 are skipped; each must be a page below the current one) plus
+ *       the current page, the page of the newest resident slot (Quest).
  *     z_j = scale * <q, k_j>, out = sum_j softmax_S(z)_j v_j, lse = log sum_j e^{z_j}.
  *  3. With SE_ATTEND_ACCUMULATE (needs score_pool): every slot of S gets its weight
  *     summed over the unit's G query heads added to its score (eq.
@@ -128,9 +128,8 @@ typedef struct se_kv_view {
  *  lse      fp32 [num_req][num_kv_heads * q_per_kv], or NULL
  *  logits   fp32 [num_units][q_per_kv][logits_stride] (z per slot), or NULL; only
  *           with sel_pages == NULL; logits_stride >= max_len
- *  ws       device workspace of se_workspace_bytes(SE_OP_DECODE_ATTEND, ...) bytes,
- *           zero-filled before its first use; every call leaves it zero-filled again
- *           where it must be (counters).  Not shared between concurrent calls.
+ *  ws       device workspace of se_workspace_bytes(SE_OP_DECODE_ATTEND, ...) bytes (no
+ *           initial contents needed).  Not shared between calls that may overlap.
  *  dev_err  int32 device word (see SE_DEVERR_*), never NULL
  */
 se_status se_decode_attend(const se_kv_view* kv, int32_t q_per_kv, const void* q,

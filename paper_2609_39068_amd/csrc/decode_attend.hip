@@ -19,10 +19,13 @@
 //   * PV layout: lane owns two adjacent columns of the V block for all 16 rows
 //     (one coalesced 256-byte row per load instruction across the wave); the
 //     page's 16*G weights are broadcast through LDS.
-// Partials (m, l, o) go to the workspace; the last work-group of a unit to
-// arrive (device-scope counter) combines them in a fixed order, writes out and
-// lse, runs the score epilogue from the per-slot weights it finds in the
-// workspace, publishes the new length and resets the counter.
+// With one work-group per unit that work-group finishes the unit itself.  With
+// several, each writes its partial (m, l, o) to the workspace and a second,
+// one-work-group-per-unit kernel combines them in a fixed order, writes out and
+// lse, runs the score epilogue and publishes the new length.  The kernel
+// boundary orders the two passes across XCDs (each XCD has its own L2), which
+// avoids a device-scope release/acquire (an L2 writeback and invalidate) in
+// every work-group.
 #include "se_common.h"
 
 namespace se {
@@ -54,7 +57,6 @@ struct AttendParams {
   float* lse;
   float* logits;
   int32_t logits_stride;
-  int32_t* counters;
   float* part;
   float* pbuf;
   float* mref;
@@ -62,14 +64,12 @@ struct AttendParams {
 };
 
 struct AttendWs {
-  size_t counters, part, pbuf, mref, total;
+  size_t part, pbuf, mref, total;
 };
 
 inline AttendWs attend_ws_layout(int units, const SplitShape& s, int G, int D) {
   AttendWs w;
   size_t off = 0;
-  w.counters = off;
-  off = align_up(off + (size_t)units * 4, 256);
   w.part = off;
   off = align_up(off + (size_t)units * s.n_split * G * (D + 2) * 4, 256);
   w.pbuf = off;
@@ -78,6 +78,61 @@ inline AttendWs attend_ws_layout(int units, const SplitShape& s, int G, int D) {
   off = align_up(off + (size_t)units * s.n_visit * G * 4, 256);
   w.total = off;
   return w;
+}
+
+// Per-unit quantities both kernels derive the same way from the inputs.
+struct UnitGeom {
+  int unit, req, kvh, L, Lp, cur_page, n_visit;
+  bool append, quest, bad;
+};
+
+__device__ __forceinline__ UnitGeom unit_geom(const AttendParams& p, int unit) {
+  UnitGeom g;
+  g.unit = unit;
+  g.req = unit / p.hkv;
+  g.kvh = unit - g.req * p.hkv;
+  g.L = p.lengths[unit];
+  g.append = p.k_new != nullptr;
+  g.Lp = g.L + (g.append ? 1 : 0);
+  g.quest = p.sel != nullptr;
+  g.bad = g.L < 0 || g.Lp < 1 || g.Lp > p.max_len || g.Lp > p.max_pages * kPage;
+  g.cur_page = g.bad ? 0 : (g.Lp - 1) / kPage;
+  g.n_visit = g.bad ? 0 : (g.quest ? p.top_k + 1 : g.cur_page + 1);
+  return g;
+}
+
+// After the unit's final (m, 1/l) per head are in fin_m / fin_il: the fused
+// score update over every visited slot (eq. background-h2o-score, summed over
+// the group; the new token's score is its weight) and the new length.
+template <int G>
+__device__ void finish_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
+                            const float* fin_il) {
+  const size_t ubase_p = (size_t)g.unit * p.n_visit_max;
+  if (p.accumulate) {
+    for (int idx = threadIdx.x; idx < g.n_visit * kPage; idx += blockDim.x) {
+      const int vp = idx >> 4;
+      const int rr = idx & (kPage - 1);
+      int lp = vp;
+      if (g.quest) {
+        lp = vp < p.top_k ? p.sel[(size_t)g.unit * p.top_k + vp] : g.cur_page;
+        if (lp < 0 || (vp < p.top_k && lp >= g.cur_page)) continue;
+      }
+      const int slot = lp * kPage + rr;
+      if (slot >= g.Lp) continue;
+      const int phys = p.block_table[(size_t)g.unit * p.max_pages + lp];
+      if (phys < 0 || (int64_t)phys >= p.num_pages) continue;
+      float a = 0.f;
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float w = p.pbuf[((ubase_p + vp) * kPage + rr) * G + h];
+        const float mr = p.mref[(ubase_p + vp) * G + h];
+        a += w * fast_exp2(mr - fin_m[h]) * fin_il[h];
+      }
+      float* up = p.score_pool + (size_t)phys * kPage + rr;
+      *up = (g.append && slot == g.L) ? a : *up + a;
+    }
+  }
+  if (g.append && threadIdx.x == 0) p.lengths[g.unit] = g.Lp;
 }
 
 template <int D, int G>
@@ -97,24 +152,16 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(const AttendParams p
   __shared__ float lds_o[NW][G][D];
   __shared__ float fin_m[G];
   __shared__ float fin_il[G];
-  __shared__ int lds_last;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int unit = blockIdx.x / p.n_split;
   const int split = blockIdx.x - unit * p.n_split;
-  const int req = unit / p.hkv;
-  const int kvh = unit - req * p.hkv;
+  const UnitGeom g = unit_geom(p, unit);
+  const int req = g.req, kvh = g.kvh, L = g.L, Lp = g.Lp, cur_page = g.cur_page, n_visit = g.n_visit;
+  const bool append = g.append, quest = g.quest, bad = g.bad;
   const int Hq = p.hkv * G;
-
-  const int L = p.lengths[unit];
-  const bool append = p.k_new != nullptr;
-  const int Lp = L + (append ? 1 : 0);
-  const bool quest = p.sel != nullptr;
-  const bool bad = L < 0 || Lp < 1 || Lp > p.max_len || Lp > p.max_pages * kPage;
-  const int cur_page = bad ? 0 : (Lp - 1) / kPage;
-  const int n_visit = bad ? 0 : (quest ? p.top_k + 1 : cur_page + 1);
   const int vbeg = split * p.pps;
   const int vend = min(vbeg + p.pps, n_visit);
 
@@ -369,79 +416,58 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(const AttendParams p
     }
   }
 
-  if (!single) {
-    // ---- arrival: the last work-group of the unit continues
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) {
-      const int prev = atomicAdd(&p.counters[unit], 1);
-      lds_last = (prev == p.n_split - 1);
-    }
-    __syncthreads();
-    if (!lds_last) return;
-    __threadfence();
-    if (tid == 0) p.counters[unit] = 0;
-    if (!bad) {
-      const int n_act = min(p.n_split, (int)ceil_div_dev(n_visit, p.pps));
-      for (int idx = tid; idx < G * D; idx += 256) {
-        const int h = idx / D;
-        const int c = idx - h * D;
-        float m = -INFINITY;
-        for (int s = 0; s < n_act; ++s) m = fmaxf(m, part_u[((size_t)s * G + h) * (D + 2)]);
-        float o = 0.f, l = 0.f;
-        for (int s = 0; s < n_act; ++s) {
-          const float* rec = part_u + ((size_t)s * G + h) * (D + 2);
-          const float f = rec[0] == -INFINITY ? 0.f : fast_exp2(rec[0] - m);
-          o += rec[2 + c] * f;
-          l += rec[1] * f;
-        }
-        p.out[((size_t)req * Hq + kvh * G + h) * D + c] = o / l;
-        if (c == 0) {
-          if (p.lse != nullptr) p.lse[(size_t)req * Hq + kvh * G + h] = (m + __log2f(l)) * kLn2;
-          fin_m[h] = m;
-          fin_il[h] = 1.f / l;
-        }
-      }
-    }
-  }
+  if (!single) return;  // the combine kernel finishes the unit
   __syncthreads();
-
   if (bad) {
     if (tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_LENGTH);
     return;
   }
+  finish_unit<G>(p, g, fin_m, fin_il);
+}
 
-  // ---- fused H2O score epilogue (eq. background-h2o-score, summed over the group)
-  if (p.accumulate) {
-    for (int idx = tid; idx < n_visit * kPage; idx += 256) {
-      const int vp = idx >> 4;
-      const int rr = idx & (kPage - 1);
-      int lp = vp;
-      if (quest) {
-        lp = vp < p.top_k ? p.sel[(size_t)unit * p.top_k + vp] : cur_page;
-        if (lp < 0 || (vp < p.top_k && lp >= cur_page)) continue;
-      }
-      const int slot = lp * kPage + rr;
-      if (slot >= Lp) continue;
-      const int phys = p.block_table[(size_t)unit * p.max_pages + lp];
-      if (phys < 0 || (int64_t)phys >= p.num_pages) continue;
-      float a = 0.f;
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-        const float w = p.pbuf[((ubase_p + vp) * kPage + rr) * G + h];
-        const float mr = p.mref[(ubase_p + vp) * G + h];
-        a += w * fast_exp2(mr - fin_m[h]) * fin_il[h];
-      }
-      float* up = p.score_pool + (size_t)phys * kPage + rr;
-      *up = (append && slot == L) ? a : *up + a;
+// Second pass when a unit is split over several work-groups: combines the
+// partials (m, l, o) in split order, writes out and lse, then finishes the unit.
+template <int D, int G>
+__global__ __launch_bounds__(256) void decode_combine_kernel(const AttendParams p) {
+  __shared__ float fin_m[G];
+  __shared__ float fin_il[G];
+  const UnitGeom g = unit_geom(p, blockIdx.x);
+  if (g.bad) {
+    if (threadIdx.x == 0) set_error(p.dev_err, SE_DEVERR_BAD_LENGTH);
+    return;
+  }
+  const int Hq = p.hkv * G;
+  const int n_act = min(p.n_split, ceil_div_dev(g.n_visit, p.pps));
+  const float* part_u = p.part + (size_t)g.unit * p.n_split * G * (D + 2);
+  for (int idx = threadIdx.x; idx < G * D; idx += blockDim.x) {
+    const int h = idx / D;
+    const int c = idx - h * D;
+    float m = -INFINITY;
+    for (int s = 0; s < n_act; ++s) m = fmaxf(m, part_u[((size_t)s * G + h) * (D + 2)]);
+    float o = 0.f, l = 0.f;
+    for (int s = 0; s < n_act; ++s) {
+      const float* rec = part_u + ((size_t)s * G + h) * (D + 2);
+      const float f = rec[0] == -INFINITY ? 0.f : fast_exp2(rec[0] - m);
+      o += rec[2 + c] * f;
+      l += rec[1] * f;
+    }
+    p.out[((size_t)g.req * Hq + g.kvh * G + h) * D + c] = o / l;
+    if (c == 0) {
+      if (p.lse != nullptr) p.lse[(size_t)g.req * Hq + g.kvh * G + h] = (m + __log2f(l)) * kLn2;
+      fin_m[h] = m;
+      fin_il[h] = 1.f / l;
     }
   }
-  if (append && tid == 0) p.lengths[unit] = Lp;
+  __syncthreads();
+  finish_unit<G>(p, g, fin_m, fin_il);
 }
 
 template <int D, int G>
 static void launch_attend(const AttendParams& prm, int grid, hipStream_t stream) {
   hipLaunchKernelGGL((decode_attend_kernel<D, G>), dim3(grid), dim3(256), 0, stream, prm);
+  if (prm.n_split > 1)
+    hipLaunchKernelGGL((decode_combine_kernel<D, G>), dim3(grid / prm.n_split), dim3(256), 0, stream,
+                       prm);
 }
 
 }  // namespace se
@@ -524,7 +550,6 @@ extern "C" se_status se_decode_attend(const se_kv_view* kv, int32_t q_per_kv, co
   prm.logits = logits;
   prm.logits_stride = logits_stride;
   char* base = static_cast<char*>(ws);
-  prm.counters = reinterpret_cast<int32_t*>(base + lay.counters);
   prm.part = reinterpret_cast<float*>(base + lay.part);
   prm.pbuf = reinterpret_cast<float*>(base + lay.pbuf);
   prm.mref = reinterpret_cast<float*>(base + lay.mref);

@@ -18,20 +18,25 @@ class H2ODecoder:
     (se_decode_attend), then retention and compaction (se_evict_compact)."""
 
     def __init__(self, view: se.KVView, q_per_kv: int, scale: float, budget: int, recent: int,
-                 max_len: int, device, report_freed: bool = False):
+                 max_len: int, device, report_freed: bool = False, ws=None, dev_err=None):
+        """``ws`` / ``dev_err`` may be shared by decoders whose calls run one
+        after another on one stream (e.g. the layers of a model)."""
         self.view, self.G, self.scale = view, q_per_kv, scale
         self.budget, self.recent, self.max_len = budget, recent, max_len
-        d = view.struct.head_dim
-        nbytes = se.se_workspace_bytes(se.SE_OP_DECODE_ATTEND, view.num_units, max_len,
-                                       view.struct.max_pages, q_per_kv, d, 0)
-        self.ws = torch.zeros(max(nbytes, 1), dtype=torch.uint8, device=device)
-        self.dev_err = torch.zeros(1, dtype=torch.int32, device=device)
+        self.ws = ws if ws is not None else self.workspace(view, q_per_kv, max_len, device)
+        self.dev_err = dev_err if dev_err is not None else torch.zeros(1, dtype=torch.int32, device=device)
         self.freed = None
         self.freed_count = None
         if report_freed:
             self.freed = torch.zeros((view.num_units, view.struct.max_pages), dtype=torch.int32,
                                      device=device)
             self.freed_count = torch.zeros(view.num_units, dtype=torch.int32, device=device)
+
+    @staticmethod
+    def workspace(view: se.KVView, q_per_kv: int, max_len: int, device) -> torch.Tensor:
+        nbytes = se.se_workspace_bytes(se.SE_OP_DECODE_ATTEND, view.num_units, max_len,
+                                       view.struct.max_pages, q_per_kv, view.struct.head_dim, 0)
+        return torch.zeros(max(nbytes, 1), dtype=torch.uint8, device=device)
 
     def attend(self, q, k_new, v_new, new_pos, out, lse=None, accumulate=True):
         se.se_decode_attend(self.view, self.G, q, k_new, v_new, new_pos, None, 0, self.scale,

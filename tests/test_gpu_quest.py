@@ -1,0 +1,178 @@
+"""Quest path on the GPU against the oracle: se_quest_summarize,
+se_quest_select (bound + top-k) and se_decode_attend over the selected pages.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import quest
+from oracle.attention import selected_attention
+from tests.oracle_bridge import (LSE_ATOL, OUT_ATOL, QUEST_RTOL, f64, gpu_unit, oracle_unit,
+                                 quest_near_tie)
+from workloads import CONFIGS, build_state, build_steps, isolated_units, scaled, to_device
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+@pytest.fixture(scope="module")
+def se():
+    import paper_2609_39068_amd as m
+    assert torch.cuda.is_available()
+    return m
+
+
+def _view(se, st):
+    return se.KVView(st.kv_pool, st.pos_pool, st.score_pool, st.meta_pool, st.block_table,
+                     st.lengths, num_kv_heads=st.w.hkv)
+
+
+def _meta(gs, u, n_pages):
+    bt = gs.block_table[u, :n_pages].to(torch.int64)
+    m = gs.meta_pool[bt].cpu().to(torch.float64).numpy()   # [n_pages, 2, d]
+    return m[:, 0], m[:, 1]
+
+
+def _run_quest(se, w, n_steps):
+    """n_steps Quest decode steps on the GPU and the oracle; compares the
+    summaries, the page scores, the selection (exact, or a near-tie under the
+    oracle's scores) and, where the selections agree, the outputs."""
+    host = build_state(w, "cpu")
+    steps = build_steps(w, host, "cpu", steps=n_steps)
+    U, G = w.units_per_layer, w.q_per_kv
+    ost = {u: oracle_unit(host, u) for u in range(U)}
+    for st in ost.values():
+        quest.attach_summaries(st)
+    gs = to_device(host, DEV)
+    view = _view(se, gs)
+    max_len = host.max_pages * 16
+    dec = se.QuestDecoder(view, G, w.scale, w.top_k, max_len, DEV)
+    dec.summarize()
+    torch.cuda.synchronize()
+    for u in range(U):
+        mn, mx = _meta(gs, u, ost[u].mn.shape[0])
+        np.testing.assert_array_equal(mn, ost[u].mn)
+        np.testing.assert_array_equal(mx, ost[u].mx)
+    scores = torch.full((U, host.max_pages), float("nan"), dtype=torch.float32, device=DEV)
+    out = torch.empty((w.num_req, w.hq, w.head_dim), dtype=torch.float32, device=DEV)
+    lse = torch.empty((w.num_req, w.hq), dtype=torch.float32, device=DEV)
+    same = ties = 0
+    for t in range(n_steps):
+        print(f"step {t}", flush=True)
+        q = steps.q[t, 0].to(DEV)
+        dec.select(q, scores)
+        dec.attend(q, steps.k_new[t, 0].to(DEV), steps.v_new[t, 0].to(DEV), steps.new_pos[t].to(DEV), out, lse)
+        torch.cuda.synchronize()
+        assert se.se_read_device_errors(dec.dev_err) == 0
+        sel_g = dec.sel.cpu().numpy()
+        sc_g = scores.cpu().double().numpy()
+        o_g, lse_g = out.cpu().double().numpy(), lse.cpu().double().numpy()
+        for u in range(U):
+            req, kvh = divmod(u, w.hkv)
+            rows = slice(kvh * G, (kvh + 1) * G)
+            st = ost[u]
+            res = quest.decode_step(st, f64(steps.q[t, 0, req, rows]), f64(steps.k_new[t, 0, req, kvh]),
+                                    f64(steps.v_new[t, 0, req, kvh]), int(steps.new_pos[t, req]),
+                                    w.scale, w.top_k)
+            n = res["n_candidates"]
+            want = res["scores"]
+            err = np.abs(sc_g[u, :n] - want) / np.maximum(1.0, np.abs(want))
+            assert err.max() <= QUEST_RTOL, f"step {t} unit {u}: page score off by {err.max()}"
+            k = min(w.top_k, n)
+            assert (sel_g[u, k:] == -1).all()
+            got = sel_g[u, :k]
+            assert (np.diff(got) > 0).all(), "selection must be ascending"
+            if got.tolist() != res["selected"].tolist():
+                assert quest_near_tie(want, got, res["selected"]), f"step {t} unit {u}: selection differs"
+                ties += 1
+                continue
+            same += 1
+            assert np.abs(o_g[req, rows] - res["o"]).max() <= OUT_ATOL, f"step {t} unit {u}"
+            assert np.abs(lse_g[req, rows] - res["lse"]).max() <= LSE_ATOL
+        # the appended token and the summaries of its page
+        for u in range(U):
+            g = gpu_unit(gs, u)
+            np.testing.assert_array_equal(g["pos"], ost[u].pos)
+            np.testing.assert_array_equal(g["K"], ost[u].K)
+            mn, mx = _meta(gs, u, ost[u].mn.shape[0])
+            np.testing.assert_array_equal(mn, ost[u].mn)
+            np.testing.assert_array_equal(mx, ost[u].mx)
+    return same, ties
+
+
+def test_quest_trajectory_8b_shape_scaled(se):
+    # 2 requests of the 8B head shape, 2000 tokens (125 pages), top-8 pages,
+    # 20 steps crossing a page boundary (2000 + 16 tokens).
+    w = scaled(CONFIGS[2], num_req=2, ctx=2000, top_k=8, steps=20)
+    same, ties = _run_quest(se, w, 20)
+    assert same >= 0.9 * 20 * w.units_per_layer
+
+
+def test_quest_variants(se):
+    # d=64 with G=2, a partial current page, more pages wanted than exist.
+    w = scaled(CONFIGS[2], num_req=2, hq=4, hkv=2, head_dim=64, ctx=90, top_k=9, steps=12)
+    same, ties = _run_quest(se, w, 12)
+    assert same >= 0.9 * 12 * w.units_per_layer
+
+
+def test_select_all_pages_is_dense(se):
+    # top_k >= number of pages: every page is read, so the step is dense attention.
+    w = scaled(CONFIGS[2], num_req=2, ctx=500, top_k=64, steps=2)
+    host = build_state(w, "cpu")
+    steps = build_steps(w, host, "cpu")
+    G = w.q_per_kv
+    dense = {}
+    for u in range(w.units_per_layer):
+        st = oracle_unit(host, u)
+        req, kvh = divmod(u, w.hkv)
+        K = np.vstack([st.K, f64(steps.k_new[0, 0, req, kvh])[None]])
+        V = np.vstack([st.V, f64(steps.v_new[0, 0, req, kvh])[None]])
+        dense[u] = selected_attention(f64(steps.q[0, 0, req, kvh * G:(kvh + 1) * G]), K, V,
+                                      np.arange(K.shape[0]), w.scale)[0]
+    gs = to_device(host, DEV)
+    dec = se.QuestDecoder(_view(se, gs), G, w.scale, w.top_k, host.max_pages * 16, DEV)
+    dec.summarize()
+    out = torch.empty((w.num_req, w.hq, w.head_dim), dtype=torch.float32, device=DEV)
+    dec.step(steps.q[0, 0].to(DEV), steps.k_new[0, 0].to(DEV), steps.v_new[0, 0].to(DEV),
+             steps.new_pos[0].to(DEV), out)
+    torch.cuda.synchronize()
+    n = 500 // 16
+    sel = dec.sel.cpu().numpy()
+    assert (sel[:, :n] == np.arange(n)).all() and (sel[:, n:] == -1).all()
+    o = out.cpu().double().numpy()
+    for u, ref in dense.items():
+        req, kvh = divmod(u, w.hkv)
+        assert np.abs(o[req, kvh * G:(kvh + 1) * G] - ref).max() <= OUT_ATOL
+
+
+@pytest.mark.parametrize("n_pages,top_k,levels", [(40, 8, 0), (40, 8, 3), (300, 64, 5), (2048, 64, 0),
+                                                  (2048, 64, 7), (10, 64, 0), (700, 1, 2), (513, 512, 4)])
+def test_select_from_given_scores_bitexact(se, n_pages, top_k, levels):
+    # With the page scores given (the same float32 values on both sides) the
+    # selection is exact, ties going to the lower page index.
+    U = 6
+    g = torch.Generator().manual_seed(n_pages * 131 + top_k + levels)
+    lengths = [16 * n_pages + int(x) for x in torch.randint(0, 16, (U,), generator=g)]
+    host = isolated_units(lengths, n_pages + 1, 128, seed=n_pages + top_k, with_scores=False, with_meta=True)
+    if levels:
+        sc = (torch.randint(0, levels, (U, n_pages + 1), generator=g).to(torch.float32) - 1) / 3.0
+    else:
+        sc = torch.randn((U, n_pages + 1), generator=g)
+    sc[0, :5] = -0.0                                   # signed zeros compare equal to +0
+    sc[0, 5:9] = 0.0
+    gs = to_device(host, DEV)
+    view = _view(se, gs)
+    sel = torch.full((U, top_k), -5, dtype=torch.int32, device=DEV)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    scores = sc.to(DEV)
+    se.se_quest_select(view, 4, None, 0.1, top_k, max(lengths), se.SE_QUEST_SCORES_GIVEN, sel, scores,
+                       n_pages + 1, None, err)
+    torch.cuda.synchronize()
+    assert se.se_read_device_errors(err) == 0
+    for u, L in enumerate(lengths):
+        n = L // 16
+        want = quest.select_pages(sc[u].double().numpy(), n, top_k)
+        got = sel[u].cpu().numpy()
+        assert got[:len(want)].tolist() == want.tolist()
+        assert (got[len(want):] == -1).all()
