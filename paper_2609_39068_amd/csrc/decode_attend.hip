@@ -9,10 +9,13 @@
 // Work decomposition.  A unit's visited pages are cut into n_split ranges; one
 // 256-thread work-group (four wavefronts) streams one range, each wavefront one
 // page at a time:
-//   * QK layout: lane = 4*r + j reads row r, columns [j*D/4, (j+1)*D/4) of the
-//     page's K block with 16-byte loads, forms bf16 pair dot products with the
-//     G query rows (v_dot2c_f32_bf16), and a quad DPP reduction gives every lane
-//     of the quad the G logits of row r; lane j keeps head j.
+//   * QK layout: 8 lanes share a K row, each with D/8 columns (16-byte loads),
+//     two passes cover the page's 16 rows; bf16 pair dot products with the G
+//     query rows (v_dot2c_f32_bf16) and a 3-step DPP reduction give every lane
+//     the G logits of its rows; each lane keeps one (row, head) pair.
+//   * Pipeline: the physical pages of a wavefront's next 64 pages are fetched
+//     by one vector load, and the next page's K and V are loaded while the
+//     current page computes (two register buffers).
 //   * Softmax: each wavefront keeps one reference maximum per head, raised
 //     (and the running sums rescaled) only when a logit exceeds it by more than
 //     2^8, so most pages need one exp2 per (row, head) and no cross-lane max.
@@ -135,16 +138,202 @@ __device__ void finish_unit(const AttendParams& p, const UnitGeom& g, const floa
   if (g.append && threadIdx.x == 0) p.lengths[g.unit] = g.Lp;
 }
 
+// Per-page coordinates a wavefront needs before it loads the page.
+constexpr int kMaxGroupPages = 1024;  // pages one work-group streams at most
+
+struct PageRef {
+  int vp;      // index in the unit's visit order (workspace row)
+  int lp;      // logical page
+  int phys;    // physical page, or -1 when the page is skipped
+  int nrows;   // resident rows of the page
+  int rn;      // row of the appended token in this page, or -1
+};
+
+// Lane coordinates of the two layouts (see the kernel).
+template <int D>
+struct Lanes {
+  static constexpr int QC = D / 8;        // K columns per lane (QK layout: 8 lanes per row)
+  static constexpr int QW = QC / 2;       // bf16 pairs per lane per head
+  static constexpr int K4 = QC / 8;       // 16-byte loads per lane per K row
+  static constexpr int RS = 128 / D;      // row sets of the PV layout
+  static constexpr int RPL = kPage / RS;  // rows per lane (PV layout)
+  static constexpr int HP = D / 2;        // lanes per row set (two columns each)
+  int r8, j8, own_row, own_head, col, rs;
+  bool owns;
+};
+
+// Loads of one page: K rows r8 and r8+8 (QK layout) and the V column pair
+// (PV layout).  Rows past the page's resident rows repeat its last row, whose
+// weight is zero.
+template <int D>
+__device__ __forceinline__ void load_k(const AttendParams& p, const Lanes<D>& ln, const PageRef& pr,
+                                       uint4 (&kb)[2 * Lanes<D>::K4]) {
+  constexpr int QC = Lanes<D>::QC, K4 = Lanes<D>::K4;
+  const uint16_t* kpage = p.kv + (size_t)pr.phys * (2 * kPage * D);
+  const int last = pr.nrows - 1;
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const int rk = min(ln.r8 + 8 * pass, last);
+#pragma unroll
+    for (int i = 0; i < K4; ++i)
+      kb[pass * K4 + i] = reinterpret_cast<const uint4*>(kpage + rk * D + ln.j8 * QC)[i];
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void load_v(const AttendParams& p, const Lanes<D>& ln, const PageRef& pr,
+                                       uint32_t (&vb)[Lanes<D>::RPL]) {
+  constexpr int RPL = Lanes<D>::RPL;
+  const uint16_t* vpage = p.kv + (size_t)pr.phys * (2 * kPage * D) + kPage * D;
+  const int last = pr.nrows - 1;
+#pragma unroll
+  for (int i = 0; i < RPL; ++i) {
+    const int rv = min(ln.rs * RPL + i, last);
+    vb[i] = *reinterpret_cast<const uint32_t*>(vpage + rv * D + ln.col);
+  }
+}
+
+// Reduce-scatter of the 8 lanes that share two K rows: on entry a[h] / b[h]
+// are the lane's partial dot products of rows r8 / r8+8 with head h; on exit
+// lane j8 holds the full sum for row r8 + 8*bit2(j8) and head j8 & 3.  Each
+// step halves the values a lane keeps and adds its partner's copy of them
+// (partners j8^7, j8^2, j8^1 via DPP row_half_mirror and quad permutations),
+// so no lane ever selects by a computed index.
+template <int G>
+__device__ __forceinline__ float row_reduce_scatter(const float (&a)[G], const float (&b)[G], int j8) {
+  constexpr int kDppHalfMirror = 0x141;
+  const bool b2 = (j8 & 4) != 0, b1 = (j8 & 2) != 0, b0 = (j8 & 1) != 0;
+  float k[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    const float keep = b2 ? b[h] : a[h];
+    const float send = b2 ? a[h] : b[h];
+    k[h] = keep + dpp_f<kDppHalfMirror>(send);
+  }
+  if constexpr (G == 4) {
+    const float k0 = b1 ? k[2] : k[0], s0 = b1 ? k[0] : k[2];
+    const float k1 = b1 ? k[3] : k[1], s1 = b1 ? k[1] : k[3];
+    const float t0 = k0 + dpp_f<kQuadXor2>(s0);
+    const float t1 = k1 + dpp_f<kQuadXor2>(s1);
+    const float kk = b0 ? t1 : t0, ss = b0 ? t0 : t1;
+    return kk + dpp_f<kQuadXor1>(ss);
+  } else if constexpr (G == 2) {
+    const float t0 = k[0] + dpp_f<kQuadXor2>(k[0]);
+    const float t1 = k[1] + dpp_f<kQuadXor2>(k[1]);
+    const float kk = b0 ? t1 : t0, ss = b0 ? t0 : t1;
+    return kk + dpp_f<kQuadXor1>(ss);
+  } else {
+    static_assert(G == 1, "groups of 1, 2 or 4 query heads");
+    const float t = k[0] + dpp_f<kQuadXor2>(k[0]);
+    return t + dpp_f<kQuadXor1>(t);
+  }
+}
+
+// Running per-wavefront softmax state: a reference maximum per head (log2
+// units, uniform across the wavefront), the lane's share of the head's sum and
+// of the weighted V columns it owns.
+template <int G>
+struct WaveSoftmax {
+  float m_ref[G];
+  float o_acc[G][2];
+  float l_own;
+  float m_own;  // m_ref of the lane's own head
+};
+
+// Logits of the lane's (row, head) pair for one page.
+template <int D, int G>
+__device__ __forceinline__ float qk_page(const Lanes<D>& ln, const uint4 (&kb)[2 * Lanes<D>::K4],
+                                         const uint32_t (&qreg)[G][Lanes<D>::QW]) {
+  constexpr int K4 = Lanes<D>::K4;
+  float accA[G], accB[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    accA[h] = 0.f;
+    accB[h] = 0.f;
+  }
+#pragma unroll
+  for (int i = 0; i < K4; ++i) {
+    const uint32_t ka[4] = {kb[i].x, kb[i].y, kb[i].z, kb[i].w};
+    const uint32_t kc[4] = {kb[K4 + i].x, kb[K4 + i].y, kb[K4 + i].z, kb[K4 + i].w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        accA[h] = dot2bf16(qreg[h][4 * i + e], ka[e], accA[h]);
+        accB[h] = dot2bf16(qreg[h][4 * i + e], kc[e], accB[h]);
+      }
+    }
+  }
+  return row_reduce_scatter<G>(accA, accB, ln.j8);
+}
+
+// Reference update, weight of the lane's pair, its workspace copy, and the
+// weights' broadcast through LDS (the page's PV follows).
+template <int D, int G>
+__device__ __forceinline__ float softmax_page(const AttendParams& p, const Lanes<D>& ln,
+                                              const PageRef& pr, float z, WaveSoftmax<G>& ws,
+                                              float* lds_pw, int lane, int unit, size_t ubase_p) {
+  constexpr float kBump = 8.0f;  // rescale only when a logit beats the reference by 2^8
+  const bool valid = ln.owns && ln.own_row < pr.nrows;
+  const float z2 = valid ? z * p.scale_log2 : -INFINITY;
+  if (p.logits != nullptr && valid)
+    p.logits[((size_t)unit * G + ln.own_head) * p.logits_stride + pr.lp * kPage + ln.own_row] = z * p.scale;
+  const bool need = valid && (z2 > ws.m_own + kBump);
+  if (__ballot(need) != 0) {
+    float mx = z2;  // lanes of one head differ in lane bits 2..5
+    mx = fmaxf(mx, shfl_xor_f(mx, 4));
+    mx = fmaxf(mx, shfl_xor_f(mx, 8));
+    mx = fmaxf(mx, shfl_xor_f(mx, 16));
+    mx = fmaxf(mx, shfl_xor_f(mx, 32));
+    // lane h (< G) is row 0 of head h, so it holds head h's page maximum
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float mh = fmaxf(ws.m_ref[h], __shfl(mx, h, kWave));
+      const float f = fast_exp2(ws.m_ref[h] - mh);
+      ws.o_acc[h][0] *= f;
+      ws.o_acc[h][1] *= f;
+      ws.m_ref[h] = mh;
+    }
+    const float m_new = fmaxf(ws.m_own, mx);
+    ws.l_own *= fast_exp2(ws.m_own - m_new);
+    ws.m_own = m_new;
+  }
+  const float pj = valid ? fast_exp2(z2 - ws.m_own) : 0.f;
+  ws.l_own += pj;
+  if (p.accumulate) {
+    if (ln.owns) p.pbuf[((ubase_p + pr.vp) * kPage + ln.own_row) * G + ln.own_head] = pj;
+    if (lane < G) p.mref[(ubase_p + pr.vp) * G + lane] = ws.m_own;
+  }
+  if (ln.owns) lds_pw[ln.own_row * G + ln.own_head] = pj;
+  wave_lds_sync();
+  return pj;
+}
+
+// o += P V for one page, the weights read back from LDS.
+template <int D, int G>
+__device__ __forceinline__ void pv_page(const Lanes<D>& ln, const uint32_t (&vb)[Lanes<D>::RPL],
+                                        WaveSoftmax<G>& ws, const float* lds_pw) {
+  constexpr int RPL = Lanes<D>::RPL;
+#pragma unroll
+  for (int i = 0; i < RPL; ++i) {
+    const int rr = ln.rs * RPL + i;
+    const float v0 = bf16lo(vb[i]);
+    const float v1 = bf16hi(vb[i]);
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float ph = lds_pw[rr * G + h];
+      ws.o_acc[h][0] = fmaf(ph, v0, ws.o_acc[h][0]);
+      ws.o_acc[h][1] = fmaf(ph, v1, ws.o_acc[h][1]);
+    }
+  }
+  wave_lds_sync();
+}
+
 template <int D, int G>
 __global__ __launch_bounds__(256) void decode_attend_kernel(const AttendParams p) {
-  constexpr int NW = 4;            // wavefronts per work-group
-  constexpr int QC = D / 4;        // K columns per lane (QK layout)
-  constexpr int QW = QC / 2;       // bf16 pairs per lane per head
-  constexpr int K4 = QC / 8;       // 16-byte loads per lane per K row chunk
-  constexpr int RS = 128 / D;      // row sets of the PV layout
-  constexpr int RPL = kPage / RS;  // rows per lane (PV layout)
-  constexpr int HP = D / 2;        // lanes per row set (two columns each)
-  constexpr float kBump = 8.0f;    // rescale only when a logit beats the reference by 2^8
+  constexpr int NW = 4;  // wavefronts per work-group
+  using LN = Lanes<D>;
+  constexpr int QC = LN::QC, QW = LN::QW, K4 = LN::K4, RS = LN::RS, RPL = LN::RPL, HP = LN::HP;
 
   __shared__ float lds_p[NW][kPage * G];
   __shared__ float lds_m[NW][G];
@@ -152,6 +341,10 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(const AttendParams p
   __shared__ float lds_o[NW][G][D];
   __shared__ float fin_m[G];
   __shared__ float fin_il[G];
+  __shared__ int lds_phys[kMaxGroupPages];
+  __shared__ int lds_lp[kMaxGroupPages];
+  __shared__ int lds_vp[kMaxGroupPages];
+  __shared__ int lds_scan[256 / kWave + 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -159,30 +352,38 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(const AttendParams p
   const int unit = blockIdx.x / p.n_split;
   const int split = blockIdx.x - unit * p.n_split;
   const UnitGeom g = unit_geom(p, unit);
-  const int req = g.req, kvh = g.kvh, L = g.L, Lp = g.Lp, cur_page = g.cur_page, n_visit = g.n_visit;
+  const int req = g.req, kvh = g.kvh, L = g.L, Lp = g.Lp, cur_page = g.cur_page;
   const bool append = g.append, quest = g.quest, bad = g.bad;
   const int Hq = p.hkv * G;
   const int vbeg = split * p.pps;
-  const int vend = min(vbeg + p.pps, n_visit);
-
+  const int vend = min(vbeg + p.pps, g.n_visit);
   const size_t ubase_p = (size_t)unit * p.n_visit_max;  // page-indexed workspace rows
 
-  // QK-layout coordinates.
-  const int r = lane >> 2;
-  const int j = lane & 3;
-  // PV-layout coordinates.
-  const int col = 2 * (lane % HP);
-  const int rs = lane / HP;
+  // QK layout: lane = 8*r8 + j8 reads columns [j8*QC, (j8+1)*QC) of rows r8
+  // (pass A) and r8 + 8 (pass B).  After the 8-lane reduction, lane j8 < 4
+  // keeps head j8 of row r8 and lane j8 >= 4 head j8-4 of row r8+8: each lane
+  // owns one (row, head) pair of the page.  PV layout: two adjacent columns,
+  // RPL rows.
+  LN ln;
+  ln.r8 = lane >> 3;
+  ln.j8 = lane & 7;
+  ln.own_row = ln.r8 + ((ln.j8 & 4) ? 8 : 0);
+  ln.own_head = ln.j8 & 3;
+  ln.owns = ln.own_head < G;
+  ln.col = 2 * (lane % HP);
+  ln.rs = lane / HP;
+  const int j8 = ln.j8;
+  const int col = ln.col;
 
   uint32_t qreg[G][QW];
   {
-    const uint16_t* qb = p.q + ((size_t)req * Hq + (size_t)kvh * G) * D + j * QC;
+    const uint16_t* qb = p.q + ((size_t)req * Hq + (size_t)kvh * G) * D + j8 * QC;
 #pragma unroll
     for (int h = 0; h < G; ++h) {
       const uint4* src = reinterpret_cast<const uint4*>(qb + (size_t)h * D);
 #pragma unroll
       for (int i = 0; i < K4; ++i) {
-        uint4 t = src[i];
+        const uint4 t = src[i];
         qreg[h][4 * i + 0] = t.x;
         qreg[h][4 * i + 1] = t.y;
         qreg[h][4 * i + 2] = t.z;
@@ -191,169 +392,140 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(const AttendParams p
     }
   }
 
-  float m_ref[G];
-  float o_acc[G][2];
+  WaveSoftmax<G> ws;
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    m_ref[h] = -INFINITY;
-    o_acc[h][0] = 0.f;
-    o_acc[h][1] = 0.f;
+    ws.m_ref[h] = -INFINITY;
+    ws.o_acc[h][0] = 0.f;
+    ws.o_acc[h][1] = 0.f;
   }
-  float l_own = 0.f;
+  ws.l_own = 0.f;
+  ws.m_own = -INFINITY;
 
-  const uint16_t* knew_row =
-      append ? p.k_new + ((size_t)req * p.hkv + kvh) * D : nullptr;
-  const uint16_t* vnew_row =
-      append ? p.v_new + ((size_t)req * p.hkv + kvh) * D : nullptr;
+  const uint16_t* knew_row = append ? p.k_new + ((size_t)req * p.hkv + kvh) * D : nullptr;
+  const uint16_t* vnew_row = append ? p.v_new + ((size_t)req * p.hkv + kvh) * D : nullptr;
 
-  for (int vp = vbeg + wave; vp < vend; vp += NW) {
-    int lp;
-    if (quest) {
-      lp = vp < p.top_k ? p.sel[(size_t)unit * p.top_k + vp] : cur_page;
-      if (lp < 0) continue;
-      if (vp < p.top_k && lp >= cur_page) {
-        if (lane == 0) set_error(p.dev_err, SE_DEVERR_BAD_SELECTION);
-        continue;
-      }
-    } else {
-      lp = vp;
-    }
-    const int phys = p.block_table[(size_t)unit * p.max_pages + lp];
-    if (phys < 0 || (int64_t)phys >= p.num_pages) {
-      if (lane == 0) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
-      continue;
-    }
-    const int row0 = lp * kPage;
-    const int nrows = min(kPage, Lp - row0);
-    const bool has_new = append && L >= row0 && L < row0 + kPage;
-    const int rn = L - row0;
-    const uint16_t* kpage = p.kv + (size_t)phys * (2 * kPage * D);
-    const uint16_t* vpage = kpage + kPage * D;
-
-    // ---- loads: K chunk (QK layout) and V column pairs (PV layout)
-    const int rk = min(r, nrows - 1);
-    const uint16_t* krow = (has_new && rk == rn) ? knew_row : kpage + rk * D;
-    uint4 kreg[K4];
-#pragma unroll
-    for (int i = 0; i < K4; ++i) kreg[i] = reinterpret_cast<const uint4*>(krow + j * QC)[i];
-    uint32_t vreg[RPL];
-#pragma unroll
-    for (int i = 0; i < RPL; ++i) {
-      const int rv = min(rs * RPL + i, nrows - 1);
-      const uint16_t* vrow = (has_new && rv == rn) ? vnew_row : vpage + rv * D;
-      vreg[i] = *reinterpret_cast<const uint32_t*>(vrow + col);
-    }
-
-    // ---- append: the new token's row enters the pool
-    if (has_new) {
-      uint16_t* kdst = const_cast<uint16_t*>(kpage) + rn * D;
-      if (r == rn) {
-#pragma unroll
-        for (int i = 0; i < K4; ++i) reinterpret_cast<uint4*>(kdst + j * QC)[i] = kreg[i];
-        if (p.meta_pool != nullptr) {
-          uint16_t* mn = p.meta_pool + (size_t)phys * 2 * D + j * QC;
-          uint16_t* mx = mn + D;
-          const uint16_t* kn = knew_row + j * QC;
-          for (int c = 0; c < QC; ++c) {
-            const uint16_t kb = kn[c];
-            if (rn == 0) {
-              mn[c] = kb;
-              mx[c] = kb;
-            } else {
-              const float kf = bf16f(kb);
-              if (kf < bf16f(mn[c])) mn[c] = kb;
-              if (kf > bf16f(mx[c])) mx[c] = kb;
-            }
-          }
+  // ---- this work-group's pages: visit index, logical and physical ids of the
+  // pages it must read, compacted and staged in LDS once, so the page stream
+  // below never waits on a dependent table load or branches around a page
+  const int n_range = max(0, vend - vbeg);
+  bool bad_sel = false, bad_page = false;
+  int n_grp = 0;
+  for (int i0 = 0; i0 < n_range; i0 += 256) {
+    const int i = i0 + tid;
+    const int vp = vbeg + i;
+    int lp = vp;
+    int ph = -1;
+    if (i < n_range) {
+      bool ok = true;
+      if (quest) {
+        lp = vp < p.top_k ? p.sel[(size_t)unit * p.top_k + vp] : cur_page;
+        if (lp < 0) ok = false;
+        if (lp >= 0 && vp < p.top_k && lp >= cur_page) {
+          bad_sel = true;
+          ok = false;
         }
       }
-      if (rn >= rs * RPL && rn < (rs + 1) * RPL)
-        *reinterpret_cast<uint32_t*>(const_cast<uint16_t*>(vpage) + rn * D + col) = vreg[rn - rs * RPL];
-      if (lane == 0) {
-        p.pos_pool[(size_t)phys * kPage + rn] = p.new_pos[req];
-        if (p.score_pool != nullptr) p.score_pool[(size_t)phys * kPage + rn] = 0.f;
+      if (ok) {
+        ph = p.block_table[(size_t)unit * p.max_pages + lp];
+        if (ph < 0 || (int64_t)ph >= p.num_pages) {
+          bad_page = true;
+          ph = -1;
+        }
       }
     }
+    int total;
+    const int rank = block_exclusive_scan<256>(ph >= 0 ? 1 : 0, lds_scan, &total);
+    if (ph >= 0) {
+      lds_phys[n_grp + rank] = ph;
+      lds_lp[n_grp + rank] = lp;
+      lds_vp[n_grp + rank] = vp;
+    }
+    n_grp += total;
+  }
+  if (bad_sel) set_error(p.dev_err, SE_DEVERR_BAD_SELECTION);
+  if (bad_page) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
 
-    // ---- logits of row r for all G heads, reduced over the quad
-    float acc[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) acc[h] = 0.f;
-#pragma unroll
-    for (int i = 0; i < K4; ++i) {
-      const uint32_t kw[4] = {kreg[i].x, kreg[i].y, kreg[i].z, kreg[i].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-#pragma unroll
-        for (int h = 0; h < G; ++h) acc[h] = dot2bf16(qreg[h][4 * i + e], kw[e], acc[h]);
+  // ---- append: the work-group whose range holds the new token's page writes
+  // its row into the pool first; no other work-group reads that page
+  const int new_vp = quest ? p.top_k : cur_page;
+  const bool mine_new = append && !bad && new_vp >= vbeg && new_vp < vend;
+  if (mine_new) {
+    const int ph = p.block_table[(size_t)unit * p.max_pages + cur_page];
+    const int rn = L - cur_page * kPage;
+    if (ph >= 0 && (int64_t)ph < p.num_pages) {
+      uint16_t* kdst = const_cast<uint16_t*>(p.kv) + (size_t)ph * (2 * kPage * D) + rn * D;
+      uint16_t* vdst = kdst + kPage * D;
+      if (tid < D / 8) {
+        reinterpret_cast<uint4*>(kdst)[tid] = reinterpret_cast<const uint4*>(knew_row)[tid];
+        reinterpret_cast<uint4*>(vdst)[tid] = reinterpret_cast<const uint4*>(vnew_row)[tid];
+      }
+      if (p.meta_pool != nullptr && tid < D) {
+        uint16_t* mn = p.meta_pool + (size_t)ph * 2 * D;
+        uint16_t* mx = mn + D;
+        const uint16_t kb = knew_row[tid];
+        if (rn == 0) {
+          mn[tid] = kb;
+          mx[tid] = kb;
+        } else {
+          const float kf = bf16f(kb);
+          if (kf < bf16f(mn[tid])) mn[tid] = kb;
+          if (kf > bf16f(mx[tid])) mx[tid] = kb;
+        }
+      }
+      if (tid == 0) {
+        p.pos_pool[(size_t)ph * kPage + rn] = p.new_pos[req];
+        if (p.score_pool != nullptr) p.score_pool[(size_t)ph * kPage + rn] = 0.f;
       }
     }
-#pragma unroll
-    for (int h = 0; h < G; ++h) acc[h] = quad_sum(acc[h]);
-    float z = acc[0];
-#pragma unroll
-    for (int h = 1; h < G; ++h) z = (j == h) ? acc[h] : z;
-    const bool valid = (r < nrows) && (j < G);
-    const float z2 = valid ? z * p.scale_log2 : -INFINITY;
-    if (p.logits != nullptr && valid)
-      p.logits[((size_t)unit * G + j) * p.logits_stride + row0 + r] = z * p.scale;
+  }
+  __syncthreads();
 
-    // ---- reference maximum: raised only when some logit beats it by 2^kBump
-    float mown = m_ref[0];
-#pragma unroll
-    for (int h = 1; h < G; ++h) mown = (j == h) ? m_ref[h] : mown;
-    const bool need = valid && (z2 > mown + kBump);
-    if (__ballot(need) != 0) {
-      float mx = z2;
-      mx = fmaxf(mx, shfl_xor_f(mx, 4));
-      mx = fmaxf(mx, shfl_xor_f(mx, 8));
-      mx = fmaxf(mx, shfl_xor_f(mx, 16));
-      mx = fmaxf(mx, shfl_xor_f(mx, 32));
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-        const float mh = fmaxf(m_ref[h], __shfl(mx, h, kWave));
-        const float f = fast_exp2(m_ref[h] - mh);
-        o_acc[h][0] *= f;
-        o_acc[h][1] *= f;
-        if (j == h) l_own *= f;
-        m_ref[h] = mh;
-      }
-      mown = m_ref[0];
-#pragma unroll
-      for (int h = 1; h < G; ++h) mown = (j == h) ? m_ref[h] : mown;
-    }
-    const float pj = valid ? fast_exp2(z2 - mown) : 0.f;
-    l_own += pj;
-    if (p.accumulate) {
-      if (j < G) p.pbuf[((ubase_p + vp) * kPage + r) * G + j] = pj;
-      if (lane < G) {
-        float mv = m_ref[0];
-#pragma unroll
-        for (int h = 1; h < G; ++h) mv = (lane == h) ? m_ref[h] : mv;
-        p.mref[(ubase_p + vp) * G + lane] = mv;
-      }
-    }
+  // Pages of this wavefront: staged entries wave + NW*i.
+  const int n_my = wave < n_grp ? (n_grp - wave + NW - 1) / NW : 0;
+  auto page_ref = [&](int i) -> PageRef {
+    PageRef pr;
+    const int gi = wave + NW * i;
+    // wave-uniform by construction: keep them in scalar registers
+    pr.vp = __builtin_amdgcn_readfirstlane(lds_vp[gi]);
+    pr.lp = __builtin_amdgcn_readfirstlane(lds_lp[gi]);
+    pr.phys = __builtin_amdgcn_readfirstlane(lds_phys[gi]);
+    pr.nrows = min(kPage, Lp - pr.lp * kPage);
+    pr.rn = -1;
+    return pr;
+  };
 
-    // ---- PV: broadcast the page's weights through LDS
-    if (j < G) lds_p[wave][r * G + j] = pj;
-    wave_lds_sync();
-#pragma unroll
-    for (int i = 0; i < RPL; ++i) {
-      const int rr = rs * RPL + i;
-      const float v0 = bf16lo(vreg[i]);
-      const float v1 = bf16hi(vreg[i]);
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-        const float ph = lds_p[wave][rr * G + h];
-        o_acc[h][0] = fmaf(ph, v0, o_acc[h][0]);
-        o_acc[h][1] = fmaf(ph, v1, o_acc[h][1]);
-      }
+  // ---- the page stream, software-pipelined on one register buffer: page
+  // i+1's K loads are issued once page i's logits are formed, its V loads
+  // once page i's PV is done, so each load has a compute phase to land in
+  uint4 kb[2 * K4];
+  uint32_t vb[RPL];
+  if (n_my > 0) {
+    PageRef cur = page_ref(0);
+    load_k<D>(p, ln, cur, kb);
+    // keep the loop's issue order (K before V) on the entry edge too, so the
+    // loop-top wait for K can leave the V loads in flight
+    __builtin_amdgcn_sched_barrier(0);
+    load_v<D>(p, ln, cur, vb);
+    for (int i = 0; i < n_my; ++i) {
+      // The prefetch is unconditional (a conditional load would make the
+      // compiler drain every load at the loop latch); after the last page it
+      // re-reads one row of the same page.
+      const bool more = i + 1 < n_my;
+      PageRef nxt = page_ref(more ? i + 1 : i);
+      if (!more) nxt.nrows = 1;
+      const float z = qk_page<D, G>(ln, kb, qreg);
+      load_k<D>(p, ln, nxt, kb);
+      softmax_page<D, G>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p);
+      pv_page<D, G>(ln, vb, ws, lds_p[wave]);
+      load_v<D>(p, ln, nxt, vb);
+      if (!more) nxt.nrows = cur.nrows;
+      cur = nxt;
     }
-    wave_lds_sync();
   }
 
   // ---- per-wavefront totals into LDS
-  float lsum = l_own;
+  float lsum = ws.l_own;  // lanes of one head differ in lane bits 2..5
   lsum += shfl_xor_f(lsum, 4);
   lsum += shfl_xor_f(lsum, 8);
   lsum += shfl_xor_f(lsum, 16);
@@ -361,22 +533,19 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(const AttendParams p
   if (RS == 2) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      o_acc[h][0] += shfl_xor_f(o_acc[h][0], 32);
-      o_acc[h][1] += shfl_xor_f(o_acc[h][1], 32);
+      ws.o_acc[h][0] += shfl_xor_f(ws.o_acc[h][0], 32);
+      ws.o_acc[h][1] += shfl_xor_f(ws.o_acc[h][1], 32);
     }
   }
   if (lane < G) {
-    float mv = m_ref[0];
-#pragma unroll
-    for (int h = 1; h < G; ++h) mv = (lane == h) ? m_ref[h] : mv;
-    lds_m[wave][lane] = mv;
+    lds_m[wave][lane] = ws.m_own;
     lds_l[wave][lane] = lsum;
   }
   if (lane < HP) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      lds_o[wave][h][col] = o_acc[h][0];
-      lds_o[wave][h][col + 1] = o_acc[h][1];
+      lds_o[wave][h][col] = ws.o_acc[h][0];
+      lds_o[wave][h][col + 1] = ws.o_acc[h][1];
     }
   }
   __syncthreads();

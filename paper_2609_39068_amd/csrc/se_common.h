@@ -53,6 +53,8 @@ inline SplitShape split_shape(int num_units, int n_visit) {
   int by_size = (int)ceil_div(n_visit, min_pages);
   if (splits > by_size) splits = by_size;
   if (splits < 1) splits = 1;
+  const int max_group_pages = 1024;  // the page table a work-group stages in LDS
+  if (splits < ceil_div(n_visit, max_group_pages)) splits = (int)ceil_div(n_visit, max_group_pages);
   int pps = (int)ceil_div(n_visit, splits);
   splits = (int)ceil_div(n_visit, pps);
   return SplitShape{n_visit, splits, pps};
