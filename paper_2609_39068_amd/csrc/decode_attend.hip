@@ -6,9 +6,10 @@
 // over the read set, out_a = sum_j softmax(z)_j v_j, and with accumulation every
 // read slot's score grows by its weight summed over the unit's G rows.
 //
-// Work decomposition.  A unit's visited pages are cut into n_split ranges; one
-// 256-thread work-group (four wavefronts) streams one range, each wavefront one
-// page at a time:
+// Work decomposition.  A unit's visited pages are cut into n_split ranges (one
+// range when there are enough units to fill the chip); one 512-thread
+// work-group (eight wavefronts) streams one range, each wavefront one page at
+// a time:
 //   * QK layout: 8 lanes share a K row, each with D/8 columns (16-byte loads),
 //     two passes cover the page's 16 rows; bf16 pair dot products with the G
 //     query rows (v_dot2c_f32_bf16) and a 3-step DPP reduction give every lane
@@ -140,6 +141,7 @@ __device__ void finish_unit(const AttendParams& p, const UnitGeom& g, const floa
 
 // Per-page coordinates a wavefront needs before it loads the page.
 constexpr int kMaxGroupPages = 1024;  // pages one work-group streams at most
+constexpr int kAttendThreads = 512;   // eight wavefronts; two work-groups per compute unit
 
 struct PageRef {
   int vp;      // index in the unit's visit order (workspace row)
@@ -330,8 +332,8 @@ __device__ __forceinline__ void pv_page(const Lanes<D>& ln, const uint32_t (&vb)
 }
 
 template <int D, int G>
-__global__ __launch_bounds__(256) void decode_attend_kernel(const AttendParams p) {
-  constexpr int NW = 4;  // wavefronts per work-group
+__global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const AttendParams p) {
+  constexpr int NW = kAttendThreads / kWave;  // wavefronts per work-group
   using LN = Lanes<D>;
   constexpr int QC = LN::QC, QW = LN::QW, K4 = LN::K4, RS = LN::RS, RPL = LN::RPL, HP = LN::HP;
 
@@ -344,7 +346,7 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(const AttendParams p
   __shared__ int lds_phys[kMaxGroupPages];
   __shared__ int lds_lp[kMaxGroupPages];
   __shared__ int lds_vp[kMaxGroupPages];
-  __shared__ int lds_scan[256 / kWave + 1];
+  __shared__ int lds_scan[kAttendThreads / kWave + 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -411,7 +413,7 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(const AttendParams p
   const int n_range = max(0, vend - vbeg);
   bool bad_sel = false, bad_page = false;
   int n_grp = 0;
-  for (int i0 = 0; i0 < n_range; i0 += 256) {
+  for (int i0 = 0; i0 < n_range; i0 += kAttendThreads) {
     const int i = i0 + tid;
     const int vp = vbeg + i;
     int lp = vp;
@@ -435,7 +437,7 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(const AttendParams p
       }
     }
     int total;
-    const int rank = block_exclusive_scan<256>(ph >= 0 ? 1 : 0, lds_scan, &total);
+    const int rank = block_exclusive_scan<kAttendThreads>(ph >= 0 ? 1 : 0, lds_scan, &total);
     if (ph >= 0) {
       lds_phys[n_grp + rank] = ph;
       lds_lp[n_grp + rank] = lp;
@@ -553,7 +555,7 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(const AttendParams p
   // ---- work-group partial (fixed wavefront order)
   const bool single = p.n_split == 1;
   float* part_u = p.part + (size_t)unit * p.n_split * G * (D + 2);
-  for (int idx = tid; idx < G * D; idx += 256) {
+  for (int idx = tid; idx < G * D; idx += kAttendThreads) {
     const int h = idx / D;
     const int c = idx - h * D;
     float ms = lds_m[0][h];
@@ -633,7 +635,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(const AttendParams 
 
 template <int D, int G>
 static void launch_attend(const AttendParams& prm, int grid, hipStream_t stream) {
-  hipLaunchKernelGGL((decode_attend_kernel<D, G>), dim3(grid), dim3(256), 0, stream, prm);
+  hipLaunchKernelGGL((decode_attend_kernel<D, G>), dim3(grid), dim3(kAttendThreads), 0, stream, prm);
   if (prm.n_split > 1)
     hipLaunchKernelGGL((decode_combine_kernel<D, G>), dim3(grid / prm.n_split), dim3(256), 0, stream,
                        prm);

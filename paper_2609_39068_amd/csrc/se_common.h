@@ -47,13 +47,13 @@ struct SplitShape {
 };
 
 inline SplitShape split_shape(int num_units, int n_visit) {
-  const int target_groups = 2048;  // about 8 work-groups per compute unit
-  const int min_pages = 8;
-  int splits = (int)ceil_div(target_groups, num_units);
+  const int resident = 512;          // two 8-wavefront work-groups on each of 256 compute units
+  const int min_pages = 16;          // at least two pages per wavefront
+  const int max_group_pages = 1024;  // the page table a work-group stages in LDS
+  int splits = (int)ceil_div(resident, num_units);
   int by_size = (int)ceil_div(n_visit, min_pages);
   if (splits > by_size) splits = by_size;
   if (splits < 1) splits = 1;
-  const int max_group_pages = 1024;  // the page table a work-group stages in LDS
   if (splits < ceil_div(n_visit, max_group_pages)) splits = (int)ceil_div(n_visit, max_group_pages);
   int pps = (int)ceil_div(n_visit, splits);
   splits = (int)ceil_div(n_visit, pps);
