@@ -39,7 +39,7 @@
  *           int32 word *dev_err (atomic OR) and the affected unit is left unchanged;
  *           read and clear the word with se_read_device_errors.
  *  Numbers. K/V/q are bf16; logits, softmax and accumulation are fp32; outputs fp32.
- *  Limits.  page_size must be 16; head_dim 64 or 128; q_per_kv 1, 2, 4 or 8.
+ *  Limits.  page_size must be 16; head_dim 64 or 128; q_per_kv 1, 2 or 4.
  */
 #ifndef SPARSE_ENGINE_H
 #define SPARSE_ENGINE_H
@@ -172,6 +172,27 @@ se_status se_accumulate_scores(const se_kv_view* kv, int32_t q_per_kv, const flo
 se_status se_evict_compact(const se_kv_view* kv, int32_t budget, int32_t recent,
                            int32_t max_len, int32_t* freed_pages, int32_t freed_stride,
                            int32_t* freed_count, int32_t* dev_err, hipStream_t stream);
+
+/*
+ * se_decode_step_h2o — one H2O decode step of one layer in one call: exactly the
+ * effect of se_decode_attend (with k_new/v_new, all resident slots read,
+ * SE_ATTEND_ACCUMULATE) followed by se_evict_compact(budget, recent) — the
+ * attention of the step and its finish_step work (Section 3.1, "Fine-Grained
+ * Lifecycle Hooks": H2O's cumulative-score update and online eviction at the end
+ * of a decode step; Appendix A.3, eqs. background-h2o-score and
+ * background-h2o-retention).  When a unit is one slot over the budget and its
+ * recent window is the run of its newest positions (every step after the first
+ * eviction), the eviction happens inside the attention pass; the other units go
+ * through the general eviction afterwards, in the same call.
+ *  Arguments as for se_decode_attend and se_evict_compact; ws is the
+ *  SE_OP_DECODE_ATTEND workspace.  budget 1 .. 8192.
+ */
+se_status se_decode_step_h2o(const se_kv_view* kv, int32_t q_per_kv, const void* q,
+                             const void* k_new, const void* v_new, const int32_t* new_pos,
+                             float scale, int32_t budget, int32_t recent, int32_t max_len,
+                             float* out, float* lse, int32_t* freed_pages, int32_t freed_stride,
+                             int32_t* freed_count, void* ws, size_t ws_bytes, int32_t* dev_err,
+                             hipStream_t stream);
 
 /*
  * se_quest_summarize — per-page key min/max for every resident page (Appendix A.3,

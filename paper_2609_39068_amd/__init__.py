@@ -4,7 +4,7 @@ selection around paged GQA decode attention, as HIP kernels behind a C-ABI
 build script, the ctypes binding and the decode-step driver."""
 
 from ._binding import (  # noqa: F401
-    EXPORTED, KVView, SparseEngineError, se_accumulate_scores, se_decode_attend,
+    EXPORTED, KVView, SparseEngineError, se_accumulate_scores, se_decode_attend, se_decode_step_h2o,
     se_evict_compact, se_quest_select, se_quest_summarize, se_read_device_errors,
     se_version, se_workspace_bytes, status_string,
     SE_ATTEND_ACCUMULATE, SE_QUEST_SCORES_GIVEN, SE_OP_DECODE_ATTEND, SE_OP_QUEST_SELECT,

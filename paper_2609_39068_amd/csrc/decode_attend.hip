@@ -65,6 +65,13 @@ struct AttendParams {
   float* pbuf;
   float* mref;
   int32_t* dev_err;
+  // fused steady-state H2O eviction (se_decode_step_h2o)
+  int32_t evict;
+  int32_t budget;
+  int32_t recent;
+  int32_t* freed_pages;
+  int32_t freed_stride;
+  int32_t* freed_count;
 };
 
 struct AttendWs {
@@ -109,34 +116,153 @@ __device__ __forceinline__ UnitGeom unit_geom(const AttendParams& p, int unit) {
 // score update over every visited slot (eq. background-h2o-score, summed over
 // the group; the new token's score is its weight) and the new length.
 template <int G>
+__device__ __forceinline__ float slot_weight(const AttendParams& p, size_t ubase_p, int vp, int rr,
+                                             const float* fin_m, const float* fin_il) {
+  float a = 0.f;
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    const float w = p.pbuf[((ubase_p + vp) * kPage + rr) * G + h];
+    const float mr = p.mref[(ubase_p + vp) * G + h];
+    a += w * fast_exp2(mr - fin_m[h]) * fin_il[h];
+  }
+  return a;
+}
+
+__device__ __forceinline__ uint32_t pos_order(int32_t pos) { return (uint32_t)pos ^ 0x80000000u; }
+
+// With se_decode_step_h2o, the step's eviction (eq. background-h2o-retention)
+// is done here when it is the steady one-slot case: the unit is one slot over
+// the budget and its recent window is the contiguous run of newest positions.
+// Every slot's new score and position stay in registers; the victim is the
+// non-window slot with the smallest (score, then larger position); the new
+// token's slot (the last one) moves into it.  Anything else is left to the
+// general eviction kernel that se_decode_step_h2o launches next.
+template <int NT, int G, int D>
 __device__ void finish_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
                             const float* fin_il) {
+  constexpr int KMAX = 8192 / NT;  // slots per thread kept in registers
+  __shared__ int red_i[NT / kWave];
+  __shared__ unsigned long long red_k[NT / kWave];
+  __shared__ int bc[2];
+  __shared__ float bc_u;
+  const int tid = threadIdx.x;
   const size_t ubase_p = (size_t)g.unit * p.n_visit_max;
-  if (p.accumulate) {
-    for (int idx = threadIdx.x; idx < g.n_visit * kPage; idx += blockDim.x) {
-      const int vp = idx >> 4;
-      const int rr = idx & (kPage - 1);
-      int lp = vp;
-      if (g.quest) {
-        lp = vp < p.top_k ? p.sel[(size_t)g.unit * p.top_k + vp] : g.cur_page;
-        if (lp < 0 || (vp < p.top_k && lp >= g.cur_page)) continue;
+  const bool fuse = p.evict && !g.quest && p.accumulate && g.Lp == p.budget + 1 && g.Lp <= NT * KMAX;
+  if (!fuse) {
+    if (p.accumulate) {
+      for (int idx = tid; idx < g.n_visit * kPage; idx += NT) {
+        const int vp = idx >> 4;
+        const int rr = idx & (kPage - 1);
+        int lp = vp;
+        if (g.quest) {
+          lp = vp < p.top_k ? p.sel[(size_t)g.unit * p.top_k + vp] : g.cur_page;
+          if (lp < 0 || (vp < p.top_k && lp >= g.cur_page)) continue;
+        }
+        const int slot = lp * kPage + rr;
+        if (slot >= g.Lp) continue;
+        const int phys = p.block_table[(size_t)g.unit * p.max_pages + lp];
+        if (phys < 0 || (int64_t)phys >= p.num_pages) continue;
+        const float a = slot_weight<G>(p, ubase_p, vp, rr, fin_m, fin_il);
+        float* up = p.score_pool + (size_t)phys * kPage + rr;
+        *up = (g.append && slot == g.L) ? a : *up + a;
       }
-      const int slot = lp * kPage + rr;
-      if (slot >= g.Lp) continue;
-      const int phys = p.block_table[(size_t)g.unit * p.max_pages + lp];
-      if (phys < 0 || (int64_t)phys >= p.num_pages) continue;
-      float a = 0.f;
+    }
+    if (tid == 0) {
+      if (g.append) p.lengths[g.unit] = g.Lp;
+      // nothing to evict: report it here, the general kernel leaves this unit alone
+      if (p.evict && g.Lp <= p.budget && p.freed_count != nullptr) p.freed_count[g.unit] = 0;
+    }
+    return;
+  }
+
+  const int32_t* bt = p.block_table + (size_t)g.unit * p.max_pages;
+  float unew[KMAX];
+  int32_t pos[KMAX];
+  int badp = 0;
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        const float w = p.pbuf[((ubase_p + vp) * kPage + rr) * G + h];
-        const float mr = p.mref[(ubase_p + vp) * G + h];
-        a += w * fast_exp2(mr - fin_m[h]) * fin_il[h];
+  for (int k = 0; k < KMAX; ++k) {
+    const int s = tid + k * NT;
+    unew[k] = 0.f;
+    pos[k] = INT32_MIN;
+    if (s < g.Lp) {
+      const int phys = bt[s >> 4];
+      if (phys < 0 || (int64_t)phys >= p.num_pages) {
+        badp = 1;
+        continue;
       }
-      float* up = p.score_pool + (size_t)phys * kPage + rr;
-      *up = (g.append && slot == g.L) ? a : *up + a;
+      const size_t a_ = (size_t)phys * kPage + (s & (kPage - 1));
+      const float a = slot_weight<G>(p, ubase_p, s >> 4, s & (kPage - 1), fin_m, fin_il);
+      const bool is_new = g.append && s == g.L;
+      unew[k] = (is_new ? 0.f : p.score_pool[a_]) + a;
+      pos[k] = is_new ? p.new_pos[g.req] : p.pos_pool[a_];
+      p.score_pool[a_] = unew[k];
     }
   }
-  if (g.append && threadIdx.x == 0) p.lengths[g.unit] = g.Lp;
+  badp = block_reduce<NT>(badp, red_i, [](int x, int y) { return x | y; });
+  const int w = min(p.recent, p.budget);
+  int32_t pmax = INT32_MIN;
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) pmax = max(pmax, pos[k]);
+  pmax = block_reduce<NT>(pmax, red_i, [](int x, int y) { return x > y ? x : y; });
+  const int64_t lo = (int64_t)pmax - w;  // the window is the positions above lo when contiguous
+  int cnt = 0;
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) cnt += (tid + k * NT < g.Lp && (int64_t)pos[k] > lo) ? 1 : 0;
+  cnt = block_reduce<NT>(cnt, red_i, [](int x, int y) { return x + y; });
+  if (badp || cnt != w) {  // scores are updated; the general kernel evicts
+    if (tid == 0 && g.append) p.lengths[g.unit] = g.Lp;
+    return;
+  }
+  unsigned long long best = ~0ull;
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) {
+    const int s = tid + k * NT;
+    if (s < g.Lp && (int64_t)pos[k] <= lo) {
+      const unsigned long long key = ((unsigned long long)float_key(unew[k]) << 32) |
+                                     (unsigned long long)(0xFFFFFFFFu - pos_order(pos[k]));
+      best = key < best ? key : best;
+    }
+  }
+  const unsigned long long kmin =
+      block_reduce<NT>(best, red_k, [](unsigned long long x, unsigned long long y) { return x < y ? x : y; });
+  const int mover = g.Lp - 1;
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) {
+    const int s = tid + k * NT;
+    if (s < g.Lp && (int64_t)pos[k] <= lo) {
+      const unsigned long long key = ((unsigned long long)float_key(unew[k]) << 32) |
+                                     (unsigned long long)(0xFFFFFFFFu - pos_order(pos[k]));
+      if (key == kmin) bc[0] = s;
+    }
+    if (s == mover) {
+      bc[1] = pos[k];
+      bc_u = unew[k];
+    }
+  }
+  __syncthreads();
+  const int victim = bc[0];
+  if (victim != mover) {
+    const int pv = bt[victim >> 4], pm = bt[mover >> 4];
+    constexpr int R4 = D / 8;  // 16-byte chunks per row
+    const uint4* src = reinterpret_cast<const uint4*>(p.kv + (size_t)pm * (2 * kPage * D) + (mover & 15) * D);
+    uint4* dst = reinterpret_cast<uint4*>(const_cast<uint16_t*>(p.kv) + (size_t)pv * (2 * kPage * D) +
+                                          (victim & 15) * D);
+    if (tid < 2 * R4) {
+      const int part = tid / R4, c = tid - part * R4;  // part 0: key row, 1: value row
+      dst[part * kPage * R4 + c] = src[part * kPage * R4 + c];
+    }
+    if (tid == 0) {
+      p.pos_pool[(size_t)pv * kPage + (victim & 15)] = bc[1];
+      p.score_pool[(size_t)pv * kPage + (victim & 15)] = bc_u;
+    }
+  }
+  if (tid == 0) {
+    p.lengths[g.unit] = p.budget;
+    const int f0 = (p.budget + kPage - 1) / kPage;
+    const int nf = (g.Lp + kPage - 1) / kPage - f0;
+    if (p.freed_pages != nullptr && nf > 0) p.freed_pages[(size_t)g.unit * p.freed_stride] = bt[f0];
+    if (p.freed_count != nullptr) p.freed_count[g.unit] = nf;
+  }
 }
 
 // Per-page coordinates a wavefront needs before it loads the page.
@@ -593,7 +719,7 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
     if (tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_LENGTH);
     return;
   }
-  finish_unit<G>(p, g, fin_m, fin_il);
+  finish_unit<kAttendThreads, G, D>(p, g, fin_m, fin_il);
 }
 
 // Second pass when a unit is split over several work-groups: combines the
@@ -630,7 +756,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(const AttendParams 
     }
   }
   __syncthreads();
-  finish_unit<G>(p, g, fin_m, fin_il);
+  finish_unit<256, G, D>(p, g, fin_m, fin_il);
 }
 
 template <int D, int G>
@@ -660,13 +786,12 @@ size_t se_attend_workspace_bytes(int32_t num_units, int32_t max_len, int32_t max
   return attend_ws_layout(num_units, s, q_per_kv, head_dim).total;
 }
 
-extern "C" se_status se_decode_attend(const se_kv_view* kv, int32_t q_per_kv, const void* q,
-                                      const void* k_new, const void* v_new,
-                                      const int32_t* new_pos, const int32_t* sel_pages,
-                                      int32_t top_k, float scale, int32_t max_len,
-                                      uint32_t flags, float* out, float* lse, float* logits,
-                                      int32_t logits_stride, void* ws, size_t ws_bytes,
-                                      int32_t* dev_err, hipStream_t stream) {
+static se_status attend_launch(const se_kv_view* kv, int32_t q_per_kv, const void* q,
+                               const void* k_new, const void* v_new, const int32_t* new_pos,
+                               const int32_t* sel_pages, int32_t top_k, float scale, int32_t max_len,
+                               uint32_t flags, float* out, float* lse, float* logits,
+                               int32_t logits_stride, void* ws, size_t ws_bytes, int32_t* dev_err,
+                               hipStream_t stream, const AttendParams* fused_evict) {
   se_status st = check_view(kv);
   if (st != SE_OK) return st;
   if (q_per_kv != 1 && q_per_kv != 2 && q_per_kv != 4) return SE_ERR_UNSUPPORTED;
@@ -693,7 +818,8 @@ extern "C" se_status se_decode_attend(const se_kv_view* kv, int32_t q_per_kv, co
   const AttendWs lay = attend_ws_layout(kv->num_units, s, q_per_kv, D);
   if (ws == nullptr || ws_bytes < lay.total) return SE_ERR_WORKSPACE;
 
-  AttendParams prm;
+  AttendParams prm = {};
+  if (fused_evict != nullptr) prm = *fused_evict;
   prm.kv = static_cast<const uint16_t*>(kv->kv_pool);
   prm.pos_pool = kv->pos_pool;
   prm.score_pool = kv->score_pool;
@@ -738,4 +864,45 @@ extern "C" se_status se_decode_attend(const se_kv_view* kv, int32_t q_per_kv, co
     else launch_attend<64, 1>(prm, (int)grid, stream);
   }
   return launch_status();
+}
+
+extern "C" se_status se_decode_attend(const se_kv_view* kv, int32_t q_per_kv, const void* q,
+                                      const void* k_new, const void* v_new,
+                                      const int32_t* new_pos, const int32_t* sel_pages,
+                                      int32_t top_k, float scale, int32_t max_len,
+                                      uint32_t flags, float* out, float* lse, float* logits,
+                                      int32_t logits_stride, void* ws, size_t ws_bytes,
+                                      int32_t* dev_err, hipStream_t stream) {
+  return attend_launch(kv, q_per_kv, q, k_new, v_new, new_pos, sel_pages, top_k, scale, max_len,
+                       flags, out, lse, logits, logits_stride, ws, ws_bytes, dev_err, stream,
+                       nullptr);
+}
+
+extern "C" se_status se_decode_step_h2o(const se_kv_view* kv, int32_t q_per_kv, const void* q,
+                                        const void* k_new, const void* v_new,
+                                        const int32_t* new_pos, float scale, int32_t budget,
+                                        int32_t recent, int32_t max_len, float* out, float* lse,
+                                        int32_t* freed_pages, int32_t freed_stride,
+                                        int32_t* freed_count, void* ws, size_t ws_bytes,
+                                        int32_t* dev_err, hipStream_t stream) {
+  if (kv == nullptr || kv->score_pool == nullptr || kv->pos_pool == nullptr)
+    return SE_ERR_INVALID_ARGUMENT;
+  if (budget < 1 || recent < 0) return SE_ERR_INVALID_ARGUMENT;
+  if (budget > 8192) return SE_ERR_UNSUPPORTED;
+  if (freed_pages != nullptr && freed_stride < kv->max_pages) return SE_ERR_INVALID_ARGUMENT;
+  AttendParams ev = {};
+  ev.evict = 1;
+  ev.budget = budget;
+  ev.recent = recent;
+  ev.freed_pages = freed_pages;
+  ev.freed_stride = freed_stride;
+  ev.freed_count = freed_count;
+  se_status st = attend_launch(kv, q_per_kv, q, k_new, v_new, new_pos, nullptr, 0, scale, max_len,
+                               SE_ATTEND_ACCUMULATE, out, lse, nullptr, 0, ws, ws_bytes, dev_err,
+                               stream, &ev);
+  if (st != SE_OK) return st;
+  // units the fused path did not finish (first steps, irregular windows) go
+  // through the general eviction; the others exit at once
+  return se_evict_launch(kv, budget, recent, max_len, freed_pages, freed_stride, freed_count,
+                         dev_err, stream, true);
 }

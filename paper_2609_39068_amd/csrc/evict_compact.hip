@@ -39,6 +39,7 @@ struct EvictParams {
   int32_t freed_stride;
   int32_t* freed_count;
   int32_t* dev_err;
+  int32_t after_fused;  // units at or under the budget were finished by se_decode_step_h2o
 };
 
 __device__ __forceinline__ uint32_t pos_key(int32_t pos) { return (uint32_t)pos ^ 0x80000000u; }
@@ -58,7 +59,7 @@ __global__ __launch_bounds__(256) void evict_compact_kernel(const EvictParams p)
   const int L = p.lengths[unit];
   const int B = p.budget;
   if (L <= B) {
-    if (tid == 0 && p.freed_count != nullptr) p.freed_count[unit] = 0;
+    if (tid == 0 && p.freed_count != nullptr && !p.after_fused) p.freed_count[unit] = 0;
     return;
   }
   if (L > p.max_len || L > p.max_pages * kPage) {
@@ -233,10 +234,9 @@ __global__ __launch_bounds__(256) void evict_compact_kernel(const EvictParams p)
 
 using namespace se;
 
-extern "C" se_status se_evict_compact(const se_kv_view* kv, int32_t budget, int32_t recent,
-                                      int32_t max_len, int32_t* freed_pages,
-                                      int32_t freed_stride, int32_t* freed_count,
-                                      int32_t* dev_err, hipStream_t stream) {
+se_status se_evict_launch(const se_kv_view* kv, int32_t budget, int32_t recent, int32_t max_len,
+                          int32_t* freed_pages, int32_t freed_stride, int32_t* freed_count,
+                          int32_t* dev_err, hipStream_t stream, bool after_fused) {
   se_status st = check_view(kv);
   if (st != SE_OK) return st;
   if (kv->kv_pool == nullptr || kv->pos_pool == nullptr || kv->score_pool == nullptr ||
@@ -260,9 +260,18 @@ extern "C" se_status se_evict_compact(const se_kv_view* kv, int32_t budget, int3
   prm.freed_stride = freed_stride;
   prm.freed_count = freed_count;
   prm.dev_err = dev_err;
+  prm.after_fused = after_fused ? 1 : 0;
   if (kv->head_dim == 128)
     hipLaunchKernelGGL((evict_compact_kernel<128>), dim3(kv->num_units), dim3(256), 0, stream, prm);
   else
     hipLaunchKernelGGL((evict_compact_kernel<64>), dim3(kv->num_units), dim3(256), 0, stream, prm);
   return launch_status();
+}
+
+extern "C" se_status se_evict_compact(const se_kv_view* kv, int32_t budget, int32_t recent,
+                                      int32_t max_len, int32_t* freed_pages,
+                                      int32_t freed_stride, int32_t* freed_count,
+                                      int32_t* dev_err, hipStream_t stream) {
+  return se_evict_launch(kv, budget, recent, max_len, freed_pages, freed_stride, freed_count,
+                         dev_err, stream, false);
 }

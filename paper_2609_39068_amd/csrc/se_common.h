@@ -209,3 +209,9 @@ __device__ void radix_select_top(int n, int k, KeyFn key_of, CandFn cand, KeyT* 
 size_t se_attend_workspace_bytes(int32_t num_units, int32_t max_len, int32_t max_pages,
                                  int32_t q_per_kv, int32_t head_dim, int32_t top_k);
 size_t se_quest_workspace_bytes(int32_t num_units, int32_t max_pages);
+
+// Launches the eviction kernel; with after_fused, units at or under the budget
+// are left untouched (their step already reported them).
+se_status se_evict_launch(const se_kv_view* kv, int32_t budget, int32_t recent, int32_t max_len,
+                          int32_t* freed_pages, int32_t freed_stride, int32_t* freed_count,
+                          int32_t* dev_err, hipStream_t stream, bool after_fused);

@@ -38,19 +38,29 @@ class H2ODecoder:
                                        view.struct.max_pages, q_per_kv, view.struct.head_dim, 0)
         return torch.zeros(max(nbytes, 1), dtype=torch.uint8, device=device)
 
-    def attend(self, q, k_new, v_new, new_pos, out, lse=None, accumulate=True):
+    def attend(self, q, k_new, v_new, new_pos, out, lse=None, accumulate=True, max_len=None):
+        """``max_len`` bounds this step's resident slots after the append (the
+        scheduler knows it); it sizes the launch.  Defaults to the capacity."""
         se.se_decode_attend(self.view, self.G, q, k_new, v_new, new_pos, None, 0, self.scale,
-                            self.max_len, se.SE_ATTEND_ACCUMULATE if accumulate else 0, out, lse,
-                            None, 0, self.ws, self.dev_err)
+                            max_len or self.max_len, se.SE_ATTEND_ACCUMULATE if accumulate else 0,
+                            out, lse, None, 0, self.ws, self.dev_err)
 
-    def evict(self):
-        se.se_evict_compact(self.view, self.budget, self.recent, self.max_len, self.freed,
+    def evict(self, max_len=None):
+        se.se_evict_compact(self.view, self.budget, self.recent, max_len or self.max_len, self.freed,
                             0 if self.freed is None else self.freed.shape[1], self.freed_count,
                             self.dev_err)
 
-    def step(self, q, k_new, v_new, new_pos, out, lse=None):
-        self.attend(q, k_new, v_new, new_pos, out, lse)
-        self.evict()
+    def step(self, q, k_new, v_new, new_pos, out, lse=None, max_len=None, fused=True):
+        """One decode step.  fused: se_decode_step_h2o (attention, score update
+        and eviction in one call); otherwise se_decode_attend then se_evict_compact."""
+        if fused:
+            se.se_decode_step_h2o(self.view, self.G, q, k_new, v_new, new_pos, self.scale, self.budget,
+                                  self.recent, max_len or self.max_len, out, lse, self.freed,
+                                  0 if self.freed is None else self.freed.shape[1], self.freed_count,
+                                  self.ws, self.dev_err)
+        else:
+            self.attend(q, k_new, v_new, new_pos, out, lse, max_len=max_len)
+            self.evict(max_len)
 
 
 class QuestDecoder:
@@ -78,11 +88,11 @@ class QuestDecoder:
                            page_scores, 0 if page_scores is None else page_scores.shape[1],
                            self.ws_select, self.dev_err)
 
-    def attend(self, q, k_new, v_new, new_pos, out, lse=None):
+    def attend(self, q, k_new, v_new, new_pos, out, lse=None, max_len=None):
         se.se_decode_attend(self.view, self.G, q, k_new, v_new, new_pos, self.sel, self.top_k,
-                            self.scale, self.max_len, 0, out, lse, None, 0, self.ws_attend,
-                            self.dev_err)
+                            self.scale, max_len or self.max_len, 0, out, lse, None, 0,
+                            self.ws_attend, self.dev_err)
 
-    def step(self, q, k_new, v_new, new_pos, out, lse=None):
+    def step(self, q, k_new, v_new, new_pos, out, lse=None, max_len=None):
         self.select(q)
-        self.attend(q, k_new, v_new, new_pos, out, lse)
+        self.attend(q, k_new, v_new, new_pos, out, lse, max_len=max_len)

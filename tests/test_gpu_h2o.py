@@ -279,3 +279,46 @@ def test_deterministic_and_resumable(se):
         assert torch.equal(x, y)
     for name in ("kv_pool", "pos_pool", "score_pool", "lengths"):
         assert torch.equal(getattr(a, name), getattr(snap, name))
+
+
+@pytest.mark.parametrize("mode", ["contiguous", "gapped", "shuffled"])
+def test_fused_step_equals_attend_then_evict(se, mode):
+    # se_decode_step_h2o must leave exactly the state that se_decode_attend +
+    # se_evict_compact leave: bit-identical pools, lengths, outputs and freed
+    # pages, whether the eviction is fused (steady, contiguous window) or not
+    # (first step, or scattered recent positions).
+    lengths = [300, 129, 129, 129, 64, 128]
+    B, w, d, G = 128, 16, 128, 4
+    host = isolated_units(lengths, 32, d, seed=77, num_kv_heads=2, position_mode=mode)
+    U = len(lengths)
+    nreq = U // 2
+    g = torch.Generator().manual_seed(3)
+    a, b = to_device(host, DEV), to_device(host, DEV)
+    max_len = 32 * 16
+    ws = torch.zeros(se.se_workspace_bytes(se.SE_OP_DECODE_ATTEND, U, max_len, 32, G, d), dtype=torch.uint8, device=DEV)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    fa = torch.full((U, 32), -3, dtype=torch.int32, device=DEV)
+    fb = fa.clone()
+    ca = torch.full((U,), -3, dtype=torch.int32, device=DEV)
+    cb = ca.clone()
+    va, vb = _view(se, a), _view(se, b)
+    for step in range(4):
+        q = torch.randn((nreq, 2 * G, d), generator=g).to(torch.bfloat16).to(DEV)
+        kn = torch.randn((nreq, 2, d), generator=g).to(torch.bfloat16).to(DEV)
+        vn = torch.randn((nreq, 2, d), generator=g).to(torch.bfloat16).to(DEV)
+        npos = torch.tensor([10_000 + 10 * step + r for r in range(nreq)], dtype=torch.int32, device=DEV)
+        oa = torch.empty((nreq, 2 * G, d), dtype=torch.float32, device=DEV)
+        ob = torch.empty_like(oa)
+        se.se_decode_attend(va, G, q, kn, vn, npos, None, 0, 0.088, max_len, se.SE_ATTEND_ACCUMULATE, oa,
+                            None, None, 0, ws, err)
+        se.se_evict_compact(va, B, w, max_len, fa, 32, ca, err)
+        se.se_decode_step_h2o(vb, G, q, kn, vn, npos, 0.088, B, w, max_len, ob, None, fb, 32, cb, ws, err)
+        torch.cuda.synchronize()
+        assert se.se_read_device_errors(err) == 0
+        assert torch.equal(oa, ob)
+        for name in ("kv_pool", "pos_pool", "score_pool", "lengths"):
+            assert torch.equal(getattr(a, name), getattr(b, name)), (step, name)
+        assert torch.equal(ca, cb), step
+        for u in range(U):
+            n = int(ca[u])
+            assert torch.equal(fa[u, :n], fb[u, :n])
