@@ -74,14 +74,14 @@ _SHARED = {}
 
 def cpu_baseline(w, K):
     """The oracle, untuned, on a bounded sample of the same workload: the
-    first request (all its KV heads, one layer) for the same K steps,
+    first six requests (all their KV heads, one layer) for the same K steps,
     one unit per worker process.  Runs before the GPU is touched; the workers
     are forked after every input has been converted to NumPy."""
     import multiprocessing as mp
     import numpy as np
     import torch
     from workloads import build_state, build_steps, scaled, unit_slots
-    sample_req = 1
+    sample_req = 6
     ws = scaled(w, num_req=sample_req, layers=1)
     host = build_state(ws, "cpu")
     steps = build_steps(ws, host, "cpu", steps=K)
