@@ -368,11 +368,13 @@ struct WaveSoftmax {
   float m_own;  // m_ref of the lane's own head
 };
 
-// Logits of the lane's (row, head) pair for one page.
+// Logits of the lane's (row, head) pair for one page.  The query rows are read
+// from LDS (one copy per work-group) instead of being held in registers, which
+// leaves room for a second page in flight.
 template <int D, int G>
 __device__ __forceinline__ float qk_page(const Lanes<D>& ln, const uint4 (&kb)[2 * Lanes<D>::K4],
-                                         const uint32_t (&qreg)[G][Lanes<D>::QW]) {
-  constexpr int K4 = Lanes<D>::K4;
+                                         const uint32_t (*lds_q)[D / 2]) {
+  constexpr int K4 = Lanes<D>::K4, QW = Lanes<D>::QW;
   float accA[G], accB[G];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
@@ -384,11 +386,13 @@ __device__ __forceinline__ float qk_page(const Lanes<D>& ln, const uint4 (&kb)[2
     const uint32_t ka[4] = {kb[i].x, kb[i].y, kb[i].z, kb[i].w};
     const uint32_t kc[4] = {kb[K4 + i].x, kb[K4 + i].y, kb[K4 + i].z, kb[K4 + i].w};
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
+    for (int h = 0; h < G; ++h) {
+      const uint4 qv = reinterpret_cast<const uint4*>(&lds_q[h][ln.j8 * QW])[i];
+      const uint32_t qw[4] = {qv.x, qv.y, qv.z, qv.w};
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        accA[h] = dot2bf16(qreg[h][4 * i + e], ka[e], accA[h]);
-        accB[h] = dot2bf16(qreg[h][4 * i + e], kc[e], accB[h]);
+      for (int e = 0; e < 4; ++e) {
+        accA[h] = dot2bf16(qw[e], ka[e], accA[h]);
+        accB[h] = dot2bf16(qw[e], kc[e], accB[h]);
       }
     }
   }
@@ -472,6 +476,7 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
   __shared__ int lds_phys[kMaxGroupPages];
   __shared__ int lds_lp[kMaxGroupPages];
   __shared__ int lds_vp[kMaxGroupPages];
+  __shared__ uint32_t lds_q[G][D / 2];  // the unit's G query rows (bf16 pairs)
   __shared__ int lds_scan[kAttendThreads / kWave + 1];
 
   const int tid = threadIdx.x;
@@ -503,21 +508,9 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
   const int j8 = ln.j8;
   const int col = ln.col;
 
-  uint32_t qreg[G][QW];
   {
-    const uint16_t* qb = p.q + ((size_t)req * Hq + (size_t)kvh * G) * D + j8 * QC;
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const uint4* src = reinterpret_cast<const uint4*>(qb + (size_t)h * D);
-#pragma unroll
-      for (int i = 0; i < K4; ++i) {
-        const uint4 t = src[i];
-        qreg[h][4 * i + 0] = t.x;
-        qreg[h][4 * i + 1] = t.y;
-        qreg[h][4 * i + 2] = t.z;
-        qreg[h][4 * i + 3] = t.w;
-      }
-    }
+    const uint4* qsrc = reinterpret_cast<const uint4*>(p.q + ((size_t)req * Hq + (size_t)kvh * G) * D);
+    if (tid < G * D / 8) reinterpret_cast<uint4*>(&lds_q[0][0])[tid] = qsrc[tid];
   }
 
   WaveSoftmax<G> ws;
@@ -623,32 +616,49 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
     return pr;
   };
 
-  // ---- the page stream, software-pipelined on one register buffer: page
-  // i+1's K loads are issued once page i's logits are formed, its V loads
-  // once page i's PV is done, so each load has a compute phase to land in
-  uint4 kb[2 * K4];
+  // ---- the page stream.  K is prefetched two pages ahead (two register
+  // buffers, pages alternate between them) and V one page ahead (one buffer):
+  // page i+2's K loads are issued once page i's logits are formed, page i+1's
+  // V loads once page i's PV is done.  The loads are unconditional (a
+  // conditional load would make the compiler drain every load at the join);
+  // past the last page they re-read one row of the last page.
+  uint4 kbA[2 * K4], kbB[2 * K4];
   uint32_t vb[RPL];
   if (n_my > 0) {
-    PageRef cur = page_ref(0);
-    load_k<D>(p, ln, cur, kb);
-    // keep the loop's issue order (K before V) on the entry edge too, so the
-    // loop-top wait for K can leave the V loads in flight
+    auto ref_or_tail = [&](int i) -> PageRef {
+      PageRef r = page_ref(i < n_my ? i : n_my - 1);
+      if (i >= n_my) r.nrows = 1;
+      return r;
+    };
+    PageRef cur = ref_or_tail(0);
+    PageRef nx1 = ref_or_tail(1);
+    load_k<D>(p, ln, cur, kbA);
+    __builtin_amdgcn_sched_barrier(0);
+    load_k<D>(p, ln, nx1, kbB);
     __builtin_amdgcn_sched_barrier(0);
     load_v<D>(p, ln, cur, vb);
-    for (int i = 0; i < n_my; ++i) {
-      // The prefetch is unconditional (a conditional load would make the
-      // compiler drain every load at the loop latch); after the last page it
-      // re-reads one row of the same page.
-      const bool more = i + 1 < n_my;
-      PageRef nxt = page_ref(more ? i + 1 : i);
-      if (!more) nxt.nrows = 1;
-      const float z = qk_page<D, G>(ln, kb, qreg);
-      load_k<D>(p, ln, nxt, kb);
-      softmax_page<D, G>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p);
-      pv_page<D, G>(ln, vb, ws, lds_p[wave]);
-      load_v<D>(p, ln, nxt, vb);
-      if (!more) nxt.nrows = cur.nrows;
-      cur = nxt;
+    for (int i = 0; i < n_my; i += 2) {
+      {
+        const PageRef nx2 = ref_or_tail(i + 2);
+        const float z = qk_page<D, G>(ln, kbA, lds_q);
+        load_k<D>(p, ln, nx2, kbA);
+        softmax_page<D, G>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p);
+        pv_page<D, G>(ln, vb, ws, lds_p[wave]);
+        load_v<D>(p, ln, nx1, vb);
+        cur = nx1;
+        nx1 = nx2;
+      }
+      if (i + 1 >= n_my) break;
+      {
+        const PageRef nx2 = ref_or_tail(i + 3);
+        const float z = qk_page<D, G>(ln, kbB, lds_q);
+        load_k<D>(p, ln, nx2, kbB);
+        softmax_page<D, G>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p);
+        pv_page<D, G>(ln, vb, ws, lds_p[wave]);
+        load_v<D>(p, ln, nx1, vb);
+        cur = nx1;
+        nx1 = nx2;
+      }
     }
   }
 
