@@ -180,10 +180,10 @@ se_status se_evict_compact(const se_kv_view* kv, int32_t budget, int32_t recent,
  * attention of the step and its finish_step work (Section 3.1, "Fine-Grained
  * Lifecycle Hooks": H2O's cumulative-score update and online eviction at the end
  * of a decode step; Appendix A.3, eqs. background-h2o-score and
- * background-h2o-retention).  When a unit is one slot over the budget and its
- * recent window is the run of its newest positions (every step after the first
- * eviction), the eviction happens inside the attention pass; the other units go
- * through the general eviction afterwards, in the same call.
+ * background-h2o-retention).  The eviction runs in the epilogue of the attention
+ * pass (one launch): a unit one slot over the budget whose recent window is the run
+ * of its newest positions (every step after the first eviction) evicts from
+ * registers; any other unit over the budget runs the general selection there.
  *  Arguments as for se_decode_attend and se_evict_compact; ws is the
  *  SE_OP_DECODE_ATTEND workspace.  budget 1 .. 8192.
  */

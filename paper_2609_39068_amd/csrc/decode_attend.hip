@@ -30,7 +30,7 @@
 // boundary orders the two passes across XCDs (each XCD has its own L2), which
 // avoids a device-scope release/acquire (an L2 writeback and invalidate) in
 // every work-group.
-#include "se_common.h"
+#include "evict_core.h"
 
 namespace se {
 
@@ -137,12 +137,36 @@ __device__ __forceinline__ uint32_t pos_order(int32_t pos) { return (uint32_t)po
 // non-window slot with the smallest (score, then larger position); the new
 // token's slot (the last one) moves into it.  Anything else is left to the
 // general eviction kernel that se_decode_step_h2o launches next.
+// The general eviction of a unit in the epilogue (after its scores are written).
+template <int NT, int D>
+__device__ void evict_in_epilogue(const AttendParams& p, const UnitGeom& g, const EvictScratch<NT>& sc) {
+  __syncthreads();
+  EvictJob job;
+  job.kv = const_cast<uint16_t*>(p.kv);
+  job.pos_pool = p.pos_pool;
+  job.score_pool = p.score_pool;
+  job.bt = p.block_table + (size_t)g.unit * p.max_pages;
+  job.lengths = p.lengths;
+  job.num_pages = p.num_pages;
+  job.unit = g.unit;
+  job.L = g.Lp;
+  job.budget = p.budget;
+  job.recent = p.recent;
+  job.max_len = p.max_len;
+  job.max_pages = p.max_pages;
+  job.freed_pages = p.freed_pages;
+  job.freed_stride = p.freed_stride;
+  job.freed_count = p.freed_count;
+  job.dev_err = p.dev_err;
+  evict_unit<NT, D>(job, sc);
+}
+
 template <int NT, int G, int D>
 __device__ void finish_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
-                            const float* fin_il) {
+                            const float* fin_il, const EvictScratch<NT>& sc) {
   constexpr int KMAX = 8192 / NT;  // slots per thread kept in registers
-  __shared__ int red_i[NT / kWave];
-  __shared__ unsigned long long red_k[NT / kWave];
+  int* const red_i = sc.red_i;
+  unsigned long long* const red_k = sc.red_u64;
   __shared__ int bc[2];
   __shared__ float bc_u;
   const int tid = threadIdx.x;
@@ -167,10 +191,13 @@ __device__ void finish_unit(const AttendParams& p, const UnitGeom& g, const floa
         *up = (g.append && slot == g.L) ? a : *up + a;
       }
     }
+    if (p.evict && !g.quest && g.Lp > p.budget) {
+      evict_in_epilogue<NT, D>(p, g, sc);  // sets the length and the freed pages
+      return;
+    }
     if (tid == 0) {
       if (g.append) p.lengths[g.unit] = g.Lp;
-      // nothing to evict: report it here, the general kernel leaves this unit alone
-      if (p.evict && g.Lp <= p.budget && p.freed_count != nullptr) p.freed_count[g.unit] = 0;
+      if (p.evict && p.freed_count != nullptr) p.freed_count[g.unit] = 0;
     }
     return;
   }
@@ -209,8 +236,8 @@ __device__ void finish_unit(const AttendParams& p, const UnitGeom& g, const floa
 #pragma unroll
   for (int k = 0; k < KMAX; ++k) cnt += (tid + k * NT < g.Lp && (int64_t)pos[k] > lo) ? 1 : 0;
   cnt = block_reduce<NT>(cnt, red_i, [](int x, int y) { return x + y; });
-  if (badp || cnt != w) {  // scores are updated; the general kernel evicts
-    if (tid == 0 && g.append) p.lengths[g.unit] = g.Lp;
+  if (badp || cnt != w) {  // scores are updated; the general path evicts
+    evict_in_epilogue<NT, D>(p, g, sc);
     return;
   }
   unsigned long long best = ~0ull;
@@ -477,6 +504,7 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
   __shared__ int lds_lp[kMaxGroupPages];
   __shared__ int lds_vp[kMaxGroupPages];
   __shared__ uint32_t lds_q[G][D / 2];  // the unit's G query rows (bf16 pairs)
+  SE_EVICT_SCRATCH(kAttendThreads, esc);
   __shared__ int lds_scan[kAttendThreads / kWave + 1];
 
   const int tid = threadIdx.x;
@@ -729,13 +757,14 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
     if (tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_LENGTH);
     return;
   }
-  finish_unit<kAttendThreads, G, D>(p, g, fin_m, fin_il);
+  finish_unit<kAttendThreads, G, D>(p, g, fin_m, fin_il, esc);
 }
 
 // Second pass when a unit is split over several work-groups: combines the
 // partials (m, l, o) in split order, writes out and lse, then finishes the unit.
 template <int D, int G>
 __global__ __launch_bounds__(256) void decode_combine_kernel(const AttendParams p) {
+  SE_EVICT_SCRATCH(256, esc);
   __shared__ float fin_m[G];
   __shared__ float fin_il[G];
   const UnitGeom g = unit_geom(p, blockIdx.x);
@@ -766,7 +795,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(const AttendParams 
     }
   }
   __syncthreads();
-  finish_unit<256, G, D>(p, g, fin_m, fin_il);
+  finish_unit<256, G, D>(p, g, fin_m, fin_il, esc);
 }
 
 template <int D, int G>
@@ -910,9 +939,5 @@ extern "C" se_status se_decode_step_h2o(const se_kv_view* kv, int32_t q_per_kv, 
   se_status st = attend_launch(kv, q_per_kv, q, k_new, v_new, new_pos, nullptr, 0, scale, max_len,
                                SE_ATTEND_ACCUMULATE, out, lse, nullptr, 0, ws, ws_bytes, dev_err,
                                stream, &ev);
-  if (st != SE_OK) return st;
-  // units the fused path did not finish (first steps, irregular windows) go
-  // through the general eviction; the others exit at once
-  return se_evict_launch(kv, budget, recent, max_len, freed_pages, freed_stride, freed_count,
-                         dev_err, stream, true);
+  return st;
 }

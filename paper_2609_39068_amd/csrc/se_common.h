@@ -162,18 +162,18 @@ __device__ __forceinline__ T block_reduce(T v, T* scratch, Op op) {
 }
 
 // Radix selection of the k largest keys among the items for which cand(i) holds
-// (blockDim.x == NT == 256).  After the call, an item is among the k largest
+// (blockDim.x == NT, NT >= 256; 8-bit digits, one histogram bin per thread).  After the call, an item is among the k largest
 // iff (key & *mask) > *prefix, or (key & *mask) == *prefix and it is one of the
 // first *k_rest such items in index order.  Needs k >= 1 and at least k candidates.
 template <int NT, typename KeyT, typename KeyFn, typename CandFn>
 __device__ void radix_select_top(int n, int k, KeyFn key_of, CandFn cand, KeyT* prefix_out,
                                  KeyT* mask_out, int* k_rest_out, unsigned* hist, int* scan_scratch,
                                  int* bcast) {
-  static_assert(NT == 256, "one bin per thread");
+  static_assert(NT >= 256 && NT % kWave == 0, "threads 0..255 own one bin each");
   KeyT prefix = 0, mask = 0;
   const int tid = threadIdx.x;
   for (int shift = (int)sizeof(KeyT) * 8 - 8; shift >= 0; shift -= 8) {
-    hist[tid] = 0;
+    if (tid < 256) hist[tid] = 0;
     __syncthreads();
     for (int i = tid; i < n; i += NT) {
       if (!cand(i)) continue;
@@ -181,10 +181,10 @@ __device__ void radix_select_top(int n, int k, KeyFn key_of, CandFn cand, KeyT* 
       if ((key & mask) == prefix) atomicAdd(&hist[(unsigned)(key >> shift) & 255u], 1u);
     }
     __syncthreads();
-    const int v = (int)hist[255 - tid];  // thread t counts digit 255 - t
+    const int v = tid < 256 ? (int)hist[255 - tid] : 0;  // thread t counts digit 255 - t
     int total;
     const int excl = block_exclusive_scan<NT>(v, scan_scratch, &total);
-    if (excl < k && excl + v >= k) {
+    if (v > 0 && excl < k && excl + v >= k) {
       bcast[0] = 255 - tid;
       bcast[1] = excl;
       bcast[2] = v;
@@ -210,8 +210,4 @@ size_t se_attend_workspace_bytes(int32_t num_units, int32_t max_len, int32_t max
                                  int32_t q_per_kv, int32_t head_dim, int32_t top_k);
 size_t se_quest_workspace_bytes(int32_t num_units, int32_t max_pages);
 
-// Launches the eviction kernel; with after_fused, units at or under the budget
-// are left untouched (their step already reported them).
-se_status se_evict_launch(const se_kv_view* kv, int32_t budget, int32_t recent, int32_t max_len,
-                          int32_t* freed_pages, int32_t freed_stride, int32_t* freed_count,
-                          int32_t* dev_err, hipStream_t stream, bool after_fused);
+
