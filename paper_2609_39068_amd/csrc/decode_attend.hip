@@ -139,7 +139,7 @@ __device__ __forceinline__ uint32_t pos_order(int32_t pos) { return (uint32_t)po
 // general eviction kernel that se_decode_step_h2o launches next.
 // The general eviction of a unit in the epilogue (after its scores are written).
 template <int NT, int D>
-__device__ void evict_in_epilogue(const AttendParams& p, const UnitGeom& g, const EvictScratch<NT>& sc) {
+__device__ __forceinline__ void evict_in_epilogue(const AttendParams& p, const UnitGeom& g, const EvictScratch<NT>& sc) {
   __syncthreads();
   EvictJob job;
   job.kv = const_cast<uint16_t*>(p.kv);
@@ -162,7 +162,7 @@ __device__ void evict_in_epilogue(const AttendParams& p, const UnitGeom& g, cons
 }
 
 template <int NT, int G, int D>
-__device__ void finish_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
+__device__ __forceinline__ void finish_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
                             const float* fin_il, const EvictScratch<NT>& sc) {
   constexpr int KMAX = 8192 / NT;  // slots per thread kept in registers
   int* const red_i = sc.red_i;
