@@ -161,47 +161,18 @@ __device__ __forceinline__ void evict_in_epilogue(const AttendParams& p, const U
   evict_unit<NT, D>(job, sc);
 }
 
+// The fused steady eviction (one slot over the budget, contiguous window):
+// scores, positions and the victim search stay in registers.
 template <int NT, int G, int D>
-__device__ __forceinline__ void finish_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
-                            const float* fin_il, const EvictScratch<NT>& sc) {
-  constexpr int KMAX = 8192 / NT;  // slots per thread kept in registers
+__device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitGeom& g, const float* fin_m,
+                                              const float* fin_il, const EvictScratch<NT>& sc) {
+  constexpr int KMAX = kMaxBudget / NT;  // slots per thread kept in registers
   int* const red_i = sc.red_i;
   unsigned long long* const red_k = sc.red_u64;
   __shared__ int bc[2];
   __shared__ float bc_u;
   const int tid = threadIdx.x;
   const size_t ubase_p = (size_t)g.unit * p.n_visit_max;
-  const bool fuse = p.evict && !g.quest && p.accumulate && g.Lp == p.budget + 1 && g.Lp <= NT * KMAX;
-  if (!fuse) {
-    if (p.accumulate) {
-      for (int idx = tid; idx < g.n_visit * kPage; idx += NT) {
-        const int vp = idx >> 4;
-        const int rr = idx & (kPage - 1);
-        int lp = vp;
-        if (g.quest) {
-          lp = vp < p.top_k ? p.sel[(size_t)g.unit * p.top_k + vp] : g.cur_page;
-          if (lp < 0 || (vp < p.top_k && lp >= g.cur_page)) continue;
-        }
-        const int slot = lp * kPage + rr;
-        if (slot >= g.Lp) continue;
-        const int phys = p.block_table[(size_t)g.unit * p.max_pages + lp];
-        if (phys < 0 || (int64_t)phys >= p.num_pages) continue;
-        const float a = slot_weight<G>(p, ubase_p, vp, rr, fin_m, fin_il);
-        float* up = p.score_pool + (size_t)phys * kPage + rr;
-        *up = (g.append && slot == g.L) ? a : *up + a;
-      }
-    }
-    if (p.evict && !g.quest && g.Lp > p.budget) {
-      evict_in_epilogue<NT, D>(p, g, sc);  // sets the length and the freed pages
-      return;
-    }
-    if (tid == 0) {
-      if (g.append) p.lengths[g.unit] = g.Lp;
-      if (p.evict && p.freed_count != nullptr) p.freed_count[g.unit] = 0;
-    }
-    return;
-  }
-
   const int32_t* bt = p.block_table + (size_t)g.unit * p.max_pages;
   float unew[KMAX];
   int32_t pos[KMAX];
@@ -290,6 +261,82 @@ __device__ __forceinline__ void finish_unit(const AttendParams& p, const UnitGeo
     if (p.freed_pages != nullptr && nf > 0) p.freed_pages[(size_t)g.unit * p.freed_stride] = bt[f0];
     if (p.freed_count != nullptr) p.freed_count[g.unit] = nf;
   }
+}
+
+
+// The score update of every visited slot, BATCH slots per thread at a time with
+// all of a batch's loads issued before its stores.
+template <int NT, int G>
+__device__ __forceinline__ void accumulate_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
+                                                const float* fin_il) {
+  constexpr int BATCH = 8;
+  const size_t ubase_p = (size_t)g.unit * p.n_visit_max;
+  const int32_t* bt = p.block_table + (size_t)g.unit * p.max_pages;
+  float fm[G], fil[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    fm[h] = fin_m[h];
+    fil[h] = fin_il[h];
+  }
+  const int n = g.n_visit * kPage;
+  for (int b0 = threadIdx.x; b0 < n; b0 += NT * BATCH) {
+    int ph[BATCH];
+    float a[BATCH];
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j) {
+      const int idx = b0 + j * NT;
+      const int vp = idx >> 4;
+      const int rr = idx & (kPage - 1);
+      int lp = vp;
+      bool ok = idx < n;
+      if (ok && g.quest) {
+        lp = vp < p.top_k ? p.sel[(size_t)g.unit * p.top_k + vp] : g.cur_page;
+        ok = lp >= 0 && (vp >= p.top_k || lp < g.cur_page);
+      }
+      ok = ok && lp * kPage + rr < g.Lp;
+      ph[j] = ok ? bt[lp] : -1;
+      a[j] = ok ? slot_weight<G>(p, ubase_p, vp, rr, fm, fil) : 0.f;
+    }
+    float u[BATCH];
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j) {
+      const int idx = b0 + j * NT;
+      const int rr = idx & (kPage - 1);
+      const bool ok = ph[j] >= 0 && (int64_t)ph[j] < p.num_pages;
+      const int vp = idx >> 4;
+      const bool fresh = g.append && !g.quest ? vp * kPage + rr == g.L
+                                               : (g.append && vp >= p.top_k && g.cur_page * kPage + rr == g.L);
+      u[j] = ok && !fresh ? p.score_pool[(size_t)ph[j] * kPage + rr] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j) {
+      const int rr = (b0 + j * NT) & (kPage - 1);
+      if (ph[j] >= 0 && (int64_t)ph[j] < p.num_pages) p.score_pool[(size_t)ph[j] * kPage + rr] = u[j] + a[j];
+    }
+  }
+}
+
+template <int NT, int G, int D, bool kCanEvict>
+__device__ __forceinline__ void finish_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
+                            const float* fin_il, const EvictScratch<NT>* scp) {
+  const int tid = threadIdx.x;
+  const bool fuse = kCanEvict && p.evict && !g.quest && p.accumulate && g.Lp == p.budget + 1 &&
+                    g.Lp <= kMaxBudget;  // the steady path holds at most kMaxBudget slots in registers
+  if (!fuse) {
+    if (p.accumulate) accumulate_unit<NT, G>(p, g, fin_m, fin_il);
+    if constexpr (kCanEvict) {
+      if (p.evict && !g.quest && g.Lp > p.budget) {
+        evict_in_epilogue<NT, D>(p, g, *scp);  // sets the length and the freed pages
+        return;
+      }
+    }
+    if (tid == 0) {
+      if (g.append) p.lengths[g.unit] = g.Lp;
+      if (kCanEvict && p.evict && p.freed_count != nullptr) p.freed_count[g.unit] = 0;
+    }
+    return;
+  }
+  if constexpr (kCanEvict) finish_steady<NT, G, D>(p, g, fin_m, fin_il, *scp);
 }
 
 // Per-page coordinates a wavefront needs before it loads the page.
@@ -757,14 +804,15 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
     if (tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_LENGTH);
     return;
   }
-  finish_unit<kAttendThreads, G, D>(p, g, fin_m, fin_il, esc);
+  finish_unit<kAttendThreads, G, D, true>(p, g, fin_m, fin_il, &esc);
 }
 
 // Second pass when a unit is split over several work-groups: combines the
 // partials (m, l, o) in split order, writes out and lse, then finishes the unit.
+constexpr int kCombineThreads = 512;
+
 template <int D, int G>
-__global__ __launch_bounds__(256) void decode_combine_kernel(const AttendParams p) {
-  SE_EVICT_SCRATCH(256, esc);
+__global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(const AttendParams p) {
   __shared__ float fin_m[G];
   __shared__ float fin_il[G];
   const UnitGeom g = unit_geom(p, blockIdx.x);
@@ -795,15 +843,39 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(const AttendParams 
     }
   }
   __syncthreads();
-  finish_unit<256, G, D>(p, g, fin_m, fin_il, esc);
+  finish_unit<kCombineThreads, G, D, false>(p, g, fin_m, fin_il, nullptr);
 }
 
+// With a split, the combine pass updates the scores and publishes the appended
+// length; the eviction (if asked for) then runs as its own kernel, whose
+// 1024-thread work-groups hold a whole long unit in registers.
 template <int D, int G>
 static void launch_attend(const AttendParams& prm, int grid, hipStream_t stream) {
   hipLaunchKernelGGL((decode_attend_kernel<D, G>), dim3(grid), dim3(kAttendThreads), 0, stream, prm);
-  if (prm.n_split > 1)
-    hipLaunchKernelGGL((decode_combine_kernel<D, G>), dim3(grid / prm.n_split), dim3(256), 0, stream,
-                       prm);
+  if (prm.n_split > 1) {
+    AttendParams cp = prm;
+    cp.evict = 0;
+    const int units = grid / prm.n_split;
+    hipLaunchKernelGGL((decode_combine_kernel<D, G>), dim3(units), dim3(kCombineThreads), 0, stream, cp);
+    if (prm.evict) {
+      EvictParams ep;
+      ep.kv = const_cast<uint16_t*>(prm.kv);
+      ep.pos_pool = prm.pos_pool;
+      ep.score_pool = prm.score_pool;
+      ep.block_table = prm.block_table;
+      ep.lengths = prm.lengths;
+      ep.num_pages = prm.num_pages;
+      ep.max_pages = prm.max_pages;
+      ep.budget = prm.budget;
+      ep.recent = prm.recent;
+      ep.max_len = prm.max_len;
+      ep.freed_pages = prm.freed_pages;
+      ep.freed_stride = prm.freed_stride;
+      ep.freed_count = prm.freed_count;
+      ep.dev_err = prm.dev_err;
+      launch_evict(ep, units, D, stream);
+    }
+  }
 }
 
 }  // namespace se

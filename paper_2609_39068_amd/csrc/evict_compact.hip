@@ -1,31 +1,18 @@
 // se_evict_compact: H2O retention (Appendix A.3, eq. background-h2o-retention) and
-// in-place compaction of the retained slots (Section 3.1), one 256-thread
-// work-group per unit running evict_unit (evict_core.h, which describes the
-// selection and the compaction).
+// in-place compaction of the retained slots (Section 3.1), one 1024-thread
+// work-group per unit running evict_unit_wide (evict_core.h, which describes the
+// selection and the compaction).  se_decode_step_h2o launches the same kernel
+// after its combine pass when a unit's attention was split.
 #include "evict_core.h"
 
 namespace se {
 
-struct EvictParams {
-  uint16_t* kv;
-  int32_t* pos_pool;
-  float* score_pool;
-  const int32_t* block_table;
-  int32_t* lengths;
-  int64_t num_pages;
-  int32_t max_pages;
-  int32_t budget;
-  int32_t recent;
-  int32_t max_len;
-  int32_t* freed_pages;
-  int32_t freed_stride;
-  int32_t* freed_count;
-  int32_t* dev_err;
-};
+constexpr int kEvictThreads = 1024;
+constexpr int kEvictSlotsPerThread = 34;  // register-resident up to 40960 slots per unit
 
 template <int D>
-__global__ __launch_bounds__(256) void evict_compact_kernel(const EvictParams p) {
-  SE_EVICT_SCRATCH(256, sc);
+__global__ __launch_bounds__(kEvictThreads) void evict_compact_kernel(const EvictParams p) {
+  SE_WIDE_SCRATCH(kEvictThreads, kEvictSlotsPerThread, sc);
   EvictJob job;
   job.kv = p.kv;
   job.pos_pool = p.pos_pool;
@@ -43,7 +30,14 @@ __global__ __launch_bounds__(256) void evict_compact_kernel(const EvictParams p)
   job.freed_stride = p.freed_stride;
   job.freed_count = p.freed_count;
   job.dev_err = p.dev_err;
-  evict_unit<256, D>(job, sc);
+  evict_unit_wide<kEvictThreads, D, kEvictSlotsPerThread>(job, sc);
+}
+
+void launch_evict(const EvictParams& p, int num_units, int head_dim, hipStream_t stream) {
+  if (head_dim == 128)
+    hipLaunchKernelGGL((evict_compact_kernel<128>), dim3(num_units), dim3(kEvictThreads), 0, stream, p);
+  else
+    hipLaunchKernelGGL((evict_compact_kernel<64>), dim3(num_units), dim3(kEvictThreads), 0, stream, p);
 }
 
 }  // namespace se
@@ -77,10 +71,7 @@ extern "C" se_status se_evict_compact(const se_kv_view* kv, int32_t budget, int3
   prm.freed_stride = freed_stride;
   prm.freed_count = freed_count;
   prm.dev_err = dev_err;
-  if (kv->head_dim == 128)
-    hipLaunchKernelGGL((evict_compact_kernel<128>), dim3(kv->num_units), dim3(256), 0, stream, prm);
-  else
-    hipLaunchKernelGGL((evict_compact_kernel<64>), dim3(kv->num_units), dim3(256), 0, stream, prm);
+  launch_evict(prm, kv->num_units, kv->head_dim, stream);
   return launch_status();
 }
 

@@ -183,6 +183,9 @@ CASES = [
     ([90, 200], 40, 80, "contiguous", 0),            # window larger than the budget
     ([5000, 4097, 8000], 4096, 512, "shuffled", 0),  # the 8B budget
     ([4097] * 6, 4096, 512, "contiguous", 1000),     # steady at the 8B budget, ties
+    ([32769, 20000], 2048, 256, "contiguous", 0),    # first step of the 8B workload
+    ([6000, 3000], 1024, 64, "contiguous", 3),       # exact score ties at the threshold
+    ([36000], 2048, 256, "shuffled", 7),             # past the register-resident size
 ]
 
 
