@@ -163,9 +163,11 @@ __device__ __forceinline__ void evict_in_epilogue(const AttendParams& p, const U
 
 // The fused steady eviction (one slot over the budget, contiguous window):
 // scores, positions and the victim search stay in registers.
+// lds_bt: the unit's page table staged in LDS, in page order.
 template <int NT, int G, int D>
 __device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitGeom& g, const float* fin_m,
-                                              const float* fin_il, const EvictScratch<NT>& sc) {
+                                              const float* fin_il, const int* lds_bt,
+                                              const EvictScratch<NT>& sc) {
   constexpr int KMAX = kMaxBudget / NT;  // slots per thread kept in registers
   int* const red_i = sc.red_i;
   unsigned long long* const red_k = sc.red_u64;
@@ -174,28 +176,46 @@ __device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitG
   const int tid = threadIdx.x;
   const size_t ubase_p = (size_t)g.unit * p.n_visit_max;
   const int32_t* bt = p.block_table + (size_t)g.unit * p.max_pages;
+  // Rows are loaded branch-free (rows past the end re-read the last slot, a bad
+  // page reads page 0 and is discarded) in groups of RG, whose loads are all in
+  // flight together; the stores come after every load, since a store between
+  // two rows' loads would keep the later loads from being issued early.
+  constexpr int RG = 4;
+  static_assert(KMAX % RG == 0, "row groups");
   float unew[KMAX];
   int32_t pos[KMAX];
+  int phys[KMAX];
   int badp = 0;
+  const int32_t pos_new = g.append ? p.new_pos[g.req] : 0;
 #pragma unroll
-  for (int k = 0; k < KMAX; ++k) {
-    const int s = tid + k * NT;
-    unew[k] = 0.f;
-    pos[k] = INT32_MIN;
-    if (s < g.Lp) {
-      const int phys = bt[s >> 4];
-      if (phys < 0 || (int64_t)phys >= p.num_pages) {
-        badp = 1;
-        continue;
-      }
-      const size_t a_ = (size_t)phys * kPage + (s & (kPage - 1));
-      const float a = slot_weight<G>(p, ubase_p, s >> 4, s & (kPage - 1), fin_m, fin_il);
-      const bool is_new = g.append && s == g.L;
-      unew[k] = (is_new ? 0.f : p.score_pool[a_]) + a;
-      pos[k] = is_new ? p.new_pos[g.req] : p.pos_pool[a_];
-      p.score_pool[a_] = unew[k];
+  for (int k0 = 0; k0 < KMAX; k0 += RG) {
+    float a[RG];
+#pragma unroll
+    for (int j = 0; j < RG; ++j) {
+      const int s = min(tid + (k0 + j) * NT, g.Lp - 1);
+      phys[k0 + j] = lds_bt[s >> 4];
+      a[j] = slot_weight<G>(p, ubase_p, s >> 4, s & (kPage - 1), fin_m, fin_il);
     }
+#pragma unroll
+    for (int j = 0; j < RG; ++j) {
+      const int k = k0 + j;
+      const int s = tid + k * NT;
+      const bool ok = phys[k] >= 0 && (int64_t)phys[k] < p.num_pages;
+      badp |= (s < g.Lp && !ok) ? 1 : 0;
+      const size_t a_ = (size_t)(ok ? phys[k] : 0) * kPage + (min(s, g.Lp - 1) & (kPage - 1));
+      const float u_old = p.score_pool[a_];
+      const int32_t q_old = p.pos_pool[a_];
+      const bool live = s < g.Lp && ok;
+      const bool is_new = g.append && s == g.L;
+      unew[k] = live ? (is_new ? 0.f : u_old) + a[j] : 0.f;
+      pos[k] = live ? (is_new ? pos_new : q_old) : INT32_MIN;
+      if (!live) phys[k] = -1;
+    }
+    __builtin_amdgcn_sched_barrier(0);
   }
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k)
+    if (phys[k] >= 0) p.score_pool[(size_t)phys[k] * kPage + ((tid + k * NT) & (kPage - 1))] = unew[k];
   badp = block_reduce<NT>(badp, red_i, [](int x, int y) { return x | y; });
   const int w = min(p.recent, p.budget);
   int32_t pmax = INT32_MIN;
@@ -316,12 +336,14 @@ __device__ __forceinline__ void accumulate_unit(const AttendParams& p, const Uni
   }
 }
 
+// lds_bt: the unit's whole page table staged in LDS in page order with every
+// page valid, or null (the steady eviction is fused only then).
 template <int NT, int G, int D, bool kCanEvict>
 __device__ __forceinline__ void finish_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
-                            const float* fin_il, const EvictScratch<NT>* scp) {
+                            const float* fin_il, const int* lds_bt, const EvictScratch<NT>* scp) {
   const int tid = threadIdx.x;
   const bool fuse = kCanEvict && p.evict && !g.quest && p.accumulate && g.Lp == p.budget + 1 &&
-                    g.Lp <= kMaxBudget;  // the steady path holds at most kMaxBudget slots in registers
+                    g.Lp <= kMaxBudget && lds_bt != nullptr;  // at most kMaxBudget slots in registers
   if (!fuse) {
     if (p.accumulate) accumulate_unit<NT, G>(p, g, fin_m, fin_il);
     if constexpr (kCanEvict) {
@@ -336,7 +358,7 @@ __device__ __forceinline__ void finish_unit(const AttendParams& p, const UnitGeo
     }
     return;
   }
-  if constexpr (kCanEvict) finish_steady<NT, G, D>(p, g, fin_m, fin_il, *scp);
+  if constexpr (kCanEvict) finish_steady<NT, G, D>(p, g, fin_m, fin_il, lds_bt, *scp);
 }
 
 // Per-page coordinates a wavefront needs before it loads the page.
@@ -804,7 +826,10 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
     if (tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_LENGTH);
     return;
   }
-  finish_unit<kAttendThreads, G, D, true>(p, g, fin_m, fin_il, &esc);
+  // the staged table is the unit's whole page table when one work-group reads
+  // every page and none was invalid
+  const bool whole_table = !quest && single && n_grp == g.n_visit;
+  finish_unit<kAttendThreads, G, D, true>(p, g, fin_m, fin_il, whole_table ? lds_phys : nullptr, &esc);
 }
 
 // Second pass when a unit is split over several work-groups: combines the
@@ -843,7 +868,7 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(const A
     }
   }
   __syncthreads();
-  finish_unit<kCombineThreads, G, D, false>(p, g, fin_m, fin_il, nullptr);
+  finish_unit<kCombineThreads, G, D, false>(p, g, fin_m, fin_il, nullptr, nullptr);
 }
 
 // With a split, the combine pass updates the scores and publishes the appended
