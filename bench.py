@@ -30,7 +30,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "decode attn+eviction tokens/s/GPU; achieved HBM GB/s vs MI355X peak"
 HBM_PEAK_GBS = 8000.0
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_attend_llama3-8b-layer-h2o_traffic.txt")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_step_h2o_llama3-8b-layer-h2o_traffic.txt")
 
 
 def parse():
@@ -156,7 +156,7 @@ def quest_attend_bytes(visited, G, D, top_k):
 
 def source_hash():
     h = hashlib.sha256()
-    for f in ("decode_attend.hip", "se_common.h"):
+    for f in ("decode_attend.hip", "evict_compact.hip", "evict_core.h", "se_common.h"):
         h.update(open(os.path.join(ROOT, "paper_2609_39068_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
