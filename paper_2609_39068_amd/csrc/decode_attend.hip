@@ -128,6 +128,33 @@ __device__ __forceinline__ float slot_weight(const AttendParams& p, size_t ubase
   return a;
 }
 
+// When one work-group holds a whole unit of at most kWeightPages<G> pages, the
+// per-slot weights and per-page reference maxima of the score update stay in
+// LDS instead of going through the workspace; the buffer is the eviction
+// scratch's holes array, which only the general eviction uses, after the scores
+// are written.
+constexpr int kWeightCap = 9216;  // floats (>= kMaxBudget ints for the holes)
+template <int G>
+constexpr int kWeightPages = kWeightCap / (kPage * G);
+static_assert(kWeightCap >= kMaxBudget, "the weight buffer doubles as the holes array");
+
+// Where the score update finds the weights: the workspace rows (global) or the
+// work-group's LDS buffer.
+struct WeightSrc {
+  const float* w;   // [visit page][16][G]
+  const float* mr;  // [visit page][G]
+};
+
+template <int G>
+__device__ __forceinline__ float slot_weight_from(const WeightSrc& src, int vp, int rr, const float* fin_m,
+                                                  const float* fin_il) {
+  float a = 0.f;
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+    a += src.w[(vp * kPage + rr) * G + h] * fast_exp2(src.mr[vp * G + h] - fin_m[h]) * fin_il[h];
+  return a;
+}
+
 __device__ __forceinline__ uint32_t pos_order(int32_t pos) { return (uint32_t)pos ^ 0x80000000u; }
 
 // With se_decode_step_h2o, the step's eviction (eq. background-h2o-retention)
@@ -166,7 +193,7 @@ __device__ __forceinline__ void evict_in_epilogue(const AttendParams& p, const U
 // lds_bt: the unit's page table staged in LDS, in page order.
 template <int NT, int G, int D>
 __device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitGeom& g, const float* fin_m,
-                                              const float* fin_il, const int* lds_bt,
+                                              const float* fin_il, const int* lds_bt, const WeightSrc& wsrc,
                                               const EvictScratch<NT>& sc) {
   constexpr int KMAX = kMaxBudget / NT;  // slots per thread kept in registers
   int* const red_i = sc.red_i;
@@ -194,7 +221,7 @@ __device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitG
     for (int j = 0; j < RG; ++j) {
       const int s = min(tid + (k0 + j) * NT, g.Lp - 1);
       phys[k0 + j] = lds_bt[s >> 4];
-      a[j] = slot_weight<G>(p, ubase_p, s >> 4, s & (kPage - 1), fin_m, fin_il);
+      a[j] = slot_weight_from<G>(wsrc, s >> 4, s & (kPage - 1), fin_m, fin_il);
     }
 #pragma unroll
     for (int j = 0; j < RG; ++j) {
@@ -288,7 +315,7 @@ __device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitG
 // all of a batch's loads issued before its stores.
 template <int NT, int G>
 __device__ __forceinline__ void accumulate_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
-                                                const float* fin_il) {
+                                                const float* fin_il, const WeightSrc& wsrc) {
   constexpr int BATCH = 8;
   const size_t ubase_p = (size_t)g.unit * p.n_visit_max;
   const int32_t* bt = p.block_table + (size_t)g.unit * p.max_pages;
@@ -315,7 +342,7 @@ __device__ __forceinline__ void accumulate_unit(const AttendParams& p, const Uni
       }
       ok = ok && lp * kPage + rr < g.Lp;
       ph[j] = ok ? bt[lp] : -1;
-      a[j] = ok ? slot_weight<G>(p, ubase_p, vp, rr, fm, fil) : 0.f;
+      a[j] = ok ? slot_weight_from<G>(wsrc, vp, rr, fm, fil) : 0.f;
     }
     float u[BATCH];
 #pragma unroll
@@ -340,12 +367,16 @@ __device__ __forceinline__ void accumulate_unit(const AttendParams& p, const Uni
 // page valid, or null (the steady eviction is fused only then).
 template <int NT, int G, int D, bool kCanEvict>
 __device__ __forceinline__ void finish_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
-                            const float* fin_il, const int* lds_bt, const EvictScratch<NT>* scp) {
+                            const float* fin_il, const int* lds_bt, const float* lds_w,
+                            const float* lds_mr, const EvictScratch<NT>* scp) {
   const int tid = threadIdx.x;
+  const size_t ubase_p = (size_t)g.unit * p.n_visit_max;
+  const WeightSrc wsrc = lds_w != nullptr ? WeightSrc{lds_w, lds_mr}
+                                          : WeightSrc{p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G};
   const bool fuse = kCanEvict && p.evict && !g.quest && p.accumulate && g.Lp == p.budget + 1 &&
                     g.Lp <= kMaxBudget && lds_bt != nullptr;  // at most kMaxBudget slots in registers
   if (!fuse) {
-    if (p.accumulate) accumulate_unit<NT, G>(p, g, fin_m, fin_il);
+    if (p.accumulate) accumulate_unit<NT, G>(p, g, fin_m, fin_il, wsrc);
     if constexpr (kCanEvict) {
       if (p.evict && !g.quest && g.Lp > p.budget) {
         evict_in_epilogue<NT, D>(p, g, *scp);  // sets the length and the freed pages
@@ -358,7 +389,7 @@ __device__ __forceinline__ void finish_unit(const AttendParams& p, const UnitGeo
     }
     return;
   }
-  if constexpr (kCanEvict) finish_steady<NT, G, D>(p, g, fin_m, fin_il, lds_bt, *scp);
+  if constexpr (kCanEvict) finish_steady<NT, G, D>(p, g, fin_m, fin_il, lds_bt, wsrc, *scp);
 }
 
 // Per-page coordinates a wavefront needs before it loads the page.
@@ -500,7 +531,8 @@ __device__ __forceinline__ float qk_page(const Lanes<D>& ln, const uint4 (&kb)[2
 template <int D, int G>
 __device__ __forceinline__ float softmax_page(const AttendParams& p, const Lanes<D>& ln,
                                               const PageRef& pr, float z, WaveSoftmax<G>& ws,
-                                              float* lds_pw, int lane, int unit, size_t ubase_p) {
+                                              float* lds_pw, int lane, int unit, size_t ubase_p,
+                                              float* lds_w, float* lds_mr, bool wl) {
   constexpr float kBump = 8.0f;  // rescale only when a logit beats the reference by 2^8
   const bool valid = ln.owns && ln.own_row < pr.nrows;
   const float z2 = valid ? z * p.scale_log2 : -INFINITY;
@@ -528,7 +560,10 @@ __device__ __forceinline__ float softmax_page(const AttendParams& p, const Lanes
   }
   const float pj = valid ? fast_exp2(z2 - ws.m_own) : 0.f;
   ws.l_own += pj;
-  if (p.accumulate) {
+  if (wl) {
+    if (ln.owns) lds_w[(pr.vp * kPage + ln.own_row) * G + ln.own_head] = pj;
+    if (lane < G) lds_mr[pr.vp * G + lane] = ws.m_own;
+  } else if (p.accumulate) {
     if (ln.owns) p.pbuf[((ubase_p + pr.vp) * kPage + ln.own_row) * G + ln.own_head] = pj;
     if (lane < G) p.mref[(ubase_p + pr.vp) * G + lane] = ws.m_own;
   }
@@ -573,7 +608,9 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
   __shared__ int lds_lp[kMaxGroupPages];
   __shared__ int lds_vp[kMaxGroupPages];
   __shared__ uint32_t lds_q[G][D / 2];  // the unit's G query rows (bf16 pairs)
-  SE_EVICT_SCRATCH(kAttendThreads, esc);
+  __shared__ float lds_w[kWeightCap];    // per-slot weights, then the eviction's holes
+  __shared__ float lds_mr[kWeightCap / kPage];
+  SE_EVICT_SCRATCH_WITH_HOLES(kAttendThreads, esc, reinterpret_cast<int*>(lds_w));
   __shared__ int lds_scan[kAttendThreads / kWave + 1];
 
   const int tid = threadIdx.x;
@@ -588,6 +625,8 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
   const int vbeg = split * p.pps;
   const int vend = min(vbeg + p.pps, g.n_visit);
   const size_t ubase_p = (size_t)unit * p.n_visit_max;  // page-indexed workspace rows
+  // the score update's weights stay in LDS when this work-group holds the whole unit
+  const bool wl = p.accumulate && p.n_split == 1 && g.n_visit <= kWeightPages<G>;
 
   // QK layout: lane = 8*r8 + j8 reads columns [j8*QC, (j8+1)*QC) of rows r8
   // (pass A) and r8 + 8 (pass B).  After the 8-lane reduction, lane j8 < 4
@@ -739,7 +778,7 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
         const PageRef nx2 = ref_or_tail(i + 2);
         const float z = qk_page<D, G>(ln, kbA, lds_q);
         load_k<D>(p, ln, nx2, kbA);
-        softmax_page<D, G>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p);
+        softmax_page<D, G>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p, lds_w, lds_mr, wl);
         pv_page<D, G>(ln, vb, ws, lds_p[wave]);
         load_v<D>(p, ln, nx1, vb);
         cur = nx1;
@@ -750,7 +789,7 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
         const PageRef nx2 = ref_or_tail(i + 3);
         const float z = qk_page<D, G>(ln, kbB, lds_q);
         load_k<D>(p, ln, nx2, kbB);
-        softmax_page<D, G>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p);
+        softmax_page<D, G>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p, lds_w, lds_mr, wl);
         pv_page<D, G>(ln, vb, ws, lds_p[wave]);
         load_v<D>(p, ln, nx1, vb);
         cur = nx1;
@@ -829,7 +868,8 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
   // the staged table is the unit's whole page table when one work-group reads
   // every page and none was invalid
   const bool whole_table = !quest && single && n_grp == g.n_visit;
-  finish_unit<kAttendThreads, G, D, true>(p, g, fin_m, fin_il, whole_table ? lds_phys : nullptr, &esc);
+  finish_unit<kAttendThreads, G, D, true>(p, g, fin_m, fin_il, whole_table ? lds_phys : nullptr,
+                                          wl ? lds_w : nullptr, lds_mr, &esc);
 }
 
 // Second pass when a unit is split over several work-groups: combines the
@@ -868,7 +908,7 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(const A
     }
   }
   __syncthreads();
-  finish_unit<kCombineThreads, G, D, false>(p, g, fin_m, fin_il, nullptr, nullptr);
+  finish_unit<kCombineThreads, G, D, false>(p, g, fin_m, fin_il, nullptr, nullptr, nullptr, nullptr);
 }
 
 // With a split, the combine pass updates the scores and publishes the appended

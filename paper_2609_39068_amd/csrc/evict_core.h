@@ -80,6 +80,16 @@ struct EvictParams {
 // Launches the eviction of every unit (head_dim 64 or 128) on `stream`.
 void launch_evict(const EvictParams& p, int num_units, int head_dim, hipStream_t stream);
 
+// The same with the holes array supplied by the caller (kMaxBudget ints of LDS
+// that it also uses for something else before the eviction starts).
+#define SE_EVICT_SCRATCH_WITH_HOLES(NT, name, holes_ptr) \
+  __shared__ unsigned name##_hist[256];                  \
+  __shared__ int name##_scan[(NT) / kWave + 1];          \
+  __shared__ int name##_bcast[4];                        \
+  __shared__ int name##_red_i[(NT) / kWave];             \
+  __shared__ unsigned long long name##_red_u64[(NT) / kWave]; \
+  const EvictScratch<NT> name{(holes_ptr), name##_hist, name##_scan, name##_bcast, name##_red_i, name##_red_u64}
+
 #define SE_EVICT_SCRATCH(NT, name)                   \
   __shared__ int name##_holes[kMaxBudget];           \
   __shared__ unsigned name##_hist[256];              \
