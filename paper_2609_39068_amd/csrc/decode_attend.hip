@@ -396,6 +396,14 @@ __device__ __forceinline__ void finish_unit(const AttendParams& p, const UnitGeo
 constexpr int kMaxGroupPages = 1024;  // pages one work-group streams at most
 constexpr int kAttendThreads = 512;   // eight wavefronts; two work-groups per compute unit
 
+// Share of a work-group's pages per wavefront slot rank, in percent.  Wavefront
+// w runs on SIMD w % 4 in the work-group's slot w / 4; with equal shares the
+// second slot's wavefronts end ~15 % after the first's (memory requests of the
+// older wavefront are served first), so the first slot takes more pages.  A
+// page's wavefront depends only on its index: the results do not depend on
+// timing.
+constexpr int kRankWeight[2] = {58, 42};
+
 struct PageRef {
   int vp;      // index in the unit's visit order (workspace row)
   int lp;      // logical page
@@ -738,11 +746,18 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
   }
   __syncthreads();
 
-  // Pages of this wavefront: staged entries wave + NW*i.
-  const int n_my = wave < n_grp ? (n_grp - wave + NW - 1) / NW : 0;
+  // Pages of this wavefront: the staged entries of its slot rank (a contiguous
+  // share of the list, sized by kRankWeight), interleaved over the rank's four
+  // wavefronts.
+  static_assert(NW == 8, "two slot ranks of four wavefronts");
+  const int srank = wave >> 2, wr = wave & 3;
+  const int n_r0 = (n_grp * kRankWeight[0] + 50) / 100;
+  const int rbeg = srank ? n_r0 : 0;
+  const int rcnt = srank ? n_grp - n_r0 : n_r0;
+  const int n_my = wr < rcnt ? (rcnt - wr + 3) / 4 : 0;
   auto page_ref = [&](int i) -> PageRef {
     PageRef pr;
-    const int gi = wave + NW * i;
+    const int gi = rbeg + wr + 4 * i;
     // wave-uniform by construction: keep them in scalar registers
     pr.vp = __builtin_amdgcn_readfirstlane(lds_vp[gi]);
     pr.lp = __builtin_amdgcn_readfirstlane(lds_lp[gi]);
