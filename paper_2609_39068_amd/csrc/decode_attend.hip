@@ -188,11 +188,125 @@ __device__ __forceinline__ void evict_in_epilogue(const AttendParams& p, const U
   evict_unit<NT, D>(job, sc);
 }
 
-// The fused steady eviction (one slot over the budget, contiguous window):
-// scores, positions and the victim search stay in registers.
-// lds_bt: the unit's page table staged in LDS, in page order.
+// The fused steady eviction (one slot over the budget, contiguous window) of a
+// unit that one work-group streamed whole: every wavefront handles the slots of
+// the pages it streamed (lane l: row l % 16 of its pages l / 16 + 4 j), whose
+// positions and old scores it fetched as soon as its own stream ended (spos,
+// su), so only LDS reads and arithmetic remain here before the reductions.
+// The staged table is the unit's page table (staged index = logical page).
+constexpr int kSteadyRows = 5;  // pages per wavefront up to 4 * kSteadyRows
+
 template <int NT, int G, int D>
 __device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitGeom& g, const float* fin_m,
+                                              const float* fin_il, const int* lds_phys, const int* lds_vp,
+                                              const WeightSrc& wsrc, int32_t (&pos)[kSteadyRows],
+                                              float (&unew)[kSteadyRows], int rbeg, int wr, int n_my,
+                                              const EvictScratch<NT>& sc) {
+  constexpr int KW = kSteadyRows;
+  int* const red_i = sc.red_i;
+  unsigned long long* const red_k = sc.red_u64;
+  __shared__ int bc[2];
+  __shared__ float bc_u;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int r = lane & (kPage - 1);
+  float fm[G], fil[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    fm[h] = fin_m[h];
+    fil[h] = fin_il[h];
+  }
+  // slot of row j of this lane, or -1
+  auto slot_of = [&](int j) -> int {
+    const int i = (lane >> 4) + 4 * j;
+    if (i >= n_my) return -1;
+    const int s = (rbeg + wr + 4 * i) * kPage + r;
+    return s < g.Lp ? s : -1;
+  };
+  // pos / unew hold the fetched positions and old scores; the scores become the new ones
+  uint32_t live = 0;
+#pragma unroll
+  for (int j = 0; j < KW; ++j) {
+    const int s = slot_of(j);
+    if (s >= 0) {
+      live |= 1u << j;
+      const int gi = s >> 4;
+      unew[j] += slot_weight_from<G>(wsrc, lds_vp[gi], r, fm, fil);
+      p.score_pool[(size_t)lds_phys[gi] * kPage + r] = unew[j];
+    }
+  }
+  const int w = min(p.recent, p.budget);
+  int32_t pmax = INT32_MIN;
+#pragma unroll
+  for (int j = 0; j < KW; ++j)
+    if ((live >> j) & 1) pmax = max(pmax, pos[j]);
+  pmax = block_reduce<NT>(pmax, red_i, [](int x, int y) { return x > y ? x : y; });
+  const int64_t lo = (int64_t)pmax - w;  // the window is the positions above lo when contiguous
+  int cnt = 0;
+#pragma unroll
+  for (int j = 0; j < KW; ++j) cnt += (((live >> j) & 1) && (int64_t)pos[j] > lo) ? 1 : 0;
+  cnt = block_reduce<NT>(cnt, red_i, [](int x, int y) { return x + y; });
+  if (cnt != w) {  // scores are updated; the general path evicts
+    evict_in_epilogue<NT, D>(p, g, sc);
+    return;
+  }
+  unsigned long long best = ~0ull;
+#pragma unroll
+  for (int j = 0; j < KW; ++j) {
+    if (((live >> j) & 1) && (int64_t)pos[j] <= lo) {
+      const unsigned long long key = ((unsigned long long)float_key(unew[j]) << 32) |
+                                     (unsigned long long)(0xFFFFFFFFu - pos_order(pos[j]));
+      best = key < best ? key : best;
+    }
+  }
+  const unsigned long long kmin =
+      block_reduce<NT>(best, red_k, [](unsigned long long x, unsigned long long y) { return x < y ? x : y; });
+  const int mover = g.Lp - 1;
+#pragma unroll
+  for (int j = 0; j < KW; ++j) {
+    if (!((live >> j) & 1)) continue;
+    const int s = slot_of(j);
+    if ((int64_t)pos[j] <= lo) {
+      const unsigned long long key = ((unsigned long long)float_key(unew[j]) << 32) |
+                                     (unsigned long long)(0xFFFFFFFFu - pos_order(pos[j]));
+      if (key == kmin) bc[0] = s;  // keys are distinct
+    }
+    if (s == mover) {
+      bc[1] = pos[j];
+      bc_u = unew[j];
+    }
+  }
+  __syncthreads();
+  const int victim = bc[0];
+  if (victim != mover) {
+    const int pv = lds_phys[victim >> 4], pm = lds_phys[mover >> 4];
+    constexpr int R4 = D / 8;  // 16-byte chunks per row
+    const uint4* src = reinterpret_cast<const uint4*>(p.kv + (size_t)pm * (2 * kPage * D) + (mover & 15) * D);
+    uint4* dst = reinterpret_cast<uint4*>(const_cast<uint16_t*>(p.kv) + (size_t)pv * (2 * kPage * D) +
+                                          (victim & 15) * D);
+    if (tid < 2 * R4) {
+      const int part = tid / R4, c = tid - part * R4;  // part 0: key row, 1: value row
+      dst[part * kPage * R4 + c] = src[part * kPage * R4 + c];
+    }
+    if (tid == 0) {
+      p.pos_pool[(size_t)pv * kPage + (victim & 15)] = bc[1];
+      p.score_pool[(size_t)pv * kPage + (victim & 15)] = bc_u;
+    }
+  }
+  if (tid == 0) {
+    p.lengths[g.unit] = p.budget;
+    const int f0 = (p.budget + kPage - 1) / kPage;
+    const int nf = (g.Lp + kPage - 1) / kPage - f0;
+    if (p.freed_pages != nullptr && nf > 0) p.freed_pages[(size_t)g.unit * p.freed_stride] = lds_phys[f0];
+    if (p.freed_count != nullptr) p.freed_count[g.unit] = nf;
+  }
+}
+
+// The same for units too long for finish_steady's per-wavefront rows: thread
+// t handles slots t + k * NT, loaded here (branch-free, in groups).  lds_bt:
+// the unit's page table staged in LDS, in page order.
+template <int NT, int G, int D>
+__device__ __forceinline__ void finish_steady_strided(const AttendParams& p, const UnitGeom& g, const float* fin_m,
                                               const float* fin_il, const int* lds_bt, const WeightSrc& wsrc,
                                               const EvictScratch<NT>& sc) {
   constexpr int KMAX = kMaxBudget / NT;  // slots per thread kept in registers
@@ -363,33 +477,29 @@ __device__ __forceinline__ void accumulate_unit(const AttendParams& p, const Uni
   }
 }
 
-// lds_bt: the unit's whole page table staged in LDS in page order with every
-// page valid, or null (the steady eviction is fused only then).
+// The score update and, with se_decode_step_h2o, the general eviction of a
+// unit, after its final (m, 1/l) per head are in fin_m / fin_il.  The weights
+// come from the work-group's LDS buffer (lds_w, lds_mr) or, when null, from the
+// workspace.
 template <int NT, int G, int D, bool kCanEvict>
 __device__ __forceinline__ void finish_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
-                            const float* fin_il, const int* lds_bt, const float* lds_w,
-                            const float* lds_mr, const EvictScratch<NT>* scp) {
+                            const float* fin_il, const float* lds_w, const float* lds_mr,
+                            const EvictScratch<NT>* scp) {
   const int tid = threadIdx.x;
   const size_t ubase_p = (size_t)g.unit * p.n_visit_max;
   const WeightSrc wsrc = lds_w != nullptr ? WeightSrc{lds_w, lds_mr}
                                           : WeightSrc{p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G};
-  const bool fuse = kCanEvict && p.evict && !g.quest && p.accumulate && g.Lp == p.budget + 1 &&
-                    g.Lp <= kMaxBudget && lds_bt != nullptr;  // at most kMaxBudget slots in registers
-  if (!fuse) {
-    if (p.accumulate) accumulate_unit<NT, G>(p, g, fin_m, fin_il, wsrc);
-    if constexpr (kCanEvict) {
-      if (p.evict && !g.quest && g.Lp > p.budget) {
-        evict_in_epilogue<NT, D>(p, g, *scp);  // sets the length and the freed pages
-        return;
-      }
+  if (p.accumulate) accumulate_unit<NT, G>(p, g, fin_m, fin_il, wsrc);
+  if constexpr (kCanEvict) {
+    if (p.evict && !g.quest && g.Lp > p.budget) {
+      evict_in_epilogue<NT, D>(p, g, *scp);  // sets the length and the freed pages
+      return;
     }
-    if (tid == 0) {
-      if (g.append) p.lengths[g.unit] = g.Lp;
-      if (kCanEvict && p.evict && p.freed_count != nullptr) p.freed_count[g.unit] = 0;
-    }
-    return;
   }
-  if constexpr (kCanEvict) finish_steady<NT, G, D>(p, g, fin_m, fin_il, lds_bt, wsrc, *scp);
+  if (tid == 0) {
+    if (g.append) p.lengths[g.unit] = g.Lp;
+    if (kCanEvict && p.evict && p.freed_count != nullptr) p.freed_count[g.unit] = 0;
+  }
 }
 
 // Per-page coordinates a wavefront needs before it loads the page.
@@ -600,7 +710,12 @@ __device__ __forceinline__ void pv_page(const Lanes<D>& ln, const uint32_t (&vb)
   wave_lds_sync();
 }
 
-template <int D, int G>
+// kWaveRows: the fused steady eviction keeps each wavefront's own slots
+// (finish_steady; units of at most kWaveRowsPages pages), else thread-strided
+// slots (finish_steady_strided).  Two instantiations, chosen on the host from
+// the step's length bound, since carrying both paths costs the shorter one
+// registers.
+template <int D, int G, bool kWaveRows>
 __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const AttendParams p) {
   constexpr int NW = kAttendThreads / kWave;  // wavefronts per work-group
   using LN = Lanes<D>;
@@ -813,6 +928,24 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
     }
   }
 
+  // ---- the fused steady eviction: this wavefront's slots' positions and old
+  // scores are fetched now (every load in flight together; rows past the end
+  // re-read a valid slot), while other wavefronts may still be streaming
+  const bool steady_any = p.evict && p.accumulate && !quest && !bad && p.n_split == 1 && Lp == p.budget + 1 &&
+                          Lp <= kMaxBudget && n_grp == g.n_visit;
+  const bool steady = kWaveRows && steady_any && (n_r0 + 3) / 4 <= 4 * kSteadyRows;
+  int32_t spos[kSteadyRows];
+  float su[kSteadyRows];
+  if (kWaveRows && steady && n_my > 0) {
+#pragma unroll
+    for (int j = 0; j < kSteadyRows; ++j) {
+      const int i = min((lane >> 4) + 4 * j, n_my - 1);
+      const size_t a = (size_t)lds_phys[rbeg + wr + 4 * i] * kPage + (lane & (kPage - 1));
+      spos[j] = p.pos_pool[a];
+      su[j] = p.score_pool[a];
+    }
+  }
+
   // ---- per-wavefront totals into LDS
   float lsum = ws.l_own;  // lanes of one head differ in lane bits 2..5
   lsum += shfl_xor_f(lsum, 4);
@@ -880,11 +1013,18 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
     if (tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_LENGTH);
     return;
   }
-  // the staged table is the unit's whole page table when one work-group reads
-  // every page and none was invalid
-  const bool whole_table = !quest && single && n_grp == g.n_visit;
-  finish_unit<kAttendThreads, G, D, true>(p, g, fin_m, fin_il, whole_table ? lds_phys : nullptr,
-                                          wl ? lds_w : nullptr, lds_mr, &esc);
+  if (kWaveRows && steady) {
+    const WeightSrc wsrc = wl ? WeightSrc{lds_w, lds_mr}
+                              : WeightSrc{p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G};
+    finish_steady<kAttendThreads, G, D>(p, g, fin_m, fin_il, lds_phys, lds_vp, wsrc, spos, su, rbeg, wr, n_my,
+                                        esc);
+  } else if (!kWaveRows && steady_any) {
+    const WeightSrc wsrc = wl ? WeightSrc{lds_w, lds_mr}
+                              : WeightSrc{p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G};
+    finish_steady_strided<kAttendThreads, G, D>(p, g, fin_m, fin_il, lds_phys, wsrc, esc);
+  } else {
+    finish_unit<kAttendThreads, G, D, true>(p, g, fin_m, fin_il, wl ? lds_w : nullptr, lds_mr, &esc);
+  }
 }
 
 // Second pass when a unit is split over several work-groups: combines the
@@ -923,15 +1063,23 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(const A
     }
   }
   __syncthreads();
-  finish_unit<kCombineThreads, G, D, false>(p, g, fin_m, fin_il, nullptr, nullptr, nullptr, nullptr);
+  finish_unit<kCombineThreads, G, D, false>(p, g, fin_m, fin_il, nullptr, nullptr, nullptr);
 }
 
 // With a split, the combine pass updates the scores and publishes the appended
 // length; the eviction (if asked for) then runs as its own kernel, whose
 // 1024-thread work-groups hold a whole long unit in registers.
+// Units of at most this many pages take the per-wavefront steady eviction: the
+// first slot rank's share of them, over four wavefronts, fits kSteadyRows rows
+// of four pages.
+constexpr int kWaveRowsPages = (4 * 4 * kSteadyRows * 100 - 50) / kRankWeight[0];
+
 template <int D, int G>
 static void launch_attend(const AttendParams& prm, int grid, hipStream_t stream) {
-  hipLaunchKernelGGL((decode_attend_kernel<D, G>), dim3(grid), dim3(kAttendThreads), 0, stream, prm);
+  if (prm.n_visit_max <= kWaveRowsPages)
+    hipLaunchKernelGGL((decode_attend_kernel<D, G, true>), dim3(grid), dim3(kAttendThreads), 0, stream, prm);
+  else
+    hipLaunchKernelGGL((decode_attend_kernel<D, G, false>), dim3(grid), dim3(kAttendThreads), 0, stream, prm);
   if (prm.n_split > 1) {
     AttendParams cp = prm;
     cp.evict = 0;
