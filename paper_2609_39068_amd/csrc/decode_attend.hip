@@ -826,40 +826,7 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
   if (bad_sel) set_error(p.dev_err, SE_DEVERR_BAD_SELECTION);
   if (bad_page) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
 
-  // ---- append: the work-group whose range holds the new token's page writes
-  // its row into the pool first; no other work-group reads that page
-  const int new_vp = quest ? p.top_k : cur_page;
-  const bool mine_new = append && !bad && new_vp >= vbeg && new_vp < vend;
-  if (mine_new) {
-    const int ph = p.block_table[(size_t)unit * p.max_pages + cur_page];
-    const int rn = L - cur_page * kPage;
-    if (ph >= 0 && (int64_t)ph < p.num_pages) {
-      uint16_t* kdst = const_cast<uint16_t*>(p.kv) + (size_t)ph * (2 * kPage * D) + rn * D;
-      uint16_t* vdst = kdst + kPage * D;
-      if (tid < D / 8) {
-        reinterpret_cast<uint4*>(kdst)[tid] = reinterpret_cast<const uint4*>(knew_row)[tid];
-        reinterpret_cast<uint4*>(vdst)[tid] = reinterpret_cast<const uint4*>(vnew_row)[tid];
-      }
-      if (p.meta_pool != nullptr && tid < D) {
-        uint16_t* mn = p.meta_pool + (size_t)ph * 2 * D;
-        uint16_t* mx = mn + D;
-        const uint16_t kb = knew_row[tid];
-        if (rn == 0) {
-          mn[tid] = kb;
-          mx[tid] = kb;
-        } else {
-          const float kf = bf16f(kb);
-          if (kf < bf16f(mn[tid])) mn[tid] = kb;
-          if (kf > bf16f(mx[tid])) mx[tid] = kb;
-        }
-      }
-      if (tid == 0) {
-        p.pos_pool[(size_t)ph * kPage + rn] = p.new_pos[req];
-        if (p.score_pool != nullptr) p.score_pool[(size_t)ph * kPage + rn] = 0.f;
-      }
-    }
-  }
-  __syncthreads();
+  __syncthreads();  // the staged tables
 
   // Pages of this wavefront: the staged entries of its slot rank (a contiguous
   // share of the list, sized by kRankWeight), interleaved over the rank's four
@@ -870,6 +837,52 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
   const int rbeg = srank ? n_r0 : 0;
   const int rcnt = srank ? n_grp - n_r0 : n_r0;
   const int n_my = wr < rcnt ? (rcnt - wr + 3) / 4 : 0;
+
+  // ---- append: the new token's page is the last one visited (the last staged
+  // entry, when it is valid); the wavefront that streams it writes the row into
+  // the pool before its first load and waits for its stores, so no other
+  // wavefront waits for the append.  Nothing else reads that page in this pass
+  // except the epilogue, which comes after a barrier.
+  {
+    const int new_vp = quest ? p.top_k : cur_page;
+    const int gl = n_grp - 1;
+    const bool mine_new = append && !bad && new_vp >= vbeg && new_vp < vend && gl >= 0 && lds_vp[gl] == new_vp;
+    const int owner_rank = gl >= n_r0 ? 1 : 0;
+    const int owner_wr = (gl - (owner_rank ? n_r0 : 0)) & 3;
+    if (mine_new && srank == owner_rank && wr == owner_wr) {
+      const int ph = lds_phys[gl];
+      const int rn = L - cur_page * kPage;
+      uint16_t* kdst = const_cast<uint16_t*>(p.kv) + (size_t)ph * (2 * kPage * D) + rn * D;
+      uint16_t* vdst = kdst + kPage * D;
+      constexpr int R4 = D / 8;  // 16-byte chunks per row
+      if (lane < 2 * R4) {
+        const uint4* src = reinterpret_cast<const uint4*>(lane < R4 ? knew_row : vnew_row);
+        uint4* dst = reinterpret_cast<uint4*>(lane < R4 ? kdst : vdst);
+        dst[lane % R4] = src[lane % R4];
+      }
+      if (p.meta_pool != nullptr) {
+        uint16_t* mn = p.meta_pool + (size_t)ph * 2 * D;
+        uint16_t* mx = mn + D;
+        for (int c = lane; c < D; c += kWave) {
+          const uint16_t kb = knew_row[c];
+          if (rn == 0) {
+            mn[c] = kb;
+            mx[c] = kb;
+          } else {
+            const float kf = bf16f(kb);
+            if (kf < bf16f(mn[c])) mn[c] = kb;
+            if (kf > bf16f(mx[c])) mx[c] = kb;
+          }
+        }
+      }
+      if (lane == 0) {
+        p.pos_pool[(size_t)ph * kPage + rn] = p.new_pos[req];
+        if (p.score_pool != nullptr) p.score_pool[(size_t)ph * kPage + rn] = 0.f;
+      }
+      __builtin_amdgcn_s_waitcnt(0);  // the stores are done before this wavefront reads the page
+    }
+  }
+
   auto page_ref = [&](int i) -> PageRef {
     PageRef pr;
     const int gi = rbeg + wr + 4 * i;
