@@ -14,6 +14,11 @@
 //   * top-k: one work-group per unit, radix selection on order-preserving
 //     integer keys of the scores; equal scores keep the lower page index; the
 //     selected pages are written in ascending order by a block scan.
+// With at least one unit per compute unit (and at most kFusedMaxPages
+// candidates), one 1024-thread work-group per unit does both: the unit's
+// block-table row and its page scores stay in LDS, the bounds stream at the
+// compute unit's full rate, and the selection runs on the LDS scores (same
+// arithmetic and the same selection as the two kernels).
 #include <climits>
 
 #include "se_common.h"
@@ -36,6 +41,7 @@ struct QuestParams {
   float* scores;
   int32_t scores_stride;
   int32_t blocks_per_unit;
+  int32_t write_scores;  // fused kernel: also store the page scores
   int32_t* dev_err;
 };
 
@@ -221,6 +227,153 @@ __global__ __launch_bounds__(256) void quest_topk_kernel(const QuestParams p) {
   }
 }
 
+// Page bounds of one unit's candidate pages [0, n) by NT threads, 8 lanes per
+// page, into lds_sc (and the global score row when write_scores is set).  The
+// block-table row is in lds_bt (-1 for an entry outside the pool).  Every
+// iteration's loads are issued before the previous page is reduced.
+template <int NT, int D, int G>
+__device__ __forceinline__ void unit_bounds(const QuestParams& p, int unit, int n, const int* lds_bt,
+                                            float* lds_sc) {
+  constexpr int CH = D / 8;   // channels per lane
+  constexpr int CW = CH / 2;  // bf16 pairs per lane
+  constexpr int C4 = CW / 4;  // 16-byte loads per lane per row
+  constexpr int SLOTS = NT / 8;
+  const int lane = threadIdx.x & 63;
+  const int g = lane & 7;
+  const int slot = threadIdx.x >> 3;
+  const int req = unit / p.hkv;
+  const int kvh = unit - req * p.hkv;
+  uint32_t qp[G][CW], qn[G][CW];
+  {
+    const uint16_t* qb = p.q + ((size_t)req * p.hkv * G + (size_t)kvh * G) * D + g * CH;
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const uint4* src = reinterpret_cast<const uint4*>(qb + (size_t)h * D);
+#pragma unroll
+      for (int i = 0; i < C4; ++i) {
+        const uint4 t = src[i];
+        const uint32_t v[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          qp[h][4 * i + e] = pos_part(v[e]);
+          qn[h][4 * i + e] = neg_part(v[e]);
+        }
+      }
+    }
+  }
+  auto load = [&](int b, uint4 (&mn)[C4], uint4 (&mx)[C4]) {
+    const int ph = lds_bt[min(b, n - 1)];
+    const uint16_t* meta = p.meta_pool + (size_t)(ph < 0 ? 0 : ph) * 2 * D + g * CH;
+#pragma unroll
+    for (int i = 0; i < C4; ++i) {
+      mn[i] = reinterpret_cast<const uint4*>(meta)[i];
+      mx[i] = reinterpret_cast<const uint4*>(meta + D)[i];
+    }
+  };
+  auto bound = [&](int b, const uint4 (&mn)[C4], const uint4 (&mx)[C4]) {
+    float acc[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) acc[h] = 0.f;
+#pragma unroll
+    for (int i = 0; i < C4; ++i) {
+      const uint32_t lo[4] = {mn[i].x, mn[i].y, mn[i].z, mn[i].w};
+      const uint32_t hi[4] = {mx[i].x, mx[i].y, mx[i].z, mx[i].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+          acc[h] = dot2bf16(qp[h][4 * i + e], hi[e], acc[h]);
+          acc[h] = dot2bf16(qn[h][4 * i + e], lo[e], acc[h]);
+        }
+      }
+    }
+    float best = -INFINITY;
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      float a = quad_sum(acc[h]);
+      a += shfl_xor_f(a, 4);
+      best = fmaxf(best, a);
+    }
+    if (b < n && g == 0) {
+      const float sc = lds_bt[b] >= 0 ? best * p.scale : -INFINITY;
+      lds_sc[b] = sc;
+      if (p.write_scores) p.scores[(size_t)unit * p.scores_stride + b] = sc;
+    }
+  };
+  const int iters = (n + SLOTS - 1) / SLOTS;
+  uint4 mnA[C4], mxA[C4], mnB[C4], mxB[C4];
+  if (iters > 0) load(slot, mnA, mxA);
+  for (int it = 0; it < iters; it += 2) {
+    load(slot + (it + 1) * SLOTS, mnB, mxB);
+    bound(slot + it * SLOTS, mnA, mxA);
+    if (it + 1 >= iters) break;
+    load(slot + (it + 2) * SLOTS, mnA, mxA);
+    bound(slot + (it + 1) * SLOTS, mnB, mxB);
+  }
+}
+
+constexpr int kFusedThreads = 1024;
+constexpr int kFusedMaxPages = 8192;
+constexpr int kFusedMinUnits = 256;  // one work-group per unit fills the compute units
+
+template <int D, int G>
+__global__ __launch_bounds__(kFusedThreads) void quest_select_fused_kernel(const QuestParams p) {
+  constexpr int NT = kFusedThreads;
+  __shared__ int lds_bt[kFusedMaxPages];
+  __shared__ float lds_sc[kFusedMaxPages];
+  __shared__ unsigned hist[256];
+  __shared__ int scan_scratch[NT / kWave + 1];
+  __shared__ int bcast[4];
+  const int tid = threadIdx.x;
+  const int unit = blockIdx.x;
+  const int L = p.lengths[unit];
+  int32_t* out = p.sel + (size_t)unit * p.top_k;
+  if (!unit_length_ok(p, L) || L / kPage > kFusedMaxPages) {
+    if (tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_LENGTH);
+    for (int i = tid; i < p.top_k; i += NT) out[i] = -1;
+    return;
+  }
+  const int n = L / kPage;
+  int bad = 0;
+  for (int i = tid; i < n; i += NT) {
+    int ph = p.block_table[(size_t)unit * p.max_pages + i];
+    if (ph < 0 || (int64_t)ph >= p.num_pages) {
+      bad = 1;
+      ph = -1;
+    }
+    lds_bt[i] = ph;
+  }
+  if (bad) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
+  __syncthreads();
+  unit_bounds<NT, D, G>(p, unit, n, lds_bt, lds_sc);
+  __syncthreads();
+  if (n <= p.top_k) {
+    for (int i = tid; i < p.top_k; i += NT) out[i] = i < n ? i : -1;
+    return;
+  }
+  auto key_of = [&](int b) { return float_key(lds_sc[b]); };
+  uint32_t prefix, mask;
+  int k_rest;
+  radix_select_top<NT, uint32_t>(n, p.top_k, key_of, [](int) { return true; }, &prefix, &mask, &k_rest, hist,
+                                 scan_scratch, bcast);
+  // keys above the threshold class, then the first k_rest of the class in index order
+  int eq_base = 0, out_base = 0;
+  for (int b0 = 0; b0 < n; b0 += NT) {
+    const int b = b0 + tid;
+    uint32_t km = 0;
+    if (b < n) km = key_of(b) & mask;
+    const int is_eq = (b < n && km == prefix) ? 1 : 0;
+    int eq_total;
+    const int eq_rank = block_exclusive_scan<NT>(is_eq, scan_scratch, &eq_total);
+    const int take = (b < n) && (km > prefix || (is_eq && eq_base + eq_rank < k_rest)) ? 1 : 0;
+    int take_total;
+    const int rank = block_exclusive_scan<NT>(take, scan_scratch, &take_total);
+    if (take) out[out_base + rank] = b;
+    eq_base += eq_total;
+    out_base += take_total;
+  }
+}
+
 }  // namespace se
 
 using namespace se;
@@ -303,6 +456,21 @@ extern "C" se_status se_quest_select(const se_kv_view* kv, int32_t q_per_kv, con
   if (!given) {
     int64_t ml = max_len;
     if (ml > (int64_t)kv->max_pages * kPage) ml = (int64_t)kv->max_pages * kPage;
+    if (kv->num_units >= kFusedMinUnits && ml / kPage <= kFusedMaxPages) {
+      prm.write_scores = page_scores != nullptr ? 1 : 0;
+      const int D = kv->head_dim;
+      const dim3 grid(kv->num_units), block(kFusedThreads);
+      if (D == 128) {
+        if (q_per_kv == 4) hipLaunchKernelGGL((quest_select_fused_kernel<128, 4>), grid, block, 0, stream, prm);
+        else if (q_per_kv == 2) hipLaunchKernelGGL((quest_select_fused_kernel<128, 2>), grid, block, 0, stream, prm);
+        else hipLaunchKernelGGL((quest_select_fused_kernel<128, 1>), grid, block, 0, stream, prm);
+      } else {
+        if (q_per_kv == 4) hipLaunchKernelGGL((quest_select_fused_kernel<64, 4>), grid, block, 0, stream, prm);
+        else if (q_per_kv == 2) hipLaunchKernelGGL((quest_select_fused_kernel<64, 2>), grid, block, 0, stream, prm);
+        else hipLaunchKernelGGL((quest_select_fused_kernel<64, 1>), grid, block, 0, stream, prm);
+      }
+      return launch_status();
+    }
     prm.blocks_per_unit = (int)ceil_div(ml / kPage > 0 ? ml / kPage : 1, kBoundPagesPerGroup);
     const int64_t grid = (int64_t)kv->num_units * prm.blocks_per_unit;
     if (grid > INT32_MAX) return SE_ERR_UNSUPPORTED;

@@ -176,3 +176,43 @@ def test_select_from_given_scores_bitexact(se, n_pages, top_k, levels):
         got = sel[u].cpu().numpy()
         assert got[:len(want)].tolist() == want.tolist()
         assert (got[len(want):] == -1).all()
+
+
+def test_fused_select_matches_two_pass(se):
+    # 256 units take the one-kernel selection (bounds and top-k in one work-group
+    # per unit); the first 16 units alone take the bound + top-k kernels.  Page
+    # scores and selections agree bit for bit, and the fused selection equals
+    # the top-k kernel's selection from the fused scores.
+    w = scaled(CONFIGS[2], ctx=3001, steps=1)
+    host = build_state(w, "cpu")
+    steps = build_steps(w, host, "cpu", steps=1)
+    gs = to_device(host, DEV)
+    view = _view(se, gs)
+    U, G, P = w.units_per_layer, w.q_per_kv, host.max_pages
+    assert U >= 256
+    max_len = P * 16
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    se.se_quest_summarize(view, max_len, err)
+    q = steps.q[0, 0].to(DEV)
+    sel_f = torch.full((U, w.top_k), -5, dtype=torch.int32, device=DEV)
+    sc_f = torch.full((U, P), float("nan"), dtype=torch.float32, device=DEV)
+    se.se_quest_select(view, G, q, w.scale, w.top_k, max_len, 0, sel_f, sc_f, P, None, err)
+    n_sub = 16
+    sub = se.KVView(gs.kv_pool, gs.pos_pool, gs.score_pool, gs.meta_pool, gs.block_table[:n_sub],
+                    gs.lengths[:n_sub], num_kv_heads=w.hkv)
+    sel_2 = torch.full((n_sub, w.top_k), -5, dtype=torch.int32, device=DEV)
+    sc_2 = torch.full((n_sub, P), float("nan"), dtype=torch.float32, device=DEV)
+    se.se_quest_select(sub, G, q[:n_sub // w.hkv].contiguous(), w.scale, w.top_k, max_len, 0, sel_2, sc_2, P,
+                       None, err)
+    sel_g = torch.full((U, w.top_k), -5, dtype=torch.int32, device=DEV)
+    se.se_quest_select(view, G, None, w.scale, w.top_k, max_len, se.SE_QUEST_SCORES_GIVEN, sel_g, sc_f, P,
+                       None, err)
+    torch.cuda.synchronize()
+    assert se.se_read_device_errors(err) == 0
+    lengths = gs.lengths.cpu().numpy()
+    for u in range(n_sub):
+        n = int(lengths[u]) // 16
+        assert torch.equal(sc_f[u, :n].view(torch.int32), sc_2[u, :n].view(torch.int32)), f"unit {u}"
+    assert torch.equal(sel_f[:n_sub], sel_2)
+    assert torch.equal(sel_f, sel_g)
+    assert (sel_f >= 0).all()
