@@ -504,15 +504,29 @@ __device__ __forceinline__ void finish_unit(const AttendParams& p, const UnitGeo
 
 // Per-page coordinates a wavefront needs before it loads the page.
 constexpr int kMaxGroupPages = 1024;  // pages one work-group streams at most
-constexpr int kAttendThreads = 512;   // eight wavefronts; two work-groups per compute unit
+// Work-group sizes: 512 threads (eight wavefronts, two work-groups per compute
+// unit, the default) or 1024 (sixteen, one per compute unit) when the launch
+// has at most one work-group per compute unit anyway: a unit then needs no
+// split (and no combine pass).
+constexpr int kAttendThreads = 512;
+constexpr int kAttendThreadsWide = 1024;
 
 // Share of a work-group's pages per wavefront slot rank, in percent.  Wavefront
-// w runs on SIMD w % 4 in the work-group's slot w / 4; with equal shares the
-// second slot's wavefronts end ~15 % after the first's (memory requests of the
-// older wavefront are served first), so the first slot takes more pages.  A
-// page's wavefront depends only on its index: the results do not depend on
-// timing.
-constexpr int kRankWeight[2] = {58, 42};
+// w runs on SIMD w % 4 in slot w / 4; with equal shares a slot's wavefronts end
+// after those of the slots before it (memory requests of older wavefronts are
+// served first: ~15 % later for the second slot), so earlier slots take more
+// pages.  A page's wavefront depends only on its index: the results do not
+// depend on timing.
+template <int NR>
+struct RankWeights;
+template <>
+struct RankWeights<2> {
+  static constexpr int w[2] = {58, 42};
+};
+template <>
+struct RankWeights<4> {
+  static constexpr int w[4] = {34, 26, 21, 19};
+};
 
 struct PageRef {
   int vp;      // index in the unit's visit order (workspace row)
@@ -715,9 +729,9 @@ __device__ __forceinline__ void pv_page(const Lanes<D>& ln, const uint32_t (&vb)
 // slots (finish_steady_strided).  Two instantiations, chosen on the host from
 // the step's length bound, since carrying both paths costs the shorter one
 // registers.
-template <int D, int G, bool kWaveRows>
-__global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const AttendParams p) {
-  constexpr int NW = kAttendThreads / kWave;  // wavefronts per work-group
+template <int D, int G, int NT, bool kWaveRows>
+__global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams p) {
+  constexpr int NW = NT / kWave;  // wavefronts per work-group
   using LN = Lanes<D>;
   constexpr int QC = LN::QC, QW = LN::QW, K4 = LN::K4, RS = LN::RS, RPL = LN::RPL, HP = LN::HP;
 
@@ -733,8 +747,8 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
   __shared__ uint32_t lds_q[G][D / 2];  // the unit's G query rows (bf16 pairs)
   __shared__ float lds_w[kWeightCap];    // per-slot weights, then the eviction's holes
   __shared__ float lds_mr[kWeightCap / kPage];
-  SE_EVICT_SCRATCH_WITH_HOLES(kAttendThreads, esc, reinterpret_cast<int*>(lds_w));
-  __shared__ int lds_scan[kAttendThreads / kWave + 1];
+  SE_EVICT_SCRATCH_WITH_HOLES(NT, esc, reinterpret_cast<int*>(lds_w));
+  __shared__ int lds_scan[NT / kWave + 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -791,7 +805,7 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
   const int n_range = max(0, vend - vbeg);
   bool bad_sel = false, bad_page = false;
   int n_grp = 0;
-  for (int i0 = 0; i0 < n_range; i0 += kAttendThreads) {
+  for (int i0 = 0; i0 < n_range; i0 += NT) {
     const int i = i0 + tid;
     const int vp = vbeg + i;
     int lp = vp;
@@ -815,7 +829,7 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
       }
     }
     int total;
-    const int rank = block_exclusive_scan<kAttendThreads>(ph >= 0 ? 1 : 0, lds_scan, &total);
+    const int rank = block_exclusive_scan<NT>(ph >= 0 ? 1 : 0, lds_scan, &total);
     if (ph >= 0) {
       lds_phys[n_grp + rank] = ph;
       lds_lp[n_grp + rank] = lp;
@@ -831,11 +845,29 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
   // Pages of this wavefront: the staged entries of its slot rank (a contiguous
   // share of the list, sized by kRankWeight), interleaved over the rank's four
   // wavefronts.
-  static_assert(NW == 8, "two slot ranks of four wavefronts");
+  constexpr int NR = NW / 4;  // slot ranks
+  static_assert(NW % 4 == 0, "four SIMDs");
   const int srank = wave >> 2, wr = wave & 3;
-  const int n_r0 = (n_grp * kRankWeight[0] + 50) / 100;
-  const int rbeg = srank ? n_r0 : 0;
-  const int rcnt = srank ? n_grp - n_r0 : n_r0;
+  const int gl = n_grp - 1;  // the last staged entry
+  int rbeg = 0, rcnt = 0, max_rcnt = 0, owner_rank = 0, owner_beg = 0;
+  {
+    int cum = 0, b = 0;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      cum += RankWeights<NR>::w[r];
+      const int e = (n_grp * cum + 50) / 100;
+      if (r == srank) {
+        rbeg = b;
+        rcnt = e - b;
+      }
+      if (gl >= b && gl < e) {
+        owner_rank = r;
+        owner_beg = b;
+      }
+      max_rcnt = max(max_rcnt, e - b);
+      b = e;
+    }
+  }
   const int n_my = wr < rcnt ? (rcnt - wr + 3) / 4 : 0;
 
   // ---- append: the new token's page is the last one visited (the last staged
@@ -845,10 +877,8 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
   // except the epilogue, which comes after a barrier.
   {
     const int new_vp = quest ? p.top_k : cur_page;
-    const int gl = n_grp - 1;
     const bool mine_new = append && !bad && new_vp >= vbeg && new_vp < vend && gl >= 0 && lds_vp[gl] == new_vp;
-    const int owner_rank = gl >= n_r0 ? 1 : 0;
-    const int owner_wr = (gl - (owner_rank ? n_r0 : 0)) & 3;
+    const int owner_wr = (gl - owner_beg) & 3;
     if (mine_new && srank == owner_rank && wr == owner_wr) {
       const int ph = lds_phys[gl];
       const int rn = L - cur_page * kPage;
@@ -946,7 +976,7 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
   // re-read a valid slot), while other wavefronts may still be streaming
   const bool steady_any = p.evict && p.accumulate && !quest && !bad && p.n_split == 1 && Lp == p.budget + 1 &&
                           Lp <= kMaxBudget && n_grp == g.n_visit;
-  const bool steady = kWaveRows && steady_any && (n_r0 + 3) / 4 <= 4 * kSteadyRows;
+  const bool steady = kWaveRows && steady_any && (max_rcnt + 3) / 4 <= 4 * kSteadyRows;
   int32_t spos[kSteadyRows];
   float su[kSteadyRows];
   if (kWaveRows && steady && n_my > 0) {
@@ -988,7 +1018,7 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
   // ---- work-group partial (fixed wavefront order)
   const bool single = p.n_split == 1;
   float* part_u = p.part + (size_t)unit * p.n_split * G * (D + 2);
-  for (int idx = tid; idx < G * D; idx += kAttendThreads) {
+  for (int idx = tid; idx < G * D; idx += NT) {
     const int h = idx / D;
     const int c = idx - h * D;
     float ms = lds_m[0][h];
@@ -1029,14 +1059,14 @@ __global__ __launch_bounds__(kAttendThreads, 4) void decode_attend_kernel(const 
   if (kWaveRows && steady) {
     const WeightSrc wsrc = wl ? WeightSrc{lds_w, lds_mr}
                               : WeightSrc{p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G};
-    finish_steady<kAttendThreads, G, D>(p, g, fin_m, fin_il, lds_phys, lds_vp, wsrc, spos, su, rbeg, wr, n_my,
+    finish_steady<NT, G, D>(p, g, fin_m, fin_il, lds_phys, lds_vp, wsrc, spos, su, rbeg, wr, n_my,
                                         esc);
   } else if (!kWaveRows && steady_any) {
     const WeightSrc wsrc = wl ? WeightSrc{lds_w, lds_mr}
                               : WeightSrc{p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G};
-    finish_steady_strided<kAttendThreads, G, D>(p, g, fin_m, fin_il, lds_phys, wsrc, esc);
+    finish_steady_strided<NT, G, D>(p, g, fin_m, fin_il, lds_phys, wsrc, esc);
   } else {
-    finish_unit<kAttendThreads, G, D, true>(p, g, fin_m, fin_il, wl ? lds_w : nullptr, lds_mr, &esc);
+    finish_unit<NT, G, D, true>(p, g, fin_m, fin_il, wl ? lds_w : nullptr, lds_mr, &esc);
   }
 }
 
@@ -1083,16 +1113,32 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(const A
 // length; the eviction (if asked for) then runs as its own kernel, whose
 // 1024-thread work-groups hold a whole long unit in registers.
 // Units of at most this many pages take the per-wavefront steady eviction: the
-// first slot rank's share of them, over four wavefronts, fits kSteadyRows rows
-// of four pages.
-constexpr int kWaveRowsPages = (4 * 4 * kSteadyRows * 100 - 50) / kRankWeight[0];
+// largest slot rank's share of them, over four wavefronts, fits kSteadyRows
+// rows of four pages.
+template <int NT>
+constexpr int wave_rows_pages() {
+  return (4 * 4 * kSteadyRows * 100 - 50) / RankWeights<NT / kWave / 4>::w[0];
+}
+
+// Launches with at most one work-group per compute unit take 1024 threads.
+inline bool attend_wide(int num_units, int n_visit) {
+  return (int64_t)num_units * ceil_div(n_visit, kMaxGroupPages) <= 256;
+}
+
+template <int D, int G, int NT>
+static void launch_attend_nt(const AttendParams& prm, int grid, hipStream_t stream) {
+  if (prm.n_visit_max <= wave_rows_pages<NT>())
+    hipLaunchKernelGGL((decode_attend_kernel<D, G, NT, true>), dim3(grid), dim3(NT), 0, stream, prm);
+  else
+    hipLaunchKernelGGL((decode_attend_kernel<D, G, NT, false>), dim3(grid), dim3(NT), 0, stream, prm);
+}
 
 template <int D, int G>
-static void launch_attend(const AttendParams& prm, int grid, hipStream_t stream) {
-  if (prm.n_visit_max <= kWaveRowsPages)
-    hipLaunchKernelGGL((decode_attend_kernel<D, G, true>), dim3(grid), dim3(kAttendThreads), 0, stream, prm);
+static void launch_attend(const AttendParams& prm, int grid, bool wide, hipStream_t stream) {
+  if (wide)
+    launch_attend_nt<D, G, kAttendThreadsWide>(prm, grid, stream);
   else
-    hipLaunchKernelGGL((decode_attend_kernel<D, G, false>), dim3(grid), dim3(kAttendThreads), 0, stream, prm);
+    launch_attend_nt<D, G, kAttendThreads>(prm, grid, stream);
   if (prm.n_split > 1) {
     AttendParams cp = prm;
     cp.evict = 0;
@@ -1166,7 +1212,9 @@ static se_status attend_launch(const se_kv_view* kv, int32_t q_per_kv, const voi
   if (!(scale > 0.f)) return SE_ERR_INVALID_ARGUMENT;
 
   const int D = kv->head_dim;
-  const SplitShape s = split_shape(kv->num_units, attend_n_visit(max_len, kv->max_pages, top_k));
+  const int n_visit = attend_n_visit(max_len, kv->max_pages, top_k);
+  const bool wide = attend_wide(kv->num_units, n_visit);
+  const SplitShape s = split_shape(kv->num_units, n_visit, wide ? 256 : 512);
   const AttendWs lay = attend_ws_layout(kv->num_units, s, q_per_kv, D);
   if (ws == nullptr || ws_bytes < lay.total) return SE_ERR_WORKSPACE;
 
@@ -1207,13 +1255,13 @@ static se_status attend_launch(const se_kv_view* kv, int32_t q_per_kv, const voi
   const int64_t grid = (int64_t)kv->num_units * s.n_split;
   if (grid > INT32_MAX) return SE_ERR_UNSUPPORTED;
   if (D == 128) {
-    if (q_per_kv == 4) launch_attend<128, 4>(prm, (int)grid, stream);
-    else if (q_per_kv == 2) launch_attend<128, 2>(prm, (int)grid, stream);
-    else launch_attend<128, 1>(prm, (int)grid, stream);
+    if (q_per_kv == 4) launch_attend<128, 4>(prm, (int)grid, wide, stream);
+    else if (q_per_kv == 2) launch_attend<128, 2>(prm, (int)grid, wide, stream);
+    else launch_attend<128, 1>(prm, (int)grid, wide, stream);
   } else {
-    if (q_per_kv == 4) launch_attend<64, 4>(prm, (int)grid, stream);
-    else if (q_per_kv == 2) launch_attend<64, 2>(prm, (int)grid, stream);
-    else launch_attend<64, 1>(prm, (int)grid, stream);
+    if (q_per_kv == 4) launch_attend<64, 4>(prm, (int)grid, wide, stream);
+    else if (q_per_kv == 2) launch_attend<64, 2>(prm, (int)grid, wide, stream);
+    else launch_attend<64, 1>(prm, (int)grid, wide, stream);
   }
   return launch_status();
 }

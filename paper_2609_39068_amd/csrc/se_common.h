@@ -46,8 +46,9 @@ struct SplitShape {
   int pps;       // pages per work-group
 };
 
-inline SplitShape split_shape(int num_units, int n_visit) {
-  const int resident = 512;          // two 8-wavefront work-groups on each of 256 compute units
+// resident: work-groups that fit the chip at once (512: two 8-wavefront
+// work-groups on each of 256 compute units; 256: one 16-wavefront one).
+inline SplitShape split_shape(int num_units, int n_visit, int resident = 512) {
   const int min_pages = 16;          // at least two pages per wavefront
   const int max_group_pages = 1024;  // the page table a work-group stages in LDS
   int splits = (int)ceil_div(resident, num_units);
