@@ -138,20 +138,29 @@ template <int G>
 constexpr int kWeightPages = kWeightCap / (kPage * G);
 static_assert(kWeightCap >= kMaxBudget, "the weight buffer doubles as the holes array");
 
-// Where the score update finds the weights: the workspace rows (global) or the
-// work-group's LDS buffer.
+// Where the score update finds the weights: visit pages below `cap` in the
+// work-group's LDS buffer, the others in the workspace rows (global).
 struct WeightSrc {
-  const float* w;   // [visit page][16][G]
-  const float* mr;  // [visit page][G]
+  const float* lw;   // LDS [visit page][16][G]
+  const float* lmr;  // LDS [visit page][G]
+  const float* gw;   // workspace, same layout
+  const float* gmr;
+  int cap;
 };
 
 template <int G>
 __device__ __forceinline__ float slot_weight_from(const WeightSrc& src, int vp, int rr, const float* fin_m,
                                                   const float* fin_il) {
   float a = 0.f;
+  if (vp < src.cap) {
 #pragma unroll
-  for (int h = 0; h < G; ++h)
-    a += src.w[(vp * kPage + rr) * G + h] * fast_exp2(src.mr[vp * G + h] - fin_m[h]) * fin_il[h];
+    for (int h = 0; h < G; ++h)
+      a += src.lw[(vp * kPage + rr) * G + h] * fast_exp2(src.lmr[vp * G + h] - fin_m[h]) * fin_il[h];
+  } else {
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+      a += src.gw[(vp * kPage + rr) * G + h] * fast_exp2(src.gmr[vp * G + h] - fin_m[h]) * fin_il[h];
+  }
   return a;
 }
 
@@ -479,16 +488,15 @@ __device__ __forceinline__ void accumulate_unit(const AttendParams& p, const Uni
 
 // The score update and, with se_decode_step_h2o, the general eviction of a
 // unit, after its final (m, 1/l) per head are in fin_m / fin_il.  The weights
-// come from the work-group's LDS buffer (lds_w, lds_mr) or, when null, from the
-// workspace.
+// of visit pages below wcap come from the work-group's LDS buffer (lds_w,
+// lds_mr), the others from the workspace.
 template <int NT, int G, int D, bool kCanEvict>
 __device__ __forceinline__ void finish_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
-                            const float* fin_il, const float* lds_w, const float* lds_mr,
+                            const float* fin_il, const float* lds_w, const float* lds_mr, int wcap,
                             const EvictScratch<NT>* scp) {
   const int tid = threadIdx.x;
   const size_t ubase_p = (size_t)g.unit * p.n_visit_max;
-  const WeightSrc wsrc = lds_w != nullptr ? WeightSrc{lds_w, lds_mr}
-                                          : WeightSrc{p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G};
+  const WeightSrc wsrc{lds_w, lds_mr, p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G, wcap};
   if (p.accumulate) accumulate_unit<NT, G>(p, g, fin_m, fin_il, wsrc);
   if constexpr (kCanEvict) {
     if (p.evict && !g.quest && g.Lp > p.budget) {
@@ -664,7 +672,7 @@ template <int D, int G>
 __device__ __forceinline__ float softmax_page(const AttendParams& p, const Lanes<D>& ln,
                                               const PageRef& pr, float z, WaveSoftmax<G>& ws,
                                               float* lds_pw, int lane, int unit, size_t ubase_p,
-                                              float* lds_w, float* lds_mr, bool wl) {
+                                              float* lds_w, float* lds_mr, int wcap) {
   constexpr float kBump = 8.0f;  // rescale only when a logit beats the reference by 2^8
   const bool valid = ln.owns && ln.own_row < pr.nrows;
   const float z2 = valid ? z * p.scale_log2 : -INFINITY;
@@ -692,7 +700,7 @@ __device__ __forceinline__ float softmax_page(const AttendParams& p, const Lanes
   }
   const float pj = valid ? fast_exp2(z2 - ws.m_own) : 0.f;
   ws.l_own += pj;
-  if (wl) {
+  if (pr.vp < wcap) {
     if (ln.owns) lds_w[(pr.vp * kPage + ln.own_row) * G + ln.own_head] = pj;
     if (lane < G) lds_mr[pr.vp * G + lane] = ws.m_own;
   } else if (p.accumulate) {
@@ -762,8 +770,9 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   const int vbeg = split * p.pps;
   const int vend = min(vbeg + p.pps, g.n_visit);
   const size_t ubase_p = (size_t)unit * p.n_visit_max;  // page-indexed workspace rows
-  // the score update's weights stay in LDS when this work-group holds the whole unit
-  const bool wl = p.accumulate && p.n_split == 1 && g.n_visit <= kWeightPages<G>;
+  // the score update's weights of visit pages below wcap stay in LDS (this
+  // work-group holds the whole unit); the rest go to the workspace
+  const int wcap = (p.accumulate && p.n_split == 1) ? kWeightPages<G> : 0;
 
   // QK layout: lane = 8*r8 + j8 reads columns [j8*QC, (j8+1)*QC) of rows r8
   // (pass A) and r8 + 8 (pass B).  After the 8-lane reduction, lane j8 < 4
@@ -951,7 +960,7 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
         const PageRef nx2 = ref_or_tail(i + 2);
         const float z = qk_page<D, G>(ln, kbA, lds_q);
         load_k<D>(p, ln, nx2, kbA);
-        softmax_page<D, G>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p, lds_w, lds_mr, wl);
+        softmax_page<D, G>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p, lds_w, lds_mr, wcap);
         pv_page<D, G>(ln, vb, ws, lds_p[wave]);
         load_v<D>(p, ln, nx1, vb);
         cur = nx1;
@@ -962,7 +971,7 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
         const PageRef nx2 = ref_or_tail(i + 3);
         const float z = qk_page<D, G>(ln, kbB, lds_q);
         load_k<D>(p, ln, nx2, kbB);
-        softmax_page<D, G>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p, lds_w, lds_mr, wl);
+        softmax_page<D, G>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p, lds_w, lds_mr, wcap);
         pv_page<D, G>(ln, vb, ws, lds_p[wave]);
         load_v<D>(p, ln, nx1, vb);
         cur = nx1;
@@ -1057,16 +1066,14 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
     return;
   }
   if (kWaveRows && steady) {
-    const WeightSrc wsrc = wl ? WeightSrc{lds_w, lds_mr}
-                              : WeightSrc{p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G};
+    const WeightSrc wsrc{lds_w, lds_mr, p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G, wcap};
     finish_steady<NT, G, D>(p, g, fin_m, fin_il, lds_phys, lds_vp, wsrc, spos, su, rbeg, wr, n_my,
                                         esc);
   } else if (!kWaveRows && steady_any) {
-    const WeightSrc wsrc = wl ? WeightSrc{lds_w, lds_mr}
-                              : WeightSrc{p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G};
+    const WeightSrc wsrc{lds_w, lds_mr, p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G, wcap};
     finish_steady_strided<NT, G, D>(p, g, fin_m, fin_il, lds_phys, wsrc, esc);
   } else {
-    finish_unit<NT, G, D, true>(p, g, fin_m, fin_il, wl ? lds_w : nullptr, lds_mr, &esc);
+    finish_unit<NT, G, D, true>(p, g, fin_m, fin_il, lds_w, lds_mr, wcap, &esc);
   }
 }
 
@@ -1106,7 +1113,7 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(const A
     }
   }
   __syncthreads();
-  finish_unit<kCombineThreads, G, D, false>(p, g, fin_m, fin_il, nullptr, nullptr, nullptr);
+  finish_unit<kCombineThreads, G, D, false>(p, g, fin_m, fin_il, nullptr, nullptr, 0, nullptr);
 }
 
 // With a split, the combine pass updates the scores and publishes the appended
