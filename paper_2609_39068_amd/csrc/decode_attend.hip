@@ -64,6 +64,7 @@ struct AttendParams {
   float* part;
   float* pbuf;
   float* mref;
+  const int32_t* order;  // unit of each work-group slot (longest first), or null: identity
   int32_t* dev_err;
   // fused steady-state H2O eviction (se_decode_step_h2o)
   int32_t evict;
@@ -75,7 +76,7 @@ struct AttendParams {
 };
 
 struct AttendWs {
-  size_t part, pbuf, mref, total;
+  size_t part, pbuf, mref, order, total;
 };
 
 inline AttendWs attend_ws_layout(int units, const SplitShape& s, int G, int D) {
@@ -87,6 +88,8 @@ inline AttendWs attend_ws_layout(int units, const SplitShape& s, int G, int D) {
   off = align_up(off + (size_t)units * s.n_visit * kPage * G * 4, 256);
   w.mref = off;
   off = align_up(off + (size_t)units * s.n_visit * G * 4, 256);
+  w.order = off;
+  off = align_up(off + (size_t)units * 4, 256);
   w.total = off;
   return w;
 }
@@ -761,8 +764,9 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int unit = blockIdx.x / p.n_split;
-  const int split = blockIdx.x - unit * p.n_split;
+  const int uslot = blockIdx.x / p.n_split;
+  const int unit = p.order != nullptr ? p.order[uslot] : uslot;
+  const int split = blockIdx.x - uslot * p.n_split;
   const UnitGeom g = unit_geom(p, unit);
   const int req = g.req, kvh = g.kvh, L = g.L, Lp = g.Lp, cur_page = g.cur_page;
   const bool append = g.append, quest = g.quest, bad = g.bad;
@@ -1077,6 +1081,44 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   }
 }
 
+// Launch order of the units when they take more than one round of work-groups:
+// longest first (a counting sort on the page count), so that the last
+// work-groups to start are the short ones and the chip drains evenly.  Units
+// with equal page counts come in any order; the results do not depend on it.
+constexpr int kOrderThreads = 1024;
+constexpr int kOrderMaxBins = 16384;
+
+__global__ __launch_bounds__(kOrderThreads) void unit_order_kernel(const int32_t* lengths, int num_units,
+                                                                   int append, int max_pages, int32_t* order) {
+  __shared__ int cnt[kOrderMaxBins];
+  __shared__ int scan[kOrderThreads / kWave + 1];
+  const int tid = threadIdx.x;
+  const int nb = max_pages + 1;  // bin max_pages - pages: page counts 0..max_pages, descending
+  auto bin_of = [&](int u) {
+    const int L = lengths[u] + append;
+    const int pages = L <= 0 ? 0 : min((L + kPage - 1) / kPage, max_pages);
+    return max_pages - pages;
+  };
+  for (int i = tid; i < nb; i += kOrderThreads) cnt[i] = 0;
+  __syncthreads();
+  for (int u = tid; u < num_units; u += kOrderThreads) atomicAdd(&cnt[bin_of(u)], 1);
+  __syncthreads();
+  // exclusive scan over the bins: each thread sums a contiguous chunk
+  const int chunk = (nb + kOrderThreads - 1) / kOrderThreads;
+  const int c0 = min(nb, tid * chunk), c1 = min(nb, c0 + chunk);
+  int local = 0;
+  for (int i = c0; i < c1; ++i) local += cnt[i];
+  int total;
+  int run = block_exclusive_scan<kOrderThreads>(local, scan, &total);
+  for (int i = c0; i < c1; ++i) {
+    const int c = cnt[i];
+    cnt[i] = run;
+    run += c;
+  }
+  __syncthreads();
+  for (int u = tid; u < num_units; u += kOrderThreads) order[atomicAdd(&cnt[bin_of(u)], 1)] = u;
+}
+
 // Second pass when a unit is split over several work-groups: combines the
 // partials (m, l, o) in split order, writes out and lse, then finishes the unit.
 constexpr int kCombineThreads = 512;
@@ -1257,6 +1299,15 @@ static se_status attend_launch(const se_kv_view* kv, int32_t q_per_kv, const voi
   prm.part = reinterpret_cast<float*>(base + lay.part);
   prm.pbuf = reinterpret_cast<float*>(base + lay.pbuf);
   prm.mref = reinterpret_cast<float*>(base + lay.mref);
+  // more than one round of work-groups over ragged units: longest first
+  prm.order = nullptr;
+  if (sel_pages == nullptr && (int64_t)kv->num_units * s.n_split > (wide ? 256 : 512) &&
+      kv->max_pages + 1 <= kOrderMaxBins) {
+    int32_t* order = reinterpret_cast<int32_t*>(base + lay.order);
+    hipLaunchKernelGGL(unit_order_kernel, dim3(1), dim3(kOrderThreads), 0, stream, kv->lengths, kv->num_units,
+                       k_new != nullptr ? 1 : 0, kv->max_pages, order);
+    prm.order = order;
+  }
   prm.dev_err = dev_err;
 
   const int64_t grid = (int64_t)kv->num_units * s.n_split;
