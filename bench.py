@@ -28,7 +28,6 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-QUEST_SAMPLE = 32  # Quest steps whose two calls are bracketed one by one
 METRIC = "decode attn+eviction tokens/s/GPU; achieved HBM GB/s vs MI355X peak"
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_step_h2o_llama3-8b-layer-h2o_traffic.txt")
@@ -243,29 +242,16 @@ def main():
         return out_
 
     def run(decs, t0, t1, bounds, events=None):
-        """events["span"]: before the first step, after it, after the last (an
-        event costs a few microseconds of GPU time, so the one-call H2O steps
-        are not bracketed one by one).  Quest: events["calls"] also bracket the
-        selection and the attention of each layer in the first QUEST_SAMPLE
-        steps, splitting the two calls."""
+        """One call per layer and step (se_decode_step_h2o / se_decode_step_quest).
+        events: before the first step, after it, after the last (an event costs a
+        few microseconds of GPU time, so calls are not bracketed one by one)."""
         for t in range(t0, t1):
             ml = bounds[t - t0]
             if events is not None and t == t0:
                 events["span"][0].record()
             for l, d in enumerate(decs):
                 q, kn, vn, npos = steps.q[t, l], steps.k_new[t, l], steps.v_new[t, l], steps.new_pos[t]
-                if w.method == "h2o":
-                    d.step(q, kn, vn, npos, out, max_len=ml)
-                    continue
-                e = events["calls"][t - t0][l] if events is not None and t - t0 < len(events["calls"]) else None
-                if e is not None:
-                    e[0].record()
-                d.select(q)
-                if e is not None:
-                    e[1].record()
-                d.attend(q, kn, vn, npos, out, max_len=ml)
-                if e is not None:
-                    e[2].record()
+                d.step(q, kn, vn, npos, out, max_len=ml)
             if events is not None:
                 if t == t0:
                     events["span"][1].record()
@@ -292,10 +278,7 @@ def main():
     torch.cuda.synchronize()
     lengths0 = state.lengths.cpu().numpy().astype(np.int64)
 
-    events = {"span": [torch.cuda.Event(enable_timing=True) for _ in range(3)], "calls": []}
-    if w.method == "quest":
-        events["calls"] = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(w.layers)]
-                           for _ in range(min(K, QUEST_SAMPLE))]
+    events = {"span": [torch.cuda.Event(enable_timing=True) for _ in range(3)]}
     torch.cuda.synchronize()
     bounds = step_bounds(lengths0, K)
     t0 = time.perf_counter()
@@ -307,22 +290,15 @@ def main():
         raise RuntimeError(f"device error bits {errs:#x} during the timed run")
 
     # per-call durations and algorithmic bytes (lengths follow the method's rule on the host)
-    first_ms, second_ms = [], []
+
     first_bytes, second_bytes = 0, 0
     L = lengths0.reshape(w.layers, U).copy()
     span = events["span"]
     step1_ms = span[0].elapsed_time(span[1])
-    if w.method == "h2o":
-        first_ms = [span[0].elapsed_time(span[2])]  # the whole timed region
+    region_ms = span[0].elapsed_time(span[2])  # the whole timed region
     step1_bytes = 0
-    sampled_first, sampled_second = 0, 0     # Quest: bytes of the bracketed calls
     for t in range(K):
         for l in range(w.layers):
-            sampled = w.method != "h2o" and t < len(events["calls"])
-            if sampled:
-                e = events["calls"][t][l]
-                first_ms.append(e[0].elapsed_time(e[1]))
-                second_ms.append(e[1].elapsed_time(e[2]))
             Lp = L[l] + 1
             if w.method == "h2o":
                 # one se_decode_step_h2o call: attention + score update + eviction
@@ -337,25 +313,24 @@ def main():
                 b1, b2 = select_bytes(n_cand, G, D, w.top_k), quest_attend_bytes(visited, G, D, w.top_k)
                 first_bytes += b1
                 second_bytes += b2
-                if sampled:
-                    sampled_first += b1
-                    sampled_second += b2
+                if t == 0:
+                    step1_bytes += b1 + b2
                 L[l] = Lp
     tokens = w.num_req * K
     value = tokens / elapsed
     if w.method == "h2o":
         # one se_decode_step_h2o call per step and layer: the attention kernel with
         # the score update and the steady eviction fused (with a split unit, as in
-        # the first step of a long context: attention, combine, eviction kernels);
-        # its average duration is the timed region over the calls in it
-        dom_name, dom_ms, dom_bytes = "se_decode_step_h2o", sum(first_ms), first_bytes
-        other = {}
+        # the first step of a long context: attention, combine, eviction kernels)
+        dom_name = "se_decode_step_h2o"
     else:
-        # per-call durations from the bracketed sample of steps
-        dom_name, dom_ms, dom_bytes = "quest_select", sum(first_ms), sampled_first
-        other = {"decode_attend": {"avg_us": 1e3 * sum(second_ms) / len(second_ms),
-                                   "algorithmic_GBps": sampled_second / (sum(second_ms) * 1e-3) / 1e9}}
-    n_launch = K * w.layers if w.method == "h2o" else len(first_ms)
+        # one se_decode_step_quest call per step and layer: page bounds, top-k and
+        # attention over the selected pages in one kernel when units fill the chip
+        dom_name = "se_decode_step_quest"
+    # the call's average duration is the timed region over the calls in it
+    dom_ms, dom_bytes = region_ms, first_bytes + second_bytes
+    other = {}
+    n_launch = K * w.layers
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     traffic = read_traffic() if (w.index == 1 and w.method == "h2o") else None
     result = {
@@ -383,7 +358,7 @@ def main():
         "kernels": other,
         "cpu_baseline": cpu,
     }
-    if w.method == "h2o" and K > 1:
+    if K > 1:
         steady_ms = dom_ms - step1_ms
         result["phases"] = {"step1_ms": round(step1_ms, 3),
                             "steady_ms_per_step": round(steady_ms / (K - 1), 4),

@@ -77,6 +77,7 @@ typedef enum se_status {
 /* Operation ids for se_workspace_bytes. */
 #define SE_OP_DECODE_ATTEND 1
 #define SE_OP_QUEST_SELECT  2
+#define SE_OP_QUEST_STEP    3
 
 /* The cache view (Section 3.1, eq. attention-view; Appendix B, "Attention View
  * Payloads").  Only the pointers an operation needs must be non-NULL. */
@@ -227,9 +228,29 @@ se_status se_quest_select(const se_kv_view* kv, int32_t q_per_kv, const void* q,
                           float* page_scores, int32_t scores_stride, void* ws, size_t ws_bytes,
                           int32_t* dev_err, hipStream_t stream);
 
+/*
+ * se_decode_step_quest — one Quest decode step of one layer in one call: exactly the
+ * effect of se_quest_select (page bounds from the min/max summaries, top_k pages per
+ * unit, written to sel_pages) followed by se_decode_attend with that selection
+ * (append, attention over the selected pages and the current page) — Section 3.1:
+ * selection before attention, changing only what attention reads; Appendix A.3,
+ * eq. background-quest-score.  When every unit is read by one work-group and a
+ * unit has at most 4608 candidate pages, the selection runs inside the attention
+ * kernel (one launch; the candidates' scores stay in LDS); otherwise the two calls
+ * run in order.
+ *  Arguments as for se_quest_select and se_decode_attend (k_new/v_new/new_pos may be
+ *  NULL together: no append).  sel_pages int32 [num_units][top_k] (output).
+ *  ws  se_workspace_bytes(SE_OP_QUEST_STEP, ..., top_k) bytes (no zero-fill needed).
+ */
+se_status se_decode_step_quest(const se_kv_view* kv, int32_t q_per_kv, const void* q,
+                               const void* k_new, const void* v_new, const int32_t* new_pos,
+                               float scale, int32_t top_k, int32_t max_len, int32_t* sel_pages,
+                               float* out, float* lse, void* ws, size_t ws_bytes, int32_t* dev_err,
+                               hipStream_t stream);
+
 /* Workspace bytes an operation needs for these sizes (0 if none).  op is one of
- * SE_OP_*; max_len as passed to the call; top_k only for SE_OP_DECODE_ATTEND with a
- * selection (0 otherwise). */
+ * SE_OP_*; max_len as passed to the call; top_k for SE_OP_DECODE_ATTEND with a
+ * selection and for SE_OP_QUEST_STEP (0 otherwise). */
 size_t se_workspace_bytes(int32_t op, int32_t num_units, int32_t max_len, int32_t max_pages,
                           int32_t q_per_kv, int32_t head_dim, int32_t top_k);
 

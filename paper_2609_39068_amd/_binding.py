@@ -32,9 +32,10 @@ SE_ATTEND_ACCUMULATE = 1
 SE_QUEST_SCORES_GIVEN = 1
 SE_OP_DECODE_ATTEND = 1
 SE_OP_QUEST_SELECT = 2
+SE_OP_QUEST_STEP = 3
 
 EXPORTED = (
-    "se_decode_attend", "se_decode_step_h2o", "se_accumulate_scores", "se_evict_compact", "se_quest_summarize",
+    "se_decode_attend", "se_decode_step_h2o", "se_decode_step_quest", "se_accumulate_scores", "se_evict_compact", "se_quest_summarize",
     "se_quest_select", "se_workspace_bytes", "se_read_device_errors", "se_status_string",
     "se_version",
 )
@@ -66,7 +67,7 @@ class se_kv_view(ctypes.Structure):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(
-            f"{LIB_PATH} is missing: build it with `python -m paper_2609_39068_amd.build` "
+            f"{LIB_PATH} is missing: build it with `python paper_2609_39068_amd/build.py` "
             "(hipcc, gfx950); there is no fallback path")
     lib = ctypes.CDLL(LIB_PATH)
     P, I32, U32, F32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32, ctypes.c_float, ctypes.c_size_t
@@ -78,6 +79,7 @@ def _load():
         "se_evict_compact": (I32, [V, I32, I32, I32, P, I32, P, P, P]),
         "se_quest_summarize": (I32, [V, I32, P, P]),
         "se_quest_select": (I32, [V, I32, P, F32, I32, I32, U32, P, P, I32, P, SZ, P, P]),
+        "se_decode_step_quest": (I32, [V, I32, P, P, P, P, F32, I32, I32, P, P, P, P, SZ, P, P]),
         "se_workspace_bytes": (SZ, [I32, I32, I32, I32, I32, I32, I32]),
         "se_read_device_errors": (I32, [P, P, P]),
         "se_status_string": (ctypes.c_char_p, [I32]),
@@ -278,3 +280,25 @@ def se_version() -> int:
 def raw_library():
     """The loaded ctypes library (for symbol checks)."""
     return _lib
+
+
+def se_decode_step_quest(view: KVView, q_per_kv, q, k_new, v_new, new_pos, scale, top_k, max_len, sel_pages,
+                         out, lse, ws, dev_err, stream=None):
+    s = view.struct
+    nreq = s.num_units // s.num_kv_heads
+    hq = s.num_kv_heads * q_per_kv
+    _need(q, nreq * hq * s.head_dim, "q")
+    _need(out, nreq * hq * s.head_dim, "out")
+    _need(lse, nreq * hq, "lse")
+    _need(k_new, s.num_units * s.head_dim, "k_new")
+    _need(v_new, s.num_units * s.head_dim, "v_new")
+    _need(new_pos, nreq, "new_pos")
+    _need(sel_pages, s.num_units * int(top_k), "sel_pages")
+    st = _lib.se_decode_step_quest(
+        view.ref(), int(q_per_kv), _ptr(q, torch.bfloat16, "q"), _ptr(k_new, torch.bfloat16, "k_new"),
+        _ptr(v_new, torch.bfloat16, "v_new"), _ptr(new_pos, torch.int32, "new_pos"), float(scale),
+        int(top_k), int(max_len), _ptr(sel_pages, torch.int32, "sel_pages"), _ptr(out, torch.float32, "out"),
+        _ptr(lse, torch.float32, "lse"), _ptr(ws, None, "ws"),
+        0 if ws is None else ws.numel() * ws.element_size(), _ptr(dev_err, torch.int32, "dev_err"),
+        _stream(stream))
+    _check("se_decode_step_quest", st)

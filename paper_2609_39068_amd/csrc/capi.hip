@@ -89,6 +89,8 @@ extern "C" size_t se_workspace_bytes(int32_t op, int32_t num_units, int32_t max_
                                        top_k > 0 ? top_k : 0);
     case SE_OP_QUEST_SELECT:
       return se_quest_workspace_bytes(num_units, max_pages);
+    case SE_OP_QUEST_STEP:
+      return se_quest_step_workspace_bytes(num_units, max_len, max_pages, q_per_kv, head_dim, top_k);
     default:
       return 0;
   }

@@ -31,6 +31,7 @@
 // avoids a device-scope release/acquire (an L2 writeback and invalidate) in
 // every work-group.
 #include "evict_core.h"
+#include "quest_core.h"
 
 namespace se {
 
@@ -50,6 +51,11 @@ struct AttendParams {
   const int32_t* new_pos;
   const int32_t* sel;
   int32_t top_k;
+  // se_decode_step_quest: the kernel selects the pages itself (Quest bound +
+  // top-k over the unit's candidate pages, which must number at most
+  // kSelectMaxPages) and writes the selection to sel before attending
+  int32_t select;
+  const uint16_t* meta;
   float scale;
   float scale_log2;
   int32_t max_len;
@@ -137,6 +143,7 @@ __device__ __forceinline__ float slot_weight(const AttendParams& p, size_t ubase
 // scratch's holes array, which only the general eviction uses, after the scores
 // are written.
 constexpr int kWeightCap = 9216;  // floats (>= kMaxBudget ints for the holes)
+constexpr int kSelectMaxPages = kWeightCap / 2;  // fused Quest selection: block-table row + scores
 template <int G>
 constexpr int kWeightPages = kWeightCap / (kPage * G);
 static_assert(kWeightCap >= kMaxBudget, "the weight buffer doubles as the holes array");
@@ -812,6 +819,32 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   const uint16_t* knew_row = append ? p.k_new + ((size_t)req * p.hkv + kvh) * D : nullptr;
   const uint16_t* vnew_row = append ? p.v_new + ((size_t)req * p.hkv + kvh) * D : nullptr;
 
+  // ---- fused Quest selection (se_decode_step_quest; one work-group per unit):
+  // the candidates' block-table row and page scores live in the weight buffer,
+  // unused by Quest; the selection goes to sel and is read back below
+  if (p.select) {
+    int32_t* sel_out = const_cast<int32_t*>(p.sel) + (size_t)unit * p.top_k;
+    const int n_cand = bad ? 0 : L / kPage;  // complete pages before the current one
+    int* const sbt = reinterpret_cast<int*>(lds_w);
+    float* const ssc = lds_w + kSelectMaxPages;
+    int badc = 0;
+    for (int i = tid; i < n_cand; i += NT) {
+      int ph = p.block_table[(size_t)unit * p.max_pages + i];
+      if (ph < 0 || (int64_t)ph >= p.num_pages) {
+        badc = 1;
+        ph = -1;
+      }
+      sbt[i] = ph;
+    }
+    if (badc) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
+    __syncthreads();
+    unit_bounds<NT, D, G>(p.meta, p.q + ((size_t)req * Hq + (size_t)kvh * G) * D, p.scale, n_cand, sbt, ssc,
+                          nullptr);
+    __syncthreads();
+    unit_topk<NT>(n_cand, p.top_k, ssc, sel_out, nullptr, esc.hist, lds_scan, esc.bcast);
+    __syncthreads();
+  }
+
   // ---- this work-group's pages: visit index, logical and physical ids of the
   // pages it must read, compacted and staged in LDS once, so the page stream
   // below never waits on a dependent table load or branches around a page
@@ -1359,4 +1392,45 @@ extern "C" se_status se_decode_step_h2o(const se_kv_view* kv, int32_t q_per_kv, 
                                SE_ATTEND_ACCUMULATE, out, lse, nullptr, 0, ws, ws_bytes, dev_err,
                                stream, &ev);
   return st;
+}
+
+size_t se_quest_step_workspace_bytes(int32_t num_units, int32_t max_len, int32_t max_pages, int32_t q_per_kv,
+                                     int32_t head_dim, int32_t top_k) {
+  const size_t a = se_attend_workspace_bytes(num_units, max_len, max_pages, q_per_kv, head_dim, top_k);
+  if (a == 0) return 0;
+  return a + se_quest_workspace_bytes(num_units, max_pages);
+}
+
+extern "C" se_status se_decode_step_quest(const se_kv_view* kv, int32_t q_per_kv, const void* q,
+                                          const void* k_new, const void* v_new, const int32_t* new_pos,
+                                          float scale, int32_t top_k, int32_t max_len, int32_t* sel_pages,
+                                          float* out, float* lse, void* ws, size_t ws_bytes, int32_t* dev_err,
+                                          hipStream_t stream) {
+  se_status st = check_view(kv);
+  if (st != SE_OK) return st;
+  if (kv->meta_pool == nullptr || sel_pages == nullptr || q == nullptr) return SE_ERR_INVALID_ARGUMENT;
+  if (top_k < 1 || top_k > 4096 || max_len < 1) return SE_ERR_INVALID_ARGUMENT;
+  const size_t a_bytes =
+      se_attend_workspace_bytes(kv->num_units, max_len, kv->max_pages, q_per_kv, kv->head_dim, top_k);
+  if (ws == nullptr || ws_bytes < a_bytes) return SE_ERR_WORKSPACE;
+  // one launch when one work-group holds each unit and the candidates fit LDS
+  const int n_visit = top_k + 1;
+  const bool wide = attend_wide(kv->num_units, n_visit);
+  const SplitShape s = split_shape(kv->num_units, n_visit, wide ? 256 : 512);
+  int64_t ml = max_len;
+  if (ml > (int64_t)kv->max_pages * kPage) ml = (int64_t)kv->max_pages * kPage;
+  if (s.n_split == 1 && ml / kPage <= kSelectMaxPages) {
+    AttendParams ex = {};
+    ex.select = 1;
+    ex.meta = static_cast<const uint16_t*>(kv->meta_pool);
+    return attend_launch(kv, q_per_kv, q, k_new, v_new, new_pos, sel_pages, top_k, scale, max_len, 0, out, lse,
+                         nullptr, 0, ws, ws_bytes, dev_err, stream, &ex);
+  }
+  // otherwise the two calls; the selection's workspace follows the attention's
+  char* base = static_cast<char*>(ws);
+  st = se_quest_select(kv, q_per_kv, q, scale, top_k, max_len, 0, sel_pages, nullptr, 0, base + a_bytes,
+                       ws_bytes - a_bytes, dev_err, stream);
+  if (st != SE_OK) return st;
+  return attend_launch(kv, q_per_kv, q, k_new, v_new, new_pos, sel_pages, top_k, scale, max_len, 0, out, lse,
+                       nullptr, 0, ws, ws_bytes, dev_err, stream, nullptr);
 }

@@ -21,7 +21,7 @@
 // arithmetic and the same selection as the two kernels).
 #include <climits>
 
-#include "se_common.h"
+#include "quest_core.h"
 
 namespace se {
 
@@ -82,18 +82,6 @@ __global__ __launch_bounds__(256) void quest_summarize_kernel(const QuestParams 
   uint16_t* meta = p.meta_pool + (size_t)phys * 2 * D;
   *reinterpret_cast<uint32_t*>(meta + 2 * lane) = mn0 | (mn1 << 16);
   *reinterpret_cast<uint32_t*>(meta + D + 2 * lane) = mx0 | (mx1 << 16);
-}
-
-// bf16 pair with negative halves zeroed (q+) or non-negative halves zeroed (q-).
-__device__ __forceinline__ uint32_t pos_part(uint32_t x) {
-  const uint32_t lo = (x & 0x8000u) ? 0u : (x & 0xffffu);
-  const uint32_t hi = (x & 0x80000000u) ? 0u : (x & 0xffff0000u);
-  return lo | hi;
-}
-__device__ __forceinline__ uint32_t neg_part(uint32_t x) {
-  const uint32_t lo = (x & 0x8000u) ? (x & 0xffffu) : 0u;
-  const uint32_t hi = (x & 0x80000000u) ? (x & 0xffff0000u) : 0u;
-  return lo | hi;
 }
 
 constexpr int kBoundPagesPerGroup = 256;
@@ -227,91 +215,6 @@ __global__ __launch_bounds__(256) void quest_topk_kernel(const QuestParams p) {
   }
 }
 
-// Page bounds of one unit's candidate pages [0, n) by NT threads, 8 lanes per
-// page, into lds_sc (and the global score row when write_scores is set).  The
-// block-table row is in lds_bt (-1 for an entry outside the pool).  Every
-// iteration's loads are issued before the previous page is reduced.
-template <int NT, int D, int G>
-__device__ __forceinline__ void unit_bounds(const QuestParams& p, int unit, int n, const int* lds_bt,
-                                            float* lds_sc) {
-  constexpr int CH = D / 8;   // channels per lane
-  constexpr int CW = CH / 2;  // bf16 pairs per lane
-  constexpr int C4 = CW / 4;  // 16-byte loads per lane per row
-  constexpr int SLOTS = NT / 8;
-  const int lane = threadIdx.x & 63;
-  const int g = lane & 7;
-  const int slot = threadIdx.x >> 3;
-  const int req = unit / p.hkv;
-  const int kvh = unit - req * p.hkv;
-  uint32_t qp[G][CW], qn[G][CW];
-  {
-    const uint16_t* qb = p.q + ((size_t)req * p.hkv * G + (size_t)kvh * G) * D + g * CH;
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const uint4* src = reinterpret_cast<const uint4*>(qb + (size_t)h * D);
-#pragma unroll
-      for (int i = 0; i < C4; ++i) {
-        const uint4 t = src[i];
-        const uint32_t v[4] = {t.x, t.y, t.z, t.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          qp[h][4 * i + e] = pos_part(v[e]);
-          qn[h][4 * i + e] = neg_part(v[e]);
-        }
-      }
-    }
-  }
-  auto load = [&](int b, uint4 (&mn)[C4], uint4 (&mx)[C4]) {
-    const int ph = lds_bt[min(b, n - 1)];
-    const uint16_t* meta = p.meta_pool + (size_t)(ph < 0 ? 0 : ph) * 2 * D + g * CH;
-#pragma unroll
-    for (int i = 0; i < C4; ++i) {
-      mn[i] = reinterpret_cast<const uint4*>(meta)[i];
-      mx[i] = reinterpret_cast<const uint4*>(meta + D)[i];
-    }
-  };
-  auto bound = [&](int b, const uint4 (&mn)[C4], const uint4 (&mx)[C4]) {
-    float acc[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) acc[h] = 0.f;
-#pragma unroll
-    for (int i = 0; i < C4; ++i) {
-      const uint32_t lo[4] = {mn[i].x, mn[i].y, mn[i].z, mn[i].w};
-      const uint32_t hi[4] = {mx[i].x, mx[i].y, mx[i].z, mx[i].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-          acc[h] = dot2bf16(qp[h][4 * i + e], hi[e], acc[h]);
-          acc[h] = dot2bf16(qn[h][4 * i + e], lo[e], acc[h]);
-        }
-      }
-    }
-    float best = -INFINITY;
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      float a = quad_sum(acc[h]);
-      a += shfl_xor_f(a, 4);
-      best = fmaxf(best, a);
-    }
-    if (b < n && g == 0) {
-      const float sc = lds_bt[b] >= 0 ? best * p.scale : -INFINITY;
-      lds_sc[b] = sc;
-      if (p.write_scores) p.scores[(size_t)unit * p.scores_stride + b] = sc;
-    }
-  };
-  const int iters = (n + SLOTS - 1) / SLOTS;
-  uint4 mnA[C4], mxA[C4], mnB[C4], mxB[C4];
-  if (iters > 0) load(slot, mnA, mxA);
-  for (int it = 0; it < iters; it += 2) {
-    load(slot + (it + 1) * SLOTS, mnB, mxB);
-    bound(slot + it * SLOTS, mnA, mxA);
-    if (it + 1 >= iters) break;
-    load(slot + (it + 2) * SLOTS, mnA, mxA);
-    bound(slot + (it + 1) * SLOTS, mnB, mxB);
-  }
-}
-
 constexpr int kFusedThreads = 1024;
 constexpr int kFusedMaxPages = 8192;
 constexpr int kFusedMinUnits = 256;  // one work-group per unit fills the compute units
@@ -345,33 +248,11 @@ __global__ __launch_bounds__(kFusedThreads) void quest_select_fused_kernel(const
   }
   if (bad) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
   __syncthreads();
-  unit_bounds<NT, D, G>(p, unit, n, lds_bt, lds_sc);
+  const int req = unit / p.hkv, kvh = unit - req * p.hkv;
+  unit_bounds<NT, D, G>(p.meta_pool, p.q + ((size_t)req * p.hkv * G + (size_t)kvh * G) * D, p.scale, n, lds_bt,
+                        lds_sc, p.write_scores ? p.scores + (size_t)unit * p.scores_stride : nullptr);
   __syncthreads();
-  if (n <= p.top_k) {
-    for (int i = tid; i < p.top_k; i += NT) out[i] = i < n ? i : -1;
-    return;
-  }
-  auto key_of = [&](int b) { return float_key(lds_sc[b]); };
-  uint32_t prefix, mask;
-  int k_rest;
-  radix_select_top<NT, uint32_t>(n, p.top_k, key_of, [](int) { return true; }, &prefix, &mask, &k_rest, hist,
-                                 scan_scratch, bcast);
-  // keys above the threshold class, then the first k_rest of the class in index order
-  int eq_base = 0, out_base = 0;
-  for (int b0 = 0; b0 < n; b0 += NT) {
-    const int b = b0 + tid;
-    uint32_t km = 0;
-    if (b < n) km = key_of(b) & mask;
-    const int is_eq = (b < n && km == prefix) ? 1 : 0;
-    int eq_total;
-    const int eq_rank = block_exclusive_scan<NT>(is_eq, scan_scratch, &eq_total);
-    const int take = (b < n) && (km > prefix || (is_eq && eq_base + eq_rank < k_rest)) ? 1 : 0;
-    int take_total;
-    const int rank = block_exclusive_scan<NT>(take, scan_scratch, &take_total);
-    if (take) out[out_base + rank] = b;
-    eq_base += eq_total;
-    out_base += take_total;
-  }
+  unit_topk<NT>(n, p.top_k, lds_sc, out, nullptr, hist, scan_scratch, bcast);
 }
 
 }  // namespace se

@@ -66,7 +66,7 @@ class H2ODecoder:
 class QuestDecoder:
     """One layer's Quest decode step: page selection (se_quest_select), then
     append + attention over the selected pages and the current page
-    (se_decode_attend)."""
+    (se_decode_attend); step() does both in one call (se_decode_step_quest)."""
 
     def __init__(self, view: se.KVView, q_per_kv: int, scale: float, top_k: int, max_len: int,
                  device):
@@ -75,7 +75,8 @@ class QuestDecoder:
         mp = view.struct.max_pages
         na = se.se_workspace_bytes(se.SE_OP_DECODE_ATTEND, view.num_units, max_len, mp, q_per_kv, d, top_k)
         nq = se.se_workspace_bytes(se.SE_OP_QUEST_SELECT, view.num_units, max_len, mp, q_per_kv, d, 0)
-        self.ws_attend = torch.zeros(max(na, 1), dtype=torch.uint8, device=device)
+        ns = se.se_workspace_bytes(se.SE_OP_QUEST_STEP, view.num_units, max_len, mp, q_per_kv, d, top_k)
+        self.ws_attend = torch.zeros(max(na, ns, 1), dtype=torch.uint8, device=device)
         self.ws_select = torch.zeros(max(nq, 1), dtype=torch.uint8, device=device)
         self.sel = torch.full((view.num_units, top_k), -1, dtype=torch.int32, device=device)
         self.dev_err = torch.zeros(1, dtype=torch.int32, device=device)
@@ -93,6 +94,11 @@ class QuestDecoder:
                             self.scale, max_len or self.max_len, 0, out, lse, None, 0,
                             self.ws_attend, self.dev_err)
 
-    def step(self, q, k_new, v_new, new_pos, out, lse=None, max_len=None):
-        self.select(q)
-        self.attend(q, k_new, v_new, new_pos, out, lse, max_len=max_len)
+    def step(self, q, k_new, v_new, new_pos, out, lse=None, max_len=None, fused=True):
+        """Selection then attention: in one call (fused), else the two calls."""
+        if not fused:
+            self.select(q)
+            self.attend(q, k_new, v_new, new_pos, out, lse, max_len=max_len)
+            return
+        se.se_decode_step_quest(self.view, self.G, q, k_new, v_new, new_pos, self.scale, self.top_k,
+                                max_len or self.max_len, self.sel, out, lse, self.ws_attend, self.dev_err)

@@ -19,7 +19,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 10, names
+    assert len(names) == 11, names
     lib = b.raw_library()
     for n in names:
         assert hasattr(lib, n), f"{n} is declared in sparse_engine.h but not exported"
@@ -92,6 +92,15 @@ def test_evict_and_quest_argument_checks():
     assert lib.se_quest_summarize(ctypes.byref(_view(meta_pool=None)), 128, 0xA000, None) == b.SE_ERR_INVALID_ARGUMENT
     assert lib.se_accumulate_scores(ctypes.byref(v), 4, 0x100, 64, 0x200, 128, 0xA000, None) == b.SE_ERR_INVALID_ARGUMENT
     assert lib.se_read_device_errors(None, None, None) == b.SE_ERR_INVALID_ARGUMENT
+    sq = lib.se_decode_step_quest
+    assert sq(ctypes.byref(_view(meta_pool=None)), 4, 0x7000, None, None, None, 0.1, 8, 128, 0x100, 0x8000,
+              None, 0x9000, 1 << 30, 0xA000, None) == b.SE_ERR_INVALID_ARGUMENT
+    assert sq(ctypes.byref(v), 4, 0x7000, None, None, None, 0.1, 8, 128, None, 0x8000,
+              None, 0x9000, 1 << 30, 0xA000, None) == b.SE_ERR_INVALID_ARGUMENT        # no sel_pages
+    assert sq(ctypes.byref(v), 4, 0x7000, None, None, None, 0.1, 0, 128, 0x100, 0x8000,
+              None, 0x9000, 1 << 30, 0xA000, None) == b.SE_ERR_INVALID_ARGUMENT        # top_k 0
+    assert sq(ctypes.byref(v), 4, 0x7000, None, None, None, 0.1, 8, 128, 0x100, 0x8000,
+              None, None, 0, 0xA000, None) == b.SE_ERR_WORKSPACE
 
 
 def test_workspace_sizes():
@@ -101,4 +110,6 @@ def test_workspace_sizes():
     nq = b.se_workspace_bytes(b.SE_OP_DECODE_ATTEND, 256, 33024, 2064, 4, 128, 64)
     assert nq >= 256 * 65 * 16 * 4 * 4 and nq < n * 4
     assert b.se_workspace_bytes(b.SE_OP_QUEST_SELECT, 256, 33024, 2064, 4, 128, 0) >= 256 * 2064 * 4
+    ns = b.se_workspace_bytes(b.SE_OP_QUEST_STEP, 256, 33024, 2064, 4, 128, 64)
+    assert ns == nq + b.se_workspace_bytes(b.SE_OP_QUEST_SELECT, 256, 33024, 2064, 4, 128, 0)
     assert b.se_workspace_bytes(99, 1, 1, 1, 1, 64, 0) == 0

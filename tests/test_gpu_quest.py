@@ -216,3 +216,38 @@ def test_fused_select_matches_two_pass(se):
     assert torch.equal(sel_f[:n_sub], sel_2)
     assert torch.equal(sel_f, sel_g)
     assert (sel_f >= 0).all()
+
+
+@pytest.mark.parametrize("num_req", [32, 2])
+def test_step_quest_equals_select_then_attend(se, num_req):
+    # se_decode_step_quest against se_quest_select + se_decode_attend on copies of
+    # one state, three steps: with 256 units the selection runs inside the
+    # attention kernel, with 16 the call falls back to the two kernels.  The
+    # selections, outputs, lse and the pools (append, Quest summaries) agree bit
+    # for bit.
+    from workloads import clone_state
+    w = scaled(CONFIGS[2], num_req=num_req, ctx=3001, steps=3)
+    host = build_state(w, "cpu")
+    steps = build_steps(w, host, "cpu", steps=3)
+    a = to_device(host, DEV)
+    b = clone_state(a)
+    U, G, P = w.units_per_layer, w.q_per_kv, host.max_pages
+    max_len = P * 16
+    da = se.QuestDecoder(_view(se, a), G, w.scale, w.top_k, max_len, DEV)
+    db = se.QuestDecoder(_view(se, b), G, w.scale, w.top_k, max_len, DEV)
+    da.summarize()
+    db.summarize()
+    shape_o = (w.num_req, w.hq, w.head_dim)
+    for t in range(3):
+        q, kn, vn, npos = (x.to(DEV) for x in (steps.q[t, 0], steps.k_new[t, 0], steps.v_new[t, 0], steps.new_pos[t]))
+        oa, ob = torch.empty(shape_o, device=DEV), torch.empty(shape_o, device=DEV)
+        la, lb = torch.empty(shape_o[:2], device=DEV), torch.empty(shape_o[:2], device=DEV)
+        da.step(q, kn, vn, npos, oa, la, fused=False)
+        db.step(q, kn, vn, npos, ob, lb, fused=True)
+        torch.cuda.synchronize()
+        assert se.se_read_device_errors(da.dev_err) == 0 and se.se_read_device_errors(db.dev_err) == 0
+        assert torch.equal(da.sel, db.sel), f"step {t}"
+        assert torch.equal(oa, ob) and torch.equal(la, lb), f"step {t}"
+    assert torch.equal(a.lengths, b.lengths)
+    assert torch.equal(a.kv_pool, b.kv_pool) and torch.equal(a.pos_pool, b.pos_pool)
+    assert torch.equal(a.meta_pool, b.meta_pool)
