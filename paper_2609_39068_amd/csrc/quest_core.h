@@ -7,6 +7,11 @@
 
 namespace se {
 
+// Set bits of a wavefront mask below this lane.
+__device__ __forceinline__ int lane_prefix_count(uint64_t m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
 // bf16 pair with negative halves zeroed (q+) or non-negative halves zeroed (q-).
 __device__ __forceinline__ uint32_t pos_part(uint32_t x) {
   const uint32_t lo = (x & 0x8000u) ? 0u : (x & 0xffffu);
@@ -105,12 +110,20 @@ __device__ __forceinline__ void unit_bounds(const uint16_t* meta_pool, const uin
 
 // The top_k pages of one unit by score (ties: lower page index), ascending, from
 // the n scores in lds_sc, by NT threads; written to out_g and out_l (either may
-// be null), -1 past the selection.  Radix selection on order-preserving keys,
-// then the selected indices ranked by block scans.
+// be null), -1 past the selection.  Radix selection (8-bit digits, most
+// significant first) on order-preserving keys: every thread adds its keys to
+// an LDS histogram, then wavefront 0 alone scans the 256 bins and picks the
+// digit (three barriers per pass).  Wavefront 0 then writes the selected
+// indices in ascending order with ballots: keys above the threshold, and the
+// lowest-indexed ones equal to it until top_k are taken.
 template <int NT>
 __device__ __forceinline__ void unit_topk(int n, int top_k, const float* lds_sc, int32_t* out_g, int32_t* out_l,
                                           unsigned* hist, int* scan_scratch, int* bcast) {
+  (void)scan_scratch;
+  static_assert(NT >= 256 && NT % kWave == 0, "threads 0..255 clear one bin each");
   const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const bool w0 = tid < kWave;
   if (n <= top_k) {
     for (int i = tid; i < top_k; i += NT) {
       const int v = i < n ? i : -1;
@@ -119,29 +132,68 @@ __device__ __forceinline__ void unit_topk(int n, int top_k, const float* lds_sc,
     }
     return;
   }
-  auto key_of = [&](int b) { return float_key(lds_sc[b]); };
-  uint32_t prefix, mask;
-  int k_rest;
-  radix_select_top<NT, uint32_t>(n, top_k, key_of, [](int) { return true; }, &prefix, &mask, &k_rest, hist,
-                                 scan_scratch, bcast);
-  // keys above the threshold class, then the first k_rest of the class in index order
-  int eq_base = 0, out_base = 0;
-  for (int b0 = 0; b0 < n; b0 += NT) {
-    const int b = b0 + tid;
-    uint32_t km = 0;
-    if (b < n) km = key_of(b) & mask;
-    const int is_eq = (b < n && km == prefix) ? 1 : 0;
-    int eq_total;
-    const int eq_rank = block_exclusive_scan<NT>(is_eq, scan_scratch, &eq_total);
-    const int take = (b < n) && (km > prefix || (is_eq && eq_base + eq_rank < k_rest)) ? 1 : 0;
-    int take_total;
-    const int rank = block_exclusive_scan<NT>(take, scan_scratch, &take_total);
-    if (take) {
-      if (out_g != nullptr) out_g[out_base + rank] = b;
-      if (out_l != nullptr) out_l[out_base + rank] = b;
+  uint32_t prefix = 0, mask = 0;
+  int k = top_k;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    if (tid < 256) hist[tid] = 0;
+    __syncthreads();
+    for (int i = tid; i < n; i += NT) {
+      const uint32_t key = float_key(lds_sc[i]);
+      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
     }
-    eq_base += eq_total;
-    out_base += take_total;
+    __syncthreads();
+    if (w0) {
+      // lane l holds digits 255-4l .. 252-4l (descending); inclusive prefix over lanes
+      int c[4], s4 = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        c[j] = (int)hist[255 - 4 * lane - j];
+        s4 += c[j];
+      }
+      int incl = s4;
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const int y = __shfl_up(incl, o, kWave);
+        if (lane >= o) incl += y;
+      }
+      int run = incl - s4;  // keys in higher digits than this lane's first
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (c[j] > 0 && run < k && run + c[j] >= k) {
+          bcast[0] = 255 - 4 * lane - j;
+          bcast[1] = run;
+          bcast[2] = c[j];
+        }
+        run += c[j];
+      }
+    }
+    __syncthreads();
+    const int d = bcast[0];
+    k -= bcast[1];
+    const int cnt = bcast[2];
+    prefix |= (uint32_t)d << shift;
+    mask |= 0xFFu << shift;
+    if (cnt == k) break;
+  }
+  // k keys equal to the threshold class (under mask) are taken, lowest index first
+  if (w0) {
+    int taken = 0, eq_seen = 0;
+    for (int b0 = 0; b0 < n; b0 += kWave) {
+      const int b = b0 + lane;
+      const uint32_t km = b < n ? (float_key(lds_sc[b]) & mask) : 0u;
+      const bool above = b < n && km > prefix;
+      const bool eq = b < n && km == prefix;
+      const uint64_t eqm = __ballot(eq);
+      const bool take = above || (eq && eq_seen + lane_prefix_count(eqm) < k);
+      const uint64_t tm = __ballot(take);
+      if (take) {
+        const int r = taken + lane_prefix_count(tm);
+        if (out_g != nullptr) out_g[r] = b;
+        if (out_l != nullptr) out_l[r] = b;
+      }
+      taken += __popcll(tm);
+      eq_seen += __popcll(eqm);
+    }
   }
 }
 

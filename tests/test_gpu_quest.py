@@ -251,3 +251,35 @@ def test_step_quest_equals_select_then_attend(se, num_req):
     assert torch.equal(a.lengths, b.lengths)
     assert torch.equal(a.kv_pool, b.kv_pool) and torch.equal(a.pos_pool, b.pos_pool)
     assert torch.equal(a.meta_pool, b.meta_pool)
+
+
+def test_fused_select_ties_match_topk_kernel(se):
+    # Many exactly equal page scores (every even page of a unit carries the
+    # summaries of its page 0): the one-kernel selection keeps the lowest page
+    # indices of the tied class, exactly as the top-k kernel does from the same
+    # scores.
+    w = scaled(CONFIGS[2], ctx=2001, steps=1)
+    host = build_state(w, "cpu")
+    steps = build_steps(w, host, "cpu", steps=1)
+    gs = to_device(host, DEV)
+    view = _view(se, gs)
+    U, G, P = w.units_per_layer, w.q_per_kv, host.max_pages
+    max_len = P * 16
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    se.se_quest_summarize(view, max_len, err)
+    n = int(gs.lengths[0]) // 16
+    bt = gs.block_table[:, :n].to(torch.int64)
+    gs.meta_pool[bt[:, 2::2]] = gs.meta_pool[bt[:, :1]]
+    q = steps.q[0, 0].to(DEV)
+    for top_k in (64, 5, n - 1):
+        sel_f = torch.full((U, top_k), -5, dtype=torch.int32, device=DEV)
+        sc_f = torch.full((U, P), float("nan"), dtype=torch.float32, device=DEV)
+        se.se_quest_select(view, G, q, w.scale, top_k, max_len, 0, sel_f, sc_f, P, None, err)
+        sel_g = torch.full((U, top_k), -5, dtype=torch.int32, device=DEV)
+        se.se_quest_select(view, G, None, w.scale, top_k, max_len, se.SE_QUEST_SCORES_GIVEN, sel_g, sc_f, P,
+                           None, err)
+        torch.cuda.synchronize()
+        assert se.se_read_device_errors(err) == 0
+        assert torch.equal(sel_f, sel_g), top_k
+        # the tied class is large: the scores really tie
+        assert (sc_f[:, 2:n:2] == sc_f[:, :1]).all()
