@@ -22,7 +22,8 @@ Readings of points the paper leaves open (each is also listed in the design doc):
   * TopK order as for H2O: larger pooled score first, then lower position.
   * After the call the score field holds s on the candidates and 0 on the
     window; retention and compaction are H2O's with the window O (retain with
-    recent = w, then the hole-fill compaction).
+    recent = w, then the hole-fill compaction).  A unit whose prompt already
+    fits the budget (L <= B) is left as it is.
 """
 
 import numpy as np
@@ -49,10 +50,10 @@ def observation_scores(Qo: np.ndarray, K: np.ndarray, pos: np.ndarray, w: int, s
     u = np.zeros(L, dtype=np.float64)
     for t in range(w):
         seen = pos <= pos[obs[t]]                     # causal: keys up to query t's position
-        for a in range(Qo.shape[1]):
-            z = scale * (K[seen] @ Qo[t, a])
-            e = np.exp(z - z.max())
-            u[seen] += e / e.sum()
+        Z = scale * (K @ Qo[t].T)                     # [L, G]: every head of the group
+        Z[~seen] = -np.inf
+        E = np.exp(Z - Z.max(axis=0))
+        u += (E / E.sum(axis=0)).sum(axis=1)
     return u
 
 
@@ -62,9 +63,12 @@ def pool_max(u: np.ndarray, pos: np.ndarray, cand: np.ndarray, kappa: int) -> np
     half = int(kappa) // 2
     s = np.zeros_like(u)
     idx = np.flatnonzero(cand)
-    for j in idx:
-        near = idx[np.abs(pos[idx] - pos[j]) <= half]
-        s[j] = u[near].max()
+    order = idx[np.argsort(pos[idx], kind="stable")]   # candidates by position
+    ps = pos[order]
+    lo = np.searchsorted(ps, ps - half, side="left")
+    hi = np.searchsorted(ps, ps + half, side="right")
+    for i, j in enumerate(order):                      # [lo, hi): |pos - pos[j]| <= half
+        s[j] = u[order[lo[i]:hi[i]]].max()
     return s
 
 
@@ -72,6 +76,10 @@ def compact_prompt(st: UnitState, Qo: np.ndarray, w: int, kappa: int, budget: in
     """Scores, pools, retains (eq. background-snapkv-retention) and compacts
     the unit's prompt; mutates st.  Returns u, s, keep, holes, movers, freed."""
     L = st.length
+    if L <= budget:
+        keep = np.ones(L, dtype=bool)
+        return {"u": None, "s": None, "keep": keep, "holes": np.zeros(0, np.int64),
+                "movers": np.zeros(0, np.int64), "freed": np.zeros(0, np.int64)}
     obs = window_slots(st.pos, w)
     cand = np.ones(L, dtype=bool)
     cand[obs] = False

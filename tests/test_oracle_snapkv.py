@@ -102,6 +102,9 @@ def test_compaction_structure(L, w, B, kappa):
     r = snapkv.compact_prompt(st, rng.standard_normal((w, G, d)), w, kappa, B, 0.25)
     n_keep = min(B, L)
     assert int(r["keep"].sum()) == n_keep and st.length == n_keep
+    if L <= B:                                                   # fits: left as it is
+        np.testing.assert_array_equal(st.K, K)
+        return
     assert set(range(L - w, L)) <= set(st.pos.tolist())          # O is retained
     kept = set(st.pos.tolist())
     for j in range(L - w):                                       # no dropped candidate beats a kept one
