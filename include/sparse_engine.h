@@ -66,7 +66,8 @@ typedef enum se_status {
 #define SE_DEVERR_CAPACITY      2u  /* an append past max_pages * page_size                */
 #define SE_DEVERR_BAD_LENGTH    4u  /* lengths[unit] < 0, or above max_len / capacity     */
 #define SE_DEVERR_BAD_SELECTION 8u  /* a sel_pages entry outside the unit's pages          */
-#define SE_DEVERR_BAD_POSITIONS 16u /* eviction found repeated positions (retained != B)  */
+#define SE_DEVERR_BAD_POSITIONS 16u /* eviction found repeated positions (retained != B),
+                                       or a SnapKV prompt not in increasing position order */
 
 /* Flags of se_decode_attend. */
 #define SE_ATTEND_ACCUMULATE 1u /* fused H2O score update (eq. background-h2o-score)   */
@@ -74,10 +75,14 @@ typedef enum se_status {
 /* Flags of se_quest_select. */
 #define SE_QUEST_SCORES_GIVEN 1u /* skip the bound; select from page_scores (input)   */
 
+/* Flags of se_snapkv_compact. */
+#define SE_SNAPKV_SCORE_ONLY 1u /* write the pooled scores; retain and compact nothing */
+
 /* Operation ids for se_workspace_bytes. */
 #define SE_OP_DECODE_ATTEND 1
 #define SE_OP_QUEST_SELECT  2
 #define SE_OP_QUEST_STEP    3
+#define SE_OP_SNAPKV        4
 
 /* The cache view (Section 3.1, eq. attention-view; Appendix B, "Attention View
  * Payloads").  Only the pointers an operation needs must be non-NULL. */
@@ -247,6 +252,42 @@ se_status se_decode_step_quest(const se_kv_view* kv, int32_t q_per_kv, const voi
                                float scale, int32_t top_k, int32_t max_len, int32_t* sel_pages,
                                float* out, float* lse, void* ws, size_t ws_bytes, int32_t* dev_err,
                                hipStream_t stream);
+
+/*
+ * se_snapkv_compact — SnapKV prompt compaction after the last prefill chunk
+ * (Appendix A.3, "SnapKV: Prompt Selection from an Observation Window", eqs.
+ * background-snapkv-score and background-snapkv-retention; Section 3.1: SnapKV's
+ * selection and eviction in finish_step after the final prompt chunk).  For every
+ * unit with L = lengths[unit] > budget (other units are not touched):
+ *   O = the last `window` slots, which hold the largest positions: the unit's slots
+ *       must hold strictly increasing positions (a prefilled prompt), else
+ *       SE_DEVERR_BAD_POSITIONS is raised and the unit is compacted on unspecified
+ *       scores;
+ *   u(j) = sum over the window positions t and the group's query heads a of
+ *       softmax_j(scale * q_{t,a} . k_j) over the slots j with pos_j <= pos of O[t]
+ *       (causal attention of the observation queries; the group's heads summed);
+ *   s(j) = max of u over the candidates (slots outside O) whose positions are
+ *       within kernel/2 of pos_j, for every candidate j (max pooling of width
+ *       `kernel`);
+ *   score_pool receives s on the candidates and 0 on O; then, unless
+ *   SE_SNAPKV_SCORE_ONLY, exactly se_evict_compact(budget, recent = window): O plus
+ *   the budget - window candidates with the largest s (ties: lower position) are
+ *   kept and compacted into slots [0, budget), and lengths[unit] = budget.
+ *  q_obs   bf16 [num_req][window][num_kv_heads * q_per_kv][head_dim]: the query of
+ *          every head at the window's positions, in increasing position order (the
+ *          prefill computed them); query head a belongs to KV head a / q_per_kv.
+ *  window  1 .. budget, window * q_per_kv <= 128; kernel odd, 1 .. 31;
+ *  scale   > 0 (softmax scale, usually 1/sqrt(head_dim)); budget window .. 8192;
+ *  flags   0 or SE_SNAPKV_SCORE_ONLY (freed_* are then unused);
+ *  freed_pages, freed_stride, freed_count, max_len as for se_evict_compact;
+ *  ws      se_workspace_bytes(SE_OP_SNAPKV, num_units, max_len, ...) bytes (no
+ *          zero-fill needed).
+ */
+se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, const void* q_obs,
+                            int32_t window, int32_t kernel, float scale, int32_t budget,
+                            int32_t max_len, uint32_t flags, int32_t* freed_pages,
+                            int32_t freed_stride, int32_t* freed_count, void* ws, size_t ws_bytes,
+                            int32_t* dev_err, hipStream_t stream);
 
 /* Workspace bytes an operation needs for these sizes (0 if none).  op is one of
  * SE_OP_*; max_len as passed to the call; top_k for SE_OP_DECODE_ATTEND with a

@@ -33,11 +33,13 @@ SE_QUEST_SCORES_GIVEN = 1
 SE_OP_DECODE_ATTEND = 1
 SE_OP_QUEST_SELECT = 2
 SE_OP_QUEST_STEP = 3
+SE_OP_SNAPKV = 4
+SE_SNAPKV_SCORE_ONLY = 1
 
 EXPORTED = (
     "se_decode_attend", "se_decode_step_h2o", "se_decode_step_quest", "se_accumulate_scores", "se_evict_compact", "se_quest_summarize",
     "se_quest_select", "se_workspace_bytes", "se_read_device_errors", "se_status_string",
-    "se_version",
+    "se_version", "se_snapkv_compact",
 )
 
 
@@ -80,6 +82,7 @@ def _load():
         "se_quest_summarize": (I32, [V, I32, P, P]),
         "se_quest_select": (I32, [V, I32, P, F32, I32, I32, U32, P, P, I32, P, SZ, P, P]),
         "se_decode_step_quest": (I32, [V, I32, P, P, P, P, F32, I32, I32, P, P, P, P, SZ, P, P]),
+        "se_snapkv_compact": (I32, [V, I32, P, I32, I32, F32, I32, I32, U32, P, I32, P, P, SZ, P, P]),
         "se_workspace_bytes": (SZ, [I32, I32, I32, I32, I32, I32, I32]),
         "se_read_device_errors": (I32, [P, P, P]),
         "se_status_string": (ctypes.c_char_p, [I32]),
@@ -302,3 +305,20 @@ def se_decode_step_quest(view: KVView, q_per_kv, q, k_new, v_new, new_pos, scale
         0 if ws is None else ws.numel() * ws.element_size(), _ptr(dev_err, torch.int32, "dev_err"),
         _stream(stream))
     _check("se_decode_step_quest", st)
+
+
+def se_snapkv_compact(view: KVView, q_per_kv, q_obs, window, kernel, scale, budget, max_len, flags,
+                      freed_pages, freed_stride, freed_count, ws, dev_err, stream=None):
+    s = view.struct
+    nreq = s.num_units // s.num_kv_heads
+    _need(q_obs, nreq * int(window) * s.num_kv_heads * q_per_kv * s.head_dim, "q_obs")
+    if freed_pages is not None:
+        _need(freed_pages, s.num_units * int(freed_stride), "freed_pages")
+    _need(freed_count, s.num_units, "freed_count")
+    st = _lib.se_snapkv_compact(
+        view.ref(), int(q_per_kv), _ptr(q_obs, torch.bfloat16, "q_obs"), int(window), int(kernel),
+        float(scale), int(budget), int(max_len), int(flags), _ptr(freed_pages, torch.int32, "freed_pages"),
+        int(freed_stride), _ptr(freed_count, torch.int32, "freed_count"), _ptr(ws, None, "ws"),
+        0 if ws is None else ws.numel() * ws.element_size(), _ptr(dev_err, torch.int32, "dev_err"),
+        _stream(stream))
+    _check("se_snapkv_compact", st)

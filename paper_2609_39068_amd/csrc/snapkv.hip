@@ -1,0 +1,475 @@
+// se_snapkv_compact: SnapKV prompt compaction (Appendix A.3, "SnapKV: Prompt
+// Selection from an Observation Window", eqs. background-snapkv-score and
+// background-snapkv-retention), applied to a unit's prompt after its last
+// prefill chunk (Section 3.1, finish_step during prefill).
+//
+// Scoring runs one work-group of four wavefronts per unit, two work-groups per
+// compute unit.  The w observation queries of the unit's G heads form
+// R = w*G <= 128 rows; wavefront v holds rows [32v, 32v + 32) in registers as
+// MFMA A operands (bf16 16x16x32 tiles: lane l holds row l%16 and contraction
+// indices 8*(l/16)..+7 of each 32-wide step).  The unit's key pages stream
+// through a two-stage LDS ring, four pages a stage: every thread loads one
+// 16-byte piece of each page (4 KB coalesced per page at head_dim 128), two
+// stages ahead, into registers, and writes it to LDS with the piece index
+// XORed with the key so that the B-operand reads (lane l: key l%16) hit
+// distinct banks.  A page (16 keys) is one B tile; the 16x16 output tile gives
+// lane l the logits of key l%16 against rows 4*(l/16)..+3 of each row tile.
+//   pass 1  row normalisers: every lane keeps, per row, a reference and the
+//           sum of exp2(c*z - reference) over its keys (c = scale*log2 e); a
+//           reference moves only when a logit passes it by more than kLazy,
+//           so most pages cost one fma, one max, one exp2 and one add per
+//           logit.  Merging the 16 key lanes of a row gives
+//           bias = log2 of the row's softmax denominator.
+//   pass 2  u(j) = sum over rows of exp2(c*z - bias) for the candidate keys:
+//           in-lane over the lane's rows, across the row groups of the
+//           wavefront with shuffles, across the wavefronts through LDS;
+//           written to the workspace.
+//   pool    s(j) = max of u over the candidates within kappa/2 positions of j,
+//           through LDS chunks with a halo; s goes to the score field of the
+//           candidates and 0 to the window's, and a slot order that is not
+//           strictly increasing in position is reported.
+// The keys are read twice: the weights need the row's normaliser, which
+// depends on every key, and keeping the logits (R floats per key) would cost
+// more than re-reading the key (2*d bytes).  The causal mask touches only the
+// last pages (window keys); slots past the length are masked there too.
+// Retention and compaction are then H2O's kernel (launch_evict) with the
+// window as its recent set.
+#include "evict_core.h"
+
+namespace se {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kSnapThreads = 256;
+constexpr int kSnapWaves = kSnapThreads / kWave;
+constexpr int kSnapMaxRows = 128;
+constexpr int kSnapMaxHalf = 15;        // kappa <= 31
+constexpr int kSnapMaxPages = 8192;     // block-table entries staged in LDS (131072 slots)
+constexpr int kSnapStagePages = 4;      // pages per ring stage
+constexpr int kSnapPoolChunk = 2048;    // slots pooled per LDS round
+constexpr int kSnapHalo = kSnapMaxHalf + 1;
+constexpr float kLazy = 20.f;           // log2 headroom before a reference moves
+constexpr float kRefInit = -1e30f;      // finite: differences stay defined
+
+struct SnapParams {
+  const uint16_t* kv;
+  const int32_t* pos_pool;
+  float* score_pool;
+  const int32_t* block_table;
+  const int32_t* lengths;
+  const uint16_t* q;  // bf16 [num_req][w][Hq][d]
+  float* u;           // fp32 [num_units][u_stride]
+  int64_t num_pages;
+  int32_t max_pages;
+  int32_t num_kv_heads;
+  int32_t q_per_kv;
+  int32_t w;
+  int32_t half;
+  int32_t budget;
+  int32_t max_len;
+  int32_t u_stride;
+  float c;  // scale * log2(e)
+  int32_t* dev_err;
+};
+
+__device__ __forceinline__ f32x4_t mfma16x16x32(const uint4& a, const uint4& b, f32x4_t acc) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                 acc, 0, 0, 0);
+}
+
+// The K block of a page in LDS: 16 keys of D/8 16-byte pieces; piece c of key
+// k sits at column c ^ (k mod D/8).
+template <int D>
+__device__ __forceinline__ int ring_offset(int key, int piece) {
+  constexpr int PC = D / 8;
+  return key * (2 * D) + ((piece ^ (key & (PC - 1))) << 4);
+}
+
+// Streams pages [pb, pe) of the unit through the LDS ring; body(j, stage)
+// runs once per stage of kSnapStagePages pages (stage j holds pages
+// pb + j*kSnapStagePages ...), every thread of the work-group taking part.
+// Loads run two stages ahead; loads past the range re-read its last page.
+template <int D, typename Body>
+__device__ __forceinline__ void stream_stages(const SnapParams& p, const int* lds_bt, uint8_t* ring, int pb, int pe,
+                                              Body body) {
+  constexpr int S = kSnapStagePages;
+  constexpr int PB = 32 * D;       // K bytes of a page
+  constexpr int PC = D / 8;        // 16-byte pieces per key
+  const int n_st = ceil_div_dev(pe - pb, S);
+  if (n_st <= 0) return;
+  // piece t of a page goes to thread t (head_dim 64: threads 128..255 repeat
+  // the loads of 0..127 and store nothing)
+  const int tid = threadIdx.x & (2 * D - 1);
+  const bool loader = (int)threadIdx.x < 2 * D;
+  const int key = tid / PC;
+  const int piece = tid & (PC - 1);
+  const int lds_off = ring_offset<D>(key, piece);
+  auto load = [&](u32x4_t(&r)[S], int st) {
+#pragma unroll
+    for (int i = 0; i < S; ++i) {
+      const int pg = min(pb + st * S + i, pe - 1);
+      r[i] = *reinterpret_cast<const u32x4_t*>(p.kv + (size_t)lds_bt[pg] * 2 * kPage * D + (size_t)tid * 8);
+    }
+  };
+  auto store = [&](const u32x4_t(&r)[S], int stage) {
+#pragma unroll
+    for (int i = 0; i < S; ++i)
+      if (loader) *reinterpret_cast<u32x4_t*>(ring + (stage * S + i) * PB + lds_off) = r[i];
+  };
+  // issue order as in the loop (stage j + 1 older than stage j + 2), so that
+  // the waits at the loop head are the same from both entries
+  u32x4_t ra[S], rb[S];
+  load(ra, 0);
+  store(ra, 0);
+  asm volatile("" ::: "memory");
+  load(rb, 1);
+  asm volatile("" ::: "memory");
+  load(ra, 2);
+  __syncthreads();
+  // both halves run every time (no exit between them), so the loop head is
+  // reached with the same loads in flight on every path
+  for (int j = 0; j < n_st; j += 2) {
+    store(rb, 1);      // stage j + 1
+    load(rb, j + 3);
+    body(j, 0);
+    __syncthreads();
+    store(ra, 0);      // stage j + 2
+    load(ra, j + 4);
+    if (j + 1 < n_st) body(j + 1, 1);
+    __syncthreads();
+  }
+}
+
+// Logits of the page at `page` (LDS) against the wavefront's row tiles:
+// acc[T][r] is row tile T, row 4*(lane/16) + r, against key lane%16.
+template <int D, int RTW>
+__device__ __forceinline__ void page_logits(const uint4 (&qa)[RTW][D / 32], const uint8_t* page, f32x4_t (&acc)[RTW]) {
+  constexpr int KS = D / 32;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int grp = lane >> 4;
+  const int col = lane & 15;
+  uint4 kb[KS];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) kb[s] = *reinterpret_cast<const uint4*>(page + ring_offset<D>(col, 4 * s + grp));
+#pragma unroll
+  for (int T = 0; T < RTW; ++T) acc[T] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < KS; ++s)
+#pragma unroll
+    for (int T = 0; T < RTW; ++T) acc[T] = mfma16x16x32(qa[T][s], kb[s], acc[T]);
+}
+
+// (ref, sum) pairs merged: the sum re-expressed against the larger reference.
+__device__ __forceinline__ void merge_norm(float& ref, float& sum, float ref2, float sum2) {
+  const float m = fmaxf(ref, ref2);
+  sum = sum * fast_exp2(ref - m) + sum2 * fast_exp2(ref2 - m);
+  ref = m;
+}
+
+// RTW: 16-row tiles per wavefront (rows of wavefront v: [16*RTW*v, 16*RTW*(v+1))).
+template <int D, int RTW>
+__global__ __launch_bounds__(kSnapThreads, 2) void snapkv_score_kernel(const SnapParams p) {
+  constexpr int KS = D / 32;
+  constexpr int S = kSnapStagePages;
+  constexpr int PB = 32 * D;
+  constexpr int kRingBytes = 2 * S * 32 * 128;  // sized for head_dim 128
+  static_assert(kRingBytes >= (kSnapPoolChunk + 2 * kSnapHalo) * 8, "the pool chunk reuses the ring");
+  __shared__ __attribute__((aligned(16))) uint8_t s_ring[kRingBytes];
+  __shared__ int s_bt[kSnapMaxPages];
+  __shared__ float s_up[2][kSnapWaves][S * kPage];
+  __shared__ int s_red[kSnapWaves];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int grp = lane >> 4;
+  const int col = lane & 15;
+  const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int unit = blockIdx.x;
+  const int L = p.lengths[unit];
+  if (L <= p.budget) return;  // the prompt already fits: nothing to score or evict
+  if (L > p.max_len || L > p.max_pages * kPage || L > kSnapMaxPages * kPage) {
+    if (tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_LENGTH);
+    return;
+  }
+  const int32_t* bt = p.block_table + (size_t)unit * p.max_pages;
+  const int n_pages = ceil_div_dev(L, kPage);
+  {
+    int bad = 0;
+    for (int i = tid; i < n_pages; i += kSnapThreads) {
+      const int ph = bt[i];
+      bad |= (ph < 0 || (int64_t)ph >= p.num_pages);
+      s_bt[i] = ph;
+    }
+    bad = block_reduce<kSnapThreads>(bad, s_red, [](int a, int b) { return a | b; });  // also publishes s_bt
+    if (bad) {
+      if (tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
+      return;
+    }
+  }
+  const int w = p.w;
+  const int G = p.q_per_kv;
+  const int R = w * G;
+  const int n_cand = L - w;  // >= 1: L > budget >= w
+  const int row0 = 16 * RTW * wv;
+
+  // ---- the wavefront's observation queries (A operands); rows past R are zero
+  uint4 qa[RTW][KS];
+  {
+    const int req = unit / p.num_kv_heads;
+    const int kvh = unit % p.num_kv_heads;
+    const int hq = p.num_kv_heads * G;
+#pragma unroll
+    for (int T = 0; T < RTW; ++T) {
+      const int row = row0 + 16 * T + col;
+      const int t = row / G;
+      const int g = row - t * G;
+      const uint16_t* src = p.q + (((size_t)req * w + t) * hq + (size_t)kvh * G + g) * D + 8 * grp;
+#pragma unroll
+      for (int s = 0; s < KS; ++s)
+        qa[T][s] = row < R ? *reinterpret_cast<const uint4*>(src + 32 * s) : uint4{0u, 0u, 0u, 0u};
+    }
+  }
+  // the queries arrive before the page stream starts, so that the stream's
+  // waits count page loads only
+#pragma unroll
+  for (int T = 0; T < RTW; ++T)
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      asm volatile("" : "+v"(qa[T][s].x), "+v"(qa[T][s].y), "+v"(qa[T][s].z), "+v"(qa[T][s].w));
+  const float c = p.c;
+  // pages [0, p_full) hold only keys every row sees (slot <= L - w)
+  const int p_full = (L - w + 1) / kPage;
+
+  // ---- pass 1: row normalisers
+  float ref[RTW][4], sum[RTW][4];
+#pragma unroll
+  for (int T = 0; T < RTW; ++T)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      ref[T][r] = kRefInit;
+      sum[T][r] = 0.f;
+    }
+  stream_stages<D>(p, s_bt, s_ring, 0, n_pages, [&](int j, int stage) {
+#pragma unroll
+    for (int i = 0; i < S; ++i) {
+      const int pg = j * S + i;
+      if (pg >= n_pages) break;
+      f32x4_t acc[RTW];
+      page_logits<D, RTW>(qa, s_ring + (stage * S + i) * PB, acc);
+      if (pg >= p_full) {
+        // causal mask: key j is seen by the rows of window position t iff
+        // j <= L - w + t (so j < L); padded rows see nothing
+        const int key = pg * kPage + col;
+#pragma unroll
+        for (int T = 0; T < RTW; ++T)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int row = row0 + 16 * T + 4 * grp + r;
+            const int lim = row < R ? L - w + row / G : -1;
+            if (key > lim) acc[T][r] = -INFINITY;
+          }
+      }
+      float dmax = -INFINITY;
+      float d[RTW][4];
+#pragma unroll
+      for (int T = 0; T < RTW; ++T)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          d[T][r] = fmaf(acc[T][r], c, -ref[T][r]);
+          dmax = fmaxf(dmax, d[T][r]);
+        }
+      if (__builtin_amdgcn_ballot_w64(dmax > kLazy) != 0) {
+        // rare: raise the references of the wavefront's rows to their logits
+#pragma unroll
+        for (int T = 0; T < RTW; ++T)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float zc = acc[T][r] * c;
+            const float m = fmaxf(ref[T][r], zc);
+            sum[T][r] *= fast_exp2(ref[T][r] - m);
+            d[T][r] = zc - m;
+            ref[T][r] = m;
+          }
+      }
+#pragma unroll
+      for (int T = 0; T < RTW; ++T)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sum[T][r] += fast_exp2(d[T][r]);
+    }
+  });
+  // merge the 16 key lanes of each row: bias = log2 of the softmax denominator
+  float bias[RTW][4];
+#pragma unroll
+  for (int T = 0; T < RTW; ++T)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+#pragma unroll
+      for (int m = 1; m < 16; m <<= 1)
+        merge_norm(ref[T][r], sum[T][r], shfl_xor_f(ref[T][r], m), shfl_xor_f(sum[T][r], m));
+      const int row = row0 + 16 * T + 4 * grp + r;
+      bias[T][r] = row < R ? ref[T][r] + __log2f(sum[T][r]) : INFINITY;
+    }
+
+  // ---- pass 2: u over the candidate keys (every row sees them; no mask)
+  float* u = p.u + (size_t)unit * p.u_stride;
+  const int cand_pages = ceil_div_dev(n_cand, kPage);
+  // the four wavefronts' partial sums of stage j are added once the stage's
+  // barrier has passed (by wavefront 0 while the next stage runs, or after
+  // the stream for the last stage)
+  auto flush = [&](int j) {
+    if (wv == 0) {
+      const int key = j * S * kPage + lane;
+      const float* up = &s_up[j & 1][0][0];
+      const float v = up[lane] + up[S * kPage + lane] + up[2 * S * kPage + lane] + up[3 * S * kPage + lane];
+      if (key < n_cand) u[key] = v;
+    }
+  };
+  static_assert(S * kPage == kWave, "wavefront 0 adds one key per lane");
+  const int n_st2 = ceil_div_dev(cand_pages, S);
+  stream_stages<D>(p, s_bt, s_ring, 0, cand_pages, [&](int j, int stage) {
+    if (j > 0) flush(j - 1);
+#pragma unroll
+    for (int i = 0; i < S; ++i) {
+      const int pg = j * S + i;
+      float us = 0.f;
+      if (pg < cand_pages) {
+        f32x4_t acc[RTW];
+        page_logits<D, RTW>(qa, s_ring + (stage * S + i) * PB, acc);
+#pragma unroll
+        for (int T = 0; T < RTW; ++T)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) us += fast_exp2(fmaf(acc[T][r], c, -bias[T][r]));
+        us += shfl_xor_f(us, 16);
+        us += shfl_xor_f(us, 32);
+      }
+      if (grp == 0) s_up[j & 1][wv][i * kPage + col] = us;
+    }
+  });
+  if (n_st2 > 0) flush(n_st2 - 1);
+  __syncthreads();  // the unit's u is complete and visible to the work-group
+
+  // ---- pool: s over the candidates, 0 over the window; positions checked
+  const int half = p.half;
+  int32_t* s_pos = reinterpret_cast<int32_t*>(s_ring);
+  float* s_u = reinterpret_cast<float*>(s_ring) + kSnapPoolChunk + 2 * kSnapHalo;
+  int bad_pos = 0;
+  for (int c0 = 0; c0 < L; c0 += kSnapPoolChunk) {
+    for (int i = tid; i < kSnapPoolChunk + 2 * kSnapHalo; i += kSnapThreads) {
+      const int j = c0 - kSnapHalo + i;
+      int32_t pj = 0;
+      float uj = -INFINITY;
+      if (j >= 0 && j < L) {
+        pj = p.pos_pool[(size_t)s_bt[j >> 4] * kPage + (j & (kPage - 1))];
+        if (j < n_cand) uj = u[j];
+      }
+      s_pos[i] = pj;
+      s_u[i] = uj;
+    }
+    __syncthreads();
+    for (int i = tid; i < kSnapPoolChunk && c0 + i < L; i += kSnapThreads) {
+      const int j = c0 + i;
+      const int x = i + kSnapHalo;
+      const int32_t pj = s_pos[x];
+      if (j > 0 && s_pos[x - 1] >= pj) bad_pos = 1;
+      float s = 0.f;
+      if (j < n_cand) {
+        s = s_u[x];
+        for (int k = 1; k <= half; ++k) {
+          // slots outside [0, n_cand) hold -inf; positions strictly increase, so
+          // the candidates within half positions are within half slots
+          if ((int64_t)pj - s_pos[x - k] <= half) s = fmaxf(s, s_u[x - k]);
+          if ((int64_t)s_pos[x + k] - pj <= half) s = fmaxf(s, s_u[x + k]);
+        }
+      }
+      p.score_pool[(size_t)s_bt[j >> 4] * kPage + (j & (kPage - 1))] = s;
+    }
+    __syncthreads();
+  }
+  bad_pos = block_reduce<kSnapThreads>(bad_pos, s_red, [](int a, int b) { return a | b; });
+  if (bad_pos && tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_POSITIONS);
+}
+
+template <int D>
+void launch_snapkv_d(const SnapParams& p, int num_units, int rows, hipStream_t stream) {
+  if (rows <= 64)
+    hipLaunchKernelGGL((snapkv_score_kernel<D, 1>), dim3(num_units), dim3(kSnapThreads), 0, stream, p);
+  else
+    hipLaunchKernelGGL((snapkv_score_kernel<D, 2>), dim3(num_units), dim3(kSnapThreads), 0, stream, p);
+}
+
+}  // namespace se
+
+using namespace se;
+
+size_t se_snapkv_workspace_bytes(int32_t num_units, int32_t max_len) {
+  if (num_units <= 0 || max_len <= 0) return 0;
+  return (size_t)num_units * align_up((size_t)max_len, 64) * sizeof(float);
+}
+
+extern "C" se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, const void* q_obs,
+                                       int32_t window, int32_t kernel, float scale, int32_t budget,
+                                       int32_t max_len, uint32_t flags, int32_t* freed_pages,
+                                       int32_t freed_stride, int32_t* freed_count, void* ws,
+                                       size_t ws_bytes, int32_t* dev_err, hipStream_t stream) {
+  se_status st = check_view(kv);
+  if (st != SE_OK) return st;
+  if (kv->kv_pool == nullptr || kv->pos_pool == nullptr || kv->score_pool == nullptr ||
+      q_obs == nullptr || dev_err == nullptr)
+    return SE_ERR_INVALID_ARGUMENT;
+  if ((flags & ~SE_SNAPKV_SCORE_ONLY) != 0) return SE_ERR_INVALID_ARGUMENT;
+  if (q_per_kv < 1 || window < 1 || budget < window || max_len < 1) return SE_ERR_INVALID_ARGUMENT;
+  if (kernel < 1 || (kernel & 1) == 0) return SE_ERR_INVALID_ARGUMENT;
+  if (!(scale > 0.f) || !(scale < INFINITY)) return SE_ERR_INVALID_ARGUMENT;
+  if (freed_pages != nullptr && freed_stride < kv->max_pages) return SE_ERR_INVALID_ARGUMENT;
+  if ((int64_t)window * q_per_kv > kSnapMaxRows || kernel / 2 > kSnapMaxHalf) return SE_ERR_UNSUPPORTED;
+  if (budget > kMaxBudget || max_len > kSnapMaxPages * kPage) return SE_ERR_UNSUPPORTED;
+  const size_t need = se_snapkv_workspace_bytes(kv->num_units, max_len);
+  if (ws == nullptr || ws_bytes < need) return SE_ERR_WORKSPACE;
+
+  SnapParams p;
+  p.kv = static_cast<const uint16_t*>(kv->kv_pool);
+  p.pos_pool = kv->pos_pool;
+  p.score_pool = kv->score_pool;
+  p.block_table = kv->block_table;
+  p.lengths = kv->lengths;
+  p.q = static_cast<const uint16_t*>(q_obs);
+  p.u = static_cast<float*>(ws);
+  p.num_pages = kv->num_pages;
+  p.max_pages = kv->max_pages;
+  p.num_kv_heads = kv->num_kv_heads;
+  p.q_per_kv = q_per_kv;
+  p.w = window;
+  p.half = kernel / 2;
+  p.budget = budget;
+  p.max_len = max_len;
+  p.u_stride = (int32_t)align_up((size_t)max_len, 64);
+  p.c = scale * kLog2e;
+  p.dev_err = dev_err;
+  const int rows = window * q_per_kv;
+  if (kv->head_dim == 128)
+    launch_snapkv_d<128>(p, kv->num_units, rows, stream);
+  else
+    launch_snapkv_d<64>(p, kv->num_units, rows, stream);
+  st = launch_status();
+  if (st != SE_OK || (flags & SE_SNAPKV_SCORE_ONLY)) return st;
+
+  EvictParams e;
+  e.kv = static_cast<uint16_t*>(kv->kv_pool);
+  e.pos_pool = kv->pos_pool;
+  e.score_pool = kv->score_pool;
+  e.block_table = kv->block_table;
+  e.lengths = kv->lengths;
+  e.num_pages = kv->num_pages;
+  e.max_pages = kv->max_pages;
+  e.budget = budget;
+  e.recent = window;
+  e.max_len = max_len;
+  e.freed_pages = freed_pages;
+  e.freed_stride = freed_stride;
+  e.freed_count = freed_count;
+  e.dev_err = dev_err;
+  launch_evict(e, kv->num_units, kv->head_dim, stream);
+  return launch_status();
+}

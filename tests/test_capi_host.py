@@ -19,7 +19,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 11, names
+    assert len(names) == 12, names
     lib = b.raw_library()
     for n in names:
         assert hasattr(lib, n), f"{n} is declared in sparse_engine.h but not exported"
@@ -103,6 +103,33 @@ def test_evict_and_quest_argument_checks():
               None, None, 0, 0xA000, None) == b.SE_ERR_WORKSPACE
 
 
+def test_snapkv_argument_checks():
+    sk = b.raw_library().se_snapkv_compact
+    v = _view()
+
+    def call(view=v, G=4, q=0x7000, window=32, kernel=7, scale=0.1, budget=256, max_len=4096, flags=0,
+             freed=None, stride=0, ws=0x9000, ws_bytes=1 << 40, err=0xA000):
+        return sk(ctypes.byref(view), G, q, window, kernel, scale, budget, max_len, flags, freed, stride,
+                  None, ws, ws_bytes, err, None)
+
+    assert call(q=None) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(window=0) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(budget=16) == b.SE_ERR_INVALID_ARGUMENT            # budget < window
+    assert call(kernel=6) == b.SE_ERR_INVALID_ARGUMENT             # even width
+    assert call(kernel=0) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(kernel=33) == b.SE_ERR_UNSUPPORTED
+    assert call(G=8, window=32) == b.SE_ERR_UNSUPPORTED            # 256 observation rows
+    assert call(flags=2) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(scale=0.0) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(budget=9000) == b.SE_ERR_UNSUPPORTED
+    assert call(max_len=131073) == b.SE_ERR_UNSUPPORTED
+    assert call(freed=0x100, stride=2) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(ws=None) == b.SE_ERR_WORKSPACE
+    assert call(ws_bytes=16) == b.SE_ERR_WORKSPACE
+    assert call(err=None) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(view=_view(score_pool=None)) == b.SE_ERR_INVALID_ARGUMENT
+
+
 def test_workspace_sizes():
     # decode: counters + split partials + per-slot weights + per-page references
     n = b.se_workspace_bytes(b.SE_OP_DECODE_ATTEND, 512, 2049, 129, 4, 128, 0)
@@ -112,4 +139,6 @@ def test_workspace_sizes():
     assert b.se_workspace_bytes(b.SE_OP_QUEST_SELECT, 256, 33024, 2064, 4, 128, 0) >= 256 * 2064 * 4
     ns = b.se_workspace_bytes(b.SE_OP_QUEST_STEP, 256, 33024, 2064, 4, 128, 64)
     assert ns == nq + b.se_workspace_bytes(b.SE_OP_QUEST_SELECT, 256, 33024, 2064, 4, 128, 0)
+    assert b.se_workspace_bytes(b.SE_OP_SNAPKV, 512, 32768, 2048, 4, 128, 0) == 512 * 32768 * 4
+    assert b.se_workspace_bytes(b.SE_OP_SNAPKV, 3, 1000, 63, 4, 128, 0) == 3 * 1024 * 4
     assert b.se_workspace_bytes(99, 1, 1, 1, 1, 64, 0) == 0

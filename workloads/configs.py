@@ -17,7 +17,7 @@ from typing import Optional, Tuple
 class Workload:
     index: int
     name: str
-    method: str                      # "h2o" or "quest"
+    method: str                      # "h2o", "quest" or "snapkv" (prompt compaction)
     num_req: int
     hq: int
     hkv: int
@@ -32,6 +32,8 @@ class Workload:
     budget: Optional[int] = None     # H2O retained budget B
     recent: Optional[int] = None     # H2O protected recent window w
     top_k: Optional[int] = None      # Quest selected pages per KV head
+    obs_window: Optional[int] = None  # SnapKV observation window w (the prompt's last w positions)
+    pool_kernel: Optional[int] = None  # SnapKV max-pooling width kappa
     hh_rate: float = 0.0             # share of positions whose key gets += hh_shift * u
     hh_shift: float = 0.0
     relevant_pages: int = 0          # Quest: pages whose keys all get += relevant_shift * u
@@ -66,6 +68,15 @@ CONFIGS = [
              steps=64, ctx=131072, initial_resident=4096, budget=4096, recent=512,
              hh_rate=0.01, hh_shift=4.0, seed=4),
 ]
+
+
+# SnapKV prompt compaction after prefill (Appendix A.3, SnapKV; Appendix D uses
+# a 32-token scoring window and pooling kernel 7): the prefilled prompt of
+# every (request, KV head) is cut from 32768 slots to the 2048 that the H2O
+# decode workload starts from, window 32 included.
+SNAPKV = Workload(5, "llama3-8b-prompt-snapkv", "snapkv", num_req=64, hq=32, hkv=8, head_dim=128,
+                  layers=1, steps=1, ctx=32768, budget=2048, obs_window=32, pool_kernel=7,
+                  hh_rate=0.01, hh_shift=4.0, seed=5)
 
 
 def scaled(w: Workload, **changes) -> Workload:

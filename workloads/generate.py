@@ -19,7 +19,7 @@ Value recipe (the workloads' own description):
   * q, K, V ~ N(0, 1) in float32, rounded to bf16;
   * one unit vector u per (layer, KV head), shared by every request, position
     and step; every query head of the group gets q += u before rounding;
-  * H2O workloads: a position is a heavy hitter with probability hh_rate,
+  * H2O and SnapKV workloads: a position is a heavy hitter with probability hh_rate,
     decided by a counter-based integer hash of (seed, layer, unit, position),
     so the initial context and later decode tokens follow the same rule; a
     heavy hitter's key gets += hh_shift * u before rounding to bf16 (for the
@@ -28,7 +28,10 @@ Value recipe (the workloads' own description):
     += relevant_shift * u on all their keys;
   * ragged / retained workloads: the last `recent` positions of the context
     plus a stratified random sample (one position per stratum, so sorted and
-    without repeats) of the older ones.
+    without repeats) of the older ones;
+  * SnapKV workload: the whole prefilled prompt is resident (slot s holds
+    position s) and the observation queries of its last obs_window positions
+    are N(0, 1) + u, rounded to bf16, like decode queries.
 No part of attention, scoring, selection or compaction is computed here.
 """
 
@@ -144,6 +147,8 @@ def build_state(w: Workload, device, generate_values: bool = True) -> PagedInput
     L0 = _initial_lengths(w, ctx, device)
     if w.method == "h2o":
         cap_slots = int(max(int(L0.max()), int(w.budget)) + 1)
+    elif w.method == "snapkv":
+        cap_slots = int(L0.max())
     else:
         cap_slots = int(L0.max()) + w.steps
     max_pages = -(-cap_slots // P)
@@ -154,7 +159,8 @@ def build_state(w: Workload, device, generate_values: bool = True) -> PagedInput
     block_table = perm.to(torch.int32).view(w.layers * U, max_pages)
     kv_pool = torch.empty((num_pages, 2, P, d), dtype=torch.bfloat16, device=device)
     pos_pool = torch.full((num_pages, P), -1, dtype=torch.int32, device=device)
-    score_pool = torch.zeros((num_pages, P), dtype=torch.float32, device=device) if w.method == "h2o" else None
+    score_pool = (torch.zeros((num_pages, P), dtype=torch.float32, device=device)
+                  if w.method in ("h2o", "snapkv") else None)
     meta_pool = torch.zeros((num_pages, 2, d), dtype=torch.bfloat16, device=device) if w.method == "quest" else None
     lengths = L0.to(torch.int32).repeat(w.layers)
 
@@ -181,7 +187,7 @@ def build_state(w: Workload, device, generate_values: bool = True) -> PagedInput
         if not generate_values:
             continue
         shift = None
-        if w.method == "h2o" and w.hh_rate > 0:
+        if w.method in ("h2o", "snapkv") and w.hh_rate > 0:
             unit_ids = torch.arange(U, device=device)[:, None].expand(U, cap)
             shift = valid & heavy_hitter(w, layer, unit_ids, pos.clamp(min=0))
             amount = w.hh_shift
@@ -230,6 +236,22 @@ def build_steps(w: Workload, state: PagedInputs, device, steps: Optional[int] = 
             k_new[t, layer] = kx.to(torch.bfloat16)
             v_new[t, layer] = torch.randn((w.num_req, w.hkv, d), generator=gv, device=device).to(torch.bfloat16)
     return StepInputs(q=q, k_new=k_new, v_new=v_new, new_pos=new_pos)
+
+
+def build_observation(w: Workload, state: PagedInputs, device, layer: int = 0) -> torch.Tensor:
+    """Observation queries of a SnapKV workload: bf16 [num_req][obs_window][hq][d],
+    query t at the t-th of the prompt's last obs_window positions."""
+    g = _gen(w, 20 + layer, device)
+    x = torch.randn((w.num_req, w.obs_window, w.hq, w.head_dim), generator=g, device=device)
+    qshift = state.uvec[layer].to(device).repeat_interleave(w.q_per_kv, dim=0)  # [hq, d]
+    return (x + qshift[None, None]).to(torch.bfloat16)
+
+
+def observation_queries(num_req: int, window: int, hq: int, head_dim: int, seed: int, device="cpu") -> torch.Tensor:
+    """N(0, 1) observation queries, bf16 [num_req][window][hq][head_dim] (single-call tests)."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed * 7919 + 23)
+    return torch.randn((num_req, window, hq, head_dim), generator=g).to(torch.bfloat16).to(device)
 
 
 def to_device(state: PagedInputs, device) -> PagedInputs:
