@@ -3,27 +3,29 @@
 // background-snapkv-retention), applied to a unit's prompt after its last
 // prefill chunk (Section 3.1, finish_step during prefill).
 //
-// Scoring runs one work-group of four wavefronts per unit, two work-groups per
-// compute unit.  The w observation queries of the unit's G heads form
-// R = w*G <= 128 rows; wavefront v holds rows [32v, 32v + 32) in registers as
-// MFMA A operands (bf16 16x16x32 tiles: lane l holds row l%16 and contraction
-// indices 8*(l/16)..+7 of each 32-wide step).  The unit's key pages stream
-// through a two-stage LDS ring, four pages a stage: every thread loads one
-// 16-byte piece of each page (4 KB coalesced per page at head_dim 128), two
-// stages ahead, into registers, and writes it to LDS with the piece index
-// XORed with the key so that the B-operand reads (lane l: key l%16) hit
-// distinct banks.  A page (16 keys) is one B tile; the 16x16 output tile gives
-// lane l the logits of key l%16 against rows 4*(l/16)..+3 of each row tile.
+// Scoring runs one work-group of eight wavefronts per unit, two work-groups
+// per compute unit.  The w observation queries of the unit's G heads form
+// R = w*G <= 128 rows in four row groups of 32; wavefront v holds row group
+// v % 4 in registers as MFMA A operands (bf16 16x16x32 tiles: lane l holds
+// row l%16 and contraction indices 8*(l/16)..+7 of each 32-wide step) and
+// takes the pages of key half v / 4 of every stage.  The unit's key pages
+// stream through a two-stage LDS ring of four pages a stage: the work-group
+// loads every page as coalesced 16-byte pieces, two stages ahead, into
+// registers, and writes them to LDS with the piece index XORed with the key
+// so that the B-operand reads (lane l: key l%16) hit distinct banks.  A page
+// (16 keys) is one B tile; the 16x16 output tile gives lane l the logits of
+// key l%16 against rows 4*(l/16)..+3 of each row tile.
 //   pass 1  row normalisers: every lane keeps, per row, a reference and the
 //           sum of exp2(c*z - reference) over its keys (c = scale*log2 e); a
 //           reference moves only when a logit passes it by more than kLazy,
 //           so most pages cost one fma, one max, one exp2 and one add per
-//           logit.  Merging the 16 key lanes of a row gives
-//           bias = log2 of the row's softmax denominator.
+//           logit.  Merging the 16 key lanes and the two key halves of a row
+//           gives bias = log2 of the row's softmax denominator.
 //   pass 2  u(j) = sum over rows of exp2(c*z - bias) for the candidate keys:
-//           in-lane over the lane's rows, across the row groups of the
-//           wavefront with shuffles, across the wavefronts through LDS;
-//           written to the workspace.
+//           in-lane over the lane's rows, across the lane groups with permlane
+//           swaps; each wavefront leaves its row group's sums in LDS, and once
+//           the stage has passed a wavefront adds the four row groups of each
+//           key of one page and writes u to the workspace.
 //   pool    s(j) = max of u over the candidates within kappa/2 positions of j,
 //           through LDS chunks with a halo; s goes to the score field of the
 //           candidates and 0 to the window's, and a slot order that is not
@@ -42,12 +44,16 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kSnapThreads = 256;
+constexpr int kSnapThreads = 512;
 constexpr int kSnapWaves = kSnapThreads / kWave;
+constexpr int kSnapRowGroups = 4;       // 32 rows each
+constexpr int kSnapHalves = kSnapWaves / kSnapRowGroups;  // key halves of a stage
 constexpr int kSnapMaxRows = 128;
 constexpr int kSnapMaxHalf = 15;        // kappa <= 31
-constexpr int kSnapMaxPages = 8192;     // block-table entries staged in LDS (131072 slots)
+constexpr int kSnapMaxPages = 8192;     // pages per unit (131072 slots)
 constexpr int kSnapStagePages = 4;      // pages per ring stage
+constexpr int kSnapHalfPages = kSnapStagePages / kSnapHalves;
+constexpr int kSnapBatches = 2;         // stages in flight per thread
 constexpr int kSnapPoolChunk = 2048;    // slots pooled per LDS round
 constexpr int kSnapHalo = kSnapMaxHalf + 1;
 constexpr float kLazy = 20.f;           // log2 headroom before a reference moves
@@ -87,58 +93,76 @@ __device__ __forceinline__ int ring_offset(int key, int piece) {
   return key * (2 * D) + ((piece ^ (key & (PC - 1))) << 4);
 }
 
-// Streams pages [pb, pe) of the unit through the LDS ring; body(j, stage)
+// Streams pages [pb, pe) of the unit through the LDS ring; body(j, slot)
 // runs once per stage of kSnapStagePages pages (stage j holds pages
-// pb + j*kSnapStagePages ...), every thread of the work-group taking part.
-// Loads run two stages ahead; loads past the range re-read its last page.
+// pb + j*kSnapStagePages ..., in ring slot j % 2), every thread of the
+// work-group taking part.  Each thread keeps kSnapBatches stages of its
+// pieces in flight in registers (a stage's loads are issued kSnapBatches - 1
+// stages before it is written to LDS); loads past the range re-read its last
+// page.  The loop is unrolled by kSnapBatches so that every batch keeps its
+// registers, and has no exit between its steps, so the loop head is reached
+// with the same loads in flight on every path.
+// A block-table entry at a wavefront-uniform index, as a scalar load: the
+// table is read-only for the whole launch, so it may go through the constant
+// address space.
+typedef const __attribute__((address_space(4))) int32_t* const_i32_ptr;
+__device__ __forceinline__ int bt_entry(const int32_t* bt, int i) {
+  return ((const_i32_ptr)bt)[__builtin_amdgcn_readfirstlane(i)];
+}
+
 template <int D, typename Body>
-__device__ __forceinline__ void stream_stages(const SnapParams& p, const int* lds_bt, uint8_t* ring, int pb, int pe,
+__device__ __forceinline__ void stream_stages(const SnapParams& p, const int32_t* bt, uint8_t* ring, int pb, int pe,
                                               Body body) {
   constexpr int S = kSnapStagePages;
-  constexpr int PB = 32 * D;       // K bytes of a page
-  constexpr int PC = D / 8;        // 16-byte pieces per key
+  constexpr int NB = kSnapBatches;
+  constexpr int PB = 32 * D;                       // K bytes of a page
+  constexpr int PC = D / 8;                        // 16-byte pieces per key
+  constexpr int PT = S * 2 * D / kSnapThreads;     // pieces per thread per stage
+  static_assert(NB % 2 == 0, "ring slots alternate within the unrolled loop");
+  static_assert(PT >= 1 && PT * kSnapThreads == S * 2 * D, "whole pages per stage");
   const int n_st = ceil_div_dev(pe - pb, S);
   if (n_st <= 0) return;
-  // piece t of a page goes to thread t (head_dim 64: threads 128..255 repeat
-  // the loads of 0..127 and store nothing)
-  const int tid = threadIdx.x & (2 * D - 1);
-  const bool loader = (int)threadIdx.x < 2 * D;
-  const int key = tid / PC;
-  const int piece = tid & (PC - 1);
-  const int lds_off = ring_offset<D>(key, piece);
-  auto load = [&](u32x4_t(&r)[S], int st) {
+  // piece g = threadIdx.x + q * kSnapThreads of a stage: page g / (2D), piece g % (2D)
+  int pg_of[PT], off_of[PT], lds_of[PT];
 #pragma unroll
-    for (int i = 0; i < S; ++i) {
-      const int pg = min(pb + st * S + i, pe - 1);
-      r[i] = *reinterpret_cast<const u32x4_t*>(p.kv + (size_t)lds_bt[pg] * 2 * kPage * D + (size_t)tid * 8);
+  for (int q = 0; q < PT; ++q) {
+    const int g = (int)threadIdx.x + q * kSnapThreads;
+    const int pp = g / (2 * D);
+    const int t = g % (2 * D);
+    pg_of[q] = __builtin_amdgcn_readfirstlane(pp);  // 2D is a multiple of the wavefront
+    off_of[q] = t * 8;
+    lds_of[q] = pp * PB + ring_offset<D>(t / PC, t % PC);
+  }
+  auto load = [&](u32x4_t(&r)[PT], int st) {
+#pragma unroll
+    for (int q = 0; q < PT; ++q) {
+      const int pg = min(pb + st * S + pg_of[q], pe - 1);  // the same in every lane of a wavefront
+      r[q] = *reinterpret_cast<const u32x4_t*>(p.kv + (size_t)bt_entry(bt, pg) * 2 * kPage * D + off_of[q]);
     }
   };
-  auto store = [&](const u32x4_t(&r)[S], int stage) {
+  auto store = [&](const u32x4_t(&r)[PT], int slot) {
 #pragma unroll
-    for (int i = 0; i < S; ++i)
-      if (loader) *reinterpret_cast<u32x4_t*>(ring + (stage * S + i) * PB + lds_off) = r[i];
+    for (int q = 0; q < PT; ++q) *reinterpret_cast<u32x4_t*>(ring + slot * S * PB + lds_of[q]) = r[q];
   };
-  // issue order as in the loop (stage j + 1 older than stage j + 2), so that
-  // the waits at the loop head are the same from both entries
-  u32x4_t ra[S], rb[S];
-  load(ra, 0);
-  store(ra, 0);
+  u32x4_t r[NB][PT];
+  load(r[0], 0);
+  store(r[0], 0);
+#pragma unroll
+  for (int b = 1; b < NB; ++b) {
+    asm volatile("" ::: "memory");  // issue order: stage b before stage b + 1
+    load(r[b], b);
+  }
   asm volatile("" ::: "memory");
-  load(rb, 1);
-  asm volatile("" ::: "memory");
-  load(ra, 2);
+  load(r[0], NB);
   __syncthreads();
-  // both halves run every time (no exit between them), so the loop head is
-  // reached with the same loads in flight on every path
-  for (int j = 0; j < n_st; j += 2) {
-    store(rb, 1);      // stage j + 1
-    load(rb, j + 3);
-    body(j, 0);
-    __syncthreads();
-    store(ra, 0);      // stage j + 2
-    load(ra, j + 4);
-    if (j + 1 < n_st) body(j + 1, 1);
-    __syncthreads();
+  for (int j = 0; j < n_st; j += NB) {
+#pragma unroll
+    for (int k = 0; k < NB; ++k) {
+      store(r[(k + 1) % NB], (k + 1) & 1);  // stage j + k + 1
+      load(r[(k + 1) % NB], j + k + 1 + NB);
+      if (j + k < n_st) body(j + k, k & 1);
+      __syncthreads();
+    }
   }
 }
 
@@ -161,6 +185,18 @@ __device__ __forceinline__ void page_logits(const uint4 (&qa)[RTW][D / 32], cons
     for (int T = 0; T < RTW; ++T) acc[T] = mfma16x16x32(qa[T][s], kb[s], acc[T]);
 }
 
+// Sum over the four 16-lane groups of a wavefront, in every lane (lane l gets
+// the sum of lanes l%16, l%16 + 16, l%16 + 32, l%16 + 48): the upper and lower
+// halves, then the odd and even 16-lane rows, exchanged by permlane swaps.
+__device__ __forceinline__ float lane_group_sum(float x) {
+  const uint32_t b = __float_as_uint(x);
+  const auto h = __builtin_amdgcn_permlane32_swap(b, b, false, false);
+  const float y = __uint_as_float(h[0]) + __uint_as_float(h[1]);
+  const uint32_t c = __float_as_uint(y);
+  const auto r = __builtin_amdgcn_permlane16_swap(c, c, false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // (ref, sum) pairs merged: the sum re-expressed against the larger reference.
 __device__ __forceinline__ void merge_norm(float& ref, float& sum, float ref2, float sum2) {
   const float m = fmaxf(ref, ref2);
@@ -168,17 +204,18 @@ __device__ __forceinline__ void merge_norm(float& ref, float& sum, float ref2, f
   ref = m;
 }
 
-// RTW: 16-row tiles per wavefront (rows of wavefront v: [16*RTW*v, 16*RTW*(v+1))).
+// RTW: 16-row tiles per row group (rows of group g: [16*RTW*g, 16*RTW*(g+1))).
 template <int D, int RTW>
-__global__ __launch_bounds__(kSnapThreads, 2) void snapkv_score_kernel(const SnapParams p) {
+__global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const SnapParams p) {
   constexpr int KS = D / 32;
   constexpr int S = kSnapStagePages;
+  constexpr int H = kSnapHalfPages;
   constexpr int PB = 32 * D;
   constexpr int kRingBytes = 2 * S * 32 * 128;  // sized for head_dim 128
   static_assert(kRingBytes >= (kSnapPoolChunk + 2 * kSnapHalo) * 8, "the pool chunk reuses the ring");
   __shared__ __attribute__((aligned(16))) uint8_t s_ring[kRingBytes];
-  __shared__ int s_bt[kSnapMaxPages];
-  __shared__ float s_up[2][kSnapWaves][S * kPage];
+  __shared__ float s_up[2][S][kSnapRowGroups][kPage];     // [stage parity][page][row group][key]
+  __shared__ float s_norm[kSnapHalves][2][kSnapMaxRows];   // [key half][ref, sum][row]
   __shared__ int s_red[kSnapWaves];
 
   const int tid = threadIdx.x;
@@ -186,6 +223,8 @@ __global__ __launch_bounds__(kSnapThreads, 2) void snapkv_score_kernel(const Sna
   const int grp = lane >> 4;
   const int col = lane & 15;
   const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int rg = wv % kSnapRowGroups;
+  const int kh = wv / kSnapRowGroups;
   const int unit = blockIdx.x;
   const int L = p.lengths[unit];
   if (L <= p.budget) return;  // the prompt already fits: nothing to score or evict
@@ -200,9 +239,8 @@ __global__ __launch_bounds__(kSnapThreads, 2) void snapkv_score_kernel(const Sna
     for (int i = tid; i < n_pages; i += kSnapThreads) {
       const int ph = bt[i];
       bad |= (ph < 0 || (int64_t)ph >= p.num_pages);
-      s_bt[i] = ph;
     }
-    bad = block_reduce<kSnapThreads>(bad, s_red, [](int a, int b) { return a | b; });  // also publishes s_bt
+    bad = block_reduce<kSnapThreads>(bad, s_red, [](int a, int b) { return a | b; });
     if (bad) {
       if (tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
       return;
@@ -212,9 +250,9 @@ __global__ __launch_bounds__(kSnapThreads, 2) void snapkv_score_kernel(const Sna
   const int G = p.q_per_kv;
   const int R = w * G;
   const int n_cand = L - w;  // >= 1: L > budget >= w
-  const int row0 = 16 * RTW * wv;
+  const int row0 = 16 * RTW * rg;
 
-  // ---- the wavefront's observation queries (A operands); rows past R are zero
+  // ---- the row group's observation queries (A operands); rows past R are zero
   uint4 qa[RTW][KS];
   {
     const int req = unit / p.num_kv_heads;
@@ -251,13 +289,15 @@ __global__ __launch_bounds__(kSnapThreads, 2) void snapkv_score_kernel(const Sna
       ref[T][r] = kRefInit;
       sum[T][r] = 0.f;
     }
-  stream_stages<D>(p, s_bt, s_ring, 0, n_pages, [&](int j, int stage) {
+  stream_stages<D>(p, bt, s_ring, 0, n_pages, [&](int j, int slot) {
+    // the half's logits first (independent MFMA chains), then the updates
+    f32x4_t acc[H][RTW];
 #pragma unroll
-    for (int i = 0; i < S; ++i) {
-      const int pg = j * S + i;
+    for (int i = 0; i < H; ++i) page_logits<D, RTW>(qa, s_ring + (slot * S + kh * H + i) * PB, acc[i]);
+#pragma unroll
+    for (int i = 0; i < H; ++i) {
+      const int pg = j * S + kh * H + i;
       if (pg >= n_pages) break;
-      f32x4_t acc[RTW];
-      page_logits<D, RTW>(qa, s_ring + (stage * S + i) * PB, acc);
       if (pg >= p_full) {
         // causal mask: key j is seen by the rows of window position t iff
         // j <= L - w + t (so j < L); padded rows see nothing
@@ -268,7 +308,7 @@ __global__ __launch_bounds__(kSnapThreads, 2) void snapkv_score_kernel(const Sna
           for (int r = 0; r < 4; ++r) {
             const int row = row0 + 16 * T + 4 * grp + r;
             const int lim = row < R ? L - w + row / G : -1;
-            if (key > lim) acc[T][r] = -INFINITY;
+            if (key > lim) acc[i][T][r] = -INFINITY;
           }
       }
       float dmax = -INFINITY;
@@ -277,7 +317,7 @@ __global__ __launch_bounds__(kSnapThreads, 2) void snapkv_score_kernel(const Sna
       for (int T = 0; T < RTW; ++T)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          d[T][r] = fmaf(acc[T][r], c, -ref[T][r]);
+          d[T][r] = fmaf(acc[i][T][r], c, -ref[T][r]);
           dmax = fmaxf(dmax, d[T][r]);
         }
       if (__builtin_amdgcn_ballot_w64(dmax > kLazy) != 0) {
@@ -286,7 +326,7 @@ __global__ __launch_bounds__(kSnapThreads, 2) void snapkv_score_kernel(const Sna
         for (int T = 0; T < RTW; ++T)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const float zc = acc[T][r] * c;
+            const float zc = acc[i][T][r] * c;
             const float m = fmaxf(ref[T][r], zc);
             sum[T][r] *= fast_exp2(ref[T][r] - m);
             d[T][r] = zc - m;
@@ -299,8 +339,8 @@ __global__ __launch_bounds__(kSnapThreads, 2) void snapkv_score_kernel(const Sna
         for (int r = 0; r < 4; ++r) sum[T][r] += fast_exp2(d[T][r]);
     }
   });
-  // merge the 16 key lanes of each row: bias = log2 of the softmax denominator
-  float bias[RTW][4];
+  // merge the 16 key lanes of each row, then the two key halves through LDS:
+  // bias = log2 of the softmax denominator
 #pragma unroll
   for (int T = 0; T < RTW; ++T)
 #pragma unroll
@@ -308,43 +348,63 @@ __global__ __launch_bounds__(kSnapThreads, 2) void snapkv_score_kernel(const Sna
 #pragma unroll
       for (int m = 1; m < 16; m <<= 1)
         merge_norm(ref[T][r], sum[T][r], shfl_xor_f(ref[T][r], m), shfl_xor_f(sum[T][r], m));
+      if (col == 0) {
+        s_norm[kh][0][row0 + 16 * T + 4 * grp + r] = ref[T][r];
+        s_norm[kh][1][row0 + 16 * T + 4 * grp + r] = sum[T][r];
+      }
+    }
+  __syncthreads();
+  float bias[RTW][4];
+#pragma unroll
+  for (int T = 0; T < RTW; ++T)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
       const int row = row0 + 16 * T + 4 * grp + r;
-      bias[T][r] = row < R ? ref[T][r] + __log2f(sum[T][r]) : INFINITY;
+      float m = s_norm[0][0][row], sm = s_norm[0][1][row];
+#pragma unroll
+      for (int h = 1; h < kSnapHalves; ++h) merge_norm(m, sm, s_norm[h][0][row], s_norm[h][1][row]);
+      bias[T][r] = row < R ? m + __log2f(sm) : INFINITY;
     }
 
   // ---- pass 2: u over the candidate keys (every row sees them; no mask)
   float* u = p.u + (size_t)unit * p.u_stride;
   const int cand_pages = ceil_div_dev(n_cand, kPage);
-  // the four wavefronts' partial sums of stage j are added once the stage's
-  // barrier has passed (by wavefront 0 while the next stage runs, or after
-  // the stream for the last stage)
+  // every wavefront leaves its row group's sum for each key of each page of
+  // stage j in LDS; once the stage's barrier has passed, wavefront v < S adds
+  // the four row groups of each key of page v (while the next stage runs, or
+  // after the stream for the last stage)
+  static_assert(S <= kSnapWaves, "one page of a stage per adding wavefront");
   auto flush = [&](int j) {
-    if (wv == 0) {
-      const int key = j * S * kPage + lane;
-      const float* up = &s_up[j & 1][0][0];
-      const float v = up[lane] + up[S * kPage + lane] + up[2 * S * kPage + lane] + up[3 * S * kPage + lane];
+    if (wv < S && lane < kPage) {
+      const float* up = &s_up[j & 1][wv][0][lane];
+      float v = 0.f;
+#pragma unroll
+      for (int g = 0; g < kSnapRowGroups; ++g) v += up[g * kPage];
+      const int key = (j * S + wv) * kPage + lane;
       if (key < n_cand) u[key] = v;
     }
   };
-  static_assert(S * kPage == kWave, "wavefront 0 adds one key per lane");
   const int n_st2 = ceil_div_dev(cand_pages, S);
-  stream_stages<D>(p, s_bt, s_ring, 0, cand_pages, [&](int j, int stage) {
+  stream_stages<D>(p, bt, s_ring, 0, cand_pages, [&](int j, int slot) {
     if (j > 0) flush(j - 1);
+    f32x4_t acc[H][RTW];
 #pragma unroll
-    for (int i = 0; i < S; ++i) {
-      const int pg = j * S + i;
-      float us = 0.f;
-      if (pg < cand_pages) {
-        f32x4_t acc[RTW];
-        page_logits<D, RTW>(qa, s_ring + (stage * S + i) * PB, acc);
+    for (int i = 0; i < H; ++i) page_logits<D, RTW>(qa, s_ring + (slot * S + kh * H + i) * PB, acc[i]);
 #pragma unroll
-        for (int T = 0; T < RTW; ++T)
+    for (int i = 0; i < H; ++i) {
+      // a sum tree over the lane's rows (independent exp2s, short add chains)
+      float e[RTW * 4];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) us += fast_exp2(fmaf(acc[T][r], c, -bias[T][r]));
-        us += shfl_xor_f(us, 16);
-        us += shfl_xor_f(us, 32);
-      }
-      if (grp == 0) s_up[j & 1][wv][i * kPage + col] = us;
+      for (int T = 0; T < RTW; ++T)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) e[4 * T + r] = fast_exp2(fmaf(acc[i][T][r], c, -bias[T][r]));
+#pragma unroll
+      for (int n = RTW * 4; n > 1; n >>= 1)
+#pragma unroll
+        for (int k = 0; k < n / 2; ++k) e[k] = e[2 * k] + e[2 * k + 1];
+      // the four lane groups (rows 4*(lane/16)..+3 of each tile) of key lane%16
+      const float us = lane_group_sum(e[0]);
+      if (grp == 0) s_up[j & 1][kh * H + i][rg][col] = us;  // pages past the candidates are never added
     }
   });
   if (n_st2 > 0) flush(n_st2 - 1);
@@ -361,7 +421,7 @@ __global__ __launch_bounds__(kSnapThreads, 2) void snapkv_score_kernel(const Sna
       int32_t pj = 0;
       float uj = -INFINITY;
       if (j >= 0 && j < L) {
-        pj = p.pos_pool[(size_t)s_bt[j >> 4] * kPage + (j & (kPage - 1))];
+        pj = p.pos_pool[(size_t)bt[j >> 4] * kPage + (j & (kPage - 1))];
         if (j < n_cand) uj = u[j];
       }
       s_pos[i] = pj;
@@ -383,7 +443,7 @@ __global__ __launch_bounds__(kSnapThreads, 2) void snapkv_score_kernel(const Sna
           if ((int64_t)s_pos[x + k] - pj <= half) s = fmaxf(s, s_u[x + k]);
         }
       }
-      p.score_pool[(size_t)s_bt[j >> 4] * kPage + (j & (kPage - 1))] = s;
+      p.score_pool[(size_t)bt[j >> 4] * kPage + (j & (kPage - 1))] = s;
     }
     __syncthreads();
   }
