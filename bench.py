@@ -15,7 +15,11 @@ bracketed by device synchronisations; per-call HIP events on the launch
 stream give each kernel's duration for the roofline figure.
 
 Prints one JSON line.  `--config N` runs another workload (0..4) for
-measurement; `--gpus N` with N > 1 is refused (single-GPU build).
+measurement; `--workload snapkv` measures SnapKV prompt compaction instead
+(se_snapkv_compact on the 8B-shaped prompt: 64 requests x 8 KV heads x 32768
+slots, window 32, pooling width 7, budget 2048; one step is one compaction of
+the whole batch from a fresh copy of the prompt); `--gpus N` with N > 1 is
+refused (single-GPU build).
 """
 
 import argparse
@@ -31,14 +35,19 @@ sys.path.insert(0, ROOT)
 METRIC = "decode attn+eviction tokens/s/GPU; achieved HBM GB/s vs MI355X peak"
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_step_h2o_llama3-8b-layer-h2o_traffic.txt")
+SNAPKV_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "snapkv_compact_llama3-8b-prompt-snapkv_traffic.txt")
+DECODE_SOURCES = ("decode_attend.hip", "evict_compact.hip", "evict_core.h", "se_common.h")
+SNAPKV_SOURCES = ("snapkv.hip", "evict_compact.hip", "evict_core.h", "se_common.h")
 
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None, help="timed decode steps (default: the workload's)")
-    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default 8; snapkv: 1)")
     ap.add_argument("--config", type=int, default=1, help="workload index 0..4")
+    ap.add_argument("--workload", choices=["decode", "snapkv"], default="decode",
+                    help="decode (the --config workload) or snapkv (prompt compaction)")
     ap.add_argument("--cpu-baseline", choices=["auto", "skip"], default="auto")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 4 GiB device copy (counter calibration under rocprofv3)")
@@ -154,24 +163,175 @@ def quest_attend_bytes(visited, G, D, top_k):
     return int(visited.sum()) * (2 * D * 2) + units * per_unit
 
 
-def source_hash():
+def snapkv_bytes(L, w, G, D, budget):
+    """Bytes se_snapkv_compact must move for units of prompt length L > budget:
+    the keys twice (the row normalisers need every key before any weight can
+    be summed), the observation queries, u written and read back, each slot's
+    position read and pooled score written; then the eviction's position and
+    score reads and the movers' K, V, position and score read and written."""
+    import numpy as np
+    L = np.asarray(L, dtype=np.int64)
+    L = L[L > budget]
+    units = int(L.shape[0])
+    score = int(L.sum()) * (2 * (D * 2) + 4 + 4 + 4 + 4) + units * (w * G * D * 2)
+    moved = np.minimum(L - budget, budget)
+    evict = int(L.sum()) * 8 + int(moved.sum()) * 2 * (2 * D * 2 + 8)
+    return score + evict
+
+
+def cpu_baseline_snapkv(w):
+    """The oracle, untuned, on a bounded sample of the SnapKV workload: the
+    first six requests (48 KV-head units of 32768 slots), one unit per worker
+    process.  Runs before the GPU is touched."""
+    import multiprocessing as mp
+    import numpy as np
+    import torch
+    from workloads import build_observation, build_state, scaled, unit_slots
+    sample_req = 6
+    ws = scaled(w, num_req=sample_req)
+    host = build_state(ws, "cpu")
+    qobs = build_observation(ws, host, "cpu")
+    G = ws.q_per_kv
+    jobs = []
+    for u in range(ws.units_per_layer):
+        req, kvh = divmod(u, ws.hkv)
+        Kt, Vt, pos, _ = unit_slots(host, u)
+        jobs.append({"K": Kt.to(torch.float64).numpy(), "V": Vt.to(torch.float64).numpy(),
+                     "pos": pos.numpy().astype(np.int64),
+                     "Qo": qobs[req, :, kvh * G:(kvh + 1) * G].to(torch.float64).numpy()})
+    _SHARED["jobs"], _SHARED["w"] = jobs, ws
+    workers = min(16, os.cpu_count() or 1, len(jobs))
+    ctx = mp.get_context("fork")
+    t0 = time.perf_counter()
+    with ctx.Pool(workers) as pool:
+        per_unit = pool.map(_oracle_snapkv_run, range(len(jobs)))
+    wall = time.perf_counter() - t0
+    return {"value": round(sample_req * ws.ctx / wall, 1), "unit": "prompt tokens/s", "cores": workers,
+            "kind": "oracle",
+            "sample": (f"{sample_req} of {w.num_req} requests ({len(jobs)} KV-head units of {ws.ctx} slots) of "
+                       f"'{w.name}', one compaction each, NumPy float64, one unit per process"),
+            "cpu_seconds": round(sum(per_unit), 2), "wall_seconds": round(wall, 2)}
+
+
+def _oracle_snapkv_run(i):
+    from threadpoolctl import threadpool_limits
+    from oracle import snapkv
+    from oracle.state import new_unit
+    job, w = _SHARED["jobs"][i], _SHARED["w"]
+    with threadpool_limits(1):
+        st = new_unit(job["K"], job["V"], job["pos"])
+        t0 = time.perf_counter()
+        snapkv.compact_prompt(st, job["Qo"], w.obs_window, w.pool_kernel, w.budget, w.scale)
+        return time.perf_counter() - t0
+
+
+def main_snapkv(args):
+    """SnapKV prompt compaction: K compactions of the whole batch, each on a
+    fresh copy of the prompt state made before its timed call."""
+    from workloads import SNAPKV
+    w = SNAPKV
+    K = int(args.steps if args.steps is not None else 5)
+    W = int(args.warmup if args.warmup is not None else 1)
+    cpu = cpu_baseline_snapkv(w) if args.cpu_baseline == "auto" else None
+    if cpu is not None:
+        print(f"cpu baseline: {cpu['value']:.1f} prompt tokens/s on {cpu['cores']} processes", file=sys.stderr,
+              flush=True)
+    import numpy as np
+    import torch
+    import paper_2609_39068_amd as se
+    from workloads import build_observation, build_state, clone_state
+
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    dev = torch.device("cuda:0")
+    state = build_state(w, dev)
+    qobs = build_observation(w, state, dev)
+    U, G, D = w.units_per_layer, w.q_per_kv, w.head_dim
+    max_len = state.max_pages * 16
+    ws = torch.empty(se.se_workspace_bytes(se.SE_OP_SNAPKV, U, max_len, state.max_pages, G, D),
+                     dtype=torch.uint8, device=dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    fcount = torch.zeros(U, dtype=torch.int32, device=dev)
+    lengths0 = state.lengths.cpu().numpy()
+
+    def call(st):
+        view = se.KVView(st.kv_pool, st.pos_pool, st.score_pool, None, st.block_table, st.lengths,
+                         num_kv_heads=w.hkv)
+        se.se_snapkv_compact(view, G, qobs, w.obs_window, w.pool_kernel, w.scale, w.budget, max_len, 0,
+                             None, 0, fcount, ws, err)
+
+    for _ in range(W):
+        c = clone_state(state)
+        call(c)
+        torch.cuda.synchronize()
+        del c
+    times, walls = [], []
+    for _ in range(K):
+        c = clone_state(state)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ev[0].record()
+        call(c)
+        ev[1].record()
+        torch.cuda.synchronize()
+        walls.append(time.perf_counter() - t0)
+        times.append(ev[0].elapsed_time(ev[1]))
+        assert int(c.lengths.max()) == w.budget
+        del c
+    errs = se.se_read_device_errors(err)
+    if errs:
+        raise RuntimeError(f"device error bits {errs:#x} during the timed run")
+    ms = float(np.mean(times))
+    elapsed = float(np.sum(walls))
+    nbytes = snapkv_bytes(lengths0, w.obs_window, G, D, w.budget)
+    achieved = nbytes / (ms * 1e-3) / 1e9
+    result = {
+        "metric": "SnapKV prompt compaction prompt-tokens/s/GPU; achieved HBM GB/s vs MI355X peak",
+        "value": round(w.num_req * w.ctx * K / elapsed, 1),
+        "unit": "prompt tokens/s",
+        "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": round(1e3 * elapsed / K, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "method": "snapkv", "batch": w.num_req, "hq": w.hq, "hkv": w.hkv,
+                   "head_dim": D, "page_size": w.page_size, "prompt": w.ctx, "window": w.obs_window,
+                   "pool_kernel": w.pool_kernel, "budget": w.budget, "accumulate": "f32",
+                   "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": "hbm", "kernel": "se_snapkv_compact", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": read_traffic(SNAPKV_TRAFFIC_SUMMARY, SNAPKV_SOURCES),
+                     "avg_launch_us": round(1e3 * ms, 3),
+                     "algorithmic_bytes_per_launch": nbytes},
+        "cpu_baseline": cpu,
+    }
+    if args.copy_calibration:
+        n = 4 << 30
+        a = torch.empty(n, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        result["copy_calibration_bytes"] = n
+    print(json.dumps(result), flush=True)
+
+
+def source_hash(files=DECODE_SOURCES):
     h = hashlib.sha256()
-    for f in ("decode_attend.hip", "evict_compact.hip", "evict_core.h", "se_common.h"):
+    for f in files:
         h.update(open(os.path.join(ROOT, "paper_2609_39068_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
 
-def read_traffic():
-    """HBM bytes per decode_attend launch from the committed rocprofv3
-    counter summary, or None when it is missing or the kernel has changed."""
-    if not os.path.exists(TRAFFIC_SUMMARY):
+def read_traffic(path=TRAFFIC_SUMMARY, files=DECODE_SOURCES):
+    """HBM bytes per call from a committed rocprofv3 counter summary, or None
+    when it is missing or the kernels have changed since it was taken."""
+    if not os.path.exists(path):
         return None
     vals = {}
-    for line in open(TRAFFIC_SUMMARY):
+    for line in open(path):
         if "=" in line and not line.lstrip().startswith("#"):
             k, v = line.split("=", 1)
             vals[k.strip()] = v.strip()
-    if vals.get("source_hash") != source_hash():
+    if vals.get("source_hash") != source_hash(files):
         return None
     try:
         return float(vals["hbm_bytes_per_launch"])
@@ -188,10 +348,13 @@ def main():
               "so N GPUs would each run this same benchmark on their share of the requests. "
               "Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
+    if args.workload == "snapkv":
+        main_snapkv(args)
+        return
     from workloads import CONFIGS
     w = CONFIGS[args.config]
     K = int(args.steps if args.steps is not None else w.steps)
-    W = int(args.warmup)
+    W = int(args.warmup if args.warmup is not None else 8)
 
     cpu = None
     if args.cpu_baseline == "auto":
