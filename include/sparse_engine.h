@@ -83,6 +83,7 @@ typedef enum se_status {
 #define SE_OP_QUEST_SELECT  2
 #define SE_OP_QUEST_STEP    3
 #define SE_OP_SNAPKV        4
+#define SE_OP_OMNIKV_SELECT 5
 
 /* The cache view (Section 3.1, eq. attention-view; Appendix B, "Attention View
  * Payloads").  Only the pointers an operation needs must be non-NULL. */
@@ -289,9 +290,49 @@ se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, const void* 
                             int32_t freed_stride, int32_t* freed_count, void* ws, size_t ws_bytes,
                             int32_t* dev_err, hipStream_t stream);
 
+/*
+ * se_omnikv_select — OmniKV's observation-layer selection (Appendix A.3, "OmniKV:
+ * Selection Reuse across Layers", eq. background-omnikv-selection), from the logits
+ * se_decode_attend wrote for every resident slot of this layer in the same step
+ * (all-slots mode, after the step's append).  Per request, with L = lengths of its
+ * units (every KV head of a request holds the same slots; unequal lengths raise
+ * SE_DEVERR_BAD_LENGTH and select nothing):
+ *   s(j) = max over the request's Hq = num_kv_heads * q_per_kv query heads a of
+ *          logits[unit(a)][a mod q_per_kv][j], for slots j < L;
+ *   sel_slots[req] = the budget slots with the largest s (ties: lower slot), in
+ *          increasing order; every slot followed by -1 when L <= budget.
+ *  logits    fp32 [num_units][q_per_kv][logits_stride] as se_decode_attend writes it
+ *  sel_slots int32 [num_req][budget] (output); budget 1 .. 8192; q_per_kv 1 .. 8
+ *  ws        se_workspace_bytes(SE_OP_OMNIKV_SELECT, num_units / num_kv_heads, max_len,
+ *            ...) bytes (no zero-fill needed)
+ */
+se_status se_omnikv_select(const se_kv_view* kv, int32_t q_per_kv, const float* logits,
+                           int32_t logits_stride, int32_t budget, int32_t max_len,
+                           int32_t* sel_slots, void* ws, size_t ws_bytes, int32_t* dev_err,
+                           hipStream_t stream);
+
+/*
+ * se_attend_slots — a sparse layer's decode step under OmniKV's reuse (Appendix A.3,
+ * eq. background-omnikv-reuse; Appendix A.1, eq. background-selected-attention with
+ * S = the selection): the append of se_decode_attend (when k_new and v_new are given),
+ * then for every unit the G query rows attend over S = the slots sel_slots[req][i]
+ * (i < sel_count) of the unit's own cache — the slots an observation layer selected,
+ * shared by the request's KV heads.  Entries < 0 are skipped; an entry at or past the
+ * unit's length (after the append) sets SE_DEVERR_BAD_SELECTION and is skipped.  An
+ * empty S gives out = 0 and lse = -inf.
+ *  q, k_new, v_new, new_pos, scale, max_len, out, lse as for se_decode_attend;
+ *  sel_slots int32 [num_req][sel_count], sel_count 1 .. 8192; q_per_kv 1, 2, 4 or 8.
+ *  No workspace; the score field is not touched.
+ */
+se_status se_attend_slots(const se_kv_view* kv, int32_t q_per_kv, const void* q, const void* k_new,
+                          const void* v_new, const int32_t* new_pos, const int32_t* sel_slots,
+                          int32_t sel_count, float scale, int32_t max_len, float* out, float* lse,
+                          int32_t* dev_err, hipStream_t stream);
+
 /* Workspace bytes an operation needs for these sizes (0 if none).  op is one of
  * SE_OP_*; max_len as passed to the call; top_k for SE_OP_DECODE_ATTEND with a
- * selection and for SE_OP_QUEST_STEP (0 otherwise). */
+ * selection and for SE_OP_QUEST_STEP (0 otherwise).  For SE_OP_OMNIKV_SELECT,
+ * num_units is the number of requests. */
 size_t se_workspace_bytes(int32_t op, int32_t num_units, int32_t max_len, int32_t max_pages,
                           int32_t q_per_kv, int32_t head_dim, int32_t top_k);
 

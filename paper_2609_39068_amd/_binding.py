@@ -34,12 +34,13 @@ SE_OP_DECODE_ATTEND = 1
 SE_OP_QUEST_SELECT = 2
 SE_OP_QUEST_STEP = 3
 SE_OP_SNAPKV = 4
+SE_OP_OMNIKV_SELECT = 5
 SE_SNAPKV_SCORE_ONLY = 1
 
 EXPORTED = (
     "se_decode_attend", "se_decode_step_h2o", "se_decode_step_quest", "se_accumulate_scores", "se_evict_compact", "se_quest_summarize",
     "se_quest_select", "se_workspace_bytes", "se_read_device_errors", "se_status_string",
-    "se_version", "se_snapkv_compact",
+    "se_version", "se_snapkv_compact", "se_omnikv_select", "se_attend_slots",
 )
 
 
@@ -83,6 +84,8 @@ def _load():
         "se_quest_select": (I32, [V, I32, P, F32, I32, I32, U32, P, P, I32, P, SZ, P, P]),
         "se_decode_step_quest": (I32, [V, I32, P, P, P, P, F32, I32, I32, P, P, P, P, SZ, P, P]),
         "se_snapkv_compact": (I32, [V, I32, P, I32, I32, F32, I32, I32, U32, P, I32, P, P, SZ, P, P]),
+        "se_omnikv_select": (I32, [V, I32, P, I32, I32, I32, P, P, SZ, P, P]),
+        "se_attend_slots": (I32, [V, I32, P, P, P, P, P, I32, F32, I32, P, P, P, P]),
         "se_workspace_bytes": (SZ, [I32, I32, I32, I32, I32, I32, I32]),
         "se_read_device_errors": (I32, [P, P, P]),
         "se_status_string": (ctypes.c_char_p, [I32]),
@@ -322,3 +325,38 @@ def se_snapkv_compact(view: KVView, q_per_kv, q_obs, window, kernel, scale, budg
         0 if ws is None else ws.numel() * ws.element_size(), _ptr(dev_err, torch.int32, "dev_err"),
         _stream(stream))
     _check("se_snapkv_compact", st)
+
+
+def se_omnikv_select(view: KVView, q_per_kv, logits, logits_stride, budget, max_len, sel_slots, ws, dev_err,
+                     stream=None):
+    s = view.struct
+    nreq = s.num_units // s.num_kv_heads
+    _need(logits, s.num_units * q_per_kv * int(logits_stride), "logits")
+    _need(sel_slots, nreq * int(budget), "sel_slots")
+    st = _lib.se_omnikv_select(
+        view.ref(), int(q_per_kv), _ptr(logits, torch.float32, "logits"), int(logits_stride), int(budget),
+        int(max_len), _ptr(sel_slots, torch.int32, "sel_slots"), _ptr(ws, None, "ws"),
+        0 if ws is None else ws.numel() * ws.element_size(), _ptr(dev_err, torch.int32, "dev_err"),
+        _stream(stream))
+    _check("se_omnikv_select", st)
+
+
+def se_attend_slots(view: KVView, q_per_kv, q, k_new, v_new, new_pos, sel_slots, sel_count, scale, max_len,
+                    out, lse, dev_err, stream=None):
+    s = view.struct
+    nreq = s.num_units // s.num_kv_heads
+    hq = s.num_kv_heads * q_per_kv
+    _need(q, nreq * hq * s.head_dim, "q")
+    _need(out, nreq * hq * s.head_dim, "out")
+    _need(lse, nreq * hq, "lse")
+    _need(k_new, s.num_units * s.head_dim, "k_new")
+    _need(v_new, s.num_units * s.head_dim, "v_new")
+    _need(new_pos, nreq, "new_pos")
+    _need(sel_slots, nreq * int(sel_count), "sel_slots")
+    st = _lib.se_attend_slots(
+        view.ref(), int(q_per_kv), _ptr(q, torch.bfloat16, "q"), _ptr(k_new, torch.bfloat16, "k_new"),
+        _ptr(v_new, torch.bfloat16, "v_new"), _ptr(new_pos, torch.int32, "new_pos"),
+        _ptr(sel_slots, torch.int32, "sel_slots"), int(sel_count), float(scale), int(max_len),
+        _ptr(out, torch.float32, "out"), _ptr(lse, torch.float32, "lse"), _ptr(dev_err, torch.int32, "dev_err"),
+        _stream(stream))
+    _check("se_attend_slots", st)

@@ -1,0 +1,487 @@
+// OmniKV cross-layer selection (Appendix A.3, "OmniKV: Selection Reuse across
+// Layers", eqs. background-omnikv-selection and background-omnikv-reuse):
+//   se_omnikv_select  at an observation layer, from the logits se_decode_attend
+//                     wrote for every resident slot: s(j) = max over the
+//                     request's query heads of z_j, then TopK_b of s per request;
+//   se_attend_slots   at a sparse layer: append the decode token, then each
+//                     KV head's group attends over the selected slots of its
+//                     own cache.
+//
+// Selection: omnikv_score_kernel takes the maximum over the request's Hq
+// logit rows (contiguous in the logits layout) for a chunk of slots, coalesced,
+// into the workspace; omnikv_topk_kernel (one 1024-thread work-group per
+// request) copies the request's scores to LDS when they fit, finds the b-th
+// largest key by an 8-bit radix selection over order-preserving keys (ties:
+// lower slot), and writes the selected slots in increasing order: every thread
+// owns a contiguous run of slots, so two block scans (of the tied count and of
+// the selected count) give each thread its output offset.
+//
+// Slot attention: one 512-thread work-group per unit.  The selected slots are
+// translated once into kv-pool row indices in LDS (the appended token's row is
+// read from k_new / v_new instead, so no wavefront reads a row another one
+// wrote).  Each wavefront takes a contiguous share of the rows, eight rows per
+// pass: for QK, 8 lanes share a key row (D/8 columns each, 16-byte loads) and
+// reduce their bf16-pair dot products over the 8 lanes; the online softmax
+// keeps one maximum per head; the pass's weights are broadcast through LDS and
+// every lane accumulates its own D/64 value columns of the 8 rows (one
+// coalesced row per load instruction).  The next pass's key and value loads
+// are issued before the current pass is reduced.  Wavefronts combine in LDS.
+#include "quest_core.h"
+
+namespace se {
+
+constexpr int kOmniScoreThreads = 256;
+constexpr int kOmniScoreSlots = 4;                      // slots per thread per block
+constexpr int kOmniTopkThreads = 1024;
+constexpr int kOmniLdsScores = 32768 + 4096;            // scores kept in LDS (144 KB)
+constexpr int kGatherThreads = 512;
+constexpr int kGatherWaves = kGatherThreads / kWave;
+constexpr int kGatherMaxSel = 8192;                     // selected slots per request
+constexpr uint32_t kNewRow = 0xFFFFFFFFu;               // the appended token (read from k_new / v_new)
+
+struct OmniSelectParams {
+  const float* logits;   // [num_units][G][stride]
+  int32_t stride;
+  const int32_t* lengths;
+  int32_t num_req;
+  int32_t num_kv_heads;
+  int32_t q_per_kv;
+  int32_t budget;
+  int32_t max_len;
+  int32_t ws_stride;
+  float* scores;         // workspace [num_req][ws_stride]
+  int32_t* sel;          // [num_req][budget]
+  int32_t* dev_err;
+};
+
+// s(j) = max over the request's Hkv * G logit rows, for slots j < L of the
+// request's first unit.
+__global__ __launch_bounds__(kOmniScoreThreads) void omnikv_score_kernel(const OmniSelectParams p) {
+  const int req = blockIdx.y;
+  const int L = p.lengths[(size_t)req * p.num_kv_heads];
+  const int rows = p.num_kv_heads * p.q_per_kv;
+  const float* lg = p.logits + (size_t)req * rows * p.stride;
+  const int base = blockIdx.x * kOmniScoreThreads * kOmniScoreSlots + threadIdx.x;
+  if (L < 0 || L > p.max_len) return;  // reported by the selection kernel
+#pragma unroll
+  for (int k = 0; k < kOmniScoreSlots; ++k) {
+    const int j = base + k * kOmniScoreThreads;
+    if (j >= L) break;
+    float s = -INFINITY;
+    for (int r = 0; r < rows; ++r) s = fmaxf(s, lg[(size_t)r * p.stride + j]);
+    p.scores[(size_t)req * p.ws_stride + j] = s;
+  }
+}
+
+__global__ __launch_bounds__(kOmniTopkThreads) void omnikv_topk_kernel(const OmniSelectParams p) {
+  __shared__ float s_sc[kOmniLdsScores];
+  __shared__ unsigned s_hist[256];
+  __shared__ int s_scan[kOmniTopkThreads / kWave + 1];
+  __shared__ int s_bcast[4];
+  const int req = blockIdx.x;
+  const int tid = threadIdx.x;
+  int32_t* out = p.sel + (size_t)req * p.budget;
+  const int L = p.lengths[(size_t)req * p.num_kv_heads];
+  int bad = (L < 0 || L > p.max_len) ? 1 : 0;
+  for (int h = 1; h < p.num_kv_heads; ++h) bad |= (p.lengths[(size_t)req * p.num_kv_heads + h] != L);
+  if (bad) {  // every unit of a request keeps the whole history: the lengths agree
+    for (int i = tid; i < p.budget; i += kOmniTopkThreads) out[i] = -1;
+    if (tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_LENGTH);
+    return;
+  }
+  const int b = p.budget;
+  if (L <= b) {
+    for (int i = tid; i < b; i += kOmniTopkThreads) out[i] = i < L ? i : -1;
+    return;
+  }
+  const float* gsc = p.scores + (size_t)req * p.ws_stride;
+  const float* sc = gsc;
+  if (L <= kOmniLdsScores) {
+    for (int i = tid; i < L; i += kOmniTopkThreads) s_sc[i] = gsc[i];
+    __syncthreads();
+    sc = s_sc;
+  }
+  uint32_t prefix, mask;
+  int k_rest;
+  radix_select_top<kOmniTopkThreads, uint32_t>(
+      L, b, [&](int i) { return float_key(sc[i]); }, [](int) { return true; }, &prefix, &mask, &k_rest, s_hist,
+      s_scan, s_bcast);
+  // thread t owns slots [t*run, (t+1)*run): count the threshold ties, rank them
+  // in slot order, then place the selected slots
+  const int run = ceil_div_dev(L, kOmniTopkThreads);
+  const int lo = min(L, tid * run), hi = min(L, lo + run);
+  int n_eq = 0;
+  for (int i = lo; i < hi; ++i) n_eq += ((float_key(sc[i]) & mask) == prefix);
+  int tot;
+  const int eq_before = block_exclusive_scan<kOmniTopkThreads>(n_eq, s_scan, &tot);
+  int n_sel = 0, e = eq_before;
+  for (int i = lo; i < hi; ++i) {
+    const uint32_t km = float_key(sc[i]) & mask;
+    if (km > prefix) {
+      ++n_sel;
+    } else if (km == prefix) {
+      n_sel += (e < k_rest);
+      ++e;
+    }
+  }
+  const int at = block_exclusive_scan<kOmniTopkThreads>(n_sel, s_scan, &tot);
+  int o = at;
+  e = eq_before;
+  for (int i = lo; i < hi; ++i) {
+    const uint32_t km = float_key(sc[i]) & mask;
+    bool take = km > prefix;
+    if (km == prefix) take = (e++ < k_rest);
+    if (take) out[o++] = i;
+  }
+}
+
+// ------------------------------------------------------------------ slot attention
+
+struct GatherParams {
+  uint16_t* kv;
+  int32_t* pos_pool;
+  const int32_t* block_table;
+  int32_t* lengths;
+  int64_t num_pages;
+  int32_t max_pages;
+  int32_t num_kv_heads;
+  const uint16_t* q;      // [num_req][Hq][D]
+  const uint16_t* k_new;  // [num_req][Hkv][D] or null
+  const uint16_t* v_new;
+  const int32_t* new_pos;
+  const int32_t* sel;     // [num_req][count]
+  int32_t count;
+  int32_t max_len;
+  float scale_log2;       // scale * log2(e)
+  float* out;             // [num_req][Hq][D]
+  float* lse;             // [num_req][Hq] or null
+  int32_t* dev_err;
+};
+
+template <int D>
+struct GatherRow {
+  static constexpr int QW = D / 16;  // 32-bit words of a key row per lane (8 lanes per row)
+  static constexpr int VW = D / 64;  // value columns per lane
+};
+
+template <int D, int G>
+__global__ __launch_bounds__(kGatherThreads, (G >= 4 ? 2 : 4)) void gather_attend_kernel(const GatherParams p) {
+  constexpr int QW = GatherRow<D>::QW;
+  constexpr int VC = GatherRow<D>::VW;
+  __shared__ uint32_t s_row[kGatherMaxSel];
+  __shared__ float s_w[kGatherWaves][8][G];
+  __shared__ float s_m[kGatherWaves][G], s_l[kGatherWaves][G];
+  __shared__ float s_o[kGatherWaves][G][D];
+  __shared__ int s_scan[kGatherWaves + 1];
+  __shared__ int s_red[kGatherWaves];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wv = tid / kWave;
+  const int unit = blockIdx.x;
+  const int req = unit / p.num_kv_heads;
+  const int kvh = unit % p.num_kv_heads;
+  const int Hq = p.num_kv_heads * G;
+  const int32_t* bt = p.block_table + (size_t)unit * p.max_pages;
+  const int L0 = p.lengths[unit];
+  const bool append = p.k_new != nullptr;
+  float* o_out = p.out + ((size_t)req * Hq + (size_t)kvh * G) * D;
+
+  // ---- append: the new token's row, position and the length
+  int fail = 0;
+  if (L0 < 0 || L0 + (append ? 1 : 0) > p.max_len) fail = SE_DEVERR_BAD_LENGTH;
+  else if (append && L0 >= p.max_pages * kPage) fail = SE_DEVERR_CAPACITY;
+  const int L = L0 + (append ? 1 : 0);
+  if (!fail && append) {
+    const int ph = bt[L0 >> 4];
+    if (ph < 0 || (int64_t)ph >= p.num_pages) {
+      fail = SE_DEVERR_BAD_PAGE;
+    } else if (wv == 0) {
+      const size_t krow = ((size_t)ph * 2 * kPage + (L0 & (kPage - 1))) * D;
+      const uint16_t* ks = p.k_new + ((size_t)req * p.num_kv_heads + kvh) * D;
+      const uint16_t* vs = p.v_new + ((size_t)req * p.num_kv_heads + kvh) * D;
+      for (int c = lane; c < D; c += kWave) {
+        p.kv[krow + c] = ks[c];
+        p.kv[krow + (size_t)kPage * D + c] = vs[c];
+      }
+      if (lane == 0) p.pos_pool[(size_t)ph * kPage + (L0 & (kPage - 1))] = p.new_pos[req];
+    }
+  }
+  if (fail) {
+    if (tid == 0) set_error(p.dev_err, fail);
+    for (int i = tid; i < G * D; i += kGatherThreads) o_out[i] = 0.f;
+    if (p.lse != nullptr && tid < G) p.lse[(size_t)req * Hq + kvh * G + tid] = -INFINITY;
+    return;
+  }
+
+  // ---- the selected rows (entries < 0 skipped; at or past L reported and skipped)
+  int n_sel = 0, bad_sel = 0, bad_page = 0;
+  const int32_t* sel = p.sel + (size_t)req * p.count;
+  for (int c0 = 0; c0 < p.count; c0 += kGatherThreads) {
+    const int i = c0 + tid;
+    const int s = i < p.count ? sel[i] : -1;
+    uint32_t row = 0;
+    bool ok = s >= 0 && s < L;
+    bad_sel |= (s >= L);
+    if (ok) {
+      if (append && s == L0) {
+        row = kNewRow;
+      } else {
+        const int ph = bt[s >> 4];
+        if (ph < 0 || (int64_t)ph >= p.num_pages) {
+          ok = false;
+          bad_page = 1;
+        } else {
+          row = (uint32_t)ph * 2 * kPage + (uint32_t)(s & (kPage - 1));
+        }
+      }
+    }
+    int tot;
+    const int at = block_exclusive_scan<kGatherThreads>(ok ? 1 : 0, s_scan, &tot);
+    if (ok && n_sel + at < kGatherMaxSel) s_row[n_sel + at] = row;
+    n_sel += tot;
+  }
+  if (tid == 0 && bad_sel) set_error(p.dev_err, SE_DEVERR_BAD_SELECTION);
+  {
+    const int bp = block_reduce<kGatherThreads>(bad_page, s_red, [](int a, int c) { return a | c; });
+    if (bp && tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
+  }
+  n_sel = min(n_sel, kGatherMaxSel);
+  __syncthreads();  // the row list and the appended row are complete
+  if (append && tid == 0) p.lengths[unit] = L;
+
+  // ---- queries: lane (row r8 = lane/8, c8 = lane%8) holds columns [c8*D/8, ...) of the G rows
+  const int c8 = lane & 7;
+  const int r8 = lane >> 3;
+  uint32_t qr[G][QW];
+  {
+    const uint16_t* qb = p.q + ((size_t)req * Hq + (size_t)kvh * G) * D + c8 * (D / 8);
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int i = 0; i < QW; i += 4) {
+        const uint4 t = *reinterpret_cast<const uint4*>(qb + (size_t)g * D + 2 * i);
+        qr[g][i] = t.x;
+        qr[g][i + 1] = t.y;
+        qr[g][i + 2] = t.z;
+        qr[g][i + 3] = t.w;
+      }
+  }
+  const uint16_t* knew = append ? p.k_new + ((size_t)req * p.num_kv_heads + kvh) * D : nullptr;
+  const uint16_t* vnew = append ? p.v_new + ((size_t)req * p.num_kv_heads + kvh) * D : nullptr;
+
+  // the wavefront's share of the rows, in passes of 8
+  const int per = ceil_div_dev(n_sel, kGatherWaves);
+  const int rb = min(n_sel, wv * per), re = min(n_sel, rb + per);
+  const int n_pass = ceil_div_dev(re - rb, 8);
+
+  struct Buf {
+    uint32_t k[QW];
+    uint32_t v[8];
+  };
+  auto load = [&](int ps, Buf& bf) {
+    const int e = min(rb + ps * 8 + r8, re - 1);
+    const uint32_t row = s_row[max(e, 0)];
+    const uint16_t* ksrc = row == kNewRow ? knew : p.kv + (size_t)row * D;
+    const uint4* k4 = reinterpret_cast<const uint4*>(ksrc + c8 * (D / 8));
+#pragma unroll
+    for (int i = 0; i < QW; i += 4) {
+      const uint4 t = k4[i / 4];
+      bf.k[i] = t.x;
+      bf.k[i + 1] = t.y;
+      bf.k[i + 2] = t.z;
+      bf.k[i + 3] = t.w;
+    }
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int er = min(rb + ps * 8 + r, re - 1);
+      const uint32_t vr = __builtin_amdgcn_readfirstlane(s_row[max(er, 0)]);  // one row per wavefront
+      const uint16_t* vsrc = vr == kNewRow ? vnew : p.kv + ((size_t)vr + kPage) * D;
+      if (VC == 2)
+        bf.v[r] = reinterpret_cast<const uint32_t*>(vsrc)[lane];
+      else
+        bf.v[r] = reinterpret_cast<const uint16_t*>(vsrc)[lane];
+    }
+  };
+
+  float m[G], l[G], acc[G][VC];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    m[g] = -INFINITY;
+    l[g] = 0.f;
+#pragma unroll
+    for (int c = 0; c < VC; ++c) acc[g][c] = 0.f;
+  }
+  Buf cur, nxt;
+  if (n_pass > 0) load(0, cur);
+  for (int ps = 0; ps < n_pass; ++ps) {
+    if (ps + 1 < n_pass) load(ps + 1, nxt);
+    // logits of row r8 for every head (reduced over the row's 8 lanes)
+    float z[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float a = 0.f;
+#pragma unroll
+      for (int i = 0; i < QW; ++i) a = dot2bf16(qr[g][i], cur.k[i], a);
+      a += shfl_xor_f(a, 1);
+      a += shfl_xor_f(a, 2);
+      a += shfl_xor_f(a, 4);
+      z[g] = rb + ps * 8 + r8 < re ? a * p.scale_log2 : -INFINITY;
+    }
+    // per head: the pass maximum over its 8 rows, rescale, weights to LDS
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float mx = z[g];
+      mx = fmaxf(mx, shfl_xor_f(mx, 8));
+      mx = fmaxf(mx, shfl_xor_f(mx, 16));
+      mx = fmaxf(mx, shfl_xor_f(mx, 32));
+      const float mn = fmaxf(m[g], mx);
+      const float corr = fast_exp2(m[g] - mn);  // m = -inf at first: 0
+      m[g] = mn;
+      l[g] *= corr;
+#pragma unroll
+      for (int c = 0; c < VC; ++c) acc[g][c] *= corr;
+      if (c8 == 0) s_w[wv][r8][g] = fast_exp2(z[g] - mn);
+    }
+    wave_lds_sync();
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      float vf[VC];
+      if (VC == 2) {
+        vf[0] = bf16lo(cur.v[r]);
+        if (VC > 1) vf[VC - 1] = bf16hi(cur.v[r]);
+      } else {
+        vf[0] = bf16f((uint16_t)cur.v[r]);
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float wgt = s_w[wv][r][g];
+        l[g] += wgt;
+#pragma unroll
+        for (int c = 0; c < VC; ++c) acc[g][c] = fmaf(wgt, vf[c], acc[g][c]);
+      }
+    }
+    wave_lds_sync();
+    if (ps + 1 < n_pass) cur = nxt;
+  }
+  // ---- combine the wavefronts
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    if (lane == 0) {
+      s_m[wv][g] = m[g];
+      s_l[wv][g] = l[g];
+    }
+#pragma unroll
+    for (int c = 0; c < VC; ++c) s_o[wv][g][lane * VC + c] = acc[g][c];
+  }
+  __syncthreads();
+  for (int i = tid; i < G * D; i += kGatherThreads) {
+    const int g = i / D, col = i % D;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kGatherWaves; ++w) M = fmaxf(M, s_m[w][g]);
+    float lsum = 0.f, o = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < kGatherWaves; ++w) {
+        const float f = s_m[w][g] == -INFINITY ? 0.f : fast_exp2(s_m[w][g] - M);
+        lsum += s_l[w][g] * f;
+        o += s_o[w][g][col] * f;
+      }
+    }
+    o_out[(size_t)g * D + col] = lsum > 0.f ? o / lsum : 0.f;
+    if (col == 0 && p.lse != nullptr)
+      p.lse[(size_t)req * Hq + kvh * G + g] = lsum > 0.f ? (M + __log2f(lsum)) * kLn2 : -INFINITY;
+  }
+}
+
+template <int D>
+void launch_gather_d(const GatherParams& p, int units, int G, hipStream_t s) {
+  switch (G) {
+    case 1: hipLaunchKernelGGL((gather_attend_kernel<D, 1>), dim3(units), dim3(kGatherThreads), 0, s, p); break;
+    case 2: hipLaunchKernelGGL((gather_attend_kernel<D, 2>), dim3(units), dim3(kGatherThreads), 0, s, p); break;
+    case 4: hipLaunchKernelGGL((gather_attend_kernel<D, 4>), dim3(units), dim3(kGatherThreads), 0, s, p); break;
+    default: hipLaunchKernelGGL((gather_attend_kernel<D, 8>), dim3(units), dim3(kGatherThreads), 0, s, p); break;
+  }
+}
+
+}  // namespace se
+
+using namespace se;
+
+size_t se_omnikv_workspace_bytes(int32_t num_req, int32_t max_len) {
+  if (num_req <= 0 || max_len <= 0) return 0;
+  return (size_t)num_req * align_up((size_t)max_len, 64) * sizeof(float);
+}
+
+extern "C" se_status se_omnikv_select(const se_kv_view* kv, int32_t q_per_kv, const float* logits,
+                                      int32_t logits_stride, int32_t budget, int32_t max_len,
+                                      int32_t* sel_slots, void* ws, size_t ws_bytes, int32_t* dev_err,
+                                      hipStream_t stream) {
+  se_status st = check_view(kv);
+  if (st != SE_OK) return st;
+  if (logits == nullptr || sel_slots == nullptr || dev_err == nullptr) return SE_ERR_INVALID_ARGUMENT;
+  if (q_per_kv < 1 || q_per_kv > 8 || budget < 1 || max_len < 1 || logits_stride < max_len)
+    return SE_ERR_INVALID_ARGUMENT;
+  if (budget > kGatherMaxSel) return SE_ERR_UNSUPPORTED;
+  const int num_req = kv->num_units / kv->num_kv_heads;
+  if (ws == nullptr || ws_bytes < se_omnikv_workspace_bytes(num_req, max_len)) return SE_ERR_WORKSPACE;
+  OmniSelectParams p;
+  p.logits = logits;
+  p.stride = logits_stride;
+  p.lengths = kv->lengths;
+  p.num_req = num_req;
+  p.num_kv_heads = kv->num_kv_heads;
+  p.q_per_kv = q_per_kv;
+  p.budget = budget;
+  p.max_len = max_len;
+  p.ws_stride = (int32_t)align_up((size_t)max_len, 64);
+  p.scores = static_cast<float*>(ws);
+  p.sel = sel_slots;
+  p.dev_err = dev_err;
+  const int chunks = (int)ceil_div(max_len, kOmniScoreThreads * kOmniScoreSlots);
+  hipLaunchKernelGGL(omnikv_score_kernel, dim3(chunks, num_req), dim3(kOmniScoreThreads), 0, stream, p);
+  hipLaunchKernelGGL(omnikv_topk_kernel, dim3(num_req), dim3(kOmniTopkThreads), 0, stream, p);
+  return launch_status();
+}
+
+extern "C" se_status se_attend_slots(const se_kv_view* kv, int32_t q_per_kv, const void* q, const void* k_new,
+                                     const void* v_new, const int32_t* new_pos, const int32_t* sel_slots,
+                                     int32_t sel_count, float scale, int32_t max_len, float* out, float* lse,
+                                     int32_t* dev_err, hipStream_t stream) {
+  se_status st = check_view(kv);
+  if (st != SE_OK) return st;
+  if (kv->kv_pool == nullptr || kv->pos_pool == nullptr || q == nullptr || sel_slots == nullptr ||
+      out == nullptr || dev_err == nullptr)
+    return SE_ERR_INVALID_ARGUMENT;
+  if ((k_new == nullptr) != (v_new == nullptr) || (k_new != nullptr && new_pos == nullptr))
+    return SE_ERR_INVALID_ARGUMENT;
+  if (sel_count < 1 || max_len < 1 || !(scale > 0.f)) return SE_ERR_INVALID_ARGUMENT;
+  if (q_per_kv != 1 && q_per_kv != 2 && q_per_kv != 4 && q_per_kv != 8) return SE_ERR_UNSUPPORTED;
+  if (sel_count > kGatherMaxSel) return SE_ERR_UNSUPPORTED;
+  if (kv->num_pages > ((int64_t)1 << 27)) return SE_ERR_UNSUPPORTED;  // row indices are 32-bit
+  GatherParams p;
+  p.kv = static_cast<uint16_t*>(kv->kv_pool);
+  p.pos_pool = kv->pos_pool;
+  p.block_table = kv->block_table;
+  p.lengths = kv->lengths;
+  p.num_pages = kv->num_pages;
+  p.max_pages = kv->max_pages;
+  p.num_kv_heads = kv->num_kv_heads;
+  p.q = static_cast<const uint16_t*>(q);
+  p.k_new = static_cast<const uint16_t*>(k_new);
+  p.v_new = static_cast<const uint16_t*>(v_new);
+  p.new_pos = new_pos;
+  p.sel = sel_slots;
+  p.count = sel_count;
+  p.max_len = max_len;
+  p.scale_log2 = scale * kLog2e;
+  p.out = out;
+  p.lse = lse;
+  p.dev_err = dev_err;
+  if (kv->head_dim == 128)
+    launch_gather_d<128>(p, kv->num_units, q_per_kv, stream);
+  else
+    launch_gather_d<64>(p, kv->num_units, q_per_kv, stream);
+  return launch_status();
+}

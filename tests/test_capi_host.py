@@ -19,7 +19,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 12, names
+    assert len(names) == 14, names
     lib = b.raw_library()
     for n in names:
         assert hasattr(lib, n), f"{n} is declared in sparse_engine.h but not exported"
@@ -130,6 +130,42 @@ def test_snapkv_argument_checks():
     assert call(view=_view(score_pool=None)) == b.SE_ERR_INVALID_ARGUMENT
 
 
+def test_omnikv_argument_checks():
+    lib = b.raw_library()
+    v = _view()
+    sel = lib.se_omnikv_select
+
+    def call_sel(view=v, G=4, logits=0x100, stride=128, budget=64, max_len=128, out=0x200, ws=0x9000,
+                 ws_bytes=1 << 30, err=0xA000):
+        return sel(ctypes.byref(view), G, logits, stride, budget, max_len, out, ws, ws_bytes, err, None)
+
+    assert call_sel(logits=None) == b.SE_ERR_INVALID_ARGUMENT
+    assert call_sel(out=None) == b.SE_ERR_INVALID_ARGUMENT
+    assert call_sel(stride=64) == b.SE_ERR_INVALID_ARGUMENT        # stride < max_len
+    assert call_sel(budget=0) == b.SE_ERR_INVALID_ARGUMENT
+    assert call_sel(G=9) == b.SE_ERR_INVALID_ARGUMENT
+    assert call_sel(budget=8193) == b.SE_ERR_UNSUPPORTED
+    assert call_sel(ws=None) == b.SE_ERR_WORKSPACE
+    assert call_sel(ws_bytes=4) == b.SE_ERR_WORKSPACE
+    assert call_sel(err=None) == b.SE_ERR_INVALID_ARGUMENT
+    att = lib.se_attend_slots
+
+    def call_att(view=v, G=4, q=0x7000, k=None, vv=None, pos=None, sel=0x300, count=16, scale=0.1, max_len=128,
+                 out=0x8000, err=0xA000):
+        return att(ctypes.byref(view), G, q, k, vv, pos, sel, count, scale, max_len, out, None, err, None)
+
+    assert call_att(q=None) == b.SE_ERR_INVALID_ARGUMENT
+    assert call_att(sel=None) == b.SE_ERR_INVALID_ARGUMENT
+    assert call_att(k=0x100) == b.SE_ERR_INVALID_ARGUMENT           # k without v
+    assert call_att(k=0x100, vv=0x200) == b.SE_ERR_INVALID_ARGUMENT  # append without positions
+    assert call_att(count=0) == b.SE_ERR_INVALID_ARGUMENT
+    assert call_att(scale=0.0) == b.SE_ERR_INVALID_ARGUMENT
+    assert call_att(G=3) == b.SE_ERR_UNSUPPORTED
+    assert call_att(count=8193) == b.SE_ERR_UNSUPPORTED
+    assert call_att(out=None) == b.SE_ERR_INVALID_ARGUMENT
+    assert call_att(err=None) == b.SE_ERR_INVALID_ARGUMENT
+
+
 def test_workspace_sizes():
     # decode: counters + split partials + per-slot weights + per-page references
     n = b.se_workspace_bytes(b.SE_OP_DECODE_ATTEND, 512, 2049, 129, 4, 128, 0)
@@ -141,4 +177,5 @@ def test_workspace_sizes():
     assert ns == nq + b.se_workspace_bytes(b.SE_OP_QUEST_SELECT, 256, 33024, 2064, 4, 128, 0)
     assert b.se_workspace_bytes(b.SE_OP_SNAPKV, 512, 32768, 2048, 4, 128, 0) == 512 * 32768 * 4
     assert b.se_workspace_bytes(b.SE_OP_SNAPKV, 3, 1000, 63, 4, 128, 0) == 3 * 1024 * 4
+    assert b.se_workspace_bytes(b.SE_OP_OMNIKV_SELECT, 32, 33000, 2063, 4, 128, 0) == 32 * 33024 * 4
     assert b.se_workspace_bytes(99, 1, 1, 1, 1, 64, 0) == 0
