@@ -15,7 +15,11 @@ bracketed by device synchronisations; per-call HIP events on the launch
 stream give each kernel's duration for the roofline figure.
 
 Prints one JSON line.  `--config N` runs another workload (0..4) for
-measurement; `--workload snapkv` measures SnapKV prompt compaction instead
+measurement; `--workload omnikv` measures OmniKV decode over a 32-layer
+8B-shaped model (32 requests, 32768-token histories, observation layers 0, 2,
+7, 13, 16, 26 attend densely and select 2048 slots that the other layers read;
+one step is one decode step through all 32 layers); `--workload snapkv`
+measures SnapKV prompt compaction instead
 (se_snapkv_compact on the 8B-shaped prompt: 64 requests x 8 KV heads x 32768
 slots, window 32, pooling width 7, budget 2048; one step is one compaction of
 the whole batch from a fresh copy of the prompt); `--gpus N` with N > 1 is
@@ -46,8 +50,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=None, help="timed decode steps (default: the workload's)")
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default 8; snapkv: 1)")
     ap.add_argument("--config", type=int, default=1, help="workload index 0..4")
-    ap.add_argument("--workload", choices=["decode", "snapkv"], default="decode",
-                    help="decode (the --config workload) or snapkv (prompt compaction)")
+    ap.add_argument("--workload", choices=["decode", "snapkv", "omnikv"], default="decode",
+                    help="decode (the --config workload), snapkv (prompt compaction) or omnikv "
+                         "(32-layer decode with OmniKV selection reuse)")
     ap.add_argument("--cpu-baseline", choices=["auto", "skip"], default="auto")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 4 GiB device copy (counter calibration under rocprofv3)")
@@ -314,6 +319,211 @@ def main_snapkv(args):
     print(json.dumps(result), flush=True)
 
 
+def omnikv_layer_bytes(L, G, D, b, observe):
+    """Bytes one layer's OmniKV decode call(s) must move for units with L slots
+    after the append.  Observation layer (se_decode_attend with logits, then
+    se_omnikv_select): every slot's K and V rows and its G logits written, then
+    read back, plus per request the max score written and read and the
+    selection written.  Sparse layer (se_attend_slots): the b selected K and V
+    rows.  Both: the G query rows, G output rows and lse, and the append (k, v
+    read; k, v, position written)."""
+    import numpy as np
+    L = np.asarray(L, dtype=np.int64)
+    units = int(L.shape[0])
+    per_unit = G * D * 2 + G * D * 4 + G * 4 + 2 * D * 2 * 2 + 4
+    if observe:
+        return int(L.sum()) * (2 * D * 2 + 2 * G * 4) + units * per_unit
+    return units * (int(b) * 2 * D * 2 + per_unit)
+
+
+def cpu_baseline_omnikv(w, K):
+    """The oracle, untuned, on a bounded sample of the OmniKV workload: two
+    requests through one observation layer and one sparse layer (same shapes:
+    32768-token histories, 8 KV heads, b = 2048) for K decode steps, one request
+    per process; only the oracle's step calls are timed.  The per-token time of
+    the 32-layer model is extrapolated as 6 observation + 26 sparse layers."""
+    import multiprocessing as mp
+    from workloads import build_state, build_steps, scaled
+    sample_req = 2
+    ws = scaled(w, num_req=sample_req, layers=2, filter_layers=(0,))
+    host = build_state(ws, "cpu")
+    steps = build_steps(ws, host, "cpu", steps=K)
+    _SHARED["host"], _SHARED["steps"], _SHARED["w"], _SHARED["K"] = host, steps, ws, K
+    ctx = mp.get_context("fork")
+    t0 = time.perf_counter()
+    with ctx.Pool(sample_req) as pool:
+        per_req = pool.map(_oracle_omnikv_run, range(sample_req))
+    wall = time.perf_counter() - t0
+    n_obs = len(w.filter_layers)
+    t_obs = sum(r[0] for r in per_req) / (sample_req * K)
+    t_sparse = sum(r[1] for r in per_req) / (sample_req * K)
+    per_token = n_obs * t_obs + (w.layers - n_obs) * t_sparse
+    return {"value": round(sample_req / per_token, 4), "unit": "tokens/s", "cores": sample_req, "kind": "oracle",
+            "sample": (f"{sample_req} of {w.num_req} requests of '{w.name}' through one observation and one sparse "
+                       f"layer for {K} decode steps, NumPy float64, one request per process; the 32-layer token "
+                       f"time is {n_obs} x observation ({t_obs:.3f} s) + {w.layers - n_obs} x sparse "
+                       f"({t_sparse:.4f} s), and value = processes / that time"),
+            "cpu_seconds": round(sum(r[0] + r[1] for r in per_req), 2), "wall_seconds": round(wall, 2)}
+
+
+def _oracle_omnikv_run(r):
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_limits
+    from oracle import omnikv
+    from oracle.state import new_unit
+    from workloads import unit_slots
+    host, steps, w, K = _SHARED["host"], _SHARED["steps"], _SHARED["w"], _SHARED["K"]
+    U = w.units_per_layer
+
+    def f64(t):
+        return t.to(torch.float64).numpy()
+
+    spent = [0.0, 0.0]   # observation, sparse
+    J = {}
+    with threadpool_limits(1):
+        for layer in range(w.layers):
+            units = []
+            for h in range(w.hkv):
+                Kt, Vt, pos, _ = unit_slots(host, layer * U + r * w.hkv + h)
+                units.append(new_unit(f64(Kt), f64(Vt), pos.numpy().astype(np.int64)))
+            for t in range(K):
+                q, kn, vn = f64(steps.q[t, layer, r]), f64(steps.k_new[t, layer, r]), f64(steps.v_new[t, layer, r])
+                p = int(steps.new_pos[t, r])
+                t0 = time.perf_counter()
+                if layer in w.filter_layers:
+                    J[t] = omnikv.filter_step(units, q, kn, vn, p, w.scale, w.budget)["J"]
+                    spent[0] += time.perf_counter() - t0
+                else:
+                    omnikv.sparse_step(units, q, kn, vn, p, w.scale, J[t])
+                    spent[1] += time.perf_counter() - t0
+    return spent
+
+
+def main_omnikv(args):
+    """K decode steps of the OmniKV workload through all layers; the state keeps
+    growing (one appended token per layer and step), so warm-up steps run on the
+    state itself before the timed ones."""
+    from workloads import OMNIKV
+    w = OMNIKV
+    K = int(args.steps if args.steps is not None else 8)
+    W = int(args.warmup if args.warmup is not None else 2)
+    if K + W > w.steps:
+        raise SystemExit(f"bench.py: --steps + --warmup must be at most {w.steps} (the slots reserved per unit)")
+    cpu = cpu_baseline_omnikv(w, 1) if args.cpu_baseline == "auto" else None
+    if cpu is not None:
+        print(f"cpu baseline: {cpu['value']:.3f} tokens/s", file=sys.stderr, flush=True)
+    import numpy as np
+    import torch
+    import paper_2609_39068_amd as se
+    from workloads import build_state, build_steps
+
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    dev = torch.device("cuda:0")
+    t_gen = time.perf_counter()
+    state = build_state(w, dev)
+    steps = build_steps(w, state, dev, steps=W + K)
+    torch.cuda.synchronize()
+    print(f"generated '{w.name}' in {time.perf_counter() - t_gen:.1f}s", file=sys.stderr, flush=True)
+    U, G, D, b = w.units_per_layer, w.q_per_kv, w.head_dim, w.budget
+    max_len = state.max_pages * 16
+    stride = -(-max_len // 64) * 64
+    views = [se.KVView(state.kv_pool, state.pos_pool, None, None, state.block_table[state.layer_rows(l)],
+                       state.lengths[state.layer_rows(l)], num_kv_heads=w.hkv) for l in range(w.layers)]
+    out = torch.empty((w.num_req, w.hq, D), dtype=torch.float32, device=dev)
+    lse = torch.empty((w.num_req, w.hq), dtype=torch.float32, device=dev)
+    logits = torch.empty(U * G * stride, dtype=torch.float32, device=dev)
+    sel = torch.empty((w.num_req, b), dtype=torch.int32, device=dev)
+    ws_att = torch.empty(se.se_workspace_bytes(se.SE_OP_DECODE_ATTEND, U, max_len, state.max_pages, G, D, 0),
+                         dtype=torch.uint8, device=dev)
+    ws_sel = torch.empty(se.se_workspace_bytes(se.SE_OP_OMNIKV_SELECT, w.num_req, max_len, state.max_pages, G, D, 0),
+                         dtype=torch.uint8, device=dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    observe = set(w.filter_layers)
+
+    def run(t0, t1, lengths, layer_events=None, span=None):
+        for t in range(t0, t1):
+            ml = int(lengths) + (t - t0) + 1
+            if span is not None and t == t0:
+                span[0].record()
+            for l in range(w.layers):
+                q, kn, vn, npos = steps.q[t, l], steps.k_new[t, l], steps.v_new[t, l], steps.new_pos[t]
+                if l in observe:
+                    se.se_decode_attend(views[l], G, q, kn, vn, npos, None, 0, w.scale, ml, 0, out, lse, logits,
+                                        stride, ws_att, err)
+                    se.se_omnikv_select(views[l], G, logits, stride, b, ml, sel, ws_sel, err)
+                else:
+                    se.se_attend_slots(views[l], G, q, kn, vn, npos, sel, b, w.scale, ml, out, lse, err)
+                if layer_events is not None and t == t0:
+                    layer_events[l].record()
+            if span is not None:
+                if t == t0:
+                    span[1].record()
+                if t == t1 - 1:
+                    span[2].record()
+
+    L0 = int(state.lengths.max())
+    run(0, W, L0)
+    torch.cuda.synchronize()
+    lengths0 = state.lengths.cpu().numpy().astype(np.int64).reshape(w.layers, U)
+    span = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    lev = [torch.cuda.Event(enable_timing=True) for _ in range(w.layers)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(W, W + K, int(lengths0.max()), lev, span)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    errs = se.se_read_device_errors(err)
+    if errs:
+        raise RuntimeError(f"device error bits {errs:#x} during the timed run")
+    region_ms = span[0].elapsed_time(span[2])
+    # per-layer times of the first timed step (events after each layer)
+    obs_ms = sparse_ms = 0.0
+    for l in range(w.layers):
+        ms = span[0].elapsed_time(lev[0]) if l == 0 else lev[l - 1].elapsed_time(lev[l])
+        if l in observe:
+            obs_ms += ms
+        else:
+            sparse_ms += ms
+    total = obs_bytes = sparse_bytes = 0
+    for t in range(K):
+        for l in range(w.layers):
+            Lp = lengths0[l] + t + 1
+            nb = omnikv_layer_bytes(Lp, G, D, b, l in observe)
+            total += nb
+            if t == 0:
+                if l in observe:
+                    obs_bytes += nb
+                else:
+                    sparse_bytes += nb
+    achieved = total / (region_ms * 1e-3) / 1e9
+    result = {
+        "metric": "OmniKV decode tokens/s/GPU (32 layers); achieved HBM GB/s vs MI355X peak",
+        "value": round(w.num_req * K / elapsed, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": round(1e3 * elapsed / K, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "method": "omnikv", "batch": w.num_req, "hq": w.hq, "hkv": w.hkv,
+                   "head_dim": D, "page_size": w.page_size, "layers": w.layers, "context": w.ctx,
+                   "selected": b, "observation_layers": list(w.filter_layers), "accumulate": "f32",
+                   "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": "hbm", "kernel": "OmniKV decode step (se_decode_attend + se_omnikv_select on "
+                                               "observation layers, se_attend_slots on the others)",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "avg_launch_us": round(1e3 * region_ms / K, 3),
+                     "algorithmic_bytes_per_launch": round(total / K)},
+        "phases": {"observation_layers_ms": round(obs_ms, 3),
+                   "observation_GBps": round(obs_bytes / (obs_ms * 1e-3) / 1e9, 1),
+                   "sparse_layers_ms": round(sparse_ms, 3),
+                   "sparse_GBps": round(sparse_bytes / (sparse_ms * 1e-3) / 1e9, 1)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
 def source_hash(files=DECODE_SOURCES):
     h = hashlib.sha256()
     for f in files:
@@ -350,6 +560,9 @@ def main():
         sys.exit(2)
     if args.workload == "snapkv":
         main_snapkv(args)
+        return
+    if args.workload == "omnikv":
+        main_omnikv(args)
         return
     from workloads import CONFIGS
     w = CONFIGS[args.config]

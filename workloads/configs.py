@@ -17,7 +17,7 @@ from typing import Optional, Tuple
 class Workload:
     index: int
     name: str
-    method: str                      # "h2o", "quest" or "snapkv" (prompt compaction)
+    method: str                      # "h2o", "quest", "snapkv" (prompt compaction) or "omnikv"
     num_req: int
     hq: int
     hkv: int
@@ -34,6 +34,7 @@ class Workload:
     top_k: Optional[int] = None      # Quest selected pages per KV head
     obs_window: Optional[int] = None  # SnapKV observation window w (the prompt's last w positions)
     pool_kernel: Optional[int] = None  # SnapKV max-pooling width kappa
+    filter_layers: Optional[Tuple[int, ...]] = None  # OmniKV observation layers (full attention + selection)
     hh_rate: float = 0.0             # share of positions whose key gets += hh_shift * u
     hh_shift: float = 0.0
     relevant_pages: int = 0          # Quest: pages whose keys all get += relevant_shift * u
@@ -77,6 +78,15 @@ CONFIGS = [
 SNAPKV = Workload(5, "llama3-8b-prompt-snapkv", "snapkv", num_req=64, hq=32, hkv=8, head_dim=128,
                   layers=1, steps=1, ctx=32768, budget=2048, obs_window=32, pool_kernel=7,
                   hh_rate=0.01, hh_shift=4.0, seed=5)
+
+
+# OmniKV decode over a 32-layer 8B-shaped model (Appendix A.3, OmniKV; Appendix D:
+# 2,048 selected tokens, Llama full-attention layers 0, 2, 7, 13, 16, 26): every
+# request keeps its whole 32768-token history in every layer; observation layers
+# attend densely and select b = 2048 slots, which the following sparse layers read.
+OMNIKV = Workload(6, "llama3-8b-32-layer-omnikv", "omnikv", num_req=32, hq=32, hkv=8, head_dim=128,
+                  layers=32, steps=32, ctx=32768, budget=2048, filter_layers=(0, 2, 7, 13, 16, 26),
+                  hh_rate=0.01, hh_shift=4.0, seed=6)
 
 
 def scaled(w: Workload, **changes) -> Workload:

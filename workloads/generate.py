@@ -29,6 +29,8 @@ Value recipe (the workloads' own description):
   * ragged / retained workloads: the last `recent` positions of the context
     plus a stratified random sample (one position per stratum, so sorted and
     without repeats) of the older ones;
+  * OmniKV workload: every layer keeps the whole history (slot s holds
+    position s), with the heavy-hitter construction of the H2O workloads;
   * SnapKV workload: the whole prefilled prompt is resident (slot s holds
     position s) and the observation queries of its last obs_window positions
     are N(0, 1) + u, rounded to bf16, like decode queries.
@@ -149,6 +151,8 @@ def build_state(w: Workload, device, generate_values: bool = True) -> PagedInput
         cap_slots = int(max(int(L0.max()), int(w.budget)) + 1)
     elif w.method == "snapkv":
         cap_slots = int(L0.max())
+    elif w.method == "omnikv":
+        cap_slots = int(L0.max()) + w.steps
     else:
         cap_slots = int(L0.max()) + w.steps
     max_pages = -(-cap_slots // P)
@@ -187,7 +191,7 @@ def build_state(w: Workload, device, generate_values: bool = True) -> PagedInput
         if not generate_values:
             continue
         shift = None
-        if w.method in ("h2o", "snapkv") and w.hh_rate > 0:
+        if w.method in ("h2o", "snapkv", "omnikv") and w.hh_rate > 0:
             unit_ids = torch.arange(U, device=device)[:, None].expand(U, cap)
             shift = valid & heavy_hitter(w, layer, unit_ids, pos.clamp(min=0))
             amount = w.hh_shift
@@ -229,7 +233,7 @@ def build_steps(w: Workload, state: PagedInputs, device, steps: Optional[int] = 
             x = torch.randn((w.num_req, w.hq, d), generator=gq, device=device)
             q[t, layer] = (x + qshift[layer][None]).to(torch.bfloat16)
             kx = torch.randn((w.num_req, w.hkv, d), generator=gk, device=device)
-            if w.method == "h2o" and w.hh_rate > 0:
+            if w.method in ("h2o", "omnikv") and w.hh_rate > 0:
                 p = new_pos[t].to(torch.int64)[:, None].expand(w.num_req, w.hkv)
                 hh = heavy_hitter(w, layer, unit_ids, p)
                 kx = kx + w.hh_shift * hh[..., None].to(kx.dtype) * state.uvec[layer][None]
