@@ -312,11 +312,9 @@ __global__ __launch_bounds__(kGatherThreads, (G >= 4 ? 2 : 4)) void gather_atten
 #pragma unroll
     for (int c = 0; c < VC; ++c) acc[g][c] = 0.f;
   }
-  Buf cur, nxt;
-  if (n_pass > 0) load(0, cur);
-  for (int ps = 0; ps < n_pass; ++ps) {
-    if (ps + 1 < n_pass) load(ps + 1, nxt);
-    // logits of row r8 for every head (reduced over the row's 8 lanes)
+  // one pass: logits of row r8 for every head (reduced over the row's 8
+  // lanes), the pass maximum per head, rescale, weights through LDS, values
+  auto pass = [&](int ps, const Buf& cur) {
     float z[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
@@ -328,7 +326,6 @@ __global__ __launch_bounds__(kGatherThreads, (G >= 4 ? 2 : 4)) void gather_atten
       a += shfl_xor_f(a, 4);
       z[g] = rb + ps * 8 + r8 < re ? a * p.scale_log2 : -INFINITY;
     }
-    // per head: the pass maximum over its 8 rows, rescale, weights to LDS
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       float mx = z[g];
@@ -362,7 +359,24 @@ __global__ __launch_bounds__(kGatherThreads, (G >= 4 ? 2 : 4)) void gather_atten
       }
     }
     wave_lds_sync();
-    if (ps + 1 < n_pass) cur = nxt;
+  };
+  // three buffers, two passes in flight while one is reduced; loads past the
+  // share re-read its last row, so every step issues the same loads and the
+  // waits stay partial (the loop is unrolled by three: every buffer keeps its
+  // registers)
+  if (n_pass > 0) {
+    Buf b0, b1, b2;
+    load(0, b0);
+    load(1, b1);
+    load(2, b2);
+    for (int ps = 0; ps < n_pass; ps += 3) {
+      pass(ps, b0);
+      load(ps + 3, b0);
+      if (ps + 1 < n_pass) pass(ps + 1, b1);
+      load(ps + 4, b1);
+      if (ps + 2 < n_pass) pass(ps + 2, b2);
+      load(ps + 5, b2);
+    }
   }
   // ---- combine the wavefronts
 #pragma unroll
