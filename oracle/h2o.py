@@ -1,4 +1,5 @@
-"""H2O decode step in float64 (oracle; test infrastructure).
+"""H2O decode step and chunk-wise prefill eviction in float64 (oracle; test
+infrastructure).
 
 Appendix A.3, "H2O: Accumulated Scores and Online Eviction":
   * before position i is processed the available set is the previously
@@ -28,6 +29,10 @@ Readings of points the paper leaves open (each is also listed in the design doc):
     position and score.  Nothing else moves.
   * Freed pages: the logical pages ceil(B/p) .. ceil(L_old/p) - 1, which hold
     no resident slot after compaction.
+  * Chunked prefill (prefill_chunk): the chunk's tokens join with score 0; the
+    scoring queries are the chunk's last s positions, each adding its causal
+    weights (over the retained slots and the chunk up to itself) before one
+    retention and compaction per chunk.
 """
 
 import numpy as np
@@ -135,4 +140,40 @@ def decode_step(st: UnitState, q: np.ndarray, k: np.ndarray, v: np.ndarray,
         keep = retain(st.pos, st.u, budget, recent)
         holes, movers, freed = compact(st, keep, budget)
         result.update(keep=keep, holes=holes, movers=movers, freed=freed)
+    return result
+
+
+def prefill_chunk(st: UnitState, K: np.ndarray, V: np.ndarray, pos: np.ndarray, Qs: np.ndarray,
+                  scale: float, budget: int, recent: int) -> dict:
+    """H2O's chunk-wise eviction during chunked prefill for one unit (Section
+    3.1: finish_step after a prefill chunk; Appendix A.3, eqs.
+    background-h2o-score and background-h2o-retention; Appendix D: scores from
+    a prefill scoring window).  Mutates ``st``.
+
+    The chunk's C tokens (K, V float64 [C, d], positions ``pos`` increasing,
+    all above the resident ones) join the cache with score 0.  Each scoring
+    query -- the last s positions of the chunk, Qs float64 [s, G, d], query t at
+    chunk position C - s + t -- reads the available set up to its own position
+    (every previously retained slot and the chunk up to it) and adds its
+    group's weights to those slots' scores, as the per-token recurrence does
+    for one query.  Then the retained set and the compaction of a decode step.
+
+    Readings (also in the design doc): the scoring queries are the chunk's last s
+    positions (s = C: every query of the chunk); GQA sum; window and TopK as
+    for decode."""
+    C = K.shape[0]
+    s = Qs.shape[0]
+    if not 1 <= s <= C:
+        raise ValueError("the scoring window must hold 1 .. C queries")
+    for c in range(C):
+        append(st, K[c], V[c], int(pos[c]))
+    for t in range(s):
+        p_t = int(pos[C - s + t])
+        S = np.flatnonzero(st.pos <= p_t)          # causal: up to the query's own position
+        _, _, alpha, _ = selected_attention(Qs[t], st.K, st.V, S, scale)
+        st.u = accumulate(st.u, S, alpha)
+    result = {"u_after_accumulate": st.u.copy(), "pos_after_append": st.pos.copy()}
+    keep = retain(st.pos, st.u, budget, recent)
+    holes, movers, freed = compact(st, keep, budget)
+    result.update(keep=keep, holes=holes, movers=movers, freed=freed)
     return result
