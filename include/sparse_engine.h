@@ -84,6 +84,7 @@ typedef enum se_status {
 #define SE_OP_QUEST_STEP    3
 #define SE_OP_SNAPKV        4
 #define SE_OP_OMNIKV_SELECT 5
+#define SE_OP_H2O_PREFILL   6
 
 /* The cache view (Section 3.1, eq. attention-view; Appendix B, "Attention View
  * Payloads").  Only the pointers an operation needs must be non-NULL. */
@@ -291,6 +292,34 @@ se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, const void* 
                             int32_t* dev_err, hipStream_t stream);
 
 /*
+ * se_h2o_prefill_chunk — H2O's chunk-wise eviction during chunked prefill (Section 3.1:
+ * finish_step after a prefill chunk; Appendix A.3, eqs. background-h2o-score and
+ * background-h2o-retention; Appendix D: prefill scores from a scoring window).  Called
+ * after the chunk's keys, values and positions were written to the last chunk_len slots
+ * of each unit (lengths[unit] = L includes them; their positions increase and exceed
+ * every older resident position).  For every unit:
+ *   the chunk's slots start from score 0; the scoring queries are the chunk's last
+ *   score_window positions: query t (t = 0 .. s-1) reads every slot up to its own
+ *   position -- all older slots and the chunk's slots up to it -- and every slot it
+ *   reads gains its weight summed over the group's G query heads (as a decode
+ *   step's update, eq. background-h2o-score, for each of the s queries);
+ *   then exactly se_evict_compact(budget, recent) (units with L <= budget keep all).
+ *  q_score      bf16 [num_req][score_window][num_kv_heads * q_per_kv][head_dim], query t
+ *               of the chunk's (chunk_len - score_window + t)-th position
+ *  score_window 1 .. chunk_len, score_window * q_per_kv <= 1024; a unit with L <
+ *               chunk_len sets SE_DEVERR_BAD_LENGTH and its scores are not updated
+ *               (the eviction still applies to it)
+ *  scale, budget, recent, max_len, freed_* as for se_evict_compact; max_len <= 131072
+ *  ws           se_workspace_bytes(SE_OP_H2O_PREFILL, num_units, max_len, max_pages,
+ *               q_per_kv, head_dim, score_window) bytes (no zero-fill needed)
+ */
+se_status se_h2o_prefill_chunk(const se_kv_view* kv, int32_t q_per_kv, const void* q_score,
+                               int32_t score_window, int32_t chunk_len, float scale, int32_t budget,
+                               int32_t recent, int32_t max_len, int32_t* freed_pages,
+                               int32_t freed_stride, int32_t* freed_count, void* ws, size_t ws_bytes,
+                               int32_t* dev_err, hipStream_t stream);
+
+/*
  * se_omnikv_select — OmniKV's observation-layer selection (Appendix A.3, "OmniKV:
  * Selection Reuse across Layers", eq. background-omnikv-selection), from the logits
  * se_decode_attend wrote for every resident slot of this layer in the same step
@@ -332,7 +361,8 @@ se_status se_attend_slots(const se_kv_view* kv, int32_t q_per_kv, const void* q,
 /* Workspace bytes an operation needs for these sizes (0 if none).  op is one of
  * SE_OP_*; max_len as passed to the call; top_k for SE_OP_DECODE_ATTEND with a
  * selection and for SE_OP_QUEST_STEP (0 otherwise).  For SE_OP_OMNIKV_SELECT,
- * num_units is the number of requests. */
+ * num_units is the number of requests; for SE_OP_H2O_PREFILL, top_k is the score
+ * window. */
 size_t se_workspace_bytes(int32_t op, int32_t num_units, int32_t max_len, int32_t max_pages,
                           int32_t q_per_kv, int32_t head_dim, int32_t top_k);
 

@@ -35,12 +35,13 @@ SE_OP_QUEST_SELECT = 2
 SE_OP_QUEST_STEP = 3
 SE_OP_SNAPKV = 4
 SE_OP_OMNIKV_SELECT = 5
+SE_OP_H2O_PREFILL = 6
 SE_SNAPKV_SCORE_ONLY = 1
 
 EXPORTED = (
     "se_decode_attend", "se_decode_step_h2o", "se_decode_step_quest", "se_accumulate_scores", "se_evict_compact", "se_quest_summarize",
     "se_quest_select", "se_workspace_bytes", "se_read_device_errors", "se_status_string",
-    "se_version", "se_snapkv_compact", "se_omnikv_select", "se_attend_slots",
+    "se_version", "se_snapkv_compact", "se_omnikv_select", "se_attend_slots", "se_h2o_prefill_chunk",
 )
 
 
@@ -85,6 +86,7 @@ def _load():
         "se_decode_step_quest": (I32, [V, I32, P, P, P, P, F32, I32, I32, P, P, P, P, SZ, P, P]),
         "se_snapkv_compact": (I32, [V, I32, P, I32, I32, F32, I32, I32, U32, P, I32, P, P, SZ, P, P]),
         "se_omnikv_select": (I32, [V, I32, P, I32, I32, I32, P, P, SZ, P, P]),
+        "se_h2o_prefill_chunk": (I32, [V, I32, P, I32, I32, F32, I32, I32, I32, P, I32, P, P, SZ, P, P]),
         "se_attend_slots": (I32, [V, I32, P, P, P, P, P, I32, F32, I32, P, P, P, P]),
         "se_workspace_bytes": (SZ, [I32, I32, I32, I32, I32, I32, I32]),
         "se_read_device_errors": (I32, [P, P, P]),
@@ -360,3 +362,20 @@ def se_attend_slots(view: KVView, q_per_kv, q, k_new, v_new, new_pos, sel_slots,
         _ptr(out, torch.float32, "out"), _ptr(lse, torch.float32, "lse"), _ptr(dev_err, torch.int32, "dev_err"),
         _stream(stream))
     _check("se_attend_slots", st)
+
+
+def se_h2o_prefill_chunk(view: KVView, q_per_kv, q_score, score_window, chunk_len, scale, budget, recent, max_len,
+                         freed_pages, freed_stride, freed_count, ws, dev_err, stream=None):
+    s = view.struct
+    nreq = s.num_units // s.num_kv_heads
+    _need(q_score, nreq * int(score_window) * s.num_kv_heads * q_per_kv * s.head_dim, "q_score")
+    if freed_pages is not None:
+        _need(freed_pages, s.num_units * int(freed_stride), "freed_pages")
+    _need(freed_count, s.num_units, "freed_count")
+    st = _lib.se_h2o_prefill_chunk(
+        view.ref(), int(q_per_kv), _ptr(q_score, torch.bfloat16, "q_score"), int(score_window), int(chunk_len),
+        float(scale), int(budget), int(recent), int(max_len), _ptr(freed_pages, torch.int32, "freed_pages"),
+        int(freed_stride), _ptr(freed_count, torch.int32, "freed_count"), _ptr(ws, None, "ws"),
+        0 if ws is None else ws.numel() * ws.element_size(), _ptr(dev_err, torch.int32, "dev_err"),
+        _stream(stream))
+    _check("se_h2o_prefill_chunk", st)

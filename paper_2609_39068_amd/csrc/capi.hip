@@ -95,6 +95,8 @@ extern "C" size_t se_workspace_bytes(int32_t op, int32_t num_units, int32_t max_
       return se_snapkv_workspace_bytes(num_units, max_len);
     case SE_OP_OMNIKV_SELECT:
       return se_omnikv_workspace_bytes(num_units, max_len);
+    case SE_OP_H2O_PREFILL:
+      return se_h2o_prefill_workspace_bytes(num_units, max_len, q_per_kv, top_k);
     default:
       return 0;
   }

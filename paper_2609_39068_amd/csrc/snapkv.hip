@@ -36,6 +36,8 @@
 // last pages (window keys); slots past the length are masked there too.
 // Retention and compaction are then H2O's kernel (launch_evict) with the
 // window as its recent set.
+#include <algorithm>
+
 #include "evict_core.h"
 
 namespace se {
@@ -76,6 +78,8 @@ struct SnapParams {
   int32_t budget;
   int32_t max_len;
   int32_t u_stride;
+  int32_t n_rb;       // row blocks of kSnapMaxRows rows (grid.y)
+  int32_t chunk;      // H2O prefill: the chunk's slots (the last ones); 0 for SnapKV
   float c;  // scale * log2(e)
   int32_t* dev_err;
 };
@@ -204,8 +208,11 @@ __device__ __forceinline__ void merge_norm(float& ref, float& sum, float ref2, f
   ref = m;
 }
 
-// RTW: 16-row tiles per row group (rows of group g: [16*RTW*g, 16*RTW*(g+1))).
-template <int D, int RTW>
+// RTW: 16-row tiles per row group (rows of group g: [16*RTW*g, 16*RTW*(g+1)) of
+// the work-group's row block blockIdx.y).  kAccum: H2O chunk scoring -- u over
+// every key (the window keys with their causal mask) into the row block's
+// partial row of the workspace, no pooling; otherwise SnapKV.
+template <int D, int RTW, bool kAccum>
 __global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const SnapParams p) {
   constexpr int KS = D / 32;
   constexpr int S = kSnapStagePages;
@@ -227,8 +234,8 @@ __global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const Sna
   const int kh = wv / kSnapRowGroups;
   const int unit = blockIdx.x;
   const int L = p.lengths[unit];
-  if (L <= p.budget) return;  // the prompt already fits: nothing to score or evict
-  if (L > p.max_len || L > p.max_pages * kPage || L > kSnapMaxPages * kPage) {
+  if (!kAccum && L <= p.budget) return;  // the prompt already fits: nothing to score or evict
+  if (L > p.max_len || L > p.max_pages * kPage || L > kSnapMaxPages * kPage || (kAccum && L < p.chunk)) {
     if (tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_LENGTH);
     return;
   }
@@ -249,8 +256,10 @@ __global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const Sna
   const int w = p.w;
   const int G = p.q_per_kv;
   const int R = w * G;
-  const int n_cand = L - w;  // >= 1: L > budget >= w
-  const int row0 = 16 * RTW * rg;
+  // SnapKV: u over the candidates (L > budget >= w, so at least one); H2O: every key
+  const int n_lim = kAccum ? L : L - w;
+  const int row0 = 16 * RTW * rg;                // within the row block
+  const int rbase = kSnapMaxRows * blockIdx.y;   // the row block's first row
 
   // ---- the row group's observation queries (A operands); rows past R are zero
   uint4 qa[RTW][KS];
@@ -260,7 +269,7 @@ __global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const Sna
     const int hq = p.num_kv_heads * G;
 #pragma unroll
     for (int T = 0; T < RTW; ++T) {
-      const int row = row0 + 16 * T + col;
+      const int row = rbase + row0 + 16 * T + col;
       const int t = row / G;
       const int g = row - t * G;
       const uint16_t* src = p.q + (((size_t)req * w + t) * hq + (size_t)kvh * G + g) * D + 8 * grp;
@@ -306,7 +315,7 @@ __global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const Sna
         for (int T = 0; T < RTW; ++T)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const int row = row0 + 16 * T + 4 * grp + r;
+            const int row = rbase + row0 + 16 * T + 4 * grp + r;
             const int lim = row < R ? L - w + row / G : -1;
             if (key > lim) acc[i][T][r] = -INFINITY;
           }
@@ -359,16 +368,17 @@ __global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const Sna
   for (int T = 0; T < RTW; ++T)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int row = row0 + 16 * T + 4 * grp + r;
+      const int row = row0 + 16 * T + 4 * grp + r;  // within the block
       float m = s_norm[0][0][row], sm = s_norm[0][1][row];
 #pragma unroll
       for (int h = 1; h < kSnapHalves; ++h) merge_norm(m, sm, s_norm[h][0][row], s_norm[h][1][row]);
-      bias[T][r] = row < R ? m + __log2f(sm) : INFINITY;
+      bias[T][r] = rbase + row < R ? m + __log2f(sm) : INFINITY;
     }
 
-  // ---- pass 2: u over the candidate keys (every row sees them; no mask)
-  float* u = p.u + (size_t)unit * p.u_stride;
-  const int cand_pages = ceil_div_dev(n_cand, kPage);
+  // ---- pass 2: SnapKV: u over the candidate keys (every row sees them; no
+  // mask); H2O: u over every key, the window keys masked as in pass 1
+  float* u = p.u + ((size_t)unit * p.n_rb + blockIdx.y) * p.u_stride;
+  const int cand_pages = ceil_div_dev(n_lim, kPage);
   // every wavefront leaves its row group's sum for each key of each page of
   // stage j in LDS; once the stage's barrier has passed, wavefront v < S adds
   // the four row groups of each key of page v (while the next stage runs, or
@@ -381,7 +391,7 @@ __global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const Sna
 #pragma unroll
       for (int g = 0; g < kSnapRowGroups; ++g) v += up[g * kPage];
       const int key = (j * S + wv) * kPage + lane;
-      if (key < n_cand) u[key] = v;
+      if (key < n_lim) u[key] = v;
     }
   };
   const int n_st2 = ceil_div_dev(cand_pages, S);
@@ -398,6 +408,18 @@ __global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const Sna
       for (int T = 0; T < RTW; ++T)
 #pragma unroll
         for (int r = 0; r < 4; ++r) e[4 * T + r] = fast_exp2(fmaf(acc[i][T][r], c, -bias[T][r]));
+      if (kAccum && j * S + kh * H + i >= p_full) {
+        // causal mask of the window keys (and of slots past the length)
+        const int key = (j * S + kh * H + i) * kPage + col;
+#pragma unroll
+        for (int T = 0; T < RTW; ++T)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int row = rbase + row0 + 16 * T + 4 * grp + r;
+            const int lim = row < R ? L - w + row / G : -1;
+            if (key > lim) e[4 * T + r] = 0.f;
+          }
+      }
 #pragma unroll
       for (int n = RTW * 4; n > 1; n >>= 1)
 #pragma unroll
@@ -408,6 +430,7 @@ __global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const Sna
     }
   });
   if (n_st2 > 0) flush(n_st2 - 1);
+  if (kAccum) return;  // the row block's partial u is written; h2o_chunk_apply_kernel adds the blocks
   __syncthreads();  // the unit's u is complete and visible to the work-group
 
   // ---- pool: s over the candidates, 0 over the window; positions checked
@@ -422,7 +445,7 @@ __global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const Sna
       float uj = -INFINITY;
       if (j >= 0 && j < L) {
         pj = p.pos_pool[(size_t)bt[j >> 4] * kPage + (j & (kPage - 1))];
-        if (j < n_cand) uj = u[j];
+        if (j < n_lim) uj = u[j];
       }
       s_pos[i] = pj;
       s_u[i] = uj;
@@ -434,10 +457,10 @@ __global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const Sna
       const int32_t pj = s_pos[x];
       if (j > 0 && s_pos[x - 1] >= pj) bad_pos = 1;
       float s = 0.f;
-      if (j < n_cand) {
+      if (j < n_lim) {
         s = s_u[x];
         for (int k = 1; k <= half; ++k) {
-          // slots outside [0, n_cand) hold -inf; positions strictly increase, so
+          // slots outside [0, n_lim) hold -inf; positions strictly increase, so
           // the candidates within half positions are within half slots
           if ((int64_t)pj - s_pos[x - k] <= half) s = fmaxf(s, s_u[x - k]);
           if ((int64_t)s_pos[x + k] - pj <= half) s = fmaxf(s, s_u[x + k]);
@@ -451,12 +474,38 @@ __global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const Sna
   if (bad_pos && tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_POSITIONS);
 }
 
-template <int D>
+template <int D, bool kAccum>
 void launch_snapkv_d(const SnapParams& p, int num_units, int rows, hipStream_t stream) {
+  const dim3 grid(num_units, p.n_rb);
   if (rows <= 64)
-    hipLaunchKernelGGL((snapkv_score_kernel<D, 1>), dim3(num_units), dim3(kSnapThreads), 0, stream, p);
+    hipLaunchKernelGGL((snapkv_score_kernel<D, 1, kAccum>), grid, dim3(kSnapThreads), 0, stream, p);
   else
-    hipLaunchKernelGGL((snapkv_score_kernel<D, 2>), dim3(num_units), dim3(kSnapThreads), 0, stream, p);
+    hipLaunchKernelGGL((snapkv_score_kernel<D, 2, kAccum>), grid, dim3(kSnapThreads), 0, stream, p);
+}
+
+constexpr int kApplyThreads = 256;
+constexpr int kApplySlots = 2048;  // slots per work-group
+
+// H2O chunk scores: score(j) = (j in the chunk ? 0 : score(j)) + the row
+// blocks' partial u (added in block order).  A unit the scoring kernel
+// rejected (length or block table) is left alone.
+__global__ __launch_bounds__(kApplyThreads) void h2o_chunk_apply_kernel(const SnapParams p) {
+  __shared__ int s_red[kApplyThreads / kWave];
+  const int unit = blockIdx.y;
+  const int L = p.lengths[unit];
+  if (L > p.max_len || L > p.max_pages * kPage || L > kSnapMaxPages * kPage || L < p.chunk) return;
+  const int32_t* bt = p.block_table + (size_t)unit * p.max_pages;
+  const int n_pages = ceil_div_dev(L, kPage);
+  int bad = 0;
+  for (int i = threadIdx.x; i < n_pages; i += kApplyThreads) bad |= (bt[i] < 0 || (int64_t)bt[i] >= p.num_pages);
+  if (block_reduce<kApplyThreads>(bad, s_red, [](int a, int b) { return a | b; })) return;
+  const int j0 = blockIdx.x * kApplySlots;
+  for (int j = j0 + threadIdx.x; j < min(L, j0 + kApplySlots); j += kApplyThreads) {
+    float u = 0.f;
+    for (int b = 0; b < p.n_rb; ++b) u += p.u[((size_t)unit * p.n_rb + b) * p.u_stride + j];
+    float* sc = p.score_pool + (size_t)bt[j >> 4] * kPage + (j & (kPage - 1));
+    *sc = (j >= L - p.chunk ? 0.f : *sc) + u;
+  }
 }
 
 }  // namespace se
@@ -508,10 +557,12 @@ extern "C" se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, c
   p.c = scale * kLog2e;
   p.dev_err = dev_err;
   const int rows = window * q_per_kv;
+  p.n_rb = 1;
+  p.chunk = 0;
   if (kv->head_dim == 128)
-    launch_snapkv_d<128>(p, kv->num_units, rows, stream);
+    launch_snapkv_d<128, false>(p, kv->num_units, rows, stream);
   else
-    launch_snapkv_d<64>(p, kv->num_units, rows, stream);
+    launch_snapkv_d<64, false>(p, kv->num_units, rows, stream);
   st = launch_status();
   if (st != SE_OK || (flags & SE_SNAPKV_SCORE_ONLY)) return st;
 
@@ -525,6 +576,81 @@ extern "C" se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, c
   e.max_pages = kv->max_pages;
   e.budget = budget;
   e.recent = window;
+  e.max_len = max_len;
+  e.freed_pages = freed_pages;
+  e.freed_stride = freed_stride;
+  e.freed_count = freed_count;
+  e.dev_err = dev_err;
+  launch_evict(e, kv->num_units, kv->head_dim, stream);
+  return launch_status();
+}
+
+size_t se_h2o_prefill_workspace_bytes(int32_t num_units, int32_t max_len, int32_t q_per_kv, int32_t window) {
+  if (num_units <= 0 || max_len <= 0 || q_per_kv <= 0 || window <= 0) return 0;
+  const size_t n_rb = (size_t)ceil_div((int64_t)window * q_per_kv, kSnapMaxRows);
+  return (size_t)num_units * n_rb * align_up((size_t)max_len, 64) * sizeof(float);
+}
+
+extern "C" se_status se_h2o_prefill_chunk(const se_kv_view* kv, int32_t q_per_kv, const void* q_score,
+                                          int32_t score_window, int32_t chunk_len, float scale, int32_t budget,
+                                          int32_t recent, int32_t max_len, int32_t* freed_pages,
+                                          int32_t freed_stride, int32_t* freed_count, void* ws, size_t ws_bytes,
+                                          int32_t* dev_err, hipStream_t stream) {
+  se_status st = check_view(kv);
+  if (st != SE_OK) return st;
+  if (kv->kv_pool == nullptr || kv->pos_pool == nullptr || kv->score_pool == nullptr || q_score == nullptr ||
+      dev_err == nullptr)
+    return SE_ERR_INVALID_ARGUMENT;
+  if (q_per_kv < 1 || score_window < 1 || chunk_len < score_window || budget < 1 || recent < 0 || max_len < 1)
+    return SE_ERR_INVALID_ARGUMENT;
+  if (!(scale > 0.f) || !(scale < INFINITY)) return SE_ERR_INVALID_ARGUMENT;
+  if (freed_pages != nullptr && freed_stride < kv->max_pages) return SE_ERR_INVALID_ARGUMENT;
+  if ((int64_t)score_window * q_per_kv > 8 * kSnapMaxRows) return SE_ERR_UNSUPPORTED;
+  if (budget > kMaxBudget || max_len > kSnapMaxPages * kPage) return SE_ERR_UNSUPPORTED;
+  if (ws == nullptr || ws_bytes < se_h2o_prefill_workspace_bytes(kv->num_units, max_len, q_per_kv, score_window))
+    return SE_ERR_WORKSPACE;
+
+  SnapParams p;
+  p.kv = static_cast<const uint16_t*>(kv->kv_pool);
+  p.pos_pool = kv->pos_pool;
+  p.score_pool = kv->score_pool;
+  p.block_table = kv->block_table;
+  p.lengths = kv->lengths;
+  p.q = static_cast<const uint16_t*>(q_score);
+  p.u = static_cast<float*>(ws);
+  p.num_pages = kv->num_pages;
+  p.max_pages = kv->max_pages;
+  p.num_kv_heads = kv->num_kv_heads;
+  p.q_per_kv = q_per_kv;
+  p.w = score_window;
+  p.half = 0;
+  p.budget = budget;
+  p.max_len = max_len;
+  p.u_stride = (int32_t)align_up((size_t)max_len, 64);
+  p.n_rb = (int32_t)ceil_div((int64_t)score_window * q_per_kv, kSnapMaxRows);
+  p.chunk = chunk_len;
+  p.c = scale * kLog2e;
+  p.dev_err = dev_err;
+  const int rows = std::min(score_window * q_per_kv, kSnapMaxRows);
+  if (kv->head_dim == 128)
+    launch_snapkv_d<128, true>(p, kv->num_units, rows, stream);
+  else
+    launch_snapkv_d<64, true>(p, kv->num_units, rows, stream);
+  hipLaunchKernelGGL(h2o_chunk_apply_kernel, dim3((unsigned)ceil_div(max_len, kApplySlots), kv->num_units),
+                     dim3(kApplyThreads), 0, stream, p);
+  st = launch_status();
+  if (st != SE_OK) return st;
+
+  EvictParams e;
+  e.kv = static_cast<uint16_t*>(kv->kv_pool);
+  e.pos_pool = kv->pos_pool;
+  e.score_pool = kv->score_pool;
+  e.block_table = kv->block_table;
+  e.lengths = kv->lengths;
+  e.num_pages = kv->num_pages;
+  e.max_pages = kv->max_pages;
+  e.budget = budget;
+  e.recent = recent;
   e.max_len = max_len;
   e.freed_pages = freed_pages;
   e.freed_stride = freed_stride;

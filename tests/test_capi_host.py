@@ -19,7 +19,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 14, names
+    assert len(names) == 15, names
     lib = b.raw_library()
     for n in names:
         assert hasattr(lib, n), f"{n} is declared in sparse_engine.h but not exported"
@@ -166,6 +166,30 @@ def test_omnikv_argument_checks():
     assert call_att(err=None) == b.SE_ERR_INVALID_ARGUMENT
 
 
+def test_h2o_prefill_argument_checks():
+    fn = b.raw_library().se_h2o_prefill_chunk
+    v = _view()
+
+    def call(view=v, G=4, q=0x7000, sw=8, chunk=64, scale=0.1, budget=32, recent=8, max_len=128, ws=0x9000,
+             ws_bytes=1 << 40, err=0xA000):
+        return fn(ctypes.byref(view), G, q, sw, chunk, scale, budget, recent, max_len, None, 0, None, ws, ws_bytes,
+                  err, None)
+
+    assert call(q=None) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(sw=0) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(sw=65) == b.SE_ERR_INVALID_ARGUMENT        # window longer than the chunk
+    assert call(budget=0) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(recent=-1) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(scale=0.0) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(G=8, sw=129, chunk=200) == b.SE_ERR_UNSUPPORTED   # 1032 scoring rows
+    assert call(budget=9000) == b.SE_ERR_UNSUPPORTED
+    assert call(max_len=131073) == b.SE_ERR_UNSUPPORTED
+    assert call(ws=None) == b.SE_ERR_WORKSPACE
+    assert call(ws_bytes=8) == b.SE_ERR_WORKSPACE
+    assert call(err=None) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(view=_view(score_pool=None)) == b.SE_ERR_INVALID_ARGUMENT
+
+
 def test_workspace_sizes():
     # decode: counters + split partials + per-slot weights + per-page references
     n = b.se_workspace_bytes(b.SE_OP_DECODE_ATTEND, 512, 2049, 129, 4, 128, 0)
@@ -178,4 +202,6 @@ def test_workspace_sizes():
     assert b.se_workspace_bytes(b.SE_OP_SNAPKV, 512, 32768, 2048, 4, 128, 0) == 512 * 32768 * 4
     assert b.se_workspace_bytes(b.SE_OP_SNAPKV, 3, 1000, 63, 4, 128, 0) == 3 * 1024 * 4
     assert b.se_workspace_bytes(b.SE_OP_OMNIKV_SELECT, 32, 33000, 2063, 4, 128, 0) == 32 * 33024 * 4
+    assert b.se_workspace_bytes(b.SE_OP_H2O_PREFILL, 10, 1000, 63, 4, 128, 128) == 10 * 4 * 1024 * 4
+    assert b.se_workspace_bytes(b.SE_OP_H2O_PREFILL, 10, 1000, 63, 4, 128, 32) == 10 * 1 * 1024 * 4
     assert b.se_workspace_bytes(99, 1, 1, 1, 1, 64, 0) == 0
