@@ -22,8 +22,13 @@ one step is one decode step through all 32 layers); `--workload snapkv`
 measures SnapKV prompt compaction instead
 (se_snapkv_compact on the 8B-shaped prompt: 64 requests x 8 KV heads x 32768
 slots, window 32, pooling width 7, budget 2048; one step is one compaction of
-the whole batch from a fresh copy of the prompt); `--gpus N` with N > 1 is
-refused (single-GPU build).
+the whole batch from a fresh copy of the prompt); `--workload h2o_prefill`
+measures H2O's chunk-wise prefill eviction (se_h2o_prefill_chunk after the
+fourth 8192-token chunk of 32768-token prompts, 8 requests x 8 KV heads, 2048
+retained + 8192 chunk slots scored by the chunk's last 128 queries of every
+head and cut back to 2048 with a 1024-token window; one step is one call from
+a fresh copy of that state); `--gpus N` with N > 1 is refused (single-GPU
+build).
 """
 
 import argparse
@@ -42,6 +47,7 @@ TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_step_h2o_llama3-8b-laye
 SNAPKV_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "snapkv_compact_llama3-8b-prompt-snapkv_traffic.txt")
 DECODE_SOURCES = ("decode_attend.hip", "evict_compact.hip", "evict_core.h", "se_common.h")
 SNAPKV_SOURCES = ("snapkv.hip", "evict_compact.hip", "evict_core.h", "se_common.h")
+PREFILL_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "h2o_prefill_chunk_llama3-8b-prefill-chunk-h2o_traffic.txt")
 
 
 def parse():
@@ -50,9 +56,10 @@ def parse():
     ap.add_argument("--steps", type=int, default=None, help="timed decode steps (default: the workload's)")
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default 8; snapkv: 1)")
     ap.add_argument("--config", type=int, default=1, help="workload index 0..4")
-    ap.add_argument("--workload", choices=["decode", "snapkv", "omnikv"], default="decode",
-                    help="decode (the --config workload), snapkv (prompt compaction) or omnikv "
-                         "(32-layer decode with OmniKV selection reuse)")
+    ap.add_argument("--workload", choices=["decode", "snapkv", "omnikv", "h2o_prefill"], default="decode",
+                    help="decode (the --config workload), snapkv (prompt compaction), omnikv "
+                         "(32-layer decode with OmniKV selection reuse) or h2o_prefill (chunk-wise "
+                         "prefill eviction)")
     ap.add_argument("--cpu-baseline", choices=["auto", "skip"], default="auto")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 4 GiB device copy (counter calibration under rocprofv3)")
@@ -319,6 +326,168 @@ def main_snapkv(args):
     print(json.dumps(result), flush=True)
 
 
+def prefill_work(L, C, s, G, D, budget):
+    """(bytes, flops) se_h2o_prefill_chunk must move and compute for units of L
+    slots whose last C joined with this chunk, scored by s queries of each of
+    the G heads.  Bytes: the keys twice (the row normalisers need every key
+    before any weight can be summed), the queries, each slot's weight sum
+    written and read back, the earlier slots' scores read and every score
+    written; then the eviction's position and score reads and the movers' K, V,
+    position and score read and written (units above the budget).  Flops: the
+    s * G logit rows against every key once (2 * D per logit)."""
+    import numpy as np
+    L = np.asarray(L, dtype=np.int64)
+    units = int(L.shape[0])
+    score = int(L.sum()) * (2 * (D * 2) + 4 + 4 + 4) + int((L - C).clip(min=0).sum()) * 4 + units * (s * G * D * 2)
+    over = L[L > budget]
+    moved = np.minimum(over - budget, budget)
+    evict = int(over.sum()) * 8 + int(moved.sum()) * 2 * (2 * D * 2 + 8)
+    flops = int(L.sum()) * s * G * 2 * D
+    return score + evict, flops
+
+
+def cpu_baseline_h2o_prefill(w):
+    """The oracle, untuned, on a bounded sample of the prefill workload: the
+    first request (8 KV-head units), one unit per worker process, each
+    taking the chunk's append, scoring and eviction.  Runs before the GPU is
+    touched."""
+    import multiprocessing as mp
+    import numpy as np
+    import torch
+    from workloads import build_observation, build_state, scaled, unit_slots
+    sample_req = 1
+    ws = scaled(w, num_req=sample_req)
+    host = build_state(ws, "cpu")
+    qs = build_observation(ws, host, "cpu")
+    G, C = ws.q_per_kv, ws.chunk
+    jobs = []
+    for u in range(ws.units_per_layer):
+        req, kvh = divmod(u, ws.hkv)
+        Kt, Vt, pos, sc = unit_slots(host, u)
+        n0 = Kt.shape[0] - C
+        f = lambda t: t.to(torch.float64).numpy()
+        jobs.append({"K": f(Kt[:n0]), "V": f(Vt[:n0]), "pos": pos[:n0].numpy().astype(np.int64),
+                     "u": sc[:n0].to(torch.float64).numpy(), "Kc": f(Kt[n0:]), "Vc": f(Vt[n0:]),
+                     "pc": pos[n0:].numpy().astype(np.int64), "Qs": f(qs[req, :, kvh * G:(kvh + 1) * G])})
+    _SHARED["jobs"], _SHARED["w"] = jobs, ws
+    workers = min(16, os.cpu_count() or 1, len(jobs))
+    ctx = mp.get_context("fork")
+    t0 = time.perf_counter()
+    with ctx.Pool(workers) as pool:
+        per_unit = pool.map(_oracle_prefill_run, range(len(jobs)))
+    wall = time.perf_counter() - t0
+    return {"value": round(sample_req * C / wall, 1), "unit": "prompt tokens/s", "cores": workers,
+            "kind": "oracle",
+            "sample": (f"{sample_req} of {w.num_req} requests ({len(jobs)} KV-head units: {C}-token chunk behind "
+                       f"{w.initial_resident - C} retained slots) of '{w.name}', one chunk each (append, "
+                       f"scoring, eviction), NumPy float64, one unit per process"),
+            "cpu_seconds": round(sum(per_unit), 2), "wall_seconds": round(wall, 2)}
+
+
+def _oracle_prefill_run(i):
+    from threadpoolctl import threadpool_limits
+    from oracle import h2o
+    from oracle.state import new_unit
+    job, w = _SHARED["jobs"][i], _SHARED["w"]
+    with threadpool_limits(1):
+        st = new_unit(job["K"], job["V"], job["pos"], job["u"])
+        t0 = time.perf_counter()
+        h2o.prefill_chunk(st, job["Kc"], job["Vc"], job["pc"], job["Qs"], w.scale, w.budget, w.recent)
+        return time.perf_counter() - t0
+
+
+def main_h2o_prefill(args):
+    """H2O chunk-wise prefill eviction: K calls over the whole batch, each on a
+    fresh copy of the state (earlier retained slots + the chunk) made before
+    its timed call."""
+    from workloads import H2O_PREFILL
+    w = H2O_PREFILL
+    K = int(args.steps if args.steps is not None else 5)
+    W = int(args.warmup if args.warmup is not None else 1)
+    cpu = cpu_baseline_h2o_prefill(w) if args.cpu_baseline == "auto" else None
+    if cpu is not None:
+        print(f"cpu baseline: {cpu['value']:.1f} prompt tokens/s on {cpu['cores']} processes", file=sys.stderr,
+              flush=True)
+    import numpy as np
+    import torch
+    import paper_2609_39068_amd as se
+    from workloads import build_observation, build_state, clone_state
+
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    dev = torch.device("cuda:0")
+    state = build_state(w, dev)
+    qs = build_observation(w, state, dev)
+    U, G, D, sw, C = w.units_per_layer, w.q_per_kv, w.head_dim, w.obs_window, w.chunk
+    max_len = state.max_pages * 16
+    ws = torch.empty(se.se_workspace_bytes(se.SE_OP_H2O_PREFILL, U, max_len, state.max_pages, G, D, sw),
+                     dtype=torch.uint8, device=dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    fcount = torch.zeros(U, dtype=torch.int32, device=dev)
+    lengths0 = state.lengths.cpu().numpy()
+
+    def call(st):
+        view = se.KVView(st.kv_pool, st.pos_pool, st.score_pool, None, st.block_table, st.lengths,
+                         num_kv_heads=w.hkv)
+        se.se_h2o_prefill_chunk(view, G, qs, sw, C, w.scale, w.budget, w.recent, max_len, None, 0, fcount,
+                                ws, err)
+
+    for _ in range(W):
+        c = clone_state(state)
+        call(c)
+        torch.cuda.synchronize()
+        del c
+    times, walls = [], []
+    for _ in range(K):
+        c = clone_state(state)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ev[0].record()
+        call(c)
+        ev[1].record()
+        torch.cuda.synchronize()
+        walls.append(time.perf_counter() - t0)
+        times.append(ev[0].elapsed_time(ev[1]))
+        assert int(c.lengths.max()) == w.budget
+        del c
+    errs = se.se_read_device_errors(err)
+    if errs:
+        raise RuntimeError(f"device error bits {errs:#x} during the timed run")
+    ms = float(np.mean(times))
+    elapsed = float(np.sum(walls))
+    nbytes, flops = prefill_work(lengths0, C, sw, G, D, w.budget)
+    achieved = nbytes / (ms * 1e-3) / 1e9
+    result = {
+        "metric": "H2O chunked-prefill eviction prompt-tokens/s/GPU; achieved HBM GB/s vs MI355X peak",
+        "value": round(w.num_req * C * K / elapsed, 1),
+        "unit": "prompt tokens/s",
+        "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": round(1e3 * elapsed / K, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "method": "h2o_prefill", "batch": w.num_req, "hq": w.hq, "hkv": w.hkv,
+                   "head_dim": D, "page_size": w.page_size, "prompt": w.ctx, "chunk": C,
+                   "retained_before": w.initial_resident - C, "scoring_window": sw, "budget": w.budget,
+                   "recent": w.recent, "accumulate": "f32", "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": "hbm", "kernel": "se_h2o_prefill_chunk", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": read_traffic(PREFILL_TRAFFIC_SUMMARY, SNAPKV_SOURCES),
+                     "avg_launch_us": round(1e3 * ms, 3),
+                     "algorithmic_bytes_per_launch": nbytes,
+                     "algorithmic_flops_per_launch": flops,
+                     "mfma_TFLOPs": round(flops / (ms * 1e-3) / 1e12, 1)},
+        "cpu_baseline": cpu,
+    }
+    if args.copy_calibration:
+        n = 4 << 30
+        a = torch.empty(n, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        result["copy_calibration_bytes"] = n
+    print(json.dumps(result), flush=True)
+
+
 def omnikv_layer_bytes(L, G, D, b, observe):
     """Bytes one layer's OmniKV decode call(s) must move for units with L slots
     after the append.  Observation layer (se_decode_attend with logits, then
@@ -563,6 +732,9 @@ def main():
         return
     if args.workload == "omnikv":
         main_omnikv(args)
+        return
+    if args.workload == "h2o_prefill":
+        main_h2o_prefill(args)
         return
     from workloads import CONFIGS
     w = CONFIGS[args.config]

@@ -162,13 +162,24 @@ def prefill_chunk(st: UnitState, K: np.ndarray, V: np.ndarray, pos: np.ndarray, 
     positions (s = C: every query of the chunk); GQA sum; window and TopK as
     for decode."""
     C = K.shape[0]
-    s = Qs.shape[0]
-    if not 1 <= s <= C:
+    if not 1 <= Qs.shape[0] <= C:
         raise ValueError("the scoring window must hold 1 .. C queries")
     for c in range(C):
         append(st, K[c], V[c], int(pos[c]))
+    return chunk_eviction(st, C, Qs, scale, budget, recent)
+
+
+def chunk_eviction(st: UnitState, C: int, Qs: np.ndarray, scale: float, budget: int, recent: int) -> dict:
+    """The part of ``prefill_chunk`` after the chunk's append: the chunk is the
+    unit's last C slots (score 0); its last s positions' queries Qs [s, G, d]
+    add their causal weights, then the retained set and the compaction.
+    Mutates ``st``."""
+    s = Qs.shape[0]
+    if not 1 <= s <= C <= st.length:
+        raise ValueError("the scoring window must hold 1 .. C queries of a resident chunk")
+    L = st.length
     for t in range(s):
-        p_t = int(pos[C - s + t])
+        p_t = int(st.pos[L - s + t])
         S = np.flatnonzero(st.pos <= p_t)          # causal: up to the query's own position
         _, _, alpha, _ = selected_attention(Qs[t], st.K, st.V, S, scale)
         st.u = accumulate(st.u, S, alpha)

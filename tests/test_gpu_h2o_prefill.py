@@ -12,7 +12,7 @@ import torch
 
 from oracle import h2o
 from tests.oracle_bridge import assert_scores_close, f64, gpu_unit, h2o_near_tie, oracle_unit
-from workloads import isolated_units, observation_queries, to_device
+from workloads import H2O_PREFILL, build_observation, build_state, isolated_units, observation_queries, to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -143,3 +143,51 @@ def test_length_below_chunk_is_reported(se):
     torch.cuda.synchronize()
     assert se.se_read_device_errors(err) & se.SE_DEVERR_BAD_LENGTH
     assert torch.equal(before, gs.score_pool)
+
+
+def test_full_workload_sampled_units(se):
+    # the 8B-shaped prefill workload at full size, in the launch configuration
+    # the benchmark times (64 units of 2048 retained + 8192 chunk slots, 128
+    # scoring queries x 4 heads = 4 row blocks, budget 2048, window 1024); the
+    # oracle takes three sampled units from the same generated state
+    w = H2O_PREFILL
+    U, G, C, sw = w.units_per_layer, w.q_per_kv, w.chunk, w.obs_window
+    gs = build_state(w, DEV)
+    qs = build_observation(w, gs, DEV)
+    sample = [0, 29, U - 1]
+    ost = {}
+    for u in sample:
+        st = oracle_unit(gs, u)
+        st.u[-C:] = 0.0                      # the chunk's stale scores: the call starts them at 0
+        ost[u] = st
+    bt = gs.block_table.cpu().numpy()
+    max_len = gs.max_pages * 16
+    ws = torch.empty(se.se_workspace_bytes(se.SE_OP_H2O_PREFILL, U, max_len, gs.max_pages, G, w.head_dim, sw),
+                     dtype=torch.uint8, device=DEV)
+    freed = torch.full((U, gs.max_pages), -7, dtype=torch.int32, device=DEV)
+    fcount = torch.zeros(U, dtype=torch.int32, device=DEV)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    print(f"full prefill workload: U={U} L={int(gs.lengths[0])} C={C} sw={sw}", flush=True)
+    se.se_h2o_prefill_chunk(_view(se, gs, w.hkv), G, qs, sw, C, w.scale, w.budget, w.recent, max_len, freed,
+                            gs.max_pages, fcount, ws, err)
+    torch.cuda.synchronize()
+    assert se.se_read_device_errors(err) == 0
+    assert bool((gs.lengths == w.budget).all())
+    fc, fp = fcount.cpu().numpy(), freed.cpu().numpy()
+    q = qs.cpu()
+    for u in sample:
+        req, h = divmod(u, w.hkv)
+        r = h2o.chunk_eviction(ost[u], C, f64(q[req, :, h * G:(h + 1) * G]), w.scale, w.budget, w.recent)
+        st, g = ost[u], gpu_unit(gs, u)
+        kept_g, kept_o = set(g["pos"].tolist()), set(st.pos.tolist())
+        if kept_g != kept_o:
+            by_pos = dict(zip(r["pos_after_append"].tolist(), r["u_after_accumulate"].tolist()))
+            assert h2o_near_tie(by_pos, kept_g, kept_o), f"unit {u}: retained sets differ"
+            continue
+        np.testing.assert_array_equal(g["pos"], st.pos)
+        np.testing.assert_array_equal(g["K"], st.K)
+        np.testing.assert_array_equal(g["V"], st.V)
+        assert_scores_close(g["u"], st.u, f"unit {u}")
+        n = len(r["freed"])
+        assert fc[u] == n
+        np.testing.assert_array_equal(fp[u, :n], bt[u, r["freed"]])

@@ -17,7 +17,7 @@ from typing import Optional, Tuple
 class Workload:
     index: int
     name: str
-    method: str                      # "h2o", "quest", "snapkv" (prompt compaction) or "omnikv"
+    method: str                      # "h2o", "quest", "snapkv" (prompt compaction), "omnikv" or "h2o_prefill"
     num_req: int
     hq: int
     hkv: int
@@ -35,6 +35,7 @@ class Workload:
     obs_window: Optional[int] = None  # SnapKV observation window w (the prompt's last w positions)
     pool_kernel: Optional[int] = None  # SnapKV max-pooling width kappa
     filter_layers: Optional[Tuple[int, ...]] = None  # OmniKV observation layers (full attention + selection)
+    chunk: Optional[int] = None      # H2O prefill: the chunk's length (its queries' last obs_window score)
     hh_rate: float = 0.0             # share of positions whose key gets += hh_shift * u
     hh_shift: float = 0.0
     relevant_pages: int = 0          # Quest: pages whose keys all get += relevant_shift * u
@@ -87,6 +88,17 @@ SNAPKV = Workload(5, "llama3-8b-prompt-snapkv", "snapkv", num_req=64, hq=32, hkv
 OMNIKV = Workload(6, "llama3-8b-32-layer-omnikv", "omnikv", num_req=32, hq=32, hkv=8, head_dim=128,
                   layers=32, steps=32, ctx=32768, budget=2048, filter_layers=(0, 2, 7, 13, 16, 26),
                   hh_rate=0.01, hh_shift=4.0, seed=6)
+
+
+# H2O chunk-wise prefill eviction (Appendix A.3, H2O; Appendix D, LongBench
+# settings: 2,048-token budget, recent ratio 0.5, 8,192-token prefill chunks, a
+# 128-query scoring window, FP32 scores): the fourth chunk of a 32768-token
+# prompt has just been written behind the 2048 slots the earlier chunks left,
+# 8 requests to a 65,536-token prefill step.  The call scores the 10240 slots
+# with the chunk's last 128 queries of every head and cuts them back to 2048.
+H2O_PREFILL = Workload(7, "llama3-8b-prefill-chunk-h2o", "h2o_prefill", num_req=8, hq=32, hkv=8, head_dim=128,
+                       layers=1, steps=1, ctx=32768, initial_resident=2048 + 8192, budget=2048, recent=1024,
+                       obs_window=128, chunk=8192, hh_rate=0.01, hh_shift=4.0, seed=7)
 
 
 def scaled(w: Workload, **changes) -> Workload:

@@ -33,7 +33,14 @@ Value recipe (the workloads' own description):
     position s), with the heavy-hitter construction of the H2O workloads;
   * SnapKV workload: the whole prefilled prompt is resident (slot s holds
     position s) and the observation queries of its last obs_window positions
-    are N(0, 1) + u, rounded to bf16, like decode queries.
+    are N(0, 1) + u, rounded to bf16, like decode queries;
+  * H2O prefill workload: the chunk's `chunk` positions sit behind a
+    stratified sample of the earlier ones (the retained slots, drawn like a
+    retained workload with the chunk as its tail); the retained slots' scores
+    are Exp(mean 0.15) (about three chunks' worth of the average weight a slot
+    receives: 128 * G weight units spread over 10240 slots), the chunk's slots
+    hold -1 (stale values the call replaces); the scoring queries are drawn like
+    SnapKV's observation queries.
 No part of attention, scoring, selection or compaction is computed here.
 """
 
@@ -127,7 +134,7 @@ def _positions(w: Workload, layer: int, ctx_u: torch.Tensor, L: torch.Tensor,
     U = L.shape[0]
     slots = torch.arange(cap, device=device, dtype=torch.int64)[None, :].expand(U, cap)
     full = (L == ctx_u)
-    recent = int(w.recent or 0)
+    recent = int(w.chunk if w.method == "h2o_prefill" else (w.recent or 0))
     n_old = (L - recent).clamp(min=0)                     # sampled older positions
     R = (ctx_u - recent).clamp(min=1)                      # older range [0, R)
     # stratum i of n_old covers [i*R//n, (i+1)*R//n); one uniform pick per stratum
@@ -149,7 +156,7 @@ def build_state(w: Workload, device, generate_values: bool = True) -> PagedInput
     L0 = _initial_lengths(w, ctx, device)
     if w.method == "h2o":
         cap_slots = int(max(int(L0.max()), int(w.budget)) + 1)
-    elif w.method == "snapkv":
+    elif w.method in ("snapkv", "h2o_prefill"):
         cap_slots = int(L0.max())
     elif w.method == "omnikv":
         cap_slots = int(L0.max()) + w.steps
@@ -164,7 +171,7 @@ def build_state(w: Workload, device, generate_values: bool = True) -> PagedInput
     kv_pool = torch.empty((num_pages, 2, P, d), dtype=torch.bfloat16, device=device)
     pos_pool = torch.full((num_pages, P), -1, dtype=torch.int32, device=device)
     score_pool = (torch.zeros((num_pages, P), dtype=torch.float32, device=device)
-                  if w.method in ("h2o", "snapkv") else None)
+                  if w.method in ("h2o", "snapkv", "h2o_prefill") else None)
     meta_pool = torch.zeros((num_pages, 2, d), dtype=torch.bfloat16, device=device) if w.method == "quest" else None
     lengths = L0.to(torch.int32).repeat(w.layers)
 
@@ -188,10 +195,16 @@ def build_state(w: Workload, device, generate_values: bool = True) -> PagedInput
         row = torch.arange(cap, device=device) % P
         valid = pos >= 0
         pos_pool.view(-1)[(page * P + row)[valid]] = pos[valid].to(torch.int32)
+        if w.method == "h2o_prefill":
+            e = torch.rand(U, cap, generator=_gen(w, 300 + layer, device), device=device, dtype=torch.float64)
+            sc = (-0.15 * torch.log1p(-e)).to(torch.float32)
+            old = torch.arange(cap, device=device)[None, :] < (L0 - int(w.chunk))[:, None]
+            sc = torch.where(old, sc, torch.full_like(sc, -1.0))
+            score_pool.view(-1)[(page * P + row)[valid]] = sc[valid]
         if not generate_values:
             continue
         shift = None
-        if w.method in ("h2o", "snapkv", "omnikv") and w.hh_rate > 0:
+        if w.method in ("h2o", "snapkv", "omnikv", "h2o_prefill") and w.hh_rate > 0:
             unit_ids = torch.arange(U, device=device)[:, None].expand(U, cap)
             shift = valid & heavy_hitter(w, layer, unit_ids, pos.clamp(min=0))
             amount = w.hh_shift
