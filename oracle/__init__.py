@@ -21,6 +21,12 @@ h2o        append, accumulated-score update, retention and the compacted
 quest      page summaries, the page upper bound, page selection and the
            sparse decode step (Appendix A.3, eqs. background-quest-summary
            and background-quest-score).
+snapkv     SnapKV observation-window scores, max pooling and prompt compaction
+           (Appendix A.3, eqs. background-snapkv-score and background-snapkv-retention).
+omnikv     OmniKV max-over-heads selection and its reuse by sparse layers
+           (Appendix A.3, eqs. background-omnikv-selection and background-omnikv-reuse).
+prune      interval prefix-cache pruning (Section 3.2, eq. prefix-pruning;
+           Appendix C.2).
 brute      independent pure-Python references (dense attention with
            ``math`` only, selection by full ``sorted``) that pin the NumPy
            code on tiny inputs.
@@ -29,13 +35,16 @@ Parity status
 -------------
 Pinned (by brute force, closed forms or the paper's invariants; see
 ``tests/test_oracle_*.py``): selected attention, score accumulation,
-H2O retention, Quest summaries, Quest bound, Quest selection.
+H2O retention, H2O chunk-wise prefill eviction, Quest summaries, Quest
+bound, Quest selection, SnapKV scores and pooling, OmniKV selection, interval
+pruning.
 
 Parity unpinned by the paper (conventions of this repository, held only by
 the oracle): the per-KV-head aggregation of H2O scores and of Quest page
 scores under GQA (sum over the group for H2O, max over the group for Quest),
-and the hole-fill order of the compacted slot layout.  The paper fixes the
-retained *set* but not the order of slots after compaction.
+the hole-fill order of the compacted slot layout and the order-keeping slot
+layout after interval pruning.  The paper fixes the retained *set* but not
+the order of slots after compaction.
 """
 
-from . import attention, brute, h2o, quest  # noqa: F401
+from . import attention, brute, h2o, omnikv, prune, quest, snapkv  # noqa: F401

@@ -55,3 +55,19 @@ def quest_page_bound(q, page_keys, scale):
         hi = max(k[c] for k in page_keys)
         total += max(q[c] * lo, q[c] * hi)
     return scale * total
+
+
+def pruned_slots(positions, lo, hi, keep):
+    """eq. prefix-pruning by walking the slots in order: a slot stays when its
+    position lies outside [lo, hi) or is one of ``keep``.  Returns the old
+    slot indices that stay, in order."""
+    keep = set(keep)
+    return [s for s, p in enumerate(positions) if not (lo <= p < hi) or p in keep]
+
+
+def interval_budget_keep(positions, scores, lo, hi, budget):
+    """The ``budget`` slots of [lo, hi) with the largest scores (ties: lower
+    position) by a full sort; returns their positions as a set."""
+    cand = [s for s in range(len(positions)) if lo <= positions[s] < hi]
+    cand.sort(key=lambda s: (-scores[s], positions[s]))
+    return {positions[s] for s in cand[:budget]}
