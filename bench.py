@@ -27,8 +27,11 @@ measures H2O's chunk-wise prefill eviction (se_h2o_prefill_chunk after the
 fourth 8192-token chunk of 32768-token prompts, 8 requests x 8 KV heads, 2048
 retained + 8192 chunk slots scored by the chunk's last 128 queries of every
 head and cut back to 2048 with a 1024-token window; one step is one call from
-a fresh copy of that state); `--gpus N` with N > 1 is refused (single-GPU
-build).
+a fresh copy of that state); `--workload prune` measures interval prefix-cache
+pruning (se_prune_interval over 8 chains x 32 layers x 8 KV heads of 32768
+resident slots: the interval [16384, 20480) cut to its 1024 best-scored slots
+per unit and the later slots closed up; one step is one call from a fresh copy
+of the cache); `--gpus N` with N > 1 is refused (single-GPU build).
 """
 
 import argparse
@@ -47,6 +50,8 @@ TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_step_h2o_llama3-8b-laye
 SNAPKV_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "snapkv_compact_llama3-8b-prompt-snapkv_traffic.txt")
 DECODE_SOURCES = ("decode_attend.hip", "evict_compact.hip", "evict_core.h", "se_common.h")
 SNAPKV_SOURCES = ("snapkv.hip", "evict_compact.hip", "evict_core.h", "se_common.h")
+PRUNE_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "prune_interval_llama3-8b-32-layer-prune-interval_traffic.txt")
+PRUNE_SOURCES = ("prune.hip", "se_common.h")
 PREFILL_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "h2o_prefill_chunk_llama3-8b-prefill-chunk-h2o_traffic.txt")
 
 
@@ -56,10 +61,10 @@ def parse():
     ap.add_argument("--steps", type=int, default=None, help="timed decode steps (default: the workload's)")
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default 8; snapkv: 1)")
     ap.add_argument("--config", type=int, default=1, help="workload index 0..4")
-    ap.add_argument("--workload", choices=["decode", "snapkv", "omnikv", "h2o_prefill"], default="decode",
+    ap.add_argument("--workload", choices=["decode", "snapkv", "omnikv", "h2o_prefill", "prune"], default="decode",
                     help="decode (the --config workload), snapkv (prompt compaction), omnikv "
-                         "(32-layer decode with OmniKV selection reuse) or h2o_prefill (chunk-wise "
-                         "prefill eviction)")
+                         "(32-layer decode with OmniKV selection reuse), h2o_prefill (chunk-wise "
+                         "prefill eviction) or prune (interval prefix-cache pruning)")
     ap.add_argument("--cpu-baseline", choices=["auto", "skip"], default="auto")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 4 GiB device copy (counter calibration under rocprofv3)")
@@ -488,6 +493,159 @@ def main_h2o_prefill(args):
     print(json.dumps(result), flush=True)
 
 
+def prune_bytes(L, n_t, moved, D):
+    """Bytes se_prune_interval must move for units of L slots, n_t of them in
+    the interval, `moved` of them changing slot: every position read once (to
+    find the interval), the interval's scores read once (the selection), and
+    each moved slot's key and value rows, position and score read and
+    written."""
+    import numpy as np
+    L, n_t, moved = (np.asarray(x, dtype=np.int64) for x in (L, n_t, moved))
+    return int(L.sum()) * 4 + int(n_t.sum()) * 4 + int(moved.sum()) * 2 * (4 * D + 8)
+
+
+def cpu_baseline_prune(w):
+    """The oracle, untuned, on a bounded sample of the pruning workload: the
+    first layer's 64 units (8 chains x 8 KV heads), one unit per worker process,
+    each taking the budget selection and the compaction.  Runs before the GPU is
+    touched."""
+    import multiprocessing as mp
+    import numpy as np
+    import torch
+    from workloads import build_state, scaled, unit_slots
+    ws = scaled(w, layers=1)
+    host = build_state(ws, "cpu")
+    jobs = []
+    for u in range(ws.units_per_layer):
+        Kt, Vt, pos, sc = unit_slots(host, u)
+        jobs.append({"K": Kt.to(torch.float64).numpy(), "V": Vt.to(torch.float64).numpy(),
+                     "pos": pos.numpy().astype(np.int64), "u": sc.to(torch.float64).numpy()})
+    del host
+    _SHARED["jobs"], _SHARED["w"] = jobs, ws
+    workers = min(16, os.cpu_count() or 1, len(jobs))
+    ctx = mp.get_context("fork")
+    t0 = time.perf_counter()
+    with ctx.Pool(workers) as pool:
+        per_unit = pool.map(_oracle_prune_run, range(len(jobs)))
+    wall = time.perf_counter() - t0
+    lo, hi = w.interval
+    share = len(jobs) / (w.layers * w.units_per_layer)      # of one call's units
+    return {"value": round(share * w.num_req * (hi - lo) / wall, 1), "unit": "interval tokens/s",
+            "cores": workers, "kind": "oracle",
+            "sample": (f"layer 0 of {w.layers} ({len(jobs)} of {w.layers * w.units_per_layer} units, 32768 slots "
+                       f"each) of '{w.name}', one pruning each (budget selection and compaction), NumPy float64, "
+                       f"one unit per process; the rate is scaled by that share of a call"),
+            "cpu_seconds": round(sum(per_unit), 2), "wall_seconds": round(wall, 2)}
+
+
+def _oracle_prune_run(i):
+    from threadpoolctl import threadpool_limits
+    from oracle import prune
+    from oracle.state import new_unit
+    job, w = _SHARED["jobs"][i], _SHARED["w"]
+    lo, hi = w.interval
+    with threadpool_limits(1):
+        st = new_unit(job["K"], job["V"], job["pos"], job["u"])
+        t0 = time.perf_counter()
+        prune.prune(st, lo, hi, prune.budget_selection(st, lo, hi, w.budget))
+        return time.perf_counter() - t0
+
+
+def main_prune(args):
+    """Interval prefix-cache pruning: K calls over every unit of every chain and
+    layer, each on a fresh copy of the cache made before its timed call."""
+    from workloads import PRUNE
+    w = PRUNE
+    K = int(args.steps if args.steps is not None else 5)
+    W = int(args.warmup if args.warmup is not None else 1)
+    cpu = cpu_baseline_prune(w) if args.cpu_baseline == "auto" else None
+    if cpu is not None:
+        print(f"cpu baseline: {cpu['value']:.1f} interval tokens/s on {cpu['cores']} processes", file=sys.stderr,
+              flush=True)
+    import numpy as np
+    import torch
+    import paper_2609_39068_amd as se
+    from workloads import build_state, clone_state
+
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    dev = torch.device("cuda:0")
+    state = build_state(w, dev)
+    U, D = w.layers * w.units_per_layer, w.head_dim
+    lo, hi = w.interval
+    max_len = state.max_pages * 16
+    iv = torch.tensor([[lo, hi]] * U, dtype=torch.int32, device=dev)
+    kb = torch.full((U,), w.budget, dtype=torch.int32, device=dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    fcount = torch.zeros(U, dtype=torch.int32, device=dev)
+    lengths0 = state.lengths.cpu().numpy()
+
+    def call(st):
+        view = se.KVView(st.kv_pool, st.pos_pool, st.score_pool, None, st.block_table, st.lengths,
+                         num_kv_heads=w.hkv)
+        se.se_prune_interval(view, iv, None, 0, kb, max_len, None, 0, fcount, err)
+
+    moved = None
+    for i in range(max(W, 1)):  # the first call (untimed) also gives the moved-slot count
+        c = clone_state(state)
+        call(c)
+        torch.cuda.synchronize()
+        if i == 0:
+            # slot s held position s before the call: a slot whose position changed was written
+            P = 16
+            s = torch.arange(max_len, device=dev)
+            pos = c.pos_pool[c.block_table.long()[:, s // P], s % P]
+            moved = ((pos != s[None, :]) & (s[None, :] < c.lengths[:, None])).sum(dim=1).cpu().numpy()
+        del c
+    times, walls = [], []
+    for _ in range(K):
+        c = clone_state(state)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ev[0].record()
+        call(c)
+        ev[1].record()
+        torch.cuda.synchronize()
+        walls.append(time.perf_counter() - t0)
+        times.append(ev[0].elapsed_time(ev[1]))
+        assert int(c.lengths.max()) == w.ctx - (hi - lo) + w.budget
+        del c
+    errs = se.se_read_device_errors(err)
+    if errs:
+        raise RuntimeError(f"device error bits {errs:#x} during the timed run")
+    ms = float(np.mean(times))
+    elapsed = float(np.sum(walls))
+    n_t = np.full(U, hi - lo)
+    nbytes = prune_bytes(lengths0, n_t, moved, D)
+    achieved = nbytes / (ms * 1e-3) / 1e9
+    result = {
+        "metric": "interval prefix-pruning interval-tokens/s/GPU; achieved HBM GB/s vs MI355X peak",
+        "value": round(w.num_req * (hi - lo) * K / elapsed, 1),
+        "unit": "interval tokens/s",
+        "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": round(1e3 * elapsed / K, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "method": "prune", "chains": w.num_req, "layers": w.layers, "hkv": w.hkv,
+                   "head_dim": D, "page_size": w.page_size, "history": w.ctx, "interval": [lo, hi],
+                   "budget": w.budget, "units": U, "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": "hbm", "kernel": "se_prune_interval", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": read_traffic(PRUNE_TRAFFIC_SUMMARY, PRUNE_SOURCES),
+                     "avg_launch_us": round(1e3 * ms, 3),
+                     "algorithmic_bytes_per_launch": nbytes, "moved_slots": int(moved.sum())},
+        "cpu_baseline": cpu,
+    }
+    if args.copy_calibration:
+        n = 4 << 30
+        a = torch.empty(n, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        result["copy_calibration_bytes"] = n
+    print(json.dumps(result), flush=True)
+
+
 def omnikv_layer_bytes(L, G, D, b, observe):
     """Bytes one layer's OmniKV decode call(s) must move for units with L slots
     after the append.  Observation layer (se_decode_attend with logits, then
@@ -735,6 +893,9 @@ def main():
         return
     if args.workload == "h2o_prefill":
         main_h2o_prefill(args)
+        return
+    if args.workload == "prune":
+        main_prune(args)
         return
     from workloads import CONFIGS
     w = CONFIGS[args.config]

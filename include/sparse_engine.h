@@ -68,6 +68,8 @@ typedef enum se_status {
 #define SE_DEVERR_BAD_SELECTION 8u  /* a sel_pages entry outside the unit's pages          */
 #define SE_DEVERR_BAD_POSITIONS 16u /* eviction found repeated positions (retained != B),
                                        or a SnapKV prompt not in increasing position order */
+#define SE_DEVERR_BAD_INTERVAL  32u /* se_prune_interval: an interval wider than the mask
+                                       row, or a negative budget                           */
 
 /* Flags of se_decode_attend. */
 #define SE_ATTEND_ACCUMULATE 1u /* fused H2O score update (eq. background-h2o-score)   */
@@ -374,6 +376,43 @@ const char* se_status_string(se_status status);
 
 /* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
 int32_t se_version(void);
+
+/*
+ * se_prune_interval — sparsity-based prefix-cache pruning of a history interval
+ * (Section 3.2, "Sparsity-Based Prefix-Cache Pruning", eq. prefix-pruning; Appendix C.2,
+ * "Pruning Metadata and Cache Operations").  For every unit, with L = lengths[unit],
+ * T = the logical positions lo <= p < hi (interval[unit] = {lo, hi}, zero-based; lo >= hi
+ * is an empty interval) and R the unit's resident positions:
+ *   I = the positions of R within T that stay:
+ *       mask mode (keep_mask != NULL): position p stays iff
+ *         keep_mask[unit * mask_stride + (p - lo)] != 0 (entries of positions that are
+ *         not resident are ignored); hi - lo must not exceed mask_stride;
+ *       budget mode (keep_budget != NULL, needs score_pool): the keep_budget[unit] slots
+ *         of T with the largest score_pool values stay (equal scores: lower position);
+ *         all of them when T holds fewer, none for 0 (a retention ratio r over a fully
+ *         resident interval is the budget r * (hi - lo), rounded by the caller);
+ *   R' = (R \ T) u I.  The slots of R' keep their relative slot order and close up
+ *   into slots [0, |R'|) with their key, value, position and score (positions are
+ *   not renumbered: the logical prefix is unchanged); lengths[unit] = |R'|.
+ *   Quest summaries (meta_pool != NULL) of the pages from the interval's first slot
+ *   on are rebuilt.  Logical pages ceil(|R'|/16) .. ceil(L/16)-1 hold no resident slot
+ *   afterwards: their physical ids go to freed_pages[unit][0..n) with n in
+ *   freed_count[unit] (either may be NULL); a unit that loses nothing reports 0.
+ * The caller applies it to idle units only: no other call on those units may be in
+ * flight (Appendix C.2: pruning touches only blocks without active references).
+ * Positions within a unit must be distinct.
+ *  interval     int32 [num_units][2] (device)
+ *  keep_mask    uint8 [num_units][mask_stride] (device) or NULL
+ *  keep_budget  int32 [num_units] (device) or NULL; exactly one of the two
+ *  max_len      bound on every unit's length, <= 131072; a unit above it, or an
+ *               interval/budget the mode rejects, sets a device error bit and is
+ *               left unchanged
+ *  freed_stride >= max_pages when freed_pages is given
+ */
+se_status se_prune_interval(const se_kv_view* kv, const int32_t* interval, const uint8_t* keep_mask,
+                            int32_t mask_stride, const int32_t* keep_budget, int32_t max_len,
+                            int32_t* freed_pages, int32_t freed_stride, int32_t* freed_count,
+                            int32_t* dev_err, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -27,6 +27,7 @@ SE_DEVERR_CAPACITY = 2
 SE_DEVERR_BAD_LENGTH = 4
 SE_DEVERR_BAD_SELECTION = 8
 SE_DEVERR_BAD_POSITIONS = 16
+SE_DEVERR_BAD_INTERVAL = 32
 
 SE_ATTEND_ACCUMULATE = 1
 SE_QUEST_SCORES_GIVEN = 1
@@ -42,6 +43,7 @@ EXPORTED = (
     "se_decode_attend", "se_decode_step_h2o", "se_decode_step_quest", "se_accumulate_scores", "se_evict_compact", "se_quest_summarize",
     "se_quest_select", "se_workspace_bytes", "se_read_device_errors", "se_status_string",
     "se_version", "se_snapkv_compact", "se_omnikv_select", "se_attend_slots", "se_h2o_prefill_chunk",
+    "se_prune_interval",
 )
 
 
@@ -88,6 +90,7 @@ def _load():
         "se_omnikv_select": (I32, [V, I32, P, I32, I32, I32, P, P, SZ, P, P]),
         "se_h2o_prefill_chunk": (I32, [V, I32, P, I32, I32, F32, I32, I32, I32, P, I32, P, P, SZ, P, P]),
         "se_attend_slots": (I32, [V, I32, P, P, P, P, P, I32, F32, I32, P, P, P, P]),
+        "se_prune_interval": (I32, [V, P, P, I32, P, I32, P, I32, P, P, P]),
         "se_workspace_bytes": (SZ, [I32, I32, I32, I32, I32, I32, I32]),
         "se_read_device_errors": (I32, [P, P, P]),
         "se_status_string": (ctypes.c_char_p, [I32]),
@@ -379,3 +382,25 @@ def se_h2o_prefill_chunk(view: KVView, q_per_kv, q_score, score_window, chunk_le
         0 if ws is None else ws.numel() * ws.element_size(), _ptr(dev_err, torch.int32, "dev_err"),
         _stream(stream))
     _check("se_h2o_prefill_chunk", st)
+
+
+def se_prune_interval(view: KVView, interval, keep_mask, mask_stride, keep_budget, max_len, freed_pages,
+                      freed_stride, freed_count, dev_err, stream=None):
+    """interval int32 [num_units][2]; exactly one of keep_mask (uint8 [num_units][mask_stride])
+    and keep_budget (int32 [num_units])."""
+    s = view.struct
+    _need(interval, 2 * s.num_units, "interval")
+    if keep_mask is not None:
+        _need(keep_mask, s.num_units * int(mask_stride), "keep_mask")
+    if keep_budget is not None:
+        _need(keep_budget, s.num_units, "keep_budget")
+    if freed_pages is not None:
+        _need(freed_pages, s.num_units * int(freed_stride), "freed_pages")
+    if freed_count is not None:
+        _need(freed_count, s.num_units, "freed_count")
+    st = _lib.se_prune_interval(
+        view.ref(), _ptr(interval, torch.int32, "interval"), _ptr(keep_mask, torch.uint8, "keep_mask"),
+        int(mask_stride), _ptr(keep_budget, torch.int32, "keep_budget"), int(max_len),
+        _ptr(freed_pages, torch.int32, "freed_pages"), int(freed_stride),
+        _ptr(freed_count, torch.int32, "freed_count"), _ptr(dev_err, torch.int32, "dev_err"), _stream(stream))
+    _check("se_prune_interval", st)

@@ -19,7 +19,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 15, names
+    assert len(names) == 16, names
     lib = b.raw_library()
     for n in names:
         assert hasattr(lib, n), f"{n} is declared in sparse_engine.h but not exported"
@@ -188,6 +188,27 @@ def test_h2o_prefill_argument_checks():
     assert call(ws_bytes=8) == b.SE_ERR_WORKSPACE
     assert call(err=None) == b.SE_ERR_INVALID_ARGUMENT
     assert call(view=_view(score_pool=None)) == b.SE_ERR_INVALID_ARGUMENT
+
+
+def test_prune_argument_checks():
+    fn = b.raw_library().se_prune_interval
+    v = _view()
+
+    def call(view=v, iv=0x7000, mask=0x7100, stride=64, budget=None, max_len=128, freed=None, fstride=0,
+             err=0xA000):
+        return fn(ctypes.byref(view), iv, mask, stride, budget, max_len, freed, fstride, None, err, None)
+
+    assert call(iv=None) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(mask=None) == b.SE_ERR_INVALID_ARGUMENT               # neither mode
+    assert call(budget=0x7200) == b.SE_ERR_INVALID_ARGUMENT           # both modes
+    assert call(stride=0) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(mask=None, budget=0x7200, view=_view(score_pool=None)) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(max_len=0) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(max_len=131073) == b.SE_ERR_UNSUPPORTED
+    assert call(freed=0x7300, fstride=7) == b.SE_ERR_INVALID_ARGUMENT  # stride below max_pages
+    assert call(err=None) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(view=_view(kv_pool=None)) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(view=_view(head_dim=96)) == b.SE_ERR_UNSUPPORTED
 
 
 def test_workspace_sizes():

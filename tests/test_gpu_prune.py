@@ -1,0 +1,218 @@
+"""Interval prefix-cache pruning on the GPU against the oracle: se_prune_interval
+in mask and budget modes, slot layout, released pages and Quest summaries.
+
+Every input comes from the seeded generators in workloads/; the oracle reads
+them before any library call touches them.  Moved rows, positions and scores
+are copies, so everything is compared exactly.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import prune, quest
+from tests.oracle_bridge import gpu_unit, oracle_unit
+from workloads import PRUNE, build_state, isolated_units, to_device, unit_slots
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+@pytest.fixture(scope="module")
+def se():
+    import paper_2609_39068_amd as m
+    assert torch.cuda.is_available()
+    return m
+
+
+def _view(se, st, hkv):
+    return se.KVView(st.kv_pool, st.pos_pool, st.score_pool, st.meta_pool, st.block_table, st.lengths,
+                     num_kv_heads=hkv)
+
+
+def _run(se, host, hkv, intervals, masks=None, budgets=None, meta=False, max_len=None, what=""):
+    """Prunes every unit on both sides and compares.  host: CPU PagedInputs."""
+    U = len(intervals)
+    max_len = max_len or host.max_pages * 16
+    ost = {u: oracle_unit(host, u) for u in range(U)}
+    gs = to_device(host, DEV)
+    view = _view(se, gs, hkv)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    if meta:
+        se.se_quest_summarize(view, max_len, err)
+        for st in ost.values():
+            quest.attach_summaries(st)
+    iv = torch.tensor(intervals, dtype=torch.int32, device=DEV).view(U, 2)
+    stride = 0
+    km = kb = None
+    if masks is not None:
+        stride = max(1, max(len(m) for m in masks))
+        km_h = torch.zeros((U, stride), dtype=torch.uint8)
+        for u, m in enumerate(masks):
+            km_h[u, :len(m)] = torch.as_tensor(np.asarray(m, dtype=np.uint8))
+        km = km_h.to(DEV)
+    else:
+        kb = torch.tensor(budgets, dtype=torch.int32, device=DEV)
+    freed = torch.full((U, host.max_pages), -7, dtype=torch.int32, device=DEV)
+    fcount = torch.full((U,), -7, dtype=torch.int32, device=DEV)
+    print(f"prune {what}: U={U} mode={'mask' if km is not None else 'budget'} meta={meta}", flush=True)
+    se.se_prune_interval(view, iv, km, stride, kb, max_len, freed, host.max_pages, fcount, err)
+    torch.cuda.synchronize()
+    assert se.se_read_device_errors(err) == 0
+    fc, fp = fcount.cpu().numpy(), freed.cpu().numpy()
+    bt = host.block_table.numpy()
+    lengths = gs.lengths.cpu().numpy()
+    for u in range(U):
+        lo, hi = intervals[u]
+        st = ost[u]
+        I = (prune.mask_selection(st, lo, hi, masks[u]) if masks is not None
+             else prune.budget_selection(st, lo, hi, budgets[u]))
+        r = prune.prune(st, lo, hi, I)
+        assert lengths[u] == st.length, f"{what} unit {u}: length {lengths[u]} != {st.length}"
+        g = gpu_unit(gs, u)
+        np.testing.assert_array_equal(g["pos"], st.pos, err_msg=f"{what} unit {u}")
+        np.testing.assert_array_equal(g["K"], st.K)
+        np.testing.assert_array_equal(g["V"], st.V)
+        np.testing.assert_array_equal(g["u"], st.u)
+        n = len(r["freed"])
+        assert fc[u] == n, f"{what} unit {u}: freed {fc[u]} != {n}"
+        np.testing.assert_array_equal(fp[u, :n], bt[u, r["freed"]])
+        if meta and st.length:
+            pages = -(-st.length // 16)
+            ph = torch.as_tensor(bt[u, :pages], dtype=torch.int64)
+            mp = gs.meta_pool.cpu()[ph].to(torch.float64).numpy()
+            np.testing.assert_array_equal(mp[:, 0], st.mn, err_msg=f"{what} unit {u} min")
+            np.testing.assert_array_equal(mp[:, 1], st.mx, err_msg=f"{what} unit {u} max")
+    return gs
+
+
+LENGTHS = [0, 1, 15, 16, 17, 64, 65, 300, 1000, 2047]
+
+
+def _intervals(rng, lengths, span_of):
+    out = []
+    for L in lengths:
+        span = span_of(L)
+        lo = int(rng.integers(-3, span + 2))
+        hi = int(lo + rng.integers(0, span + 3))
+        out.append((lo, hi))
+    return out
+
+
+@pytest.mark.parametrize("d", [128, 64])
+def test_mask_mode_shuffled(se, d):
+    # slots in random position order (as hole-fill compaction leaves them), ragged
+    # lengths across the round and page boundaries, random intervals and masks
+    rng = np.random.default_rng(d)
+    host = isolated_units(LENGTHS, 130, d, 11, num_kv_heads=2, position_mode="shuffled")
+    iv = _intervals(rng, LENGTHS, lambda L: 4 * L + 8)
+    masks = [rng.integers(0, 2, max(hi - lo, 0)) for lo, hi in iv]
+    _run(se, host, 2, iv, masks=masks, what=f"mask d={d}")
+
+
+@pytest.mark.parametrize("levels", [0, 3])
+def test_budget_mode(se, levels):
+    # scores continuous or on 3 levels (exact ties broken by position); budgets
+    # from 0 to above the interval's count
+    rng = np.random.default_rng(17 + levels)
+    host = isolated_units(LENGTHS, 130, 128, 13, num_kv_heads=2, position_mode="shuffled", score_levels=levels)
+    iv = _intervals(rng, LENGTHS, lambda L: 4 * L + 8)
+    budgets = [int(rng.integers(0, max(L // 2, 1) + 3)) for L in LENGTHS]
+    _run(se, host, 2, iv, budgets=budgets, what=f"budget levels={levels}")
+
+
+def test_contiguous_history_long_units(se):
+    # a prefix cache: slot s holds position s; unaligned intervals in the middle,
+    # at the start and at the end, units of many rounds (up to 40000 slots)
+    lengths = [40000, 40000, 9000, 9000, 5000, 5000]
+    host = isolated_units(lengths, 2504, 128, 21, num_kv_heads=2, position_mode="contiguous")
+    base = [1000 * u for u in range(len(lengths))]      # the generator's position offset
+    iv = [(base[0] + 20003, base[0] + 24100), (base[1] + 0, base[1] + 777), (base[2] + 8000, base[2] + 9100),
+          (base[3] + 17, base[3] + 8999), (base[4] + 4990, base[4] + 5001), (base[5] - 100, base[5] + 6000)]
+    budgets = [1024, 100, 0, 2000, 3, 0]
+    _run(se, host, 2, iv, budgets=budgets, what="contiguous budget")
+    rng = np.random.default_rng(5)
+    masks = [(rng.random(hi - lo) < 0.3).astype(np.uint8) for lo, hi in iv]
+    _run(se, host, 2, iv, masks=masks, what="contiguous mask")
+
+
+def test_degenerate_cases(se):
+    # empty interval, nothing resident in the interval, everything kept by the
+    # mask, everything removed (length 0 after), budget above the count
+    lengths = [200, 200, 200, 200, 200, 200]
+    host = isolated_units(lengths, 16, 128, 31, num_kv_heads=2, position_mode="gapped")
+    pos0 = [unit_slots(host, u)[2].numpy() for u in range(6)]
+    iv = [(50, 50), (10**6, 10**6 + 5), (0, 900), (-5, 10**4), (int(pos0[4][10]), int(pos0[4][11])), (100, 400)]
+    masks = [np.ones(0), np.ones(5), np.ones(900), np.zeros(10**4 + 5), np.ones(iv[4][1] - iv[4][0]), np.zeros(300)]
+    gs = _run(se, host, 2, iv, masks=masks, what="degenerate mask")
+    assert int(gs.lengths[3]) == 0
+    budgets = [0, 3, 10**5, 0, 1, 10**4]
+    _run(se, host, 2, iv, budgets=budgets, what="degenerate budget")
+
+
+def test_quest_summaries_rebuilt(se):
+    lengths = [500, 777, 64, 1300]
+    host = isolated_units(lengths, 90, 128, 41, num_kv_heads=2, position_mode="contiguous", with_meta=True)
+    iv = [(100, 350), (1000 + 0, 1000 + 700), (2000 + 30, 2000 + 40), (3000 + 1, 3000 + 1299)]
+    _run(se, host, 2, iv, budgets=[40, 0, 5, 17], meta=True, what="quest budget")
+    rng = np.random.default_rng(9)
+    masks = [(rng.random(hi - lo) < 0.5).astype(np.uint8) for lo, hi in iv]
+    _run(se, host, 2, iv, masks=masks, meta=True, what="quest mask")
+
+
+def test_errors_leave_units_unchanged(se):
+    host = isolated_units([100, 100, 100, 100], 8, 64, 3, num_kv_heads=2, position_mode="contiguous")
+    gs = to_device(host, DEV)
+    view = _view(se, gs, 2)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    kv0, pos0 = gs.kv_pool.clone(), gs.pos_pool.clone()
+    iv = torch.tensor([[0, 50], [1000, 1100], [2000, 2010], [3000, 3001]], dtype=torch.int32, device=DEV)
+    km = torch.ones((4, 20), dtype=torch.uint8, device=DEV)             # rows narrower than units 0 and 1's intervals
+    se.se_prune_interval(view, iv, km, 20, None, 128, None, 0, None, err)
+    torch.cuda.synchronize()
+    assert se.se_read_device_errors(err) == se.SE_DEVERR_BAD_INTERVAL
+    kb = torch.tensor([-1, 3, 3, 3], dtype=torch.int32, device=DEV)
+    gs.lengths[3] = 200                                                 # above max_len below
+    se.se_prune_interval(view, iv, None, 0, kb, 128, None, 0, None, err)
+    torch.cuda.synchronize()
+    e = se.se_read_device_errors(err)
+    assert e == se.SE_DEVERR_BAD_INTERVAL | se.SE_DEVERR_BAD_LENGTH
+    assert gs.lengths.cpu().tolist() == [100, 3, 93, 200]
+    assert torch.equal(gs.pos_pool[gs.block_table[0].long()], pos0[gs.block_table[0].long()])
+    assert torch.equal(gs.kv_pool[gs.block_table[3].long()], kv0[gs.block_table[3].long()])
+
+
+def test_full_workload_sampled_units(se):
+    # the benchmark's call at full size: 8 chains x 32 layers x 8 KV heads of
+    # 32768 slots, interval [16384, 20480) cut to 1024 slots by score; the oracle
+    # takes four sampled units from the same generated state
+    w = PRUNE
+    gs = build_state(w, DEV)
+    U = w.layers * w.units_per_layer
+    sample = [0, 777, 1500, U - 1]
+    ost = {u: oracle_unit(gs, u) for u in sample}
+    bt = {u: gs.block_table[u].cpu().numpy() for u in sample}
+    lo, hi = w.interval
+    iv = torch.tensor([[lo, hi]] * U, dtype=torch.int32, device=DEV)
+    kb = torch.full((U,), w.budget, dtype=torch.int32, device=DEV)
+    freed = torch.full((U, gs.max_pages), -7, dtype=torch.int32, device=DEV)
+    fcount = torch.zeros(U, dtype=torch.int32, device=DEV)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    view = _view(se, gs, w.hkv)
+    print(f"full prune workload: U={U} L={int(gs.lengths[0])} interval=({lo}, {hi}) budget={w.budget}", flush=True)
+    se.se_prune_interval(view, iv, None, 0, kb, gs.max_pages * 16, freed, gs.max_pages, fcount, err)
+    torch.cuda.synchronize()
+    assert se.se_read_device_errors(err) == 0
+    want = w.ctx - (hi - lo) + w.budget
+    assert bool((gs.lengths == want).all())
+    fc = fcount.cpu().numpy()
+    for u in sample:
+        st = ost[u]
+        r = prune.prune(st, lo, hi, prune.budget_selection(st, lo, hi, w.budget))
+        g = gpu_unit(gs, u)
+        np.testing.assert_array_equal(g["pos"], st.pos)
+        np.testing.assert_array_equal(g["K"], st.K)
+        np.testing.assert_array_equal(g["V"], st.V)
+        np.testing.assert_array_equal(g["u"], st.u)
+        assert fc[u] == len(r["freed"])
+        np.testing.assert_array_equal(freed[u, :fc[u]].cpu().numpy(), bt[u][r["freed"]])

@@ -17,7 +17,8 @@ from typing import Optional, Tuple
 class Workload:
     index: int
     name: str
-    method: str                      # "h2o", "quest", "snapkv" (prompt compaction), "omnikv" or "h2o_prefill"
+    method: str                      # "h2o", "quest", "snapkv" (prompt compaction), "omnikv", "h2o_prefill"
+                                     # or "prune" (interval prefix-cache pruning)
     num_req: int
     hq: int
     hkv: int
@@ -36,6 +37,7 @@ class Workload:
     pool_kernel: Optional[int] = None  # SnapKV max-pooling width kappa
     filter_layers: Optional[Tuple[int, ...]] = None  # OmniKV observation layers (full attention + selection)
     chunk: Optional[int] = None      # H2O prefill: the chunk's length (its queries' last obs_window score)
+    interval: Optional[Tuple[int, int]] = None  # prefix pruning: the history interval [lo, hi) pruned
     hh_rate: float = 0.0             # share of positions whose key gets += hh_shift * u
     hh_shift: float = 0.0
     relevant_pages: int = 0          # Quest: pages whose keys all get += relevant_shift * u
@@ -99,6 +101,16 @@ OMNIKV = Workload(6, "llama3-8b-32-layer-omnikv", "omnikv", num_req=32, hq=32, h
 H2O_PREFILL = Workload(7, "llama3-8b-prefill-chunk-h2o", "h2o_prefill", num_req=8, hq=32, hkv=8, head_dim=128,
                        layers=1, steps=1, ctx=32768, initial_resident=2048 + 8192, budget=2048, recent=1024,
                        obs_window=128, chunk=8192, hh_rate=0.01, hh_shift=4.0, seed=7)
+
+
+# Interval prefix-cache pruning (Section 3.2, "Sparsity-Based Prefix-Cache
+# Pruning"; Appendix C.2): 8 idle agent chains of an 8B-shaped 32-layer model,
+# each with its whole 32768-token history resident in every layer (slot s holds
+# position s), prune a 4096-token tool-result interval [16384, 20480) to a
+# quarter of its tokens (budget 1024 per (layer, KV head) unit, the scoring
+# policy's scores in the score field); the 12288 later slots close up behind it.
+PRUNE = Workload(8, "llama3-8b-32-layer-prune-interval", "prune", num_req=8, hq=32, hkv=8, head_dim=128,
+                 layers=32, steps=1, ctx=32768, budget=1024, interval=(16384, 20480), seed=8)
 
 
 def scaled(w: Workload, **changes) -> Workload:

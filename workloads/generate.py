@@ -40,7 +40,10 @@ Value recipe (the workloads' own description):
     are Exp(mean 0.15) (about three chunks' worth of the average weight a slot
     receives: 128 * G weight units spread over 10240 slots), the chunk's slots
     hold -1 (stale values the call replaces); the scoring queries are drawn like
-    SnapKV's observation queries.
+    SnapKV's observation queries;
+  * prefix-pruning workload: every layer keeps the whole history (slot s holds
+    position s, keys N(0, 1) without heavy hitters) and the score field holds a
+    scoring policy's output, U(0, 1) per slot.
 No part of attention, scoring, selection or compaction is computed here.
 """
 
@@ -156,7 +159,7 @@ def build_state(w: Workload, device, generate_values: bool = True) -> PagedInput
     L0 = _initial_lengths(w, ctx, device)
     if w.method == "h2o":
         cap_slots = int(max(int(L0.max()), int(w.budget)) + 1)
-    elif w.method in ("snapkv", "h2o_prefill"):
+    elif w.method in ("snapkv", "h2o_prefill", "prune"):
         cap_slots = int(L0.max())
     elif w.method == "omnikv":
         cap_slots = int(L0.max()) + w.steps
@@ -171,7 +174,7 @@ def build_state(w: Workload, device, generate_values: bool = True) -> PagedInput
     kv_pool = torch.empty((num_pages, 2, P, d), dtype=torch.bfloat16, device=device)
     pos_pool = torch.full((num_pages, P), -1, dtype=torch.int32, device=device)
     score_pool = (torch.zeros((num_pages, P), dtype=torch.float32, device=device)
-                  if w.method in ("h2o", "snapkv", "h2o_prefill") else None)
+                  if w.method in ("h2o", "snapkv", "h2o_prefill", "prune") else None)
     meta_pool = torch.zeros((num_pages, 2, d), dtype=torch.bfloat16, device=device) if w.method == "quest" else None
     lengths = L0.to(torch.int32).repeat(w.layers)
 
@@ -200,6 +203,9 @@ def build_state(w: Workload, device, generate_values: bool = True) -> PagedInput
             sc = (-0.15 * torch.log1p(-e)).to(torch.float32)
             old = torch.arange(cap, device=device)[None, :] < (L0 - int(w.chunk))[:, None]
             sc = torch.where(old, sc, torch.full_like(sc, -1.0))
+            score_pool.view(-1)[(page * P + row)[valid]] = sc[valid]
+        if w.method == "prune":
+            sc = torch.rand(U, cap, generator=_gen(w, 400 + layer, device), device=device).to(torch.float32)
             score_pool.view(-1)[(page * P + row)[valid]] = sc[valid]
         if not generate_values:
             continue
