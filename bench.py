@@ -29,7 +29,7 @@ retained + 8192 chunk slots scored by the chunk's last 128 queries of every
 head and cut back to 2048 with a 1024-token window; one step is one call from
 a fresh copy of that state); `--workload prune` measures interval prefix-cache
 pruning (se_prune_interval over 8 chains x 32 layers x 8 KV heads of 32768
-resident slots: the interval [16384, 20480) cut to its 1024 best-scored slots
+resident slots: the interval [16384, 20480) cut to its 819 best-scored slots
 per unit and the later slots closed up; one step is one call from a fresh copy
 of the cache); `--gpus N` with N > 1 is refused (single-GPU build).
 """

@@ -184,7 +184,7 @@ def test_errors_leave_units_unchanged(se):
 
 def test_full_workload_sampled_units(se):
     # the benchmark's call at full size: 8 chains x 32 layers x 8 KV heads of
-    # 32768 slots, interval [16384, 20480) cut to 1024 slots by score; the oracle
+    # 32768 slots, interval [16384, 20480) cut to 819 slots by score; the oracle
     # takes four sampled units from the same generated state
     w = PRUNE
     gs = build_state(w, DEV)

@@ -106,11 +106,12 @@ H2O_PREFILL = Workload(7, "llama3-8b-prefill-chunk-h2o", "h2o_prefill", num_req=
 # Interval prefix-cache pruning (Section 3.2, "Sparsity-Based Prefix-Cache
 # Pruning"; Appendix C.2): 8 idle agent chains of an 8B-shaped 32-layer model,
 # each with its whole 32768-token history resident in every layer (slot s holds
-# position s), prune a 4096-token tool-result interval [16384, 20480) to a
-# quarter of its tokens (budget 1024 per (layer, KV head) unit, the scoring
+# position s), prune a 4096-token tool-result interval [16384, 20480) to 20 % of
+# its tokens (Section 4.3, "Quality of Prefix Pruning": 20 % of the targeted tool
+# results' tokens retained; budget 819 per (layer, KV head) unit, the scoring
 # policy's scores in the score field); the 12288 later slots close up behind it.
 PRUNE = Workload(8, "llama3-8b-32-layer-prune-interval", "prune", num_req=8, hq=32, hkv=8, head_dim=128,
-                 layers=32, steps=1, ctx=32768, budget=1024, interval=(16384, 20480), seed=8)
+                 layers=32, steps=1, ctx=32768, budget=819, interval=(16384, 20480), seed=8)
 
 
 def scaled(w: Workload, **changes) -> Workload:
