@@ -36,6 +36,14 @@
 // last pages (window keys); slots past the length are masked there too.
 // Retention and compaction are then H2O's kernel (launch_evict) with the
 // window as its recent set.
+//
+// H2O chunk scoring (se_h2o_prefill_chunk) runs the same kernel over every key
+// with the causal mask in both passes, one row block of up to 128 scoring rows
+// per work-group (grid.y), one work-group per CU.  There the stages made only
+// of pages below the window run pipelined: stage j's MFMAs are issued in the
+// same branch-free block as the exponentials of stage j - 1's logits (the two
+// stages' logits alternate between two register sets), and four stages of
+// loads are in flight; the remaining pages go through the per-page path.
 #include <algorithm>
 
 #include "evict_core.h"
@@ -51,6 +59,7 @@ constexpr int kSnapWaves = kSnapThreads / kWave;
 constexpr int kSnapRowGroups = 4;       // 32 rows each
 constexpr int kSnapHalves = kSnapWaves / kSnapRowGroups;  // key halves of a stage
 constexpr int kSnapMaxRows = 128;
+constexpr int kPrefillBlockRows = 128;  // rows of a work-group in H2O chunk scoring
 constexpr int kSnapMaxHalf = 15;        // kappa <= 31
 constexpr int kSnapMaxPages = 8192;     // pages per unit (131072 slots)
 constexpr int kSnapStagePages = 4;      // pages per ring stage
@@ -114,11 +123,10 @@ __device__ __forceinline__ int bt_entry(const int32_t* bt, int i) {
   return ((const_i32_ptr)bt)[__builtin_amdgcn_readfirstlane(i)];
 }
 
-template <int D, typename Body>
+template <int D, int NB, typename Body>
 __device__ __forceinline__ void stream_stages(const SnapParams& p, const int32_t* bt, uint8_t* ring, int pb, int pe,
                                               Body body) {
   constexpr int S = kSnapStagePages;
-  constexpr int NB = kSnapBatches;
   constexpr int PB = 32 * D;                       // K bytes of a page
   constexpr int PC = D / 8;                        // 16-byte pieces per key
   constexpr int PT = S * 2 * D / kSnapThreads;     // pieces per thread per stage
@@ -212,8 +220,10 @@ __device__ __forceinline__ void merge_norm(float& ref, float& sum, float ref2, f
 // the work-group's row block blockIdx.y).  kAccum: H2O chunk scoring -- u over
 // every key (the window keys with their causal mask) into the row block's
 // partial row of the workspace, no pooling; otherwise SnapKV.
-template <int D, int RTW, bool kAccum>
-__global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const SnapParams p) {
+template <int D, int RTW, bool kAccum, bool kPipe, int kOcc>
+__global__ __launch_bounds__(kSnapThreads, kOcc) void snapkv_score_kernel(const SnapParams p) {
+  // stages in flight per thread: four when one work-group holds the CU
+  constexpr int kNB = kOcc <= 2 ? 2 * kSnapBatches : kSnapBatches;
   constexpr int KS = D / 32;
   constexpr int S = kSnapStagePages;
   constexpr int H = kSnapHalfPages;
@@ -259,7 +269,7 @@ __global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const Sna
   // SnapKV: u over the candidates (L > budget >= w, so at least one); H2O: every key
   const int n_lim = kAccum ? L : L - w;
   const int row0 = 16 * RTW * rg;                // within the row block
-  const int rbase = kSnapMaxRows * blockIdx.y;   // the row block's first row
+  const int rbase = (kAccum ? kPrefillBlockRows : kSnapMaxRows) * blockIdx.y;  // the row block's first row
 
   // ---- the row group's observation queries (A operands); rows past R are zero
   uint4 qa[RTW][KS];
@@ -298,54 +308,116 @@ __global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const Sna
       ref[T][r] = kRefInit;
       sum[T][r] = 0.f;
     }
-  stream_stages<D>(p, bt, s_ring, 0, n_pages, [&](int j, int slot) {
+  // one page's logits into the references and sums
+  auto norm_page = [&](const f32x4_t(&a)[RTW]) {
+    float dmax = -INFINITY;
+    float d[RTW][4];
+#pragma unroll
+    for (int T = 0; T < RTW; ++T)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        d[T][r] = fmaf(a[T][r], c, -ref[T][r]);
+        dmax = fmaxf(dmax, d[T][r]);
+      }
+    if (__builtin_amdgcn_ballot_w64(dmax > kLazy) != 0) {
+      // rare: raise the references of the wavefront's rows to their logits
+#pragma unroll
+      for (int T = 0; T < RTW; ++T)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float zc = a[T][r] * c;
+          const float m = fmaxf(ref[T][r], zc);
+          sum[T][r] *= fast_exp2(ref[T][r] - m);
+          d[T][r] = zc - m;
+          ref[T][r] = m;
+        }
+    }
+#pragma unroll
+    for (int T = 0; T < RTW; ++T)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sum[T][r] += fast_exp2(d[T][r]);
+  };
+  // the causal mask of a page holding window keys: key j is seen by the rows
+  // of window position t iff j <= L - w + t (so j < L); padded rows see nothing
+  auto causal_mask = [&](f32x4_t(&a)[RTW], int pg, float masked) {
+    const int key = pg * kPage + col;
+#pragma unroll
+    for (int T = 0; T < RTW; ++T)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rbase + row0 + 16 * T + 4 * grp + r;
+        const int lim = row < R ? L - w + row / G : -1;
+        if (key > lim) a[T][r] = masked;
+      }
+  };
+  // Whole stages of pages below p_full run pipelined: the stage's MFMAs are
+  // issued beside the exponentials of the previous stage's logits, in one
+  // branch-free block (the reference check of a stage is one ballot after
+  // its exponentials; the rare raise redoes the stage page by page).
+  const int pe1 = kPipe ? min(p_full, n_pages) / S * S : 0;
+  if (kPipe) {
+    // the logits of two stages: a stage in ring slot k leaves its logits in
+    // accs[k] and reads the previous stage's from accs[k ^ 1] (the ring slot
+    // is a constant in each unrolled step, so nothing is copied); -inf logits
+    // add nothing
+    f32x4_t accs[2][H][RTW];
+#pragma unroll
+    for (int i = 0; i < H; ++i)
+#pragma unroll
+      for (int T = 0; T < RTW; ++T) accs[1][i][T] = f32x4_t{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    auto norm_stage = [&](const f32x4_t(&prev)[H][RTW]) {
+      float t[RTW][4];
+      float dmax = -INFINITY;
+#pragma unroll
+      for (int T = 0; T < RTW; ++T)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+#pragma unroll
+          for (int i = 0; i < H; ++i) {
+            const float d = fmaf(prev[i][T][r], c, -ref[T][r]);
+            dmax = fmaxf(dmax, d);
+            t[T][r] = i == 0 ? fast_exp2(d) : t[T][r] + fast_exp2(d);
+          }
+        }
+      // the exponentials stay here, beside the stage's MFMAs, rather than
+      // sinking past the rare branch that does not use them
+#pragma unroll
+      for (int T = 0; T < RTW; ++T)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) asm volatile("" ::"v"(t[T][r]));
+      if (__builtin_amdgcn_ballot_w64(dmax > kLazy) != 0) {
+#pragma unroll
+        for (int i = 0; i < H; ++i) norm_page(prev[i]);
+#pragma unroll
+        for (int T = 0; T < RTW; ++T)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) t[T][r] = 0.f;
+      }
+#pragma unroll
+      for (int T = 0; T < RTW; ++T)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sum[T][r] += t[T][r];
+    };
+    stream_stages<D, kNB>(p, bt, s_ring, 0, pe1, [&](int j, int slot) {
+#pragma unroll
+      for (int i = 0; i < H; ++i) page_logits<D, RTW>(qa, s_ring + (slot * S + kh * H + i) * PB, accs[slot][i]);
+      norm_stage(accs[slot ^ 1]);
+    });
+    if ((pe1 / S) & 1) norm_stage(accs[0]);  // the last stage
+    else norm_stage(accs[1]);
+  }
+  // the remaining pages one at a time, masked where they hold window keys
+  stream_stages<D, kNB>(p, bt, s_ring, pe1, n_pages, [&](int j, int slot) {
     // the half's logits first (independent MFMA chains), then the updates
     f32x4_t acc[H][RTW];
 #pragma unroll
     for (int i = 0; i < H; ++i) page_logits<D, RTW>(qa, s_ring + (slot * S + kh * H + i) * PB, acc[i]);
 #pragma unroll
     for (int i = 0; i < H; ++i) {
-      const int pg = j * S + kh * H + i;
+      const int pg = pe1 + j * S + kh * H + i;
       if (pg >= n_pages) break;
-      if (pg >= p_full) {
-        // causal mask: key j is seen by the rows of window position t iff
-        // j <= L - w + t (so j < L); padded rows see nothing
-        const int key = pg * kPage + col;
-#pragma unroll
-        for (int T = 0; T < RTW; ++T)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int row = rbase + row0 + 16 * T + 4 * grp + r;
-            const int lim = row < R ? L - w + row / G : -1;
-            if (key > lim) acc[i][T][r] = -INFINITY;
-          }
-      }
-      float dmax = -INFINITY;
-      float d[RTW][4];
-#pragma unroll
-      for (int T = 0; T < RTW; ++T)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          d[T][r] = fmaf(acc[i][T][r], c, -ref[T][r]);
-          dmax = fmaxf(dmax, d[T][r]);
-        }
-      if (__builtin_amdgcn_ballot_w64(dmax > kLazy) != 0) {
-        // rare: raise the references of the wavefront's rows to their logits
-#pragma unroll
-        for (int T = 0; T < RTW; ++T)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float zc = acc[i][T][r] * c;
-            const float m = fmaxf(ref[T][r], zc);
-            sum[T][r] *= fast_exp2(ref[T][r] - m);
-            d[T][r] = zc - m;
-            ref[T][r] = m;
-          }
-      }
-#pragma unroll
-      for (int T = 0; T < RTW; ++T)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) sum[T][r] += fast_exp2(d[T][r]);
+      if (pg >= p_full) causal_mask(acc[i], pg, -INFINITY);
+      norm_page(acc[i]);
     }
   });
   // merge the 16 key lanes of each row, then the two key halves through LDS:
@@ -394,42 +466,73 @@ __global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const Sna
       if (key < n_lim) u[key] = v;
     }
   };
+  // a page's weights summed over the lane's rows (a tree: independent exp2s,
+  // short add chains), then over the four lane groups (rows 4*(lane/16)..+3
+  // of each tile) of key lane%16
+  auto page_sum = [&](const f32x4_t(&a)[RTW]) {
+    float e[RTW * 4];
+#pragma unroll
+    for (int T = 0; T < RTW; ++T)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) e[4 * T + r] = fast_exp2(fmaf(a[T][r], c, -bias[T][r]));
+#pragma unroll
+    for (int n = RTW * 4; n > 1; n >>= 1)
+#pragma unroll
+      for (int k = 0; k < n / 2; ++k) e[k] = e[2 * k] + e[2 * k + 1];
+    return lane_group_sum(e[0]);
+  };
+  // Pipelined whole stages as in pass 1 (SnapKV: every candidate page; H2O:
+  // the pages below p_full): stage j's MFMAs beside stage j - 1's sums, which
+  // go to LDS, and stage j - 2's flush.
+  const int pe2 = kPipe ? (kAccum ? min(p_full, cand_pages) : cand_pages) / S * S : 0;
+  const int n1 = pe2 / S;
+  if (kPipe) {
+    f32x4_t accs[2][H][RTW];  // as in pass 1; -inf logits: zero weights
+#pragma unroll
+    for (int i = 0; i < H; ++i)
+#pragma unroll
+      for (int T = 0; T < RTW; ++T) accs[1][i][T] = f32x4_t{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    auto sums_to_lds = [&](int j, const f32x4_t(&prev)[H][RTW]) {  // the sums of stage j
+      float us[H];
+#pragma unroll
+      for (int i = 0; i < H; ++i) us[i] = page_sum(prev[i]);
+      if (grp == 0)
+#pragma unroll
+        for (int i = 0; i < H; ++i) s_up[j & 1][kh * H + i][rg][col] = us[i];
+    };
+    stream_stages<D, kNB>(p, bt, s_ring, 0, pe2, [&](int j, int slot) {
+      if (j >= 2) flush(j - 2);
+#pragma unroll
+      for (int i = 0; i < H; ++i) page_logits<D, RTW>(qa, s_ring + (slot * S + kh * H + i) * PB, accs[slot][i]);
+      sums_to_lds(j - 1, accs[slot ^ 1]);  // stage -1: zeros into the slot stage 1 fills before its flush
+    });
+    if (n1 >= 2) flush(n1 - 2);
+    if (n1 >= 1) {
+      if (n1 & 1) sums_to_lds(n1 - 1, accs[0]);
+      else sums_to_lds(n1 - 1, accs[1]);
+    }
+    __syncthreads();
+    if (n1 >= 1) flush(n1 - 1);
+    __syncthreads();
+  }
+  // the remaining candidate pages one stage at a time (stage j = n1 + local)
   const int n_st2 = ceil_div_dev(cand_pages, S);
-  stream_stages<D>(p, bt, s_ring, 0, cand_pages, [&](int j, int slot) {
-    if (j > 0) flush(j - 1);
+  stream_stages<D, kNB>(p, bt, s_ring, pe2, cand_pages, [&](int jl, int slot) {
+    const int j = n1 + jl;
+    if (jl > 0) flush(j - 1);
     f32x4_t acc[H][RTW];
 #pragma unroll
     for (int i = 0; i < H; ++i) page_logits<D, RTW>(qa, s_ring + (slot * S + kh * H + i) * PB, acc[i]);
 #pragma unroll
     for (int i = 0; i < H; ++i) {
-      // a sum tree over the lane's rows (independent exp2s, short add chains)
-      float e[RTW * 4];
-#pragma unroll
-      for (int T = 0; T < RTW; ++T)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) e[4 * T + r] = fast_exp2(fmaf(acc[i][T][r], c, -bias[T][r]));
-      if (kAccum && j * S + kh * H + i >= p_full) {
-        // causal mask of the window keys (and of slots past the length)
-        const int key = (j * S + kh * H + i) * kPage + col;
-#pragma unroll
-        for (int T = 0; T < RTW; ++T)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int row = rbase + row0 + 16 * T + 4 * grp + r;
-            const int lim = row < R ? L - w + row / G : -1;
-            if (key > lim) e[4 * T + r] = 0.f;
-          }
-      }
-#pragma unroll
-      for (int n = RTW * 4; n > 1; n >>= 1)
-#pragma unroll
-        for (int k = 0; k < n / 2; ++k) e[k] = e[2 * k] + e[2 * k + 1];
-      // the four lane groups (rows 4*(lane/16)..+3 of each tile) of key lane%16
-      const float us = lane_group_sum(e[0]);
+      const int pg = j * S + kh * H + i;
+      // H2O: the causal mask of the window keys (and of slots past the length)
+      if (kAccum && pg >= p_full) causal_mask(acc[i], pg, -INFINITY);
+      const float us = page_sum(acc[i]);
       if (grp == 0) s_up[j & 1][kh * H + i][rg][col] = us;  // pages past the candidates are never added
     }
   });
-  if (n_st2 > 0) flush(n_st2 - 1);
+  if (n_st2 > n1) flush(n_st2 - 1);
   if (kAccum) return;  // the row block's partial u is written; h2o_chunk_apply_kernel adds the blocks
   __syncthreads();  // the unit's u is complete and visible to the work-group
 
@@ -477,10 +580,15 @@ __global__ __launch_bounds__(kSnapThreads, 4) void snapkv_score_kernel(const Sna
 template <int D, bool kAccum>
 void launch_snapkv_d(const SnapParams& p, int num_units, int rows, hipStream_t stream) {
   const dim3 grid(num_units, p.n_rb);
+  // H2O chunk scoring: one work-group per CU (grid = units x row blocks), the
+  // pipelined stages and a deeper stream; SnapKV: two work-groups per CU, in
+  // which the pipelined form would not fit the registers
+  constexpr int occ = kAccum ? 2 : 4;
+  constexpr bool pipe = kAccum;
   if (rows <= 64)
-    hipLaunchKernelGGL((snapkv_score_kernel<D, 1, kAccum>), grid, dim3(kSnapThreads), 0, stream, p);
+    hipLaunchKernelGGL((snapkv_score_kernel<D, 1, kAccum, pipe, occ>), grid, dim3(kSnapThreads), 0, stream, p);
   else
-    hipLaunchKernelGGL((snapkv_score_kernel<D, 2, kAccum>), grid, dim3(kSnapThreads), 0, stream, p);
+    hipLaunchKernelGGL((snapkv_score_kernel<D, 2, kAccum, pipe, occ>), grid, dim3(kSnapThreads), 0, stream, p);
 }
 
 constexpr int kApplyThreads = 256;
@@ -587,7 +695,7 @@ extern "C" se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, c
 
 size_t se_h2o_prefill_workspace_bytes(int32_t num_units, int32_t max_len, int32_t q_per_kv, int32_t window) {
   if (num_units <= 0 || max_len <= 0 || q_per_kv <= 0 || window <= 0) return 0;
-  const size_t n_rb = (size_t)ceil_div((int64_t)window * q_per_kv, kSnapMaxRows);
+  const size_t n_rb = (size_t)ceil_div((int64_t)window * q_per_kv, kPrefillBlockRows);
   return (size_t)num_units * n_rb * align_up((size_t)max_len, 64) * sizeof(float);
 }
 
@@ -627,11 +735,11 @@ extern "C" se_status se_h2o_prefill_chunk(const se_kv_view* kv, int32_t q_per_kv
   p.budget = budget;
   p.max_len = max_len;
   p.u_stride = (int32_t)align_up((size_t)max_len, 64);
-  p.n_rb = (int32_t)ceil_div((int64_t)score_window * q_per_kv, kSnapMaxRows);
+  p.n_rb = (int32_t)ceil_div((int64_t)score_window * q_per_kv, kPrefillBlockRows);
   p.chunk = chunk_len;
   p.c = scale * kLog2e;
   p.dev_err = dev_err;
-  const int rows = std::min(score_window * q_per_kv, kSnapMaxRows);
+  const int rows = std::min(score_window * q_per_kv, kPrefillBlockRows);
   if (kv->head_dim == 128)
     launch_snapkv_d<128, true>(p, kv->num_units, rows, stream);
   else
