@@ -65,7 +65,7 @@ __device__ __forceinline__ uint64_t prune_key(float score, int32_t pos) {
 }
 
 template <int D>
-__global__ __launch_bounds__(kPruneThreads) void prune_interval_kernel(const PruneParams p) {
+__global__ __launch_bounds__(kPruneThreads, 4) void prune_interval_kernel(const PruneParams p) {
   constexpr int NT = kPruneThreads;
   constexpr int PPS = 4 * D / 16;            // 16-byte pieces of a slot's key and value rows
   constexpr int KP = D / 8;                  // of them in the key row
@@ -198,20 +198,35 @@ __global__ __launch_bounds__(kPruneThreads) void prune_interval_kernel(const Pru
   const uint8_t* kmrow = by_mask ? p.keep_mask + (size_t)unit * p.mask_stride : nullptr;
   const int r0 = first & ~(kPruneRound - 1);
   int base = r0;  // slots kept below the round: every slot below `first` stays in place
+  // A lane's keep flag needs its slot's position, then the mask byte at that
+  // position (or the slot's score): both are fetched ahead -- the position two
+  // rounds ahead, the second input one round ahead -- so that a round waits
+  // only for its own rows.  Those slots are above every destination written
+  // before their round, so the values read are the ones the round decides on.
+  auto load_pos = [&](int s) -> int32_t { return s < L ? p.pos_pool[slot_addr(s)] : INT_MIN; };
+  auto load_aux = [&](int s, int32_t ps) -> float {
+    if (s >= L || !in_t(ps)) return 0.f;
+    if (by_mask) return (float)kmrow[(int64_t)ps - lo];
+    return keep_none ? 0.f : p.score_pool[slot_addr(s)];
+  };
+  auto keep_of = [&](int s, int32_t ps, float aux) -> bool {
+    if (s >= L) return false;
+    if (!in_t(ps)) return true;
+    if (by_mask) return aux != 0.f;
+    return !keep_none && (prune_key(aux, ps) & kmask) >= kprefix;
+  };
+  int32_t pos0 = load_pos(r0 + lane);
+  float aux0 = load_aux(r0 + lane, pos0);
+  int32_t pos1 = load_pos(r0 + kPruneRound + lane);
   for (int c0 = r0; c0 < L; c0 += kPruneRound) {
-    bool keep = false;
-    {
-      const int s = c0 + lane;
-      if (s < L) {
-        const size_t a = slot_addr(s);
-        const int32_t ps = p.pos_pool[a];
-        if (!in_t(ps)) keep = true;
-        else if (by_mask) keep = kmrow[(int64_t)ps - lo] != 0;
-        else if (!keep_none) keep = (prune_key(p.score_pool[a], ps) & kmask) >= kprefix;
-      }
-    }
+    const bool keep = keep_of(c0 + lane, pos0, aux0);
+    const float aux1 = load_aux(c0 + kPruneRound + lane, pos1);
+    const int32_t pos2 = load_pos(c0 + 2 * kPruneRound + lane);
     const uint64_t bits = __builtin_amdgcn_ballot_w64(keep);  // the same in every wavefront
     const int n_keep = __popcll(bits);
+    pos0 = pos1;
+    aux0 = aux1;
+    pos1 = pos2;
     if (bits == (n_keep == 64 ? ~0ull : ((1ull << n_keep) - 1)) && base == c0) {
       base += n_keep;  // the round's kept slots are its first ones and already in place
       continue;
