@@ -10,11 +10,13 @@
 // Selection: omnikv_score_kernel takes the maximum over the request's Hq
 // logit rows (contiguous in the logits layout) for a chunk of slots, coalesced,
 // into the workspace; omnikv_topk_kernel (one 1024-thread work-group per
-// request) copies the request's scores to LDS when they fit, finds the b-th
-// largest key by an 8-bit radix selection over order-preserving keys (ties:
-// lower slot), and writes the selected slots in increasing order: every thread
-// owns a contiguous run of slots, so two block scans (of the tied count and of
-// the selected count) give each thread its output offset.
+// request) copies the request's scores to LDS when they fit (eight loads in
+// flight per thread), finds the b-th largest key by an 8-bit radix selection
+// over order-preserving keys (ties: lower slot; the histogram replicated over
+// eight LDS copies, so that lanes sharing a digit update different words), and
+// writes the selected slots in increasing order: every thread owns a
+// contiguous run of slots, so two block scans (of the tied count and of the
+// selected count) give each thread its output offset.
 //
 // Slot attention: one 512-thread work-group per unit.  The selected slots are
 // translated once into kv-pool row indices in LDS (the appended token's row is
@@ -34,6 +36,8 @@ constexpr int kOmniScoreThreads = 256;
 constexpr int kOmniScoreSlots = 4;                      // slots per thread per block
 constexpr int kOmniTopkThreads = 1024;
 constexpr int kOmniLdsScores = 32768 + 4096;            // scores kept in LDS (144 KB)
+constexpr int kOmniHistCopies = 8;                      // radix histogram copies (8 KB of LDS)
+constexpr int kOmniRowBatch = 8;                        // logit rows in flight per thread
 constexpr int kGatherThreads = 512;
 constexpr int kGatherWaves = kGatherThreads / kWave;
 constexpr int kGatherMaxSel = 8192;                     // selected slots per request
@@ -49,20 +53,98 @@ struct OmniSelectParams {
   int32_t budget;
   int32_t max_len;
   int32_t ws_stride;
+  int32_t vec4;          // logits rows 16-byte aligned: four slots per load
   float* scores;         // workspace [num_req][ws_stride]
   int32_t* sel;          // [num_req][budget]
   int32_t* dev_err;
 };
 
+// radix_select_top (se_common.h) with the histogram replicated COPIES times (copy = lane
+// mod COPIES, copies 257 words apart, so in different banks): lanes that share
+// a digit -- most of them in the first passes over scores of similar
+// magnitude -- then update different LDS words instead of serialising on one.
+// `hist` holds COPIES * 257 words.
+template <int NT, int COPIES, typename KeyT, typename KeyFn, typename CandFn>
+__device__ void radix_select_top_rep(int n, int k, KeyFn key_of, CandFn cand, KeyT* prefix_out, KeyT* mask_out,
+                                     int* k_rest_out, unsigned* hist, int* scan_scratch, int* bcast) {
+  static_assert(NT >= 256 && NT % kWave == 0, "threads 0..255 own one bin each");
+  constexpr int kStride = 257;
+  KeyT prefix = 0, mask = 0;
+  const int tid = threadIdx.x;
+  unsigned* const my_hist = hist + (tid % COPIES) * kStride;
+  for (int shift = (int)sizeof(KeyT) * 8 - 8; shift >= 0; shift -= 8) {
+    for (int i = tid; i < COPIES * kStride; i += NT) hist[i] = 0;
+    __syncthreads();
+    for (int i = tid; i < n; i += NT) {
+      if (!cand(i)) continue;
+      const KeyT key = key_of(i);
+      if ((key & mask) == prefix) atomicAdd(&my_hist[(unsigned)(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    int v = 0;  // thread t counts digit 255 - t over the copies
+    if (tid < 256)
+#pragma unroll
+      for (int c = 0; c < COPIES; ++c) v += (int)hist[c * kStride + 255 - tid];
+    int total;
+    const int excl = block_exclusive_scan<NT>(v, scan_scratch, &total);
+    if (v > 0 && excl < k && excl + v >= k) {
+      bcast[0] = 255 - tid;
+      bcast[1] = excl;
+      bcast[2] = v;
+    }
+    __syncthreads();
+    const int d = bcast[0];
+    k -= bcast[1];
+    const int cnt = bcast[2];
+    __syncthreads();
+    prefix |= (KeyT)d << shift;
+    mask |= (KeyT)0xFF << shift;
+    if (cnt == k) break;
+  }
+  *prefix_out = prefix;
+  *mask_out = mask;
+  *k_rest_out = k;
+}
+
 // s(j) = max over the request's Hkv * G logit rows, for slots j < L of the
-// request's first unit.
+// request's first unit.  With aligned rows a thread takes four consecutive
+// slots per 16-byte load and keeps eight rows' loads in flight (slots past L up
+// to the next multiple of four get scores nobody reads: they stay inside the
+// rows, whose stride is a multiple of four at least max_len).
 __global__ __launch_bounds__(kOmniScoreThreads) void omnikv_score_kernel(const OmniSelectParams p) {
   const int req = blockIdx.y;
   const int L = p.lengths[(size_t)req * p.num_kv_heads];
   const int rows = p.num_kv_heads * p.q_per_kv;
   const float* lg = p.logits + (size_t)req * rows * p.stride;
-  const int base = blockIdx.x * kOmniScoreThreads * kOmniScoreSlots + threadIdx.x;
   if (L < 0 || L > p.max_len) return;  // reported by the selection kernel
+  if (p.vec4) {
+    const int j0 = (blockIdx.x * kOmniScoreThreads + threadIdx.x) * kOmniScoreSlots;
+    if (j0 >= L) return;
+    float4 m = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+    int r = 0;
+    for (; r + kOmniRowBatch <= rows; r += kOmniRowBatch) {
+      float4 v[kOmniRowBatch];
+#pragma unroll
+      for (int k = 0; k < kOmniRowBatch; ++k) v[k] = *reinterpret_cast<const float4*>(lg + (size_t)(r + k) * p.stride + j0);
+#pragma unroll
+      for (int k = 0; k < kOmniRowBatch; ++k) {
+        m.x = fmaxf(m.x, v[k].x);
+        m.y = fmaxf(m.y, v[k].y);
+        m.z = fmaxf(m.z, v[k].z);
+        m.w = fmaxf(m.w, v[k].w);
+      }
+    }
+    for (; r < rows; ++r) {
+      const float4 v = *reinterpret_cast<const float4*>(lg + (size_t)r * p.stride + j0);
+      m.x = fmaxf(m.x, v.x);
+      m.y = fmaxf(m.y, v.y);
+      m.z = fmaxf(m.z, v.z);
+      m.w = fmaxf(m.w, v.w);
+    }
+    *reinterpret_cast<float4*>(p.scores + (size_t)req * p.ws_stride + j0) = m;
+    return;
+  }
+  const int base = blockIdx.x * kOmniScoreThreads * kOmniScoreSlots + threadIdx.x;
 #pragma unroll
   for (int k = 0; k < kOmniScoreSlots; ++k) {
     const int j = base + k * kOmniScoreThreads;
@@ -74,8 +156,8 @@ __global__ __launch_bounds__(kOmniScoreThreads) void omnikv_score_kernel(const O
 }
 
 __global__ __launch_bounds__(kOmniTopkThreads) void omnikv_topk_kernel(const OmniSelectParams p) {
-  __shared__ float s_sc[kOmniLdsScores];
-  __shared__ unsigned s_hist[256];
+  __shared__ __attribute__((aligned(16))) float s_sc[kOmniLdsScores];
+  __shared__ unsigned s_hist[kOmniHistCopies * 257];
   __shared__ int s_scan[kOmniTopkThreads / kWave + 1];
   __shared__ int s_bcast[4];
   const int req = blockIdx.x;
@@ -97,13 +179,45 @@ __global__ __launch_bounds__(kOmniTopkThreads) void omnikv_topk_kernel(const Omn
   const float* gsc = p.scores + (size_t)req * p.ws_stride;
   const float* sc = gsc;
   if (L <= kOmniLdsScores) {
-    for (int i = tid; i < L; i += kOmniTopkThreads) s_sc[i] = gsc[i];
+    // eight loads in flight per thread (16-byte ones when the rows are aligned)
+    constexpr int NB = 8;
+    int done = 0;
+    if (p.vec4) {
+      const int n4 = L / 4;
+      for (int i = tid; i < n4; i += kOmniTopkThreads * NB) {
+        float4 v[NB];
+#pragma unroll
+        for (int k = 0; k < NB; ++k) {
+          const int x = i + k * kOmniTopkThreads;
+          if (x < n4) v[k] = reinterpret_cast<const float4*>(gsc)[x];
+        }
+#pragma unroll
+        for (int k = 0; k < NB; ++k) {
+          const int x = i + k * kOmniTopkThreads;
+          if (x < n4) reinterpret_cast<float4*>(s_sc)[x] = v[k];
+        }
+      }
+      done = 4 * n4;
+    }
+    for (int i = done + tid; i < L; i += kOmniTopkThreads * NB) {
+      float v[NB];
+#pragma unroll
+      for (int k = 0; k < NB; ++k) {
+        const int x = i + k * kOmniTopkThreads;
+        if (x < L) v[k] = gsc[x];
+      }
+#pragma unroll
+      for (int k = 0; k < NB; ++k) {
+        const int x = i + k * kOmniTopkThreads;
+        if (x < L) s_sc[x] = v[k];
+      }
+    }
     __syncthreads();
     sc = s_sc;
   }
   uint32_t prefix, mask;
   int k_rest;
-  radix_select_top<kOmniTopkThreads, uint32_t>(
+  radix_select_top_rep<kOmniTopkThreads, kOmniHistCopies, uint32_t>(
       L, b, [&](int i) { return float_key(sc[i]); }, [](int) { return true; }, &prefix, &mask, &k_rest, s_hist,
       s_scan, s_bcast);
   // thread t owns slots [t*run, (t+1)*run): count the threshold ties, rank them
@@ -450,6 +564,8 @@ extern "C" se_status se_omnikv_select(const se_kv_view* kv, int32_t q_per_kv, co
   p.budget = budget;
   p.max_len = max_len;
   p.ws_stride = (int32_t)align_up((size_t)max_len, 64);
+  p.vec4 = (reinterpret_cast<uintptr_t>(logits) % 16 == 0 && logits_stride % 4 == 0 &&
+            reinterpret_cast<uintptr_t>(ws) % 16 == 0) ? 1 : 0;
   p.scores = static_cast<float*>(ws);
   p.sel = sel_slots;
   p.dev_err = dev_err;

@@ -135,12 +135,14 @@ def test_long_context_selection_from_workspace(se):
     _run_step(se, [40000], 1, 4, 128, 2048, seed=4, max_diverged=1)
 
 
-def test_select_from_given_logits_with_ties(se):
+@pytest.mark.parametrize("G,L,stride", [(4, 1000, 1024), (4, 1000, 1027), (3, 1001, 1024), (5, 999, 1000)])
+def test_select_from_given_logits_with_ties(se, G, L, stride):
     # logits taken as given (integer levels, many exact ties): the selection is
-    # bit-exact against the oracle's TopK over max-over-heads scores
-    hkv, G, nreq, L, budget = 2, 4, 3, 1000, 97
-    g = torch.Generator().manual_seed(5)
-    stride = 1024
+    # bit-exact against the oracle's TopK over max-over-heads scores; rows in
+    # 16-byte aligned strides (four slots per load, 8 / 6 / 10 rows per request)
+    # and an unaligned stride
+    hkv, nreq, budget = 2, 3, 97
+    g = torch.Generator().manual_seed(5 + G + stride)
     logits = torch.randint(0, 7, (nreq * hkv * G, stride), generator=g).to(torch.float32)
     st = isolated_units([L] * (nreq * hkv), 64, 64, 1, num_kv_heads=hkv)
     gs = to_device(st, DEV)
