@@ -89,6 +89,7 @@ struct SnapParams {
   int32_t u_stride;
   int32_t n_rb;       // row blocks of kSnapMaxRows rows (grid.y)
   int32_t chunk;      // H2O prefill: the chunk's slots (the last ones); 0 for SnapKV
+  int32_t vec4;       // H2O prefill: score pool and workspace 16-byte aligned
   float c;  // scale * log2(e)
   int32_t* dev_err;
 };
@@ -607,12 +608,37 @@ __global__ __launch_bounds__(kApplyThreads) void h2o_chunk_apply_kernel(const Sn
   int bad = 0;
   for (int i = threadIdx.x; i < n_pages; i += kApplyThreads) bad |= (bt[i] < 0 || (int64_t)bt[i] >= p.num_pages);
   if (block_reduce<kApplyThreads>(bad, s_red, [](int a, int b) { return a | b; })) return;
+  // four consecutive slots per thread (one page holds them): 16-byte loads of
+  // the partial rows and of the scores when the buffers are aligned
   const int j0 = blockIdx.x * kApplySlots;
-  for (int j = j0 + threadIdx.x; j < min(L, j0 + kApplySlots); j += kApplyThreads) {
-    float u = 0.f;
-    for (int b = 0; b < p.n_rb; ++b) u += p.u[((size_t)unit * p.n_rb + b) * p.u_stride + j];
+  const int j1 = min(L, j0 + kApplySlots);
+  const int cs = L - p.chunk;  // the chunk's first slot
+  const float* ub = p.u + (size_t)unit * p.n_rb * p.u_stride;
+  for (int j = j0 + 4 * (int)threadIdx.x; j < j1; j += 4 * kApplyThreads) {
     float* sc = p.score_pool + (size_t)bt[j >> 4] * kPage + (j & (kPage - 1));
-    *sc = (j >= L - p.chunk ? 0.f : *sc) + u;
+    if (p.vec4 && j + 4 <= j1) {
+      float4 u = *reinterpret_cast<const float4*>(ub + j);
+      for (int b = 1; b < p.n_rb; ++b) {
+        const float4 v = *reinterpret_cast<const float4*>(ub + (size_t)b * p.u_stride + j);
+        u.x += v.x;
+        u.y += v.y;
+        u.z += v.z;
+        u.w += v.w;
+      }
+      float4 o = *reinterpret_cast<const float4*>(sc);
+      o.x = (j >= cs ? 0.f : o.x) + u.x;
+      o.y = (j + 1 >= cs ? 0.f : o.y) + u.y;
+      o.z = (j + 2 >= cs ? 0.f : o.z) + u.z;
+      o.w = (j + 3 >= cs ? 0.f : o.w) + u.w;
+      *reinterpret_cast<float4*>(sc) = o;
+    } else {
+      for (int t = j; t < min(j + 4, j1); ++t) {
+        float u = ub[t];
+        for (int b = 1; b < p.n_rb; ++b) u += ub[(size_t)b * p.u_stride + t];
+        float* st = sc + (t - j);
+        *st = (t >= cs ? 0.f : *st) + u;
+      }
+    }
   }
 }
 
@@ -667,6 +693,7 @@ extern "C" se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, c
   const int rows = window * q_per_kv;
   p.n_rb = 1;
   p.chunk = 0;
+  p.vec4 = 0;
   if (kv->head_dim == 128)
     launch_snapkv_d<128, false>(p, kv->num_units, rows, stream);
   else
@@ -737,6 +764,7 @@ extern "C" se_status se_h2o_prefill_chunk(const se_kv_view* kv, int32_t q_per_kv
   p.u_stride = (int32_t)align_up((size_t)max_len, 64);
   p.n_rb = (int32_t)ceil_div((int64_t)score_window * q_per_kv, kPrefillBlockRows);
   p.chunk = chunk_len;
+  p.vec4 = (reinterpret_cast<uintptr_t>(kv->score_pool) % 16 == 0 && reinterpret_cast<uintptr_t>(ws) % 16 == 0) ? 1 : 0;
   p.c = scale * kLog2e;
   p.dev_err = dev_err;
   const int rows = std::min(score_window * q_per_kv, kPrefillBlockRows);
