@@ -45,7 +45,14 @@ struct EvictJob {
   int32_t freed_stride;
   int32_t* freed_count;
   int32_t* dev_err;
+  int32_t* moves = nullptr;  // deferred moves: count, then holes, then movers (kMoveListInts ints)
 };
+
+// A unit's deferred move list: moves[0] = n, holes at moves[kMoveHoles + r],
+// movers at moves[kMoveMovers + r], r < n (slot indices).
+constexpr int kMoveHoles = 64;
+constexpr int kMoveMovers = kMoveHoles + kMaxBudget;
+constexpr int kMoveListInts = kMoveMovers + kMaxBudget;
 
 // LDS the caller provides.
 template <int NT>
@@ -75,6 +82,10 @@ struct EvictParams {
   int32_t freed_stride;
   int32_t* freed_count;
   int32_t* dev_err;
+  // When set (kMoveListInts ints per unit), the selection kernel leaves each
+  // unit's holes and movers here and a second kernel, several work-groups per
+  // unit, moves the rows.
+  int32_t* moves = nullptr;
 };
 
 // Launches the eviction of every unit (head_dim 64 or 128) on `stream`.
@@ -716,10 +727,16 @@ __device__ __forceinline__ void evict_unit_wide(const EvictJob& p, const WideScr
   }
   __syncthreads();
 
+  if (p.moves != nullptr) {  // the moves are left to evict_move_kernel
+    for (int r = tid; r < n_moves; r += NT) {
+      p.moves[kMoveHoles + r] = sc.holes[r];
+      p.moves[kMoveMovers + r] = ws.movers[r];
+    }
+    if (tid == 0) p.moves[0] = n_moves;
+  } else {
   // ---- mover r's key and value rows go to hole r; one 16-byte chunk per
   // thread, and the threads of chunks 0 and 1 also carry the position and the
   // score (nothing else reads a mover's source entry or a hole's old one)
-  {
     constexpr int C = D / 8;            // chunks per row
     constexpr int TPM = 2 * C;          // threads per mover (key row, then value row)
     constexpr int MPP = NT / TPM;       // movers per pass

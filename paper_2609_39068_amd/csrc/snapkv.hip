@@ -646,9 +646,15 @@ __global__ __launch_bounds__(kApplyThreads) void h2o_chunk_apply_kernel(const Sn
 
 using namespace se;
 
+// Workspace: the per-slot sums, then (256-byte aligned) the eviction's deferred
+// move lists, kMoveListInts ints per unit.
+static size_t snapkv_sums_bytes(int32_t num_units, int32_t max_len) {
+  return align_up((size_t)num_units * align_up((size_t)max_len, 64) * sizeof(float), 256);
+}
+
 size_t se_snapkv_workspace_bytes(int32_t num_units, int32_t max_len) {
   if (num_units <= 0 || max_len <= 0) return 0;
-  return (size_t)num_units * align_up((size_t)max_len, 64) * sizeof(float);
+  return snapkv_sums_bytes(num_units, max_len) + (size_t)num_units * kMoveListInts * sizeof(int32_t);
 }
 
 extern "C" se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, const void* q_obs,
@@ -716,14 +722,21 @@ extern "C" se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, c
   e.freed_stride = freed_stride;
   e.freed_count = freed_count;
   e.dev_err = dev_err;
+  e.moves = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + snapkv_sums_bytes(kv->num_units, max_len));
   launch_evict(e, kv->num_units, kv->head_dim, stream);
   return launch_status();
 }
 
+// Workspace: the row blocks' partial sums, then the eviction's move lists.
+static size_t prefill_sums_bytes(int32_t num_units, int32_t max_len, int32_t q_per_kv, int32_t window) {
+  const size_t n_rb = (size_t)ceil_div((int64_t)window * q_per_kv, kPrefillBlockRows);
+  return align_up((size_t)num_units * n_rb * align_up((size_t)max_len, 64) * sizeof(float), 256);
+}
+
 size_t se_h2o_prefill_workspace_bytes(int32_t num_units, int32_t max_len, int32_t q_per_kv, int32_t window) {
   if (num_units <= 0 || max_len <= 0 || q_per_kv <= 0 || window <= 0) return 0;
-  const size_t n_rb = (size_t)ceil_div((int64_t)window * q_per_kv, kPrefillBlockRows);
-  return (size_t)num_units * n_rb * align_up((size_t)max_len, 64) * sizeof(float);
+  return prefill_sums_bytes(num_units, max_len, q_per_kv, window) +
+         (size_t)num_units * kMoveListInts * sizeof(int32_t);
 }
 
 extern "C" se_status se_h2o_prefill_chunk(const se_kv_view* kv, int32_t q_per_kv, const void* q_score,
@@ -792,6 +805,8 @@ extern "C" se_status se_h2o_prefill_chunk(const se_kv_view* kv, int32_t q_per_kv
   e.freed_stride = freed_stride;
   e.freed_count = freed_count;
   e.dev_err = dev_err;
+  e.moves = reinterpret_cast<int32_t*>(static_cast<char*>(ws) +
+                                       prefill_sums_bytes(kv->num_units, max_len, q_per_kv, score_window));
   launch_evict(e, kv->num_units, kv->head_dim, stream);
   return launch_status();
 }

@@ -220,9 +220,10 @@ def test_workspace_sizes():
     assert b.se_workspace_bytes(b.SE_OP_QUEST_SELECT, 256, 33024, 2064, 4, 128, 0) >= 256 * 2064 * 4
     ns = b.se_workspace_bytes(b.SE_OP_QUEST_STEP, 256, 33024, 2064, 4, 128, 64)
     assert ns == nq + b.se_workspace_bytes(b.SE_OP_QUEST_SELECT, 256, 33024, 2064, 4, 128, 0)
-    assert b.se_workspace_bytes(b.SE_OP_SNAPKV, 512, 32768, 2048, 4, 128, 0) == 512 * 32768 * 4
-    assert b.se_workspace_bytes(b.SE_OP_SNAPKV, 3, 1000, 63, 4, 128, 0) == 3 * 1024 * 4
+    moves = (64 + 2 * 8192) * 4       # per unit: the eviction's deferred move lists
+    assert b.se_workspace_bytes(b.SE_OP_SNAPKV, 512, 32768, 2048, 4, 128, 0) == 512 * 32768 * 4 + 512 * moves
+    assert b.se_workspace_bytes(b.SE_OP_SNAPKV, 3, 1000, 63, 4, 128, 0) == 3 * 1024 * 4 + 3 * moves
     assert b.se_workspace_bytes(b.SE_OP_OMNIKV_SELECT, 32, 33000, 2063, 4, 128, 0) == 32 * 33024 * 4
-    assert b.se_workspace_bytes(b.SE_OP_H2O_PREFILL, 10, 1000, 63, 4, 128, 128) == 10 * 4 * 1024 * 4
-    assert b.se_workspace_bytes(b.SE_OP_H2O_PREFILL, 10, 1000, 63, 4, 128, 32) == 10 * 1 * 1024 * 4
+    assert b.se_workspace_bytes(b.SE_OP_H2O_PREFILL, 10, 1000, 63, 4, 128, 128) == 10 * 4 * 1024 * 4 + 10 * moves
+    assert b.se_workspace_bytes(b.SE_OP_H2O_PREFILL, 10, 1000, 63, 4, 128, 32) == 10 * 1 * 1024 * 4 + 10 * moves
     assert b.se_workspace_bytes(99, 1, 1, 1, 1, 64, 0) == 0
