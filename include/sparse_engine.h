@@ -280,12 +280,14 @@ se_status se_decode_step_quest(const se_kv_view* kv, int32_t q_per_kv, const voi
  *  q_obs   bf16 [num_req][window][num_kv_heads * q_per_kv][head_dim]: the query of
  *          every head at the window's positions, in increasing position order (the
  *          prefill computed them); query head a belongs to KV head a / q_per_kv.
- *  window  1 .. budget, window * q_per_kv <= 128; kernel odd, 1 .. 31;
+ *  window  1 .. budget, window * q_per_kv <= 1024 (above 128 rows the scores are summed over
+ *          row blocks of 128 rows, and the workspace query needs top_k = window);
+ *          kernel odd, 1 .. 31;
  *  scale   > 0 (softmax scale, usually 1/sqrt(head_dim)); budget window .. 8192;
  *  flags   0 or SE_SNAPKV_SCORE_ONLY (freed_* are then unused);
  *  freed_pages, freed_stride, freed_count, max_len as for se_evict_compact;
- *  ws      se_workspace_bytes(SE_OP_SNAPKV, num_units, max_len, ...) bytes (no
- *          zero-fill needed).
+ *  ws      se_workspace_bytes(SE_OP_SNAPKV, num_units, max_len, max_pages, q_per_kv,
+ *          head_dim, window) bytes (no zero-fill needed).
  */
 se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, const void* q_obs,
                             int32_t window, int32_t kernel, float scale, int32_t budget,

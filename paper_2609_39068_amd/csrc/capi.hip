@@ -92,7 +92,7 @@ extern "C" size_t se_workspace_bytes(int32_t op, int32_t num_units, int32_t max_
     case SE_OP_QUEST_STEP:
       return se_quest_step_workspace_bytes(num_units, max_len, max_pages, q_per_kv, head_dim, top_k);
     case SE_OP_SNAPKV:
-      return se_snapkv_workspace_bytes(num_units, max_len);
+      return se_snapkv_workspace_bytes(num_units, max_len, q_per_kv, top_k);
     case SE_OP_OMNIKV_SELECT:
       return se_omnikv_workspace_bytes(num_units, max_len);
     case SE_OP_H2O_PREFILL:

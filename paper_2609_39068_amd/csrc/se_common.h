@@ -210,7 +210,7 @@ __device__ void radix_select_top(int n, int k, KeyFn key_of, CandFn cand, KeyT* 
 size_t se_attend_workspace_bytes(int32_t num_units, int32_t max_len, int32_t max_pages,
                                  int32_t q_per_kv, int32_t head_dim, int32_t top_k);
 size_t se_quest_workspace_bytes(int32_t num_units, int32_t max_pages);
-size_t se_snapkv_workspace_bytes(int32_t num_units, int32_t max_len);
+size_t se_snapkv_workspace_bytes(int32_t num_units, int32_t max_len, int32_t q_per_kv, int32_t window);
 size_t se_omnikv_workspace_bytes(int32_t num_req, int32_t max_len);
 size_t se_h2o_prefill_workspace_bytes(int32_t num_units, int32_t max_len, int32_t q_per_kv, int32_t window);
 size_t se_quest_step_workspace_bytes(int32_t num_units, int32_t max_len, int32_t max_pages, int32_t q_per_kv,

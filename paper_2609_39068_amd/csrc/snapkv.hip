@@ -90,6 +90,7 @@ struct SnapParams {
   int32_t n_rb;       // row blocks of kSnapMaxRows rows (grid.y)
   int32_t chunk;      // H2O prefill: the chunk's slots (the last ones); 0 for SnapKV
   int32_t vec4;       // H2O prefill: score pool and workspace 16-byte aligned
+  int32_t snap_wide;  // SnapKV scored in row blocks (accumulate mode): skip units at or under the budget
   float c;  // scale * log2(e)
   int32_t* dev_err;
 };
@@ -217,6 +218,55 @@ __device__ __forceinline__ void merge_norm(float& ref, float& sum, float ref2, f
   ref = m;
 }
 
+// Max pooling (SnapKV's s): s(j) = max of u over the candidates (slots [0,
+// n_lim)) within `half` positions of j, 0 on the window, written to the score
+// field, through LDS chunks with a halo; a slot order that is not strictly
+// increasing in position is reported.  u_of(j) gives u(j) for j < n_lim.
+template <typename UFn>
+__device__ __forceinline__ void snapkv_pool(const SnapParams& p, const int32_t* bt, int L, int n_lim, UFn u_of,
+                                            uint8_t* scratch, int* s_red) {
+  const int tid = threadIdx.x;
+  const int half = p.half;
+  int32_t* s_pos = reinterpret_cast<int32_t*>(scratch);
+  float* s_u = reinterpret_cast<float*>(scratch) + kSnapPoolChunk + 2 * kSnapHalo;
+  int bad_pos = 0;
+  for (int c0 = 0; c0 < L; c0 += kSnapPoolChunk) {
+    for (int i = tid; i < kSnapPoolChunk + 2 * kSnapHalo; i += kSnapThreads) {
+      const int j = c0 - kSnapHalo + i;
+      int32_t pj = 0;
+      float uj = -INFINITY;
+      if (j >= 0 && j < L) {
+        pj = p.pos_pool[(size_t)bt[j >> 4] * kPage + (j & (kPage - 1))];
+        if (j < n_lim) uj = u_of(j);
+      }
+      s_pos[i] = pj;
+      s_u[i] = uj;
+    }
+    __syncthreads();
+    for (int i = tid; i < kSnapPoolChunk && c0 + i < L; i += kSnapThreads) {
+      const int j = c0 + i;
+      const int x = i + kSnapHalo;
+      const int32_t pj = s_pos[x];
+      if (j > 0 && s_pos[x - 1] >= pj) bad_pos = 1;
+      float s = 0.f;
+      if (j < n_lim) {
+        s = s_u[x];
+        for (int k = 1; k <= half; ++k) {
+          // slots outside [0, n_lim) hold -inf; positions strictly increase, so
+          // the candidates within half positions are within half slots
+          if ((int64_t)pj - s_pos[x - k] <= half) s = fmaxf(s, s_u[x - k]);
+          if ((int64_t)s_pos[x + k] - pj <= half) s = fmaxf(s, s_u[x + k]);
+        }
+      }
+      p.score_pool[(size_t)bt[j >> 4] * kPage + (j & (kPage - 1))] = s;
+    }
+    __syncthreads();
+  }
+  bad_pos = block_reduce<kSnapThreads>(bad_pos, s_red, [](int a, int b) { return a | b; });
+  if (bad_pos && tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_POSITIONS);
+}
+
+
 // RTW: 16-row tiles per row group (rows of group g: [16*RTW*g, 16*RTW*(g+1)) of
 // the work-group's row block blockIdx.y).  kAccum: H2O chunk scoring -- u over
 // every key (the window keys with their causal mask) into the row block's
@@ -245,7 +295,7 @@ __global__ __launch_bounds__(kSnapThreads, kOcc) void snapkv_score_kernel(const 
   const int kh = wv / kSnapRowGroups;
   const int unit = blockIdx.x;
   const int L = p.lengths[unit];
-  if (!kAccum && L <= p.budget) return;  // the prompt already fits: nothing to score or evict
+  if ((!kAccum || p.snap_wide) && L <= p.budget) return;  // the prompt already fits: nothing to score or evict
   if (L > p.max_len || L > p.max_pages * kPage || L > kSnapMaxPages * kPage || (kAccum && L < p.chunk)) {
     if (tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_LENGTH);
     return;
@@ -537,45 +587,7 @@ __global__ __launch_bounds__(kSnapThreads, kOcc) void snapkv_score_kernel(const 
   if (kAccum) return;  // the row block's partial u is written; h2o_chunk_apply_kernel adds the blocks
   __syncthreads();  // the unit's u is complete and visible to the work-group
 
-  // ---- pool: s over the candidates, 0 over the window; positions checked
-  const int half = p.half;
-  int32_t* s_pos = reinterpret_cast<int32_t*>(s_ring);
-  float* s_u = reinterpret_cast<float*>(s_ring) + kSnapPoolChunk + 2 * kSnapHalo;
-  int bad_pos = 0;
-  for (int c0 = 0; c0 < L; c0 += kSnapPoolChunk) {
-    for (int i = tid; i < kSnapPoolChunk + 2 * kSnapHalo; i += kSnapThreads) {
-      const int j = c0 - kSnapHalo + i;
-      int32_t pj = 0;
-      float uj = -INFINITY;
-      if (j >= 0 && j < L) {
-        pj = p.pos_pool[(size_t)bt[j >> 4] * kPage + (j & (kPage - 1))];
-        if (j < n_lim) uj = u[j];
-      }
-      s_pos[i] = pj;
-      s_u[i] = uj;
-    }
-    __syncthreads();
-    for (int i = tid; i < kSnapPoolChunk && c0 + i < L; i += kSnapThreads) {
-      const int j = c0 + i;
-      const int x = i + kSnapHalo;
-      const int32_t pj = s_pos[x];
-      if (j > 0 && s_pos[x - 1] >= pj) bad_pos = 1;
-      float s = 0.f;
-      if (j < n_lim) {
-        s = s_u[x];
-        for (int k = 1; k <= half; ++k) {
-          // slots outside [0, n_lim) hold -inf; positions strictly increase, so
-          // the candidates within half positions are within half slots
-          if ((int64_t)pj - s_pos[x - k] <= half) s = fmaxf(s, s_u[x - k]);
-          if ((int64_t)s_pos[x + k] - pj <= half) s = fmaxf(s, s_u[x + k]);
-        }
-      }
-      p.score_pool[(size_t)bt[j >> 4] * kPage + (j & (kPage - 1))] = s;
-    }
-    __syncthreads();
-  }
-  bad_pos = block_reduce<kSnapThreads>(bad_pos, s_red, [](int a, int b) { return a | b; });
-  if (bad_pos && tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_POSITIONS);
+  snapkv_pool(p, bt, L, n_lim, [&](int j) { return u[j]; }, s_ring, s_red);
 }
 
 template <int D, bool kAccum>
@@ -590,6 +602,29 @@ void launch_snapkv_d(const SnapParams& p, int num_units, int rows, hipStream_t s
     hipLaunchKernelGGL((snapkv_score_kernel<D, 1, kAccum, pipe, occ>), grid, dim3(kSnapThreads), 0, stream, p);
   else
     hipLaunchKernelGGL((snapkv_score_kernel<D, 2, kAccum, pipe, occ>), grid, dim3(kSnapThreads), 0, stream, p);
+}
+
+// SnapKV with more than 128 scoring rows: the scoring kernel ran in its
+// accumulate mode (row blocks of 128 rows, partial sums per block); this
+// kernel adds the blocks' partials in block order and pools.  A unit the
+// scoring kernel rejected (length or block table) is left alone.
+__global__ __launch_bounds__(kSnapThreads) void snapkv_pool_kernel(const SnapParams p) {
+  __shared__ __attribute__((aligned(16))) uint8_t s_scr[(kSnapPoolChunk + 2 * kSnapHalo) * 8];
+  __shared__ int s_red[kSnapWaves];
+  const int unit = blockIdx.x;
+  const int L = p.lengths[unit];
+  if (L <= p.budget || L > p.max_len || L > p.max_pages * kPage || L > kSnapMaxPages * kPage) return;
+  const int32_t* bt = p.block_table + (size_t)unit * p.max_pages;
+  const int n_pages = ceil_div_dev(L, kPage);
+  int bad = 0;
+  for (int i = threadIdx.x; i < n_pages; i += kSnapThreads) bad |= (bt[i] < 0 || (int64_t)bt[i] >= p.num_pages);
+  if (block_reduce<kSnapThreads>(bad, s_red, [](int a, int b) { return a | b; })) return;
+  const float* ub = p.u + (size_t)unit * p.n_rb * p.u_stride;
+  snapkv_pool(p, bt, L, L - p.w, [&](int j) {
+    float u = ub[j];
+    for (int b = 1; b < p.n_rb; ++b) u += ub[(size_t)b * p.u_stride + j];
+    return u;
+  }, s_scr, s_red);
 }
 
 constexpr int kApplyThreads = 256;
@@ -646,15 +681,22 @@ __global__ __launch_bounds__(kApplyThreads) void h2o_chunk_apply_kernel(const Sn
 
 using namespace se;
 
-// Workspace: the per-slot sums, then (256-byte aligned) the eviction's deferred
-// move lists, kMoveListInts ints per unit.
-static size_t snapkv_sums_bytes(int32_t num_units, int32_t max_len) {
-  return align_up((size_t)num_units * align_up((size_t)max_len, 64) * sizeof(float), 256);
+// Workspace: the per-slot sums (one row per row block of 128 scoring rows),
+// then (256-byte aligned) the eviction's deferred move lists, kMoveListInts
+// ints per unit.  window = 0 sizes for at most 128 rows.
+static int snapkv_row_blocks(int32_t q_per_kv, int32_t window) {
+  const int64_t rows = (int64_t)window * q_per_kv;
+  return rows > kSnapMaxRows ? (int)ceil_div(rows, kPrefillBlockRows) : 1;
 }
 
-size_t se_snapkv_workspace_bytes(int32_t num_units, int32_t max_len) {
+static size_t snapkv_sums_bytes(int32_t num_units, int32_t max_len, int n_rb) {
+  return align_up((size_t)num_units * n_rb * align_up((size_t)max_len, 64) * sizeof(float), 256);
+}
+
+size_t se_snapkv_workspace_bytes(int32_t num_units, int32_t max_len, int32_t q_per_kv, int32_t window) {
   if (num_units <= 0 || max_len <= 0) return 0;
-  return snapkv_sums_bytes(num_units, max_len) + (size_t)num_units * kMoveListInts * sizeof(int32_t);
+  return snapkv_sums_bytes(num_units, max_len, snapkv_row_blocks(q_per_kv, window)) +
+         (size_t)num_units * kMoveListInts * sizeof(int32_t);
 }
 
 extern "C" se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, const void* q_obs,
@@ -672,9 +714,10 @@ extern "C" se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, c
   if (kernel < 1 || (kernel & 1) == 0) return SE_ERR_INVALID_ARGUMENT;
   if (!(scale > 0.f) || !(scale < INFINITY)) return SE_ERR_INVALID_ARGUMENT;
   if (freed_pages != nullptr && freed_stride < kv->max_pages) return SE_ERR_INVALID_ARGUMENT;
-  if ((int64_t)window * q_per_kv > kSnapMaxRows || kernel / 2 > kSnapMaxHalf) return SE_ERR_UNSUPPORTED;
+  if ((int64_t)window * q_per_kv > 8 * kSnapMaxRows || kernel / 2 > kSnapMaxHalf) return SE_ERR_UNSUPPORTED;
   if (budget > kMaxBudget || max_len > kSnapMaxPages * kPage) return SE_ERR_UNSUPPORTED;
-  const size_t need = se_snapkv_workspace_bytes(kv->num_units, max_len);
+  const int n_rb = snapkv_row_blocks(q_per_kv, window);
+  const size_t need = se_snapkv_workspace_bytes(kv->num_units, max_len, q_per_kv, window);
   if (ws == nullptr || ws_bytes < need) return SE_ERR_WORKSPACE;
 
   SnapParams p;
@@ -697,13 +740,22 @@ extern "C" se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, c
   p.c = scale * kLog2e;
   p.dev_err = dev_err;
   const int rows = window * q_per_kv;
-  p.n_rb = 1;
+  p.n_rb = n_rb;
   p.chunk = 0;
   p.vec4 = 0;
-  if (kv->head_dim == 128)
-    launch_snapkv_d<128, false>(p, kv->num_units, rows, stream);
-  else
-    launch_snapkv_d<64, false>(p, kv->num_units, rows, stream);
+  p.snap_wide = n_rb > 1;
+  if (n_rb == 1) {  // one work-group per unit scores and pools
+    if (kv->head_dim == 128)
+      launch_snapkv_d<128, false>(p, kv->num_units, rows, stream);
+    else
+      launch_snapkv_d<64, false>(p, kv->num_units, rows, stream);
+  } else {  // row blocks of 128 rows score every key, then the pool kernel adds them
+    if (kv->head_dim == 128)
+      launch_snapkv_d<128, true>(p, kv->num_units, kPrefillBlockRows, stream);
+    else
+      launch_snapkv_d<64, true>(p, kv->num_units, kPrefillBlockRows, stream);
+    hipLaunchKernelGGL(snapkv_pool_kernel, dim3(kv->num_units), dim3(kSnapThreads), 0, stream, p);
+  }
   st = launch_status();
   if (st != SE_OK || (flags & SE_SNAPKV_SCORE_ONLY)) return st;
 
@@ -722,7 +774,7 @@ extern "C" se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, c
   e.freed_stride = freed_stride;
   e.freed_count = freed_count;
   e.dev_err = dev_err;
-  e.moves = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + snapkv_sums_bytes(kv->num_units, max_len));
+  e.moves = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + snapkv_sums_bytes(kv->num_units, max_len, n_rb));
   launch_evict(e, kv->num_units, kv->head_dim, stream);
   return launch_status();
 }
@@ -777,6 +829,7 @@ extern "C" se_status se_h2o_prefill_chunk(const se_kv_view* kv, int32_t q_per_kv
   p.u_stride = (int32_t)align_up((size_t)max_len, 64);
   p.n_rb = (int32_t)ceil_div((int64_t)score_window * q_per_kv, kPrefillBlockRows);
   p.chunk = chunk_len;
+  p.snap_wide = 0;
   p.vec4 = (reinterpret_cast<uintptr_t>(kv->score_pool) % 16 == 0 && reinterpret_cast<uintptr_t>(ws) % 16 == 0) ? 1 : 0;
   p.c = scale * kLog2e;
   p.dev_err = dev_err;

@@ -118,7 +118,8 @@ def test_snapkv_argument_checks():
     assert call(kernel=6) == b.SE_ERR_INVALID_ARGUMENT             # even width
     assert call(kernel=0) == b.SE_ERR_INVALID_ARGUMENT
     assert call(kernel=33) == b.SE_ERR_UNSUPPORTED
-    assert call(G=8, window=32) == b.SE_ERR_UNSUPPORTED            # 256 observation rows
+    assert call(G=8, window=129, budget=256) == b.SE_ERR_UNSUPPORTED  # 1032 observation rows
+    assert call(G=8, window=32, ws_bytes=8) == b.SE_ERR_WORKSPACE     # 256 rows: two sum rows per unit
     assert call(flags=2) == b.SE_ERR_INVALID_ARGUMENT
     assert call(scale=0.0) == b.SE_ERR_INVALID_ARGUMENT
     assert call(budget=9000) == b.SE_ERR_UNSUPPORTED
@@ -223,6 +224,9 @@ def test_workspace_sizes():
     moves = (64 + 2 * 8192) * 4       # per unit: the eviction's deferred move lists
     assert b.se_workspace_bytes(b.SE_OP_SNAPKV, 512, 32768, 2048, 4, 128, 0) == 512 * 32768 * 4 + 512 * moves
     assert b.se_workspace_bytes(b.SE_OP_SNAPKV, 3, 1000, 63, 4, 128, 0) == 3 * 1024 * 4 + 3 * moves
+    # more than 128 observation rows (window 32 x G 8): a sum row per 128-row block
+    assert b.se_workspace_bytes(b.SE_OP_SNAPKV, 3, 1000, 63, 8, 128, 32) == 3 * 2 * 1024 * 4 + 3 * moves
+    assert b.se_workspace_bytes(b.SE_OP_SNAPKV, 3, 1000, 63, 4, 128, 32) == 3 * 1024 * 4 + 3 * moves
     assert b.se_workspace_bytes(b.SE_OP_OMNIKV_SELECT, 32, 33000, 2063, 4, 128, 0) == 32 * 33024 * 4
     assert b.se_workspace_bytes(b.SE_OP_H2O_PREFILL, 10, 1000, 63, 4, 128, 128) == 10 * 4 * 1024 * 4 + 10 * moves
     assert b.se_workspace_bytes(b.SE_OP_H2O_PREFILL, 10, 1000, 63, 4, 128, 32) == 10 * 1 * 1024 * 4 + 10 * moves

@@ -34,8 +34,8 @@ def _view(se, st, hkv):
 def _call(se, gs, hkv, G, qobs, window, kappa, scale, budget, flags=0):
     U = gs.lengths.numel()
     max_len = gs.max_pages * 16
-    ws = torch.empty(se.se_workspace_bytes(se.SE_OP_SNAPKV, U, max_len, gs.max_pages, G, gs.kv_pool.shape[-1]),
-                     dtype=torch.uint8, device=DEV)
+    ws = torch.empty(se.se_workspace_bytes(se.SE_OP_SNAPKV, U, max_len, gs.max_pages, G, gs.kv_pool.shape[-1],
+                                           window), dtype=torch.uint8, device=DEV)
     freed = torch.full((U, gs.max_pages), -7, dtype=torch.int32, device=DEV)
     fcount = torch.full((U,), -7, dtype=torch.int32, device=DEV)
     err = torch.zeros(1, dtype=torch.int32, device=DEV)
@@ -144,6 +144,23 @@ def test_isolated_units(se, G, window, kappa, d, budget):
     _compare(se, host, qobs, hkv, G, window, kappa, scale, budget, max_diverged=1)
 
 
+@pytest.mark.parametrize("G,window,kappa,d,budget", [
+    (8, 32, 7, 128, 256),    # the paper's window with G = 8: 256 rows, two row blocks
+    (4, 100, 5, 64, 160),    # 400 rows: four row blocks, the last one partial
+    (2, 129, 3, 128, 300),   # 258 rows: a third block of two rows
+])
+def test_more_than_128_observation_rows(se, G, window, kappa, d, budget):
+    # window x G above 128: row blocks of 128 rows score every key, the pool
+    # kernel adds their partial sums in block order and pools
+    hkv = 2
+    lengths = [budget, budget + 1, 700, 1601]
+    host = isolated_units(lengths, max_pages=101, head_dim=d, seed=3 + G + window, num_kv_heads=hkv,
+                          position_mode="gapped")
+    qobs = observation_queries(len(lengths) // hkv, window, hkv * G, d, seed=window + 1)
+    scale = float(np.float32(1.0 / np.sqrt(d)))
+    _compare(se, host, qobs, hkv, G, window, kappa, scale, budget, max_diverged=1)
+
+
 def test_gapped_positions(se):
     # sorted positions with gaps: a neighbourhood holds only the candidates within
     # kappa/2 positions, fewer than kappa/2 slots on a side
@@ -154,13 +171,14 @@ def test_gapped_positions(se):
     _compare(se, host, qobs, 1, 4, 16, 9, float(np.float32(1 / np.sqrt(128))), 300, max_diverged=1)
 
 
-def test_unsorted_positions_are_reported(se):
+@pytest.mark.parametrize("G,window", [(2, 8), (8, 40)])
+def test_unsorted_positions_are_reported(se, G, window):
     lengths = [500]
     host = isolated_units(lengths, max_pages=40, head_dim=64, seed=8, num_kv_heads=1,
                           position_mode="shuffled")
     gs = to_device(host, DEV)
-    qobs = observation_queries(1, 8, 2, 64, seed=9).to(DEV)
-    _, _, err = _call(se, gs, 1, 2, qobs, 8, 3, 0.125, 100)
+    qobs = observation_queries(1, window, G, 64, seed=9).to(DEV)
+    _, _, err = _call(se, gs, 1, G, qobs, window, 3, 0.125, 100)
     assert err & se.SE_DEVERR_BAD_POSITIONS
 
 
