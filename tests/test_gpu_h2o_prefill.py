@@ -191,3 +191,41 @@ def test_full_workload_sampled_units(se):
         n = len(r["freed"])
         assert fc[u] == n
         np.testing.assert_array_equal(fp[u, :n], bt[u, r["freed"]])
+
+
+def test_maximum_length(se):
+    # a unit at the call's maximum length (131072 slots), its last 4096 slots the
+    # chunk, scored by 16 queries of 4 heads; the eviction takes its streaming
+    # path for a unit this long
+    L, C, sw, G, d, budget, recent = 131072, 4096, 16, 4, 128, 2048, 1024
+    host = isolated_units([L], 8192, d, 23, num_kv_heads=1, position_mode="contiguous")
+    st = oracle_unit(host, 0)
+    st.u[-C:] = 0.0                          # the chunk starts from 0
+    qs = observation_queries(1, sw, G, d, 24)
+    scale = float(np.float32(1 / np.sqrt(d)))
+    gs = to_device(host, DEV)
+    ws = torch.empty(se.se_workspace_bytes(se.SE_OP_H2O_PREFILL, 1, L, 8192, G, d, sw), dtype=torch.uint8,
+                     device=DEV)
+    freed = torch.full((1, 8192), -7, dtype=torch.int32, device=DEV)
+    fcount = torch.zeros(1, dtype=torch.int32, device=DEV)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    print(f"maximum length: L={L} C={C} sw={sw}", flush=True)
+    se.se_h2o_prefill_chunk(_view(se, gs, 1), G, qs.to(DEV), sw, C, scale, budget, recent, L, freed, 8192, fcount,
+                            ws, err)
+    torch.cuda.synchronize()
+    assert se.se_read_device_errors(err) == 0
+    assert int(gs.lengths[0]) == budget
+    r = h2o.chunk_eviction(st, C, f64(qs[0]), scale, budget, recent)
+    g = gpu_unit(gs, 0)
+    kept_g, kept_o = set(g["pos"].tolist()), set(st.pos.tolist())
+    if kept_g != kept_o:
+        by_pos = dict(zip(r["pos_after_append"].tolist(), r["u_after_accumulate"].tolist()))
+        assert h2o_near_tie(by_pos, kept_g, kept_o), "retained sets differ"
+        return
+    np.testing.assert_array_equal(g["pos"], st.pos)
+    np.testing.assert_array_equal(g["K"], st.K)
+    np.testing.assert_array_equal(g["V"], st.V)
+    assert_scores_close(g["u"], st.u, "maximum length")
+    n = len(r["freed"])
+    assert int(fcount[0]) == n
+    np.testing.assert_array_equal(freed[0, :n].cpu().numpy(), host.block_table.numpy()[0, r["freed"]])

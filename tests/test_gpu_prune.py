@@ -216,3 +216,16 @@ def test_full_workload_sampled_units(se):
         np.testing.assert_array_equal(g["u"], st.u)
         assert fc[u] == len(r["freed"])
         np.testing.assert_array_equal(freed[u, :fc[u]].cpu().numpy(), bt[u][r["freed"]])
+
+
+def test_maximum_unit_length(se):
+    # units at the call's maximum length (131072 slots, 8192 pages): an interval
+    # in the middle, and one covering the whole history (a selection among all
+    # 131072 slots)
+    L = 131072
+    host = isolated_units([L, L], 8192, 128, 51, num_kv_heads=2, position_mode="contiguous")
+    iv = [(60000, 70001), (1000, 1000 + L)]            # unit 1 holds positions s + 1000
+    _run(se, host, 2, iv, budgets=[2500, 5000], what="maximum length budget")
+    rng = np.random.default_rng(12)
+    masks = [(rng.random(hi - lo) < 0.1).astype(np.uint8) for lo, hi in iv]
+    _run(se, host, 2, iv, masks=masks, what="maximum length mask")

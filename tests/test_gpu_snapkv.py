@@ -161,6 +161,15 @@ def test_more_than_128_observation_rows(se, G, window, kappa, d, budget):
     _compare(se, host, qobs, hkv, G, window, kappa, scale, budget, max_diverged=1)
 
 
+def test_maximum_prompt_length(se):
+    # one prompt at the call's maximum length (131072 slots, 8192 pages): the
+    # eviction takes its streaming path for units this long
+    host = isolated_units([131072], max_pages=8192, head_dim=128, seed=17, num_kv_heads=1,
+                          position_mode="contiguous")
+    qobs = observation_queries(1, 32, 4, 128, seed=18)
+    _compare(se, host, qobs, 1, 4, 32, 7, float(np.float32(1 / np.sqrt(128))), 2048, max_diverged=1)
+
+
 def test_gapped_positions(se):
     # sorted positions with gaps: a neighbourhood holds only the candidates within
     # kappa/2 positions, fewer than kappa/2 slots on a side
