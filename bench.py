@@ -754,18 +754,12 @@ def main_omnikv(args):
     print(f"generated '{w.name}' in {time.perf_counter() - t_gen:.1f}s", file=sys.stderr, flush=True)
     U, G, D, b = w.units_per_layer, w.q_per_kv, w.head_dim, w.budget
     max_len = state.max_pages * 16
-    stride = -(-max_len // 64) * 64
     views = [se.KVView(state.kv_pool, state.pos_pool, None, None, state.block_table[state.layer_rows(l)],
                        state.lengths[state.layer_rows(l)], num_kv_heads=w.hkv) for l in range(w.layers)]
     out = torch.empty((w.num_req, w.hq, D), dtype=torch.float32, device=dev)
     lse = torch.empty((w.num_req, w.hq), dtype=torch.float32, device=dev)
-    logits = torch.empty(U * G * stride, dtype=torch.float32, device=dev)
-    sel = torch.empty((w.num_req, b), dtype=torch.int32, device=dev)
-    ws_att = torch.empty(se.se_workspace_bytes(se.SE_OP_DECODE_ATTEND, U, max_len, state.max_pages, G, D, 0),
-                         dtype=torch.uint8, device=dev)
-    ws_sel = torch.empty(se.se_workspace_bytes(se.SE_OP_OMNIKV_SELECT, w.num_req, max_len, state.max_pages, G, D, 0),
-                         dtype=torch.uint8, device=dev)
-    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    dec = se.OmniKVDecoder(G, w.scale, b, w.filter_layers, U, w.hkv, max_len, state.max_pages, D, dev)
+    err = dec.dev_err
     observe = set(w.filter_layers)
 
     def run(t0, t1, lengths, layer_events=None, span=None):
@@ -774,13 +768,8 @@ def main_omnikv(args):
             if span is not None and t == t0:
                 span[0].record()
             for l in range(w.layers):
-                q, kn, vn, npos = steps.q[t, l], steps.k_new[t, l], steps.v_new[t, l], steps.new_pos[t]
-                if l in observe:
-                    se.se_decode_attend(views[l], G, q, kn, vn, npos, None, 0, w.scale, ml, 0, out, lse, logits,
-                                        stride, ws_att, err)
-                    se.se_omnikv_select(views[l], G, logits, stride, b, ml, sel, ws_sel, err)
-                else:
-                    se.se_attend_slots(views[l], G, q, kn, vn, npos, sel, b, w.scale, ml, out, lse, err)
+                dec.layer(l, views[l], steps.q[t, l], steps.k_new[t, l], steps.v_new[t, l], steps.new_pos[t], out,
+                          lse, ml)
                 if layer_events is not None and t == t0:
                     layer_events[l].record()
             if span is not None:

@@ -14,4 +14,4 @@ from ._binding import (  # noqa: F401
     SE_DEVERR_BAD_PAGE, SE_DEVERR_CAPACITY, SE_DEVERR_BAD_LENGTH, SE_DEVERR_BAD_SELECTION,
     SE_DEVERR_BAD_POSITIONS, SE_DEVERR_BAD_INTERVAL,
 )
-from .decode import H2ODecoder, QuestDecoder  # noqa: F401
+from .decode import H2ODecoder, OmniKVDecoder, QuestDecoder  # noqa: F401

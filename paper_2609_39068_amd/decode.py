@@ -3,7 +3,8 @@
 The paper's lifecycle (Section 3.1, "Fine-Grained Lifecycle Hooks") runs
 Quest's query-dependent page selection in build_decode_selection, before
 attention, and H2O's score update plus online eviction in finish_step, after
-it.  These drivers issue exactly that sequence of library calls on the
+it; OmniKV selects at its observation layers and the later layers reuse that
+selection.  These drivers issue exactly that sequence of library calls on the
 current stream, with workspaces allocated once up front; they never wait for
 the device.
 """
@@ -102,3 +103,45 @@ class QuestDecoder:
             return
         se.se_decode_step_quest(self.view, self.G, q, k_new, v_new, new_pos, self.scale, self.top_k,
                                 max_len or self.max_len, self.sel, out, lse, self.ws_attend, self.dev_err)
+
+
+class OmniKVDecoder:
+    """A model's OmniKV decode step, layer by layer (Appendix A.3, OmniKV): an
+    observation layer appends, attends over every slot keeping the logits
+    (se_decode_attend) and selects the b slots with the largest logit over the
+    request's heads (se_omnikv_select); each later layer, until the next
+    observation layer, appends and attends over that selection of its own cache
+    (se_attend_slots).  The selection and the buffers are shared by the layers,
+    whose calls run one after another on one stream."""
+
+    def __init__(self, q_per_kv: int, scale: float, budget: int, observation_layers, num_units: int,
+                 num_kv_heads: int, max_len: int, max_pages: int, head_dim: int, device):
+        self.G, self.scale, self.budget, self.max_len = q_per_kv, scale, budget, max_len
+        self.observe = set(int(l) for l in observation_layers)
+        num_req = num_units // num_kv_heads
+        self.stride = -(-max_len // 64) * 64
+        self.logits = torch.empty(num_units * q_per_kv * self.stride, dtype=torch.float32, device=device)
+        self.sel = torch.full((num_req, budget), -1, dtype=torch.int32, device=device)
+        na = se.se_workspace_bytes(se.SE_OP_DECODE_ATTEND, num_units, max_len, max_pages, q_per_kv, head_dim, 0)
+        ns = se.se_workspace_bytes(se.SE_OP_OMNIKV_SELECT, num_req, max_len, max_pages, q_per_kv, head_dim, 0)
+        self.ws_attend = torch.empty(max(na, 1), dtype=torch.uint8, device=device)
+        self.ws_select = torch.empty(max(ns, 1), dtype=torch.uint8, device=device)
+        self.dev_err = torch.zeros(1, dtype=torch.int32, device=device)
+        self.selected = False
+
+    def layer(self, l: int, view: se.KVView, q, k_new, v_new, new_pos, out, lse=None, max_len=None):
+        """Layer l's step.  ``max_len`` bounds the slots after this step's append
+        (defaults to the capacity).  The first layer of a step must be an
+        observation layer, so that the sparse layers read this step's selection."""
+        ml = max_len or self.max_len
+        if l in self.observe:
+            se.se_decode_attend(view, self.G, q, k_new, v_new, new_pos, None, 0, self.scale, ml, 0, out, lse,
+                                self.logits, self.stride, self.ws_attend, self.dev_err)
+            se.se_omnikv_select(view, self.G, self.logits, self.stride, self.budget, ml, self.sel,
+                                self.ws_select, self.dev_err)
+            self.selected = True
+        else:
+            if not self.selected:
+                raise RuntimeError("OmniKV: a sparse layer before any observation layer has selected")
+            se.se_attend_slots(view, self.G, q, k_new, v_new, new_pos, self.sel, self.budget, self.scale, ml,
+                               out, lse, self.dev_err)

@@ -233,3 +233,49 @@ def test_attend_slots_group_sizes(se, G, d):
     for r in range(2):
         assert np.abs(out.cpu().double().numpy()[r] - want[r]["o"]).max() <= OUT_ATOL
         assert np.abs(lse.cpu().double().numpy()[r] - want[r]["lse"]).max() <= LSE_ATOL
+
+
+def test_decoder_layers_against_the_oracle(se):
+    # OmniKVDecoder over three layers (observation layer 0, sparse layers 1 and
+    # 2 reading its selection): each layer's outputs against the oracle's
+    # filter_step / sparse_step with the selection of layer 0
+    hkv, G, d, budget, ctx = 2, 4, 64, 40, [300, 150]
+    nreq = len(ctx)
+    lengths = [L for L in ctx for _ in range(hkv)]
+    max_pages = -(-(max(ctx) + 1) // 16) + 1
+    layers = [isolated_units(lengths, max_pages, d, 60 + l, num_kv_heads=hkv, position_mode="contiguous")
+              for l in range(3)]
+    ins = [_inputs(nreq, hkv, G, d, 70 + 10 * l) for l in range(3)]
+    npos = torch.tensor(ctx, dtype=torch.int32)
+    scale = float(np.float32(1 / np.sqrt(d)))
+    want = [[None] * nreq for _ in range(3)]
+    for r in range(nreq):
+        units = [[oracle_unit(layers[l], r * hkv + h) for h in range(hkv)] for l in range(3)]
+        q, k, v = ins[0]
+        f = omnikv.filter_step(units[0], f64(q[r]), f64(k[r]), f64(v[r]), ctx[r], scale, budget)
+        want[0][r] = f
+        for l in (1, 2):
+            q, k, v = ins[l]
+            want[l][r] = omnikv.sparse_step(units[l], f64(q[r]), f64(k[r]), f64(v[r]), ctx[r], scale, f["J"])
+    gs = [to_device(st, DEV) for st in layers]
+    views = [_view(se, g, hkv) for g in gs]
+    max_len = max(ctx) + 1
+    dec = se.OmniKVDecoder(G, scale, budget, [0], nreq * hkv, hkv, max_len, max_pages, d, DEV)
+    for l in range(3):
+        q, k, v = (t.to(DEV) for t in ins[l])
+        out = torch.empty((nreq, hkv * G, d), dtype=torch.float32, device=DEV)
+        lse = torch.empty((nreq, hkv * G), dtype=torch.float32, device=DEV)
+        print(f"decoder layer {l}", flush=True)
+        dec.layer(l, views[l], q, k, v, npos.to(DEV), out, lse, max_len)
+        torch.cuda.synchronize()
+        assert se.se_read_device_errors(dec.dev_err) == 0
+        if l == 0:
+            sel = dec.sel.cpu().numpy()
+            for r in range(nreq):
+                s = want[0][r]["s"]
+                assert _near_tie_sets(s, sel[r].tolist(), want[0][r]["J"].tolist()), f"request {r} selection"
+                if set(sel[r].tolist()) != set(want[0][r]["J"].tolist()):
+                    return  # a near-tie swap: the sparse layers legitimately read other rows
+        for r in range(nreq):
+            np.testing.assert_allclose(out[r].cpu().numpy(), want[l][r]["o"], atol=OUT_ATOL, rtol=0)
+            np.testing.assert_allclose(lse[r].cpu().numpy(), want[l][r]["lse"], atol=LSE_ATOL, rtol=0)
