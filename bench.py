@@ -52,6 +52,8 @@ DECODE_SOURCES = ("decode_attend.hip", "evict_compact.hip", "evict_core.h", "se_
 SNAPKV_SOURCES = ("snapkv.hip", "evict_compact.hip", "evict_core.h", "se_common.h")
 PRUNE_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "prune_interval_llama3-8b-32-layer-prune-interval_traffic.txt")
 PRUNE_SOURCES = ("prune.hip", "se_common.h")
+OMNIKV_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "omnikv_step_llama3-8b-32-layer-omnikv_traffic.txt")
+OMNIKV_SOURCES = ("decode_attend.hip", "omnikv.hip", "quest_core.h", "evict_core.h", "se_common.h")
 PREFILL_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "h2o_prefill_chunk_llama3-8b-prefill-chunk-h2o_traffic.txt")
 
 
@@ -828,7 +830,8 @@ def main_omnikv(args):
         "roofline": {"bound": "hbm", "kernel": "OmniKV decode step (se_decode_attend + se_omnikv_select on "
                                                "observation layers, se_attend_slots on the others)",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": read_traffic(OMNIKV_TRAFFIC_SUMMARY, OMNIKV_SOURCES),
                      "avg_launch_us": round(1e3 * region_ms / K, 3),
                      "algorithmic_bytes_per_launch": round(total / K)},
         "phases": {"observation_layers_ms": round(obs_ms, 3),
@@ -837,6 +840,13 @@ def main_omnikv(args):
                    "sparse_GBps": round(sparse_bytes / (sparse_ms * 1e-3) / 1e9, 1)},
         "cpu_baseline": cpu,
     }
+    if args.copy_calibration:
+        n = 4 << 30
+        a = torch.empty(n, dtype=torch.uint8, device=dev)
+        bb = torch.empty_like(a)
+        bb.copy_(a)
+        torch.cuda.synchronize()
+        result["copy_calibration_bytes"] = n
     print(json.dumps(result), flush=True)
 
 
