@@ -1,9 +1,11 @@
 /*
  * sparse_engine.h — C-ABI of the sparse-first decode hot path on MI355X (gfx950).
  *
- * The library implements the per-step work of two sparse-attention methods over
- * a paged, per-KV-head KV cache, following the SparseEngine paper's statement of
- * the problem:
+ * The library implements the per-step work of sparse-attention methods over a
+ * paged, per-KV-head KV cache (H2O and Quest decode; SnapKV prompt compaction;
+ * OmniKV cross-layer selection; H2O chunk-wise prefill eviction; interval
+ * prefix-cache pruning), following the SparseEngine paper's statement of the
+ * problem:
  *   - the cache manager owns layout, position mapping and write/update/release
  *     (Section 3.1, "Method-Customized CacheManager");
  *   - attention reads a view of the cache: o = Attention(q, BuildView(C, I))
@@ -13,7 +15,9 @@
  *   - H2O grows accumulated scores and evicts to a budget with a protected recent
  *     window (Appendix A.3, eqs. background-h2o-score, background-h2o-retention);
  *   - Quest ranks pages by a min/max upper bound of the logits and reads the best
- *     pages (Appendix A.3, eqs. background-quest-summary, background-quest-score).
+ *     pages (Appendix A.3, eqs. background-quest-summary, background-quest-score);
+ *   - SnapKV, OmniKV and the prefill and pruning operations are declared below,
+ *     each with the passages that define it.
  *
  * Conventions shared by every call
  * --------------------------------
