@@ -5,8 +5,9 @@
 //
 // Scoring runs one work-group of eight wavefronts per unit, two work-groups
 // per compute unit.  The w observation queries of the unit's G heads form
-// R = w*G <= 128 rows in four row groups of 32; wavefront v holds row group
-// v % 4 in registers as MFMA A operands (bf16 16x16x32 tiles: lane l holds
+// R = w*G rows; up to 128 of them sit in four row groups of 32 (more rows:
+// see the accumulate mode below); wavefront v holds row group v % 4 in
+// registers as MFMA A operands (bf16 16x16x32 tiles: lane l holds
 // row l%16 and contraction indices 8*(l/16)..+7 of each 32-wide step) and
 // takes the pages of key half v / 4 of every stage.  The unit's key pages
 // stream through a two-stage LDS ring of four pages a stage: the work-group
@@ -36,6 +37,12 @@
 // last pages (window keys); slots past the length are masked there too.
 // Retention and compaction are then H2O's kernel (launch_evict) with the
 // window as its recent set.
+//
+// SnapKV with more than 128 rows (up to 1024) runs the kernel in the
+// accumulate mode of the chunk scoring below: each row block of 128 rows
+// writes its partial u per key (the causal mask reaches only window keys),
+// and snapkv_pool_kernel adds the blocks in block order and pools over the
+// candidates.
 //
 // H2O chunk scoring (se_h2o_prefill_chunk) runs the same kernel over every key
 // with the causal mask in both passes, one row block of up to 128 scoring rows
