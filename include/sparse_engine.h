@@ -138,6 +138,9 @@ typedef struct se_kv_view {
  *  scale    logit scale, normally 1/sqrt(head_dim) rounded to float32
  *  max_len  upper bound on the resident slots of any unit after the append; sizes
  *           the launch.  A unit above it sets SE_DEVERR_BAD_LENGTH and is skipped.
+ *           So does an empty unit without an append (nothing to attend): its rows
+ *           of out and lse are left as they were.  With an append an empty unit
+ *           holds one slot and attends it (out = its value row).
  *  out      fp32 [num_req][num_kv_heads * q_per_kv][head_dim]
  *  lse      fp32 [num_req][num_kv_heads * q_per_kv], or NULL
  *  logits   fp32 [num_units][q_per_kv][logits_stride] (z per slot), or NULL; only
