@@ -880,7 +880,7 @@ def read_traffic(path=TRAFFIC_SUMMARY, files=DECODE_SOURCES):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on one GPU only; every unit (request, KV head) is independent, "
+        print("bench.py measures one GPU: every unit (request, KV head) is independent, "
               "so N GPUs would each run this same benchmark on their share of the requests. "
               "Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)

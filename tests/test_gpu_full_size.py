@@ -12,7 +12,7 @@ import torch
 from oracle import h2o, quest
 from tests.oracle_bridge import (OUT_ATOL, QUEST_RTOL, assert_scores_close, f64, gpu_unit,
                                  h2o_near_tie, oracle_unit, quest_near_tie)
-from workloads import CONFIGS, build_state, build_steps
+from workloads import LAYER_H2O, LAYER_QUEST, MODEL_H2O, RAGGED_H2O, build_state, build_steps
 
 pytestmark = pytest.mark.gpu
 
@@ -90,31 +90,31 @@ def _run_h2o_sampled(se, w, n_steps, n_sample):
     return checked, diverged
 
 
-def test_config1_full_size(se):
+def test_8b_layer_h2o_full_size(se):
     # 64 requests x 8 KV heads, 32768-token contexts: step 1 evicts 32769 -> 2048
     # (radix path), step 2 is the steady one-slot eviction.
-    w = CONFIGS[1]
+    w = LAYER_H2O
     checked, diverged = _run_h2o_sampled(se, w, 2, 8)
     assert len(diverged) <= 2 and checked >= 12
 
 
-def test_config3_full_size(se):
+def test_ragged_batch_h2o_full_size(se):
     # 128 requests, ragged per-head lengths 1024..4096, budget 4096.
-    w = CONFIGS[3]
+    w = RAGGED_H2O
     checked, diverged = _run_h2o_sampled(se, w, 2, 12)
     assert len(diverged) <= 2 and checked >= 20
 
 
-def test_config4_full_size(se):
+def test_32_layer_h2o_full_size(se):
     # 32 layers x 256 requests x 8 KV heads at 4096 retained tokens (~137 GB of KV).
-    w = CONFIGS[4]
+    w = MODEL_H2O
     checked, diverged = _run_h2o_sampled(se, w, 2, 12)
     assert len(diverged) <= 2 and checked >= 20
 
 
-def test_config2_full_size(se):
+def test_8b_layer_quest_full_size(se):
     # Quest over 2048 pages per KV head, top-64, 32 requests.
-    w = CONFIGS[2]
+    w = LAYER_QUEST
     print(f"generating {w.name}", flush=True)
     gs = build_state(w, DEV)
     steps = build_steps(w, gs, DEV, steps=2)

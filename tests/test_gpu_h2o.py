@@ -14,7 +14,7 @@ from oracle import h2o
 from oracle.attention import selected_attention
 from tests.oracle_bridge import (LSE_ATOL, OUT_ATOL, assert_scores_close, f64, gpu_unit,
                                  h2o_near_tie, oracle_unit)
-from workloads import CONFIGS, build_state, build_steps, clone_state, isolated_units, scaled, to_device
+from workloads import LAYER_H2O, TINY_H2O, build_state, build_steps, clone_state, isolated_units, scaled, to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -99,8 +99,8 @@ def _run_h2o(se, w, n_steps, check_every=1, units=None):
     return checked, diverged
 
 
-def test_config0_tiny_step(se):
-    w = CONFIGS[0]
+def test_tiny_h2o_step(se):
+    w = TINY_H2O
     checked, diverged = _run_h2o(se, w, 1)
     assert checked == w.units_per_layer and not diverged
 
@@ -109,7 +109,7 @@ def test_trajectory_8b_shape_scaled(se):
     # 4 requests of the 8B head shape, a ragged initial context (1000 = 62.5
     # pages), budget 256 with a 32-token window: the first step takes the
     # radix path (1001 -> 256), the rest the steady one-slot path.
-    w = scaled(CONFIGS[1], num_req=4, ctx=1000, budget=256, recent=32, steps=20)
+    w = scaled(LAYER_H2O, num_req=4, ctx=1000, budget=256, recent=32, steps=20)
     checked, diverged = _run_h2o(se, w, 20)
     assert len(diverged) <= w.units_per_layer // 4, diverged
     assert checked >= 0.75 * 20 * w.units_per_layer
@@ -117,27 +117,27 @@ def test_trajectory_8b_shape_scaled(se):
 
 def test_trajectory_small_window_long_run(se):
     # d=64, G=2, budget not a multiple of the page size, window of 3.
-    w = scaled(CONFIGS[0], num_req=3, hq=4, hkv=2, ctx=150, budget=100, recent=3, steps=40)
+    w = scaled(TINY_H2O, num_req=3, hq=4, hkv=2, ctx=150, budget=100, recent=3, steps=40)
     checked, diverged = _run_h2o(se, w, 40)
     assert len(diverged) <= 2 and checked >= 0.75 * 40 * w.units_per_layer
 
 
 @pytest.mark.parametrize("G,d", [(1, 128), (2, 64), (4, 64)])
 def test_head_group_and_dim_variants(se, G, d):
-    w = scaled(CONFIGS[0], num_req=2, hq=2 * G, hkv=2, head_dim=d, ctx=300, budget=64, recent=16, steps=3)
+    w = scaled(TINY_H2O, num_req=2, hq=2 * G, hkv=2, head_dim=d, ctx=300, budget=64, recent=16, steps=3)
     checked, diverged = _run_h2o(se, w, 3)
     assert not diverged and checked == 3 * w.units_per_layer
 
 
 def test_budget_covers_context_is_dense(se):
     # B >= L: TopK keeps everything (no eviction) and attention is dense.
-    w = scaled(CONFIGS[1], num_req=2, ctx=200, budget=400, recent=8, steps=3)
+    w = scaled(LAYER_H2O, num_req=2, ctx=200, budget=400, recent=8, steps=3)
     checked, diverged = _run_h2o(se, w, 3)
     assert not diverged and checked == 3 * w.units_per_layer
 
 
 def test_unfused_accumulate_matches_fused(se):
-    w = scaled(CONFIGS[1], num_req=2, ctx=700, budget=2048, recent=8, steps=1)
+    w = scaled(LAYER_H2O, num_req=2, ctx=700, budget=2048, recent=8, steps=1)
     host = build_state(w, "cpu")
     steps = build_steps(w, host, "cpu")
     a, b = to_device(host, DEV), to_device(host, DEV)
@@ -251,7 +251,7 @@ def test_device_errors_are_reported(se):
 def test_deterministic_and_resumable(se):
     # Two runs from the same state give bit-identical results, and a run that
     # is snapshotted and restored midway continues bit-identically.
-    w = scaled(CONFIGS[1], num_req=2, ctx=600, budget=128, recent=16, steps=6)
+    w = scaled(LAYER_H2O, num_req=2, ctx=600, budget=128, recent=16, steps=6)
     host = build_state(w, "cpu")
     steps = build_steps(w, host, "cpu")
     max_len = host.max_pages * 16

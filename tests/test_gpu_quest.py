@@ -9,7 +9,7 @@ from oracle import quest
 from oracle.attention import selected_attention
 from tests.oracle_bridge import (LSE_ATOL, OUT_ATOL, QUEST_RTOL, f64, gpu_unit, oracle_unit,
                                  quest_near_tie)
-from workloads import CONFIGS, build_state, build_steps, isolated_units, scaled, to_device
+from workloads import LAYER_QUEST, build_state, build_steps, isolated_units, scaled, to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -104,21 +104,21 @@ def _run_quest(se, w, n_steps):
 def test_quest_trajectory_8b_shape_scaled(se):
     # 2 requests of the 8B head shape, 2000 tokens (125 pages), top-8 pages,
     # 20 steps crossing a page boundary (2000 + 16 tokens).
-    w = scaled(CONFIGS[2], num_req=2, ctx=2000, top_k=8, steps=20)
+    w = scaled(LAYER_QUEST, num_req=2, ctx=2000, top_k=8, steps=20)
     same, ties = _run_quest(se, w, 20)
     assert same >= 0.9 * 20 * w.units_per_layer
 
 
 def test_quest_variants(se):
     # d=64 with G=2, a partial current page, more pages wanted than exist.
-    w = scaled(CONFIGS[2], num_req=2, hq=4, hkv=2, head_dim=64, ctx=90, top_k=9, steps=12)
+    w = scaled(LAYER_QUEST, num_req=2, hq=4, hkv=2, head_dim=64, ctx=90, top_k=9, steps=12)
     same, ties = _run_quest(se, w, 12)
     assert same >= 0.9 * 12 * w.units_per_layer
 
 
 def test_select_all_pages_is_dense(se):
     # top_k >= number of pages: every page is read, so the step is dense attention.
-    w = scaled(CONFIGS[2], num_req=2, ctx=500, top_k=64, steps=2)
+    w = scaled(LAYER_QUEST, num_req=2, ctx=500, top_k=64, steps=2)
     host = build_state(w, "cpu")
     steps = build_steps(w, host, "cpu")
     G = w.q_per_kv
@@ -183,7 +183,7 @@ def test_fused_select_matches_two_pass(se):
     # per unit); the first 16 units alone take the bound + top-k kernels.  Page
     # scores and selections agree bit for bit, and the fused selection equals
     # the top-k kernel's selection from the fused scores.
-    w = scaled(CONFIGS[2], ctx=3001, steps=1)
+    w = scaled(LAYER_QUEST, ctx=3001, steps=1)
     host = build_state(w, "cpu")
     steps = build_steps(w, host, "cpu", steps=1)
     gs = to_device(host, DEV)
@@ -226,7 +226,7 @@ def test_step_quest_equals_select_then_attend(se, num_req):
     # selections, outputs, lse and the pools (append, Quest summaries) agree bit
     # for bit.
     from workloads import clone_state
-    w = scaled(CONFIGS[2], num_req=num_req, ctx=3001, steps=3)
+    w = scaled(LAYER_QUEST, num_req=num_req, ctx=3001, steps=3)
     host = build_state(w, "cpu")
     steps = build_steps(w, host, "cpu", steps=3)
     a = to_device(host, DEV)
@@ -258,7 +258,7 @@ def test_fused_select_ties_match_topk_kernel(se):
     # summaries of its page 0): the one-kernel selection keeps the lowest page
     # indices of the tied class, exactly as the top-k kernel does from the same
     # scores.
-    w = scaled(CONFIGS[2], ctx=2001, steps=1)
+    w = scaled(LAYER_QUEST, ctx=2001, steps=1)
     host = build_state(w, "cpu")
     steps = build_steps(w, host, "cpu", steps=1)
     gs = to_device(host, DEV)

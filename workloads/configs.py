@@ -74,6 +74,10 @@ CONFIGS = [
 ]
 
 
+# The decode workloads by name.
+TINY_H2O, LAYER_H2O, LAYER_QUEST, RAGGED_H2O, MODEL_H2O = CONFIGS
+
+
 # SnapKV prompt compaction after prefill (Appendix A.3, SnapKV; Appendix D uses
 # a 32-token scoring window and pooling kernel 7): the prefilled prompt of
 # every (request, KV head) is cut from 32768 slots to the 2048 that the H2O
