@@ -16,7 +16,7 @@ Section 3.1 ("Method-Customized CacheManager"): physical eviction updates the
 retained-slot mapping and the context length, then releases the discarded
 slots.
 
-Readings of points the paper leaves open (each is also listed in the design doc):
+Readings of points the paper leaves open:
   * GQA: a KV head's score grows by the *sum* of the weights of its G query
     heads (parity unpinned by the paper; a convention held here).
   * The window W is the min(w, B) slots with the largest logical positions.
@@ -158,7 +158,7 @@ def prefill_chunk(st: UnitState, K: np.ndarray, V: np.ndarray, pos: np.ndarray, 
     group's weights to those slots' scores, as the per-token recurrence does
     for one query.  Then the retained set and the compaction of a decode step.
 
-    Readings (also in the design doc): the scoring queries are the chunk's last s
+    Readings: the scoring queries are the chunk's last s
     positions (s = C: every query of the chunk); GQA sum; window and TopK as
     for decode."""
     C = K.shape[0]

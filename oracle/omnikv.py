@@ -11,7 +11,7 @@ background-omnikv-selection and background-omnikv-reuse):
     own cache and computes its own weights over them (selected attention,
     Appendix A.1, eq. background-selected-attention, with S = J).
 
-Readings of points the paper leaves open (each is also listed in the design doc):
+Readings of points the paper leaves open:
   * heads: every query head of the request (all KV heads' groups), so J is
     one set per request, shared by its KV heads;
   * the available positions at the filter layer include the current token

@@ -11,7 +11,7 @@ Appendix C.2, "Pruning Metadata and Cache Operations":
   * the logical prefix is unchanged and the resident set becomes
     R' = (R minus T) union I; the slots outside R' are released.
 
-Readings of points the paper leaves open (each is also listed in the design doc):
+Readings of points the paper leaves open:
   * the mask is indexed by position offset inside the interval (entry i says
     whether position lo + i is kept); entries for positions that are not
     resident have nothing to keep and are ignored;

@@ -12,7 +12,7 @@ Appendix A.3, "Quest: Query-Dependent Page Selection":
 Section 3.1: selection only changes which resident entries attention reads
 (eq. attention-view); nothing is evicted.
 
-Readings of points the paper leaves open (each is also listed in the design doc):
+Readings of points the paper leaves open:
   * GQA: a KV head ranks pages by the *maximum* of the estimates of its G
     query heads (parity unpinned by the paper; a convention held here).
   * The page holding the newest token (the current page) is always read and

@@ -11,7 +11,7 @@ background-snapkv-score and background-snapkv-retention):
   * with budget B >= w the retained prompt is O plus the TopK_{B-w} of s over
     the earlier positions, selected separately for every head.
 
-Readings of points the paper leaves open (each is also listed in the design doc):
+Readings of points the paper leaves open:
   * GQA: a KV head's u(j) sums the weights of its G query heads (as for H2O;
     parity unpinned by the paper, a convention held here).
   * The observation queries are inputs (the prefill computed them): query t
