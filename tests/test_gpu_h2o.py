@@ -186,6 +186,8 @@ CASES = [
     ([32769, 20000], 2048, 256, "contiguous", 0),    # first step of the 8B workload
     ([6000, 3000], 1024, 64, "contiguous", 3),       # exact score ties at the threshold
     ([36000], 2048, 256, "shuffled", 7),             # past the register-resident size
+    ([8193, 12000], 8192, 512, "shuffled", 0),       # the largest budget
+    ([3, 1, 2, 0], 1, 1, "gapped", 2),               # budget 1: only the newest position stays
 ]
 
 
@@ -284,23 +286,31 @@ def test_deterministic_and_resumable(se):
         assert torch.equal(getattr(a, name), getattr(snap, name))
 
 
+FUSED_CASES = [
+    # lengths, budget, window, block-table row length
+    ([300, 129, 129, 129, 64, 128], 128, 16, 32),
+    ([8193, 8192, 9000, 8192], 8192, 512, 570),   # the largest budget: long units, weights past LDS
+    ([2, 1, 5, 0], 1, 1, 2),                      # budget 1: the window is the newest slot
+]
+
+
 @pytest.mark.parametrize("mode", ["contiguous", "gapped", "shuffled"])
-def test_fused_step_equals_attend_then_evict(se, mode):
+@pytest.mark.parametrize("lengths,B,w,P", FUSED_CASES)
+def test_fused_step_equals_attend_then_evict(se, mode, lengths, B, w, P):
     # se_decode_step_h2o must leave exactly the state that se_decode_attend +
     # se_evict_compact leave: bit-identical pools, lengths, outputs and freed
     # pages, whether the eviction is fused (steady, contiguous window) or not
     # (first step, or scattered recent positions).
-    lengths = [300, 129, 129, 129, 64, 128]
-    B, w, d, G = 128, 16, 128, 4
-    host = isolated_units(lengths, 32, d, seed=77, num_kv_heads=2, position_mode=mode)
+    d, G = 128, 4
+    host = isolated_units(lengths, P, d, seed=77 + B, num_kv_heads=2, position_mode=mode)
     U = len(lengths)
     nreq = U // 2
     g = torch.Generator().manual_seed(3)
     a, b = to_device(host, DEV), to_device(host, DEV)
-    max_len = 32 * 16
-    ws = torch.zeros(se.se_workspace_bytes(se.SE_OP_DECODE_ATTEND, U, max_len, 32, G, d), dtype=torch.uint8, device=DEV)
+    max_len = P * 16
+    ws = torch.zeros(se.se_workspace_bytes(se.SE_OP_DECODE_ATTEND, U, max_len, P, G, d), dtype=torch.uint8, device=DEV)
     err = torch.zeros(1, dtype=torch.int32, device=DEV)
-    fa = torch.full((U, 32), -3, dtype=torch.int32, device=DEV)
+    fa = torch.full((U, P), -3, dtype=torch.int32, device=DEV)
     fb = fa.clone()
     ca = torch.full((U,), -3, dtype=torch.int32, device=DEV)
     cb = ca.clone()
@@ -309,13 +319,13 @@ def test_fused_step_equals_attend_then_evict(se, mode):
         q = torch.randn((nreq, 2 * G, d), generator=g).to(torch.bfloat16).to(DEV)
         kn = torch.randn((nreq, 2, d), generator=g).to(torch.bfloat16).to(DEV)
         vn = torch.randn((nreq, 2, d), generator=g).to(torch.bfloat16).to(DEV)
-        npos = torch.tensor([10_000 + 10 * step + r for r in range(nreq)], dtype=torch.int32, device=DEV)
+        npos = torch.tensor([1_000_000 + 10 * step + r for r in range(nreq)], dtype=torch.int32, device=DEV)
         oa = torch.empty((nreq, 2 * G, d), dtype=torch.float32, device=DEV)
         ob = torch.empty_like(oa)
         se.se_decode_attend(va, G, q, kn, vn, npos, None, 0, 0.088, max_len, se.SE_ATTEND_ACCUMULATE, oa,
                             None, None, 0, ws, err)
-        se.se_evict_compact(va, B, w, max_len, fa, 32, ca, err)
-        se.se_decode_step_h2o(vb, G, q, kn, vn, npos, 0.088, B, w, max_len, ob, None, fb, 32, cb, ws, err)
+        se.se_evict_compact(va, B, w, max_len, fa, P, ca, err)
+        se.se_decode_step_h2o(vb, G, q, kn, vn, npos, 0.088, B, w, max_len, ob, None, fb, P, cb, ws, err)
         torch.cuda.synchronize()
         assert se.se_read_device_errors(err) == 0
         assert torch.equal(oa, ob)
