@@ -116,6 +116,14 @@ def test_quest_variants(se):
     assert same >= 0.9 * 12 * w.units_per_layer
 
 
+def test_largest_top_k(se):
+    # top_k = 4096 of 4200 candidate pages: the attention reads 4097 pages per
+    # unit, more than one work-group holds, so it is split and combined.
+    w = scaled(LAYER_QUEST, num_req=1, ctx=16 * 4200 + 5, top_k=4096, steps=2)
+    same, ties = _run_quest(se, w, 2)
+    assert same >= 0.9 * 2 * w.units_per_layer
+
+
 def test_select_all_pages_is_dense(se):
     # top_k >= number of pages: every page is read, so the step is dense attention.
     w = scaled(LAYER_QUEST, num_req=2, ctx=500, top_k=64, steps=2)
@@ -147,7 +155,8 @@ def test_select_all_pages_is_dense(se):
 
 
 @pytest.mark.parametrize("n_pages,top_k,levels", [(40, 8, 0), (40, 8, 3), (300, 64, 5), (2048, 64, 0),
-                                                  (2048, 64, 7), (10, 64, 0), (700, 1, 2), (513, 512, 4)])
+                                                  (2048, 64, 7), (10, 64, 0), (700, 1, 2), (513, 512, 4),
+                                                  (5000, 4096, 3), (4097, 4096, 0)])
 def test_select_from_given_scores_bitexact(se, n_pages, top_k, levels):
     # With the page scores given (the same float32 values on both sides) the
     # selection is exact, ties going to the lower page index.
