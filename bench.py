@@ -1037,7 +1037,6 @@ def main():
         dom_name = "se_decode_step_quest"
     # the call's average duration is the timed region over the calls in it
     dom_ms, dom_bytes = region_ms, first_bytes + second_bytes
-    other = {}
     n_launch = K * w.layers
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     traffic = read_traffic() if (w.index == 1 and w.method == "h2o") else None
@@ -1063,7 +1062,6 @@ def main():
                      "traffic": traffic, "avg_launch_us": round(1e3 * dom_ms / n_launch, 3),
                      "algorithmic_bytes_per_launch": round(dom_bytes / n_launch)},
         "step_GBps": round((first_bytes + second_bytes) / elapsed / 1e9, 1),
-        "kernels": other,
         "cpu_baseline": cpu,
     }
     if K > 1:
