@@ -1,10 +1,12 @@
-"""H2O path on the GPU against the oracle: se_decode_attend (append, attention,
-fused score update), se_accumulate_scores, se_evict_compact.
+"""H2O path on the GPU against the oracle: se_decode_step_h2o (append,
+attention, fused score update and eviction) over whole trajectories,
+se_decode_attend, se_accumulate_scores and se_evict_compact.
 
-Every input comes from the seeded generators in workloads/; the oracle reads
-them before any library call touches them.
+Every input comes from the seeded generators in workloads/.  Trajectories
+follow the step protocol of tests/protocol.py: the oracle takes each step from
+the GPU's pre-step state, and retention and compaction are compared bit for
+bit on the GPU's own fp32 scores.
 """
-import math
 
 import numpy as np
 import pytest
@@ -12,9 +14,10 @@ import torch
 
 from oracle import h2o
 from oracle.attention import selected_attention
-from tests.oracle_bridge import (LSE_ATOL, OUT_ATOL, assert_scores_close, f64, gpu_unit,
-                                 h2o_near_tie, oracle_unit)
-from workloads import LAYER_H2O, TINY_H2O, build_state, build_steps, clone_state, isolated_units, scaled, to_device
+from tests.oracle_bridge import assert_scores_close, f64, gpu_unit, oracle_unit
+from tests.protocol import h2o_trajectory
+from workloads import (LAYER_H2O, TINY_H2O, build_state, build_steps, clone_state, isolated_units, scaled, step_bounds,
+                       to_device)
 
 pytestmark = pytest.mark.gpu
 
@@ -33,107 +36,49 @@ def _view(se, st):
                      st.lengths, num_kv_heads=st.w.hkv)
 
 
-def _run_h2o(se, w, n_steps, check_every=1, units=None):
-    """Runs n_steps H2O decode steps on the GPU and the oracle side by side,
-    comparing outputs, lse, scores after accumulation, retained sets and the
-    compacted layout.  Returns (checked unit-steps, diverged units)."""
-    host = build_state(w, "cpu")
-    steps = build_steps(w, host, "cpu", steps=n_steps)
-    U = w.units_per_layer
-    units = list(range(U)) if units is None else units
-    ost = {u: oracle_unit(host, u) for u in units}
-    gs = to_device(host, DEV)
-    view = _view(se, gs)
-    max_len = host.max_pages * 16
-    dec = se.H2ODecoder(view, w.q_per_kv, w.scale, w.budget, w.recent, max_len, DEV, report_freed=True)
-    out = torch.empty((w.num_req, w.hq, w.head_dim), dtype=torch.float32, device=DEV)
-    lse = torch.empty((w.num_req, w.hq), dtype=torch.float32, device=DEV)
-    G = w.q_per_kv
-    diverged, checked = set(), 0
-    for t in range(n_steps):
-        q, kn, vn, npos = (steps.q[t, 0].to(DEV), steps.k_new[t, 0].to(DEV),
-                           steps.v_new[t, 0].to(DEV), steps.new_pos[t].to(DEV))
-        print(f"step {t}", flush=True)
-        dec.attend(q, kn, vn, npos, out, lse)
-        torch.cuda.synchronize()
-        pre = {u: gpu_unit(gs, u) for u in units if u not in diverged}
-        dec.evict()
-        torch.cuda.synchronize()
-        assert se.se_read_device_errors(dec.dev_err) == 0
-        o_gpu, lse_gpu = out.cpu().double().numpy(), lse.cpu().double().numpy()
-        fc = dec.freed_count.cpu().numpy()
-        fp = dec.freed.cpu().numpy()
-        bt = host.block_table.numpy()
-        for u in units:
-            if u in diverged:
-                continue
-            req, kvh = divmod(u, w.hkv)
-            rows = slice(kvh * G, (kvh + 1) * G)
-            st = ost[u]
-            L_old = st.length + 1
-            res = h2o.decode_step(st, f64(steps.q[t, 0, req, rows]), f64(steps.k_new[t, 0, req, kvh]),
-                                  f64(steps.v_new[t, 0, req, kvh]), int(steps.new_pos[t, req]),
-                                  w.scale, w.budget, w.recent)
-            err = np.abs(o_gpu[req, rows] - res["o"]).max()
-            assert err <= OUT_ATOL, f"step {t} unit {u}: output off by {err}"
-            assert np.abs(lse_gpu[req, rows] - res["lse"]).max() <= LSE_ATOL
-            g = pre[u]
-            np.testing.assert_array_equal(g["pos"], res["pos_after_append"])
-            assert_scores_close(g["u"], res["u_after_accumulate"], f"step {t} unit {u}")
-            after = gpu_unit(gs, u)
-            kept_g, kept_o = set(after["pos"].tolist()), set(st.pos.tolist())
-            if kept_g != kept_o:
-                ou = dict(zip(res["pos_after_append"].tolist(), res["u_after_accumulate"].tolist()))
-                assert h2o_near_tie(ou, kept_g, kept_o), f"step {t} unit {u}: retained sets differ"
-                diverged.add(u)
-                continue
-            np.testing.assert_array_equal(after["pos"], st.pos)
-            np.testing.assert_array_equal(after["K"], st.K)
-            np.testing.assert_array_equal(after["V"], st.V)
-            assert_scores_close(after["u"], st.u, f"step {t} unit {u} after compaction")
-            n_freed = len(res["freed"])
-            assert fc[u] == n_freed
-            np.testing.assert_array_equal(fp[u, :n_freed], bt[u, res["freed"]])
-            assert L_old - len(st.pos) == max(0, L_old - w.budget)
-            checked += 1
-    return checked, diverged
+def _run_h2o(se, w, n_steps):
+    """n_steps fused H2O steps (se_decode_step_h2o with the benchmark's per-step
+    max_len) on a device-generated workload, every unit checked against the
+    oracle at every step (tests/protocol.py).  Returns unit-steps checked."""
+    print(f"workload {w.name}: {w.units_per_layer} units, {n_steps} steps", flush=True)
+    gs = build_state(w, DEV)
+    steps = build_steps(w, gs, DEV, steps=n_steps)
+    bounds = step_bounds(w, gs.lengths.cpu().tolist(), n_steps)
+    checked, _ = h2o_trajectory(se, gs, steps, n_steps, {l: range(w.units_per_layer) for l in range(w.layers)},
+                                q_per_kv=w.q_per_kv, scale=w.scale, budget=w.budget, recent=w.recent,
+                                bounds=bounds, device=DEV)
+    return checked
 
 
 def test_tiny_h2o_step(se):
     w = TINY_H2O
-    checked, diverged = _run_h2o(se, w, 1)
-    assert checked == w.units_per_layer and not diverged
+    assert _run_h2o(se, w, 1) == w.units_per_layer
 
 
 def test_trajectory_8b_shape_scaled(se):
     # 4 requests of the 8B head shape, a ragged initial context (1000 = 62.5
     # pages), budget 256 with a 32-token window: the first step takes the
-    # radix path (1001 -> 256), the rest the steady one-slot path.
+    # general retention (1001 -> 256), the rest the steady one-slot path.
     w = scaled(LAYER_H2O, num_req=4, ctx=1000, budget=256, recent=32, steps=20)
-    checked, diverged = _run_h2o(se, w, 20)
-    assert len(diverged) <= w.units_per_layer // 4, diverged
-    assert checked >= 0.75 * 20 * w.units_per_layer
+    assert _run_h2o(se, w, 20) == 20 * w.units_per_layer
 
 
 def test_trajectory_small_window_long_run(se):
     # d=64, G=2, budget not a multiple of the page size, window of 3.
     w = scaled(TINY_H2O, num_req=3, hq=4, hkv=2, ctx=150, budget=100, recent=3, steps=40)
-    checked, diverged = _run_h2o(se, w, 40)
-    assert len(diverged) <= 2 and checked >= 0.75 * 40 * w.units_per_layer
+    assert _run_h2o(se, w, 40) == 40 * w.units_per_layer
 
 
 @pytest.mark.parametrize("G,d", [(1, 128), (2, 64), (4, 64)])
 def test_head_group_and_dim_variants(se, G, d):
     w = scaled(TINY_H2O, num_req=2, hq=2 * G, hkv=2, head_dim=d, ctx=300, budget=64, recent=16, steps=3)
-    checked, diverged = _run_h2o(se, w, 3)
-    assert not diverged and checked == 3 * w.units_per_layer
+    assert _run_h2o(se, w, 3) == 3 * w.units_per_layer
 
 
 def test_budget_covers_context_is_dense(se):
     # B >= L: TopK keeps everything (no eviction) and attention is dense.
     w = scaled(LAYER_H2O, num_req=2, ctx=200, budget=400, recent=8, steps=3)
-    checked, diverged = _run_h2o(se, w, 3)
-    assert not diverged and checked == 3 * w.units_per_layer
+    assert _run_h2o(se, w, 3) == 3 * w.units_per_layer
 
 
 def test_unfused_accumulate_matches_fused(se):

@@ -1,5 +1,6 @@
 """Quest path on the GPU against the oracle: se_quest_summarize,
-se_quest_select (bound + top-k) and se_decode_attend over the selected pages.
+se_quest_select (bound + top-k), se_decode_attend over the selected pages and
+se_decode_step_quest (both in one call).
 """
 import numpy as np
 import pytest
@@ -7,9 +8,9 @@ import torch
 
 from oracle import quest
 from oracle.attention import selected_attention
-from tests.oracle_bridge import (LSE_ATOL, OUT_ATOL, QUEST_RTOL, f64, gpu_unit, oracle_unit,
-                                 quest_near_tie)
-from workloads import LAYER_QUEST, build_state, build_steps, isolated_units, scaled, to_device
+from tests.oracle_bridge import OUT_ATOL, f64, oracle_unit
+from tests.protocol import quest_trajectory
+from workloads import LAYER_QUEST, build_state, build_steps, isolated_units, scaled, step_bounds, to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -28,100 +29,38 @@ def _view(se, st):
                      st.lengths, num_kv_heads=st.w.hkv)
 
 
-def _meta(gs, u, n_pages):
-    bt = gs.block_table[u, :n_pages].to(torch.int64)
-    m = gs.meta_pool[bt].cpu().to(torch.float64).numpy()   # [n_pages, 2, d]
-    return m[:, 0], m[:, 1]
-
-
 def _run_quest(se, w, n_steps):
-    """n_steps Quest decode steps on the GPU and the oracle; compares the
-    summaries, the page scores, the selection (exact, or a near-tie under the
-    oracle's scores) and, where the selections agree, the outputs."""
-    host = build_state(w, "cpu")
-    steps = build_steps(w, host, "cpu", steps=n_steps)
-    U, G = w.units_per_layer, w.q_per_kv
-    ost = {u: oracle_unit(host, u) for u in range(U)}
-    for st in ost.values():
-        quest.attach_summaries(st)
-    gs = to_device(host, DEV)
-    view = _view(se, gs)
-    max_len = host.max_pages * 16
-    dec = se.QuestDecoder(view, G, w.scale, w.top_k, max_len, DEV)
-    dec.summarize()
-    torch.cuda.synchronize()
-    for u in range(U):
-        mn, mx = _meta(gs, u, ost[u].mn.shape[0])
-        np.testing.assert_array_equal(mn, ost[u].mn)
-        np.testing.assert_array_equal(mx, ost[u].mx)
-    scores = torch.full((U, host.max_pages), float("nan"), dtype=torch.float32, device=DEV)
-    out = torch.empty((w.num_req, w.hq, w.head_dim), dtype=torch.float32, device=DEV)
-    lse = torch.empty((w.num_req, w.hq), dtype=torch.float32, device=DEV)
-    same = ties = 0
-    for t in range(n_steps):
-        print(f"step {t}", flush=True)
-        q = steps.q[t, 0].to(DEV)
-        dec.select(q, scores)
-        dec.attend(q, steps.k_new[t, 0].to(DEV), steps.v_new[t, 0].to(DEV), steps.new_pos[t].to(DEV), out, lse)
-        torch.cuda.synchronize()
-        assert se.se_read_device_errors(dec.dev_err) == 0
-        sel_g = dec.sel.cpu().numpy()
-        sc_g = scores.cpu().double().numpy()
-        o_g, lse_g = out.cpu().double().numpy(), lse.cpu().double().numpy()
-        for u in range(U):
-            req, kvh = divmod(u, w.hkv)
-            rows = slice(kvh * G, (kvh + 1) * G)
-            st = ost[u]
-            res = quest.decode_step(st, f64(steps.q[t, 0, req, rows]), f64(steps.k_new[t, 0, req, kvh]),
-                                    f64(steps.v_new[t, 0, req, kvh]), int(steps.new_pos[t, req]),
-                                    w.scale, w.top_k)
-            n = res["n_candidates"]
-            want = res["scores"]
-            err = np.abs(sc_g[u, :n] - want) / np.maximum(1.0, np.abs(want))
-            assert err.max() <= QUEST_RTOL, f"step {t} unit {u}: page score off by {err.max()}"
-            k = min(w.top_k, n)
-            assert (sel_g[u, k:] == -1).all()
-            got = sel_g[u, :k]
-            assert (np.diff(got) > 0).all(), "selection must be ascending"
-            if got.tolist() != res["selected"].tolist():
-                assert quest_near_tie(want, got, res["selected"]), f"step {t} unit {u}: selection differs"
-                ties += 1
-                continue
-            same += 1
-            assert np.abs(o_g[req, rows] - res["o"]).max() <= OUT_ATOL, f"step {t} unit {u}"
-            assert np.abs(lse_g[req, rows] - res["lse"]).max() <= LSE_ATOL
-        # the appended token and the summaries of its page
-        for u in range(U):
-            g = gpu_unit(gs, u)
-            np.testing.assert_array_equal(g["pos"], ost[u].pos)
-            np.testing.assert_array_equal(g["K"], ost[u].K)
-            mn, mx = _meta(gs, u, ost[u].mn.shape[0])
-            np.testing.assert_array_equal(mn, ost[u].mn)
-            np.testing.assert_array_equal(mx, ost[u].mx)
-    return same, ties
+    """n_steps Quest decode steps (se_decode_step_quest with the benchmark's
+    per-step max_len) on a device-generated workload, every unit checked at
+    every step by the protocol of tests/protocol.py: page scores, the
+    selection (exact on the GPU's fp32 scores), outputs over that selection,
+    the appended slot and its page's summary.  Returns unit-steps checked."""
+    gs = build_state(w, DEV)
+    steps = build_steps(w, gs, DEV, steps=n_steps)
+    bounds = step_bounds(w, gs.lengths.cpu().tolist(), n_steps)
+    n, _ = quest_trajectory(se, gs, steps, n_steps, range(w.units_per_layer), q_per_kv=w.q_per_kv,
+                            scale=w.scale, top_k=w.top_k, bounds=bounds, device=DEV)
+    return n
 
 
 def test_quest_trajectory_8b_shape_scaled(se):
     # 2 requests of the 8B head shape, 2000 tokens (125 pages), top-8 pages,
     # 20 steps crossing a page boundary (2000 + 16 tokens).
     w = scaled(LAYER_QUEST, num_req=2, ctx=2000, top_k=8, steps=20)
-    same, ties = _run_quest(se, w, 20)
-    assert same >= 0.9 * 20 * w.units_per_layer
+    assert _run_quest(se, w, 20) == 20 * w.units_per_layer
 
 
 def test_quest_variants(se):
     # d=64 with G=2, a partial current page, more pages wanted than exist.
     w = scaled(LAYER_QUEST, num_req=2, hq=4, hkv=2, head_dim=64, ctx=90, top_k=9, steps=12)
-    same, ties = _run_quest(se, w, 12)
-    assert same >= 0.9 * 12 * w.units_per_layer
+    assert _run_quest(se, w, 12) == 12 * w.units_per_layer
 
 
 def test_largest_top_k(se):
     # top_k = 4096 of 4200 candidate pages: the attention reads 4097 pages per
     # unit, more than one work-group holds, so it is split and combined.
     w = scaled(LAYER_QUEST, num_req=1, ctx=16 * 4200 + 5, top_k=4096, steps=2)
-    same, ties = _run_quest(se, w, 2)
-    assert same >= 0.9 * 2 * w.units_per_layer
+    assert _run_quest(se, w, 2) == 2 * w.units_per_layer
 
 
 def test_select_all_pages_is_dense(se):

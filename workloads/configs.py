@@ -121,3 +121,17 @@ PRUNE = Workload(8, "llama3-8b-32-layer-prune-interval", "prune", num_req=8, hq=
 def scaled(w: Workload, **changes) -> Workload:
     """A variant of a workload with some sizes changed (test cases)."""
     return replace(w, **changes)
+
+
+def step_bounds(w: Workload, lengths, n: int):
+    """Per-step upper bounds of any unit's resident slots after that step's
+    append, as a scheduler knows them from the lengths at the start: H2O
+    units grow by one per step up to the budget (then hold B + 1 after the
+    append), Quest units grow by one per step.  ``lengths`` holds the initial
+    resident slots of every unit (any integer sequence)."""
+    L = max(int(x) for x in lengths)
+    out = []
+    for _ in range(int(n)):
+        out.append(L + 1)
+        L = min(L + 1, int(w.budget)) if w.method == "h2o" else L + 1
+    return out

@@ -318,9 +318,11 @@ def isolated_units(lengths, max_pages: int, head_dim: int, seed: int, *, num_kv_
     """Units with given resident lengths for single-call tests.
 
     position_mode: "contiguous" (slot s has position s + offset), "shuffled"
-    (distinct random positions in random slot order, as compaction leaves them)
-    or "gapped" (sorted random distinct positions, so recent positions are not
-    contiguous).  score_levels > 0 draws scores from that many distinct values
+    (distinct random positions in random slot order, as compaction leaves them),
+    "gapped" (sorted random distinct positions, so recent positions are not
+    contiguous) or "permuted" (positions 0 .. L-1 in random slot order: a
+    contiguous recent run scattered over the slots, as steady-state eviction
+    leaves it).  score_levels > 0 draws scores from that many distinct values
     (many exact ties); 0 draws continuous uniform scores.  Scores are float32.
     """
     U = len(lengths)
@@ -341,6 +343,8 @@ def isolated_units(lengths, max_pages: int, head_dim: int, seed: int, *, num_kv_
             pos = torch.randperm(4 * L + 8, generator=g)[:L]
         elif position_mode == "gapped":
             pos = torch.sort(torch.randperm(4 * L + 8, generator=g)[:L]).values
+        elif position_mode == "permuted":
+            pos = torch.randperm(L, generator=g).to(torch.int64)
         else:
             raise ValueError(position_mode)
         s = torch.arange(L)
