@@ -212,6 +212,31 @@ se_status se_decode_step_h2o(const se_kv_view* kv, int32_t q_per_kv, const void*
                              hipStream_t stream);
 
 /*
+ * se_decode_step_h2o_noalloc — se_decode_step_h2o for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same step, bit for bit, with the
+ * workspace taken from a static device array of se_static_scratch_bytes()
+ * bytes (256 MiB) that the library holds on each GPU it runs on until the
+ * process ends.  The call allocates nothing; the first call on a device looks
+ * up that device's copy of the array.
+ *  Arguments as for se_decode_step_h2o without ws / ws_bytes.
+ *  Returns SE_ERR_WORKSPACE when se_workspace_bytes(SE_OP_DECODE_ATTEND,
+ *  num_units, max_len, max_pages, q_per_kv, head_dim, 0) exceeds the array
+ *  (for example 512 units of 32769 slots need 289 MB; a steady 4096-slot step
+ *  of 2048 units needs 147 MB).  Every call on one GPU shares the array, so
+ *  calls that may overlap on one GPU (different streams, or concurrent host
+ *  threads) race: serialize them.  The array needs no initial contents.
+ */
+se_status se_decode_step_h2o_noalloc(const se_kv_view* kv, int32_t q_per_kv, const void* q,
+                                     const void* k_new, const void* v_new, const int32_t* new_pos,
+                                     float scale, int32_t budget, int32_t recent, int32_t max_len,
+                                     float* out, float* lse, int32_t* freed_pages, int32_t freed_stride,
+                                     int32_t* freed_count, int32_t* dev_err, hipStream_t stream);
+
+/* Bytes of the static device array se_decode_step_h2o_noalloc uses. */
+size_t se_static_scratch_bytes(void);
+
+/*
  * se_quest_summarize — per-page key min/max for every resident page (Appendix A.3,
  * eq. background-quest-summary): for each unit and logical page b < ceil(L/16),
  * meta_pool[page][0][c] = min and [1][c] = max of k[c] over the page's slots < L.

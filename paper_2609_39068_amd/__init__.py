@@ -5,6 +5,7 @@ build script, the ctypes binding and the decode-step driver."""
 
 from ._binding import (  # noqa: F401
     EXPORTED, KVView, SparseEngineError, se_accumulate_scores, se_decode_attend, se_decode_step_h2o,
+    se_decode_step_h2o_noalloc, se_static_scratch_bytes,
     se_decode_step_quest, se_snapkv_compact, se_omnikv_select, se_attend_slots,
     se_h2o_prefill_chunk, se_prune_interval,
     se_evict_compact, se_quest_select, se_quest_summarize, se_read_device_errors,

@@ -43,7 +43,7 @@ EXPORTED = (
     "se_decode_attend", "se_decode_step_h2o", "se_decode_step_quest", "se_accumulate_scores", "se_evict_compact", "se_quest_summarize",
     "se_quest_select", "se_workspace_bytes", "se_read_device_errors", "se_status_string",
     "se_version", "se_snapkv_compact", "se_omnikv_select", "se_attend_slots", "se_h2o_prefill_chunk",
-    "se_prune_interval",
+    "se_prune_interval", "se_decode_step_h2o_noalloc", "se_static_scratch_bytes",
 )
 
 
@@ -81,6 +81,8 @@ def _load():
     sig = {
         "se_decode_attend": (I32, [V, I32, P, P, P, P, P, I32, F32, I32, U32, P, P, P, I32, P, SZ, P, P]),
         "se_decode_step_h2o": (I32, [V, I32, P, P, P, P, F32, I32, I32, I32, P, P, P, I32, P, P, SZ, P, P]),
+        "se_decode_step_h2o_noalloc": (I32, [V, I32, P, P, P, P, F32, I32, I32, I32, P, P, P, I32, P, P, P]),
+        "se_static_scratch_bytes": (SZ, []),
         "se_accumulate_scores": (I32, [V, I32, P, I32, P, I32, P, P]),
         "se_evict_compact": (I32, [V, I32, I32, I32, P, I32, P, P, P]),
         "se_quest_summarize": (I32, [V, I32, P, P]),
@@ -226,6 +228,34 @@ def se_decode_step_h2o(view: KVView, q_per_kv, q, k_new, v_new, new_pos, scale, 
         0 if ws is None else ws.numel() * ws.element_size(), _ptr(dev_err, torch.int32, "dev_err"),
         _stream(stream))
     _check("se_decode_step_h2o", st)
+
+
+def se_decode_step_h2o_noalloc(view: KVView, q_per_kv, q, k_new, v_new, new_pos, scale, budget, recent,
+                               max_len, out, lse, freed_pages, freed_stride, freed_count, dev_err, stream=None):
+    s = view.struct
+    nreq = s.num_units // s.num_kv_heads
+    hq = s.num_kv_heads * q_per_kv
+    _need(q, nreq * hq * s.head_dim, "q")
+    _need(out, nreq * hq * s.head_dim, "out")
+    _need(lse, nreq * hq, "lse")
+    _need(k_new, s.num_units * s.head_dim, "k_new")
+    _need(v_new, s.num_units * s.head_dim, "v_new")
+    _need(new_pos, nreq, "new_pos")
+    if freed_pages is not None:
+        _need(freed_pages, s.num_units * int(freed_stride), "freed_pages")
+    _need(freed_count, s.num_units, "freed_count")
+    st = _lib.se_decode_step_h2o_noalloc(
+        view.ref(), q_per_kv, _ptr(q, torch.bfloat16, "q"), _ptr(k_new, torch.bfloat16, "k_new"),
+        _ptr(v_new, torch.bfloat16, "v_new"), _ptr(new_pos, torch.int32, "new_pos"), float(scale),
+        int(budget), int(recent), int(max_len), _ptr(out, torch.float32, "out"),
+        _ptr(lse, torch.float32, "lse"), _ptr(freed_pages, torch.int32, "freed_pages"),
+        int(freed_stride), _ptr(freed_count, torch.int32, "freed_count"), _ptr(dev_err, torch.int32, "dev_err"),
+        _stream(stream))
+    _check("se_decode_step_h2o_noalloc", st)
+
+
+def se_static_scratch_bytes() -> int:
+    return int(_lib.se_static_scratch_bytes())
 
 
 def se_accumulate_scores(view: KVView, q_per_kv, logits, logits_stride, lse, max_len, dev_err,

@@ -30,6 +30,8 @@
 // boundary orders the two passes across XCDs (each XCD has its own L2), which
 // avoids a device-scope release/acquire (an L2 writeback and invalidate) in
 // every work-group.
+#include <mutex>
+
 #include "evict_core.h"
 #include "quest_core.h"
 
@@ -1392,6 +1394,53 @@ extern "C" se_status se_decode_step_h2o(const se_kv_view* kv, int32_t q_per_kv, 
                                SE_ATTEND_ACCUMULATE, out, lse, nullptr, 0, ws, ws_bytes, dev_err,
                                stream, &ev);
   return st;
+}
+
+// ---- se_decode_step_h2o_noalloc: the same step with the workspace in a
+// file-scope device array instead of a caller's buffer.  In host code the
+// array's name is only a stand-in for the symbol: its device address (one per
+// GPU, since every device loads its own copy of the code object) is looked up
+// once per device with hipGetSymbolAddress and kept here.
+constexpr size_t kStaticScratchBytes = size_t(256) << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxScratchDevices] = {};
+
+se_status static_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return SE_ERR_HIP;
+  if (dev < 0 || dev >= kMaxScratchDevices) return SE_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch[dev] == nullptr) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return SE_ERR_HIP;
+    g_scratch[dev] = ptr;
+  }
+  *out = g_scratch[dev];
+  return SE_OK;
+}
+}  // namespace
+
+extern "C" size_t se_static_scratch_bytes(void) { return kStaticScratchBytes; }
+
+extern "C" se_status se_decode_step_h2o_noalloc(const se_kv_view* kv, int32_t q_per_kv, const void* q,
+                                                const void* k_new, const void* v_new, const int32_t* new_pos,
+                                                float scale, int32_t budget, int32_t recent, int32_t max_len,
+                                                float* out, float* lse, int32_t* freed_pages, int32_t freed_stride,
+                                                int32_t* freed_count, int32_t* dev_err, hipStream_t stream) {
+  se_status st = check_view(kv);
+  if (st != SE_OK) return st;
+  if (max_len <= 0) return SE_ERR_INVALID_ARGUMENT;
+  const size_t need = se_attend_workspace_bytes(kv->num_units, max_len, kv->max_pages, q_per_kv, kv->head_dim, 0);
+  if (need > kStaticScratchBytes) return SE_ERR_WORKSPACE;
+  void* ws = nullptr;
+  st = static_scratch(&ws);
+  if (st != SE_OK) return st;
+  return se_decode_step_h2o(kv, q_per_kv, q, k_new, v_new, new_pos, scale, budget, recent, max_len, out, lse,
+                            freed_pages, freed_stride, freed_count, ws, kStaticScratchBytes, dev_err, stream);
 }
 
 size_t se_quest_step_workspace_bytes(int32_t num_units, int32_t max_len, int32_t max_pages, int32_t q_per_kv,

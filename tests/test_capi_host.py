@@ -19,7 +19,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 16, names
+    assert len(names) == 18, names
     lib = b.raw_library()
     for n in names:
         assert hasattr(lib, n), f"{n} is declared in sparse_engine.h but not exported"
@@ -101,6 +101,21 @@ def test_evict_and_quest_argument_checks():
               None, 0x9000, 1 << 30, 0xA000, None) == b.SE_ERR_INVALID_ARGUMENT        # top_k 0
     assert sq(ctypes.byref(v), 4, 0x7000, None, None, None, 0.1, 8, 128, 0x100, 0x8000,
               None, None, 0, 0xA000, None) == b.SE_ERR_WORKSPACE
+
+
+def test_noalloc_step_argument_checks():
+    # refused on the host before any device call: a bad view, a bad bound, and a
+    # size whose workspace exceeds the static array (512 units x 2049 pages)
+    na = b.raw_library().se_decode_step_h2o_noalloc
+
+    def call(view, max_len=128):
+        return na(ctypes.byref(view), 4, 0x7000, 0x100, 0x200, 0x300, 0.1, 64, 8, max_len, 0x8000, None, None, 0,
+                  None, 0xA000, None)
+
+    assert b.raw_library().se_static_scratch_bytes() == 256 << 20
+    assert call(_view(page_size=8)) == b.SE_ERR_UNSUPPORTED
+    assert call(_view(), max_len=0) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(_view(num_units=512, num_kv_heads=8, max_pages=2049), max_len=2049 * 16) == b.SE_ERR_WORKSPACE
 
 
 def test_snapkv_argument_checks():
