@@ -1,37 +1,43 @@
 #!/usr/bin/env python3
 """Decode attention + eviction benchmark on one MI355X.
 
-Default workload: the Llama-3-8B-shaped single layer with H2O (64 requests,
-Hq=32, Hkv=8, d=128, 32768-token contexts, budget 2048 with a 256-token
-window, 256 decode steps).  One timed step is one decode step of the whole
-batch through the hot path: se_decode_attend (append, split-K attention,
-fused score update) then se_evict_compact (retention + compaction).  The
-first step evicts 32769 -> 2048 per head; later steps evict one slot.
+Default workload (the headline): the 32-layer Llama-3-8B-shaped H2O decode loop
+(256 requests, Hq=32, Hkv=8, d=128, 4096 retained tokens per KV head and layer
+of a 131072-token context, budget 4096 with a 512-token window; ~137 GB of KV
+resident in HBM).  One timed step is one decode step of the whole batch
+through all 32 layers: one se_decode_step_h2o call per layer (append,
+attention, fused score update and one-slot eviction in one launch).  `value`
+is requests x steps / wall time between device synchronisations; `roofline`
+is the dominant kernel's algorithmic bytes per launch over its average launch
+time (HIP events around the timed region, on the launch stream).  The
+single-layer 8B-shaped workloads (H2O layer, Quest layer, ragged batch) run
+after it with the same step counts and are reported under `other_configs`.
 
-Protocol: the state is generated on the device (seeded), warm-up steps run on
-a copy that is then dropped, and the K timed steps start from the generated
-state with every input already resident in HBM.  The timed region is
-bracketed by device synchronisations; per-call HIP events on the launch
-stream give each kernel's duration for the roofline figure.
+Protocol: the state is generated on the device (seeded); warm-up steps run on
+a copy of a single-layer state (then dropped) or, for the 32-layer state, on
+the state itself; the K timed steps then start with every input resident in
+HBM, with the per-step length bound a scheduler knows (workloads.step_bounds).
+`cpu_baseline` is the oracle on 64 units of the headline workload, timed on
+the host before the GPU is touched and extrapolated to the whole batch.
 
-Prints one JSON line.  `--config N` runs another workload (0..4) for
-measurement; `--workload omnikv` measures OmniKV decode over a 32-layer
-8B-shaped model (32 requests, 32768-token histories, observation layers 0, 2,
-7, 13, 16, 26 attend densely and select 2048 slots that the other layers read;
-one step is one decode step through all 32 layers); `--workload snapkv`
-measures SnapKV prompt compaction instead
-(se_snapkv_compact on the 8B-shaped prompt: 64 requests x 8 KV heads x 32768
-slots, window 32, pooling width 7, budget 2048; one step is one compaction of
-the whole batch from a fresh copy of the prompt); `--workload h2o_prefill`
-measures H2O's chunk-wise prefill eviction (se_h2o_prefill_chunk after the
-fourth 8192-token chunk of 32768-token prompts, 8 requests x 8 KV heads, 2048
-retained + 8192 chunk slots scored by the chunk's last 128 queries of every
-head and cut back to 2048 with a 1024-token window; one step is one call from
-a fresh copy of that state); `--workload prune` measures interval prefix-cache
-pruning (se_prune_interval over 8 chains x 32 layers x 8 KV heads of 32768
-resident slots: the interval [16384, 20480) cut to its 819 best-scored slots
-per unit and the later slots closed up; one step is one call from a fresh copy
-of the cache); `--gpus N` with N > 1 is refused (single-GPU build).
+Prints one JSON line.  `--config N` makes workload N (0..4) the headline;
+`--workload omnikv` measures OmniKV decode over a 32-layer 8B-shaped model (32
+requests, 32768-token histories, observation layers 0, 2, 7, 13, 16, 26
+attend densely and select 2048 slots that the other layers read; one step is
+one decode step through all 32 layers); `--workload snapkv` measures SnapKV
+prompt compaction (se_snapkv_compact on the 8B-shaped prompt: 64 requests x 8
+KV heads x 32768 slots, window 32, pooling width 7, budget 2048; one step is
+one compaction of the whole batch from a fresh copy of the prompt);
+`--workload h2o_prefill` measures H2O's chunk-wise prefill eviction
+(se_h2o_prefill_chunk after the fourth 8192-token chunk of 32768-token
+prompts, 8 requests x 8 KV heads, 2048 retained + 8192 chunk slots scored by
+the chunk's last 128 queries of every head and cut back to 2048 with a
+1024-token window; one step is one call from a fresh copy of that state);
+`--workload prune` measures interval prefix-cache pruning (se_prune_interval
+over 8 chains x 32 layers x 8 KV heads of 32768 resident slots: the interval
+[16384, 20480) cut to its 819 best-scored slots per unit and the later slots
+closed up; one step is one call from a fresh copy of the cache); `--gpus N`
+with N > 1 is refused (single-GPU build).
 """
 
 import argparse
@@ -60,9 +66,12 @@ PREFILL_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "h2o_prefill_chunk_llam
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=None, help="timed decode steps (default: the workload's)")
-    ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default 8; snapkv: 1)")
-    ap.add_argument("--config", type=int, default=1, help="workload index 0..4")
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed decode steps (default: 20 for the 32-layer workload, else the workload's)")
+    ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default 5; snapkv and prefill: 1)")
+    ap.add_argument("--config", type=int, default=4, help="decode workload index 0..4 (default 4, the headline)")
+    ap.add_argument("--only", action="store_true",
+                    help="with --config 4: skip the single-layer workloads 1-3 reported under other_configs")
     ap.add_argument("--workload", choices=["decode", "snapkv", "omnikv", "h2o_prefill", "prune"], default="decode",
                     help="decode (the --config workload), snapkv (prompt compaction), omnikv "
                          "(32-layer decode with OmniKV selection reuse), h2o_prefill (chunk-wise "
@@ -98,18 +107,22 @@ def _oracle_unit_run(i):
 
 
 _SHARED = {}
+CPU_SAMPLE_UNITS = 64
 
 
 def cpu_baseline(w, K):
-    """The oracle, untuned, on a bounded sample of the same workload: the
-    first six requests (all their KV heads, one layer) for the same K steps,
-    one unit per worker process.  Runs before the GPU is touched; the workers
-    are forked after every input has been converted to NumPy."""
+    """The oracle, untuned, on a bounded sample of the workload: 64 units of
+    one layer (the first 64 // Hkv requests, every KV head, the workload's
+    per-unit shapes and value recipe) for the same K decode steps, one unit per
+    worker process, before the GPU is touched.  Units are independent, so the
+    whole step extrapolates linearly: the mean CPU time per unit-step times the
+    workload's units per layer and layers, spread over the worker processes,
+    gives the oracle's full-batch step time; value = requests / that time."""
     import multiprocessing as mp
     import numpy as np
     import torch
     from workloads import build_state, build_steps, scaled, unit_slots
-    sample_req = 6
+    sample_req = max(1, CPU_SAMPLE_UNITS // w.hkv)
     ws = scaled(w, num_req=sample_req, layers=1)
     host = build_state(ws, "cpu")
     steps = build_steps(ws, host, "cpu", steps=K)
@@ -133,53 +146,59 @@ def cpu_baseline(w, K):
     with ctx.Pool(workers) as pool:
         per_unit = pool.map(_oracle_unit_run, range(len(jobs)))
     wall = time.perf_counter() - t0
-    return {"value": round(sample_req * K / wall, 2), "unit": "tokens/s", "cores": workers, "kind": "oracle",
-            "sample": (f"{sample_req} of {w.num_req} requests ({len(jobs)} KV-head units, 1 layer) of "
-                       f"'{w.name}', {K} decode steps each, NumPy float64, one unit per process"),
+    unit_step_s = sum(per_unit) / (len(jobs) * K)
+    step_s = unit_step_s * w.units_per_layer * w.layers / workers
+    return {"value": round(w.num_req / step_s, 3), "unit": "tokens/s", "cores": workers, "kind": "oracle",
+            "sample": (f"{len(jobs)} units (requests 0..{sample_req - 1}, all {ws.hkv} KV heads, one layer) of "
+                       f"'{w.name}' for {K} decode steps each, NumPy float64, one unit per process; "
+                       f"{1e3 * unit_step_s:.2f} ms per unit-step, extrapolated to {w.units_per_layer} units x "
+                       f"{w.layers} layers on {workers} processes = {step_s:.3f} s per step of {w.num_req} requests"),
+            "per_unit_step_ms": round(1e3 * unit_step_s, 3),
             "cpu_seconds": round(sum(per_unit), 2), "wall_seconds": round(wall, 2)}
 
 
 # --------------------------------------------------------------------- algorithmic bytes
 
-def attend_bytes(lengths_post, G, D, append=True):
-    """Bytes se_decode_attend must move for one call (H2O, every slot read):
-    per slot the K and V rows plus the score read and write; per unit the G
-    query rows (bf16), the G output rows (fp32) and G lse values, and the
-    appended token (k, v read; k, v, position, score written)."""
-    slots = int(lengths_post.sum())
-    units = int(lengths_post.shape[0])
-    per_slot = 2 * D * 2 + 8
-    per_unit = G * D * 2 + G * D * 4 + G * 4 + (2 * D * 2 * 2 + 8 if append else 0)
-    return slots * per_slot + units * per_unit
-
-
-def evict_bytes(lengths_post, budget, D):
-    """Bytes se_evict_compact must move: every resident slot's score and
-    position once, and each moved slot's K and V rows, position and score
-    read and written (the steady state moves at most one slot)."""
+def h2o_step_bytes(L_pre, budget, G, D, moves):
+    """Bytes one se_decode_step_h2o call must move for units holding L_pre
+    slots before the step: every slot's K and V rows and its score read and
+    written, plus its position where the unit evicts (L_pre + 1 > budget);
+    per unit the G query rows (bf16), the G output rows (fp32) and the append
+    (k, v read; k, v, position and score written); each moved slot's K, V,
+    position and score read and written (``moves`` per unit)."""
     import numpy as np
-    L = lengths_post
-    over = L > budget
-    reads = int((L[over]).sum()) * 8
-    moved = np.minimum(np.maximum(L - budget, 0), budget)   # upper bound of movers per unit
-    per_move = 2 * (2 * D * 2 + 8)
-    return reads + int(moved[over].sum()) * per_move
+    Lp = np.asarray(L_pre, dtype=np.int64) + 1
+    ev = Lp > budget
+    per_unit = G * D * 2 + G * D * 4 + 2 * D * 2 * 2 + 8
+    move = 2 * (2 * D * 2 + 8)
+    slots = int(Lp.sum()) * (2 * D * 2 + 8) + int(Lp[ev].sum()) * 4
+    return slots + Lp.shape[0] * per_unit + int(np.asarray(moves).sum()) * move
 
 
-def select_bytes(n_cand, G, D, top_k):
-    """se_quest_select: every candidate page's min and max rows, its score
-    written and read back, the G query rows, the top_k selected ids."""
-    units = int(n_cand.shape[0])
-    return int(n_cand.sum()) * (2 * D * 2 + 8) + units * (G * D * 2 + top_k * 4)
+def quest_step_bytes(L_pre, G, D, top_k):
+    """Bytes one se_decode_step_quest call must move for units holding L_pre
+    slots before the step: the min and max rows of every candidate page (the
+    complete pages before the current one), the K and V rows of the top_k
+    selected pages and of the current page's resident slots, the G query rows,
+    the G output rows, the append (k, v read; k, v and position written; the
+    current page's min and max read and written) and the selection written."""
+    import numpy as np
+    L = np.asarray(L_pre, dtype=np.int64)
+    n_cand = L // 16
+    visited = np.minimum(n_cand, top_k) * 16 + (L % 16 + 1)
+    per_unit = G * D * 2 + G * D * 4 + 2 * D * 2 * 2 + 4 + 2 * (2 * D * 2) + top_k * 4
+    return int(n_cand.sum()) * (2 * D * 2) + int(visited.sum()) * (2 * D * 2) + L.shape[0] * per_unit
 
 
-def quest_attend_bytes(visited, G, D, top_k):
-    """se_decode_attend over a selection: the visited slots' K and V rows; per
-    unit the query, output, appended token (with its page's min/max read and
-    written) and the selected page ids."""
-    units = int(visited.shape[0])
-    per_unit = G * D * 2 + G * D * 4 + 2 * D * 2 * 2 + 8 + 2 * (2 * D * 2) + top_k * 4
-    return int(visited.sum()) * (2 * D * 2) + units * per_unit
+def attend_kernel_name(units, n_visit, G, D):
+    """The decode_attend_kernel instantiation a launch of these sizes runs (the
+    library's rule: 1024 threads when the units fit one work-group per compute
+    unit, else 512; per-wavefront rows for the fused steady eviction when the
+    largest wavefront slot's share of the pages fits them)."""
+    wide = units * -(-n_visit // 1024) <= 256
+    nt = 1024 if wide else 512
+    rows = (4 * 4 * 5 * 100 - 50) // (34 if wide else 58)
+    return f"decode_attend_kernel<{D},{G},{nt},{'true' if n_visit <= rows else 'false'}>"
 
 
 def snapkv_bytes(L, w, G, D, budget):
@@ -857,9 +876,9 @@ def source_hash(files=DECODE_SOURCES):
     return h.hexdigest()[:16]
 
 
-def read_traffic(path=TRAFFIC_SUMMARY, files=DECODE_SOURCES):
-    """HBM bytes per call from a committed rocprofv3 counter summary, or None
-    when it is missing or the kernels have changed since it was taken."""
+def read_summary(path, files=DECODE_SOURCES):
+    """The numeric fields of a committed rocprofv3 counter summary, or None when
+    it is missing or the kernels have changed since it was taken."""
     if not os.path.exists(path):
         return None
     vals = {}
@@ -869,13 +888,210 @@ def read_traffic(path=TRAFFIC_SUMMARY, files=DECODE_SOURCES):
             vals[k.strip()] = v.strip()
     if vals.get("source_hash") != source_hash(files):
         return None
-    try:
-        return float(vals["hbm_bytes_per_launch"])
-    except (KeyError, ValueError):
-        return None
+    out = {}
+    for k, v in vals.items():
+        try:
+            out[k] = float(v)
+        except ValueError:
+            pass
+    return out
+
+
+def read_traffic(path=TRAFFIC_SUMMARY, files=DECODE_SOURCES):
+    """HBM bytes per call from a committed counter summary (or None)."""
+    vals = read_summary(path, files)
+    return None if vals is None else vals.get("hbm_bytes_per_launch")
+
+
+def decode_traffic_path(w):
+    return os.path.join(ROOT, "profiles", f"decode_step_{w.method}_{w.name}_traffic.txt")
+
+
+def split_count(units, n_visit):
+    """Work-groups per unit of a decode launch (the library's split rule)."""
+    wide = units * -(-n_visit // 1024) <= 256
+    resident = 256 if wide else 512
+    splits = min(-(-resident // units), -(-n_visit // 16))
+    splits = max(splits, 1, -(-n_visit // 1024))
+    pps = -(-n_visit // splits)
+    return -(-n_visit // pps)
 
 
 # --------------------------------------------------------------------- GPU run
+
+def slot_positions(st, n):
+    """int32 [units, n]: the positions of every unit's slots [0, n)."""
+    import torch
+    s = torch.arange(n, device=st.block_table.device)
+    page = st.block_table[:, :(n + 15) // 16].to(torch.int64)[:, s // 16]
+    return st.pos_pool[page, (s % 16)[None, :].expand_as(page)]
+
+
+def run_decode(w, K, W, se, dev):
+    """K timed decode steps of workload w (every layer, one call per layer and
+    step) after W warm-up steps; returns the measurement (no tensors)."""
+    import numpy as np
+    import torch
+    from workloads import build_state, build_steps, clone_state, step_bounds
+
+    t_gen = time.perf_counter()
+    state = build_state(w, dev)
+    keep_going = w.layers > 1          # too large to copy: warm up on the state itself
+    n_inputs = K + W if keep_going else max(K, W, 1)
+    steps = build_steps(w, state, dev, steps=n_inputs)
+    torch.cuda.synchronize()
+    print(f"generated '{w.name}' in {time.perf_counter() - t_gen:.1f}s", file=sys.stderr, flush=True)
+
+    U, G, D = w.units_per_layer, w.q_per_kv, w.head_dim
+    max_len = state.max_pages * 16
+    out = torch.empty((w.num_req, w.hq, D), dtype=torch.float32, device=dev)
+
+    def make(st):
+        views = [se.KVView(st.kv_pool, st.pos_pool, st.score_pool, st.meta_pool,
+                           st.block_table[st.layer_rows(l)], st.lengths[st.layer_rows(l)],
+                           num_kv_heads=w.hkv) for l in range(w.layers)]
+        if w.method == "h2o":
+            ws = se.H2ODecoder.workspace(views[0], G, max_len, dev)
+            err = torch.zeros(1, dtype=torch.int32, device=dev)
+            return [se.H2ODecoder(v, G, w.scale, w.budget, w.recent, max_len, dev, ws=ws, dev_err=err)
+                    for v in views]
+        decs = [se.QuestDecoder(v, G, w.scale, w.top_k, max_len, dev) for v in views]
+        for d in decs:
+            d.summarize()
+        return decs
+
+    def run(decs, t0, t1, bounds, span=None):
+        """One call per layer and step (se_decode_step_h2o / se_decode_step_quest)
+        with the step's length bound.  span: events before the first step, after
+        it and after the last (an event costs a few microseconds of GPU time, so
+        calls are not bracketed one by one)."""
+        for t in range(t0, t1):
+            ml = bounds[t - t0]
+            if span is not None and t == t0:
+                span[0].record()
+            for l, d in enumerate(decs):
+                d.step(steps.q[t, l], steps.k_new[t, l], steps.v_new[t, l], steps.new_pos[t], out, max_len=ml)
+            if span is not None:
+                if t == t0:
+                    span[1].record()
+                if t == t1 - 1:
+                    span[2].record()
+
+    host_len = state.lengths.cpu().numpy().astype(np.int64)
+    # the first step is not the steady one when a unit holds more than B + 1
+    # slots after its append: count the slots it moves (the compaction's
+    # movers) on the warm-up copy, which takes the same step on the same inputs
+    first_general = w.method == "h2o" and int(host_len.max()) + 1 > w.budget + 1
+    moves1 = None
+    t_base = 0
+    if keep_going:
+        if first_general:
+            raise SystemExit("bench.py: a multi-layer workload must start in the steady state")
+        decs = make(state)
+        if W > 0:
+            run(decs, 0, W, step_bounds(w, host_len, W))
+            t_base = W
+    else:
+        scratch = clone_state(state)
+        sdecs = make(scratch)
+        bw = step_bounds(w, host_len, max(W, 1))
+        if first_general:
+            before = slot_positions(scratch, w.budget)
+            run(sdecs, 0, 1, bw[:1])
+            after = slot_positions(scratch, w.budget)
+            moves1 = (before != after).sum(dim=1).cpu().numpy() * (host_len + 1 > w.budget)
+            run(sdecs, 1, W, bw[1:])
+        else:
+            run(sdecs, 0, W, bw)
+        torch.cuda.synchronize()
+        del scratch, sdecs
+        torch.cuda.empty_cache()
+        decs = make(state)
+    torch.cuda.synchronize()
+    lengths0 = state.lengths.cpu().numpy().astype(np.int64).reshape(w.layers, U)
+    bounds = step_bounds(w, lengths0.reshape(-1), K)
+
+    span = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(decs, t_base, t_base + K, bounds, span)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    errs = se.se_read_device_errors(decs[0].dev_err)
+    if errs:
+        raise RuntimeError(f"device error bits {errs:#x} during the timed run")
+    step1_ms = span[0].elapsed_time(span[1])
+    region_ms = span[0].elapsed_time(span[2])
+
+    # algorithmic bytes per step (lengths follow the method's rule on the host)
+    L = lengths0.copy()
+    step_bytes = []
+    for t in range(K):
+        b = 0
+        for l in range(w.layers):
+            if w.method == "h2o":
+                # a steady step moves one slot per evicting unit (the newest slot,
+                # always in the window, fills the victim's)
+                mv = moves1 if (t == 0 and moves1 is not None) else (L[l] + 1 > w.budget).astype(np.int64)
+                b += h2o_step_bytes(L[l], w.budget, G, D, mv)
+                L[l] = np.minimum(L[l] + 1, w.budget)
+            else:
+                b += quest_step_bytes(L[l], G, D, w.top_k)
+                L[l] = L[l] + 1
+        step_bytes.append(b)
+
+    def n_visit_of(ml):
+        return w.top_k + 1 if w.method == "quest" else -(-min(ml, max_len) // 16)
+
+    def kernels(ml):
+        nv = n_visit_of(ml)
+        name = attend_kernel_name(U, nv, G, D)
+        if w.method == "quest":
+            return name + " (page bounds, top-k and attention)"
+        ns = split_count(U, nv)
+        if ns > 1:
+            return f"{name} x {ns} work-groups per unit + decode_combine_kernel + evict_compact_kernel"
+        return name + " (score update and eviction in the epilogue)"
+
+    calls = w.layers
+    traffic = read_summary(decode_traffic_path(w))
+    phases = {}
+    if moves1 is not None and K > 1:
+        steady_ms = region_ms - step1_ms
+        sb = sum(step_bytes[1:])
+        phases["step1"] = {"kernels": kernels(bounds[0]), "ms": round(step1_ms, 4),
+                           "algorithmic_bytes_per_launch": step_bytes[0] // calls,
+                           "moved_slots": int(moves1.sum()),
+                           "GBps": round(step_bytes[0] / (step1_ms * 1e-3) / 1e9, 1),
+                           "traffic": None if traffic is None else traffic.get("hbm_bytes_step1")}
+        phases["steady"] = {"kernels": kernels(bounds[1]), "ms_per_step": round(steady_ms / (K - 1), 4),
+                            "algorithmic_bytes_per_launch": round(sb / ((K - 1) * calls)),
+                            "GBps": round(sb / (steady_ms * 1e-3) / 1e9, 1),
+                            "traffic": None if traffic is None else traffic.get("hbm_bytes_steady")}
+        dom_ms, dom_bytes, dom_launches, dom_ml = steady_ms, sb, (K - 1) * calls, bounds[1]
+    else:
+        dom_ms, dom_bytes, dom_launches, dom_ml = region_ms, sum(step_bytes), K * calls, bounds[0]
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    roof = {"bound": "hbm", "kernel": attend_kernel_name(U, n_visit_of(dom_ml), G, D),
+            "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None if traffic is None else traffic.get("hbm_bytes_steady"),
+            "avg_launch_us": round(1e3 * dom_ms / dom_launches, 3),
+            "algorithmic_bytes_per_launch": round(dom_bytes / dom_launches),
+            "launches": dom_launches,
+            "window": "steady steps 2..K" if moves1 is not None and K > 1 else "all timed steps"}
+    return {"w": w, "value": w.num_req * K / elapsed, "ms_per_step": 1e3 * elapsed / K, "region_ms": region_ms,
+            "roofline": roof, "phases": phases, "step_GBps": round(sum(step_bytes) / elapsed / 1e9, 1)}
+
+
+def config_fields(w):
+    return {"workload": w.name, "method": w.method, "batch": w.num_req, "hq": w.hq, "hkv": w.hkv,
+            "head_dim": w.head_dim, "page_size": w.page_size, "layers": w.layers,
+            "context": w.ctx if w.ctx is not None else list(w.ctx_log_range),
+            "resident": w.initial_resident if w.initial_resident is not None else w.retained_range,
+            "budget": w.budget, "recent": w.recent, "top_k": w.top_k, "accumulate": "f32",
+            "parallelism": "none (1 GPU)"}
+
 
 def main():
     args = parse()
@@ -898,177 +1114,59 @@ def main():
         return
     from workloads import CONFIGS
     w = CONFIGS[args.config]
-    K = int(args.steps if args.steps is not None else w.steps)
-    W = int(args.warmup if args.warmup is not None else 8)
+    K = int(args.steps if args.steps is not None else (20 if w.layers > 1 else w.steps))
+    W = int(args.warmup if args.warmup is not None else 5)
+    if w.layers > 1 and K + W > w.steps:
+        raise SystemExit(f"bench.py: --steps + --warmup must be at most {w.steps} for '{w.name}'")
 
     cpu = None
     if args.cpu_baseline == "auto":
         cpu = cpu_baseline(w, K)
-        print(f"cpu baseline: {cpu['value']:.1f} tokens/s on {cpu['cores']} processes", file=sys.stderr, flush=True)
+        print(f"cpu baseline: {cpu['value']:.3f} tokens/s on {cpu['cores']} processes", file=sys.stderr,
+              flush=True)
 
-    import numpy as np
     import torch
     import paper_2609_39068_amd as se
-    from workloads import build_state, build_steps, clone_state
 
     assert torch.cuda.is_available(), "bench.py needs the GPU"
     dev = torch.device("cuda:0")
-    t_gen = time.perf_counter()
-    state = build_state(w, dev)
-    keep_going = w.layers > 1          # too large to copy: warm up on the state itself
-    n_inputs = K + (W if keep_going else max(W, 0))
-    steps = build_steps(w, state, dev, steps=max(n_inputs, 1))
-    torch.cuda.synchronize()
-    print(f"generated '{w.name}' in {time.perf_counter() - t_gen:.1f}s", file=sys.stderr, flush=True)
-
-    U, G, D = w.units_per_layer, w.q_per_kv, w.head_dim
-    max_len = state.max_pages * 16
-    out = torch.empty((w.num_req, w.hq, D), dtype=torch.float32, device=dev)
-
-    def make(st):
-        views = [se.KVView(st.kv_pool, st.pos_pool, st.score_pool, st.meta_pool,
-                           st.block_table[st.layer_rows(l)], st.lengths[st.layer_rows(l)],
-                           num_kv_heads=w.hkv) for l in range(w.layers)]
-        if w.method == "h2o":
-            ws = se.H2ODecoder.workspace(views[0], G, max_len, dev)
-            err = torch.zeros(1, dtype=torch.int32, device=dev)
-            return [se.H2ODecoder(v, G, w.scale, w.budget, w.recent, max_len, dev, ws=ws, dev_err=err)
-                    for v in views]
-        decs = [se.QuestDecoder(v, G, w.scale, w.top_k, max_len, dev) for v in views]
-        for d in decs:
-            d.summarize()
-        return decs
-
-    def step_bounds(lengths, n):
-        """Per-step upper bounds of the resident slots after the append, as a
-        scheduler knows them (H2O: min(L + 1, B + 1); Quest: L + 1)."""
-        L = lengths.astype(np.int64).copy()
-        out_ = []
-        for _ in range(n):
-            out_.append(int(L.max()) + 1)
-            L = np.minimum(L + 1, w.budget) if w.method == "h2o" else L + 1
-        return out_
-
-    def run(decs, t0, t1, bounds, events=None):
-        """One call per layer and step (se_decode_step_h2o / se_decode_step_quest).
-        events: before the first step, after it, after the last (an event costs a
-        few microseconds of GPU time, so calls are not bracketed one by one)."""
-        for t in range(t0, t1):
-            ml = bounds[t - t0]
-            if events is not None and t == t0:
-                events["span"][0].record()
-            for l, d in enumerate(decs):
-                q, kn, vn, npos = steps.q[t, l], steps.k_new[t, l], steps.v_new[t, l], steps.new_pos[t]
-                d.step(q, kn, vn, npos, out, max_len=ml)
-            if events is not None:
-                if t == t0:
-                    events["span"][1].record()
-                if t == t1 - 1:
-                    events["span"][2].record()
-
-    # warm-up
-    t_base = 0
-    host_len = state.lengths.cpu().numpy()
-    if W > 0:
-        if keep_going:
-            decs = make(state)
-            run(decs, 0, W, step_bounds(host_len, W))
-            t_base = W
-        else:
-            scratch = clone_state(state)
-            run(make(scratch), 0, W, step_bounds(host_len, W))
-            torch.cuda.synchronize()
-            del scratch
-            torch.cuda.empty_cache()
-            decs = make(state)
-    else:
-        decs = make(state)
-    torch.cuda.synchronize()
-    lengths0 = state.lengths.cpu().numpy().astype(np.int64)
-
-    events = {"span": [torch.cuda.Event(enable_timing=True) for _ in range(3)]}
-    torch.cuda.synchronize()
-    bounds = step_bounds(lengths0, K)
-    t0 = time.perf_counter()
-    run(decs, t_base, t_base + K, bounds, events)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    errs = se.se_read_device_errors(decs[0].dev_err)
-    if errs:
-        raise RuntimeError(f"device error bits {errs:#x} during the timed run")
-
-    # per-call durations and algorithmic bytes (lengths follow the method's rule on the host)
-
-    first_bytes, second_bytes = 0, 0
-    L = lengths0.reshape(w.layers, U).copy()
-    span = events["span"]
-    step1_ms = span[0].elapsed_time(span[1])
-    region_ms = span[0].elapsed_time(span[2])  # the whole timed region
-    step1_bytes = 0
-    for t in range(K):
-        for l in range(w.layers):
-            Lp = L[l] + 1
-            if w.method == "h2o":
-                # one se_decode_step_h2o call: attention + score update + eviction
-                b = attend_bytes(Lp, G, D) + evict_bytes(Lp, w.budget, D)
-                first_bytes += b
-                if t == 0:
-                    step1_bytes += b
-                L[l] = np.minimum(Lp, w.budget)
-            else:
-                n_cand = L[l] // 16
-                visited = np.minimum(n_cand, w.top_k) * 16 + ((Lp - 1) % 16 + 1)
-                b1, b2 = select_bytes(n_cand, G, D, w.top_k), quest_attend_bytes(visited, G, D, w.top_k)
-                first_bytes += b1
-                second_bytes += b2
-                if t == 0:
-                    step1_bytes += b1 + b2
-                L[l] = Lp
-    tokens = w.num_req * K
-    value = tokens / elapsed
-    if w.method == "h2o":
-        # one se_decode_step_h2o call per step and layer: the attention kernel with
-        # the score update and the steady eviction fused (with a split unit, as in
-        # the first step of a long context: attention, combine, eviction kernels)
-        dom_name = "se_decode_step_h2o"
-    else:
-        # one se_decode_step_quest call per step and layer: page bounds, top-k and
-        # attention over the selected pages in one kernel when units fill the chip
-        dom_name = "se_decode_step_quest"
-    # the call's average duration is the timed region over the calls in it
-    dom_ms, dom_bytes = region_ms, first_bytes + second_bytes
-    n_launch = K * w.layers
-    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
-    traffic = read_traffic() if (w.index == 1 and w.method == "h2o") else None
+    r = run_decode(w, K, W, se, dev)
+    torch.cuda.empty_cache()
     result = {
         "metric": METRIC,
-        "value": round(value, 1),
+        "value": round(r["value"], 1),
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": K,
         "warmup": W,
-        "ms_per_step": round(1e3 * elapsed / K, 4),
+        "ms_per_step": round(r["ms_per_step"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": w.name, "method": w.method, "batch": w.num_req, "hq": w.hq, "hkv": w.hkv,
-                   "head_dim": D, "page_size": w.page_size, "layers": w.layers, "context": w.ctx,
-                   "budget": w.budget, "recent": w.recent, "top_k": w.top_k, "accumulate": "f32",
-                   "parallelism": "none (1 GPU)"},
-        "roofline": {"bound": "hbm", "kernel": dom_name, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic, "avg_launch_us": round(1e3 * dom_ms / n_launch, 3),
-                     "algorithmic_bytes_per_launch": round(dom_bytes / n_launch)},
-        "step_GBps": round((first_bytes + second_bytes) / elapsed / 1e9, 1),
+        "config": config_fields(w),
+        "roofline": r["roofline"],
+        "step_GBps": r["step_GBps"],
         "cpu_baseline": cpu,
     }
-    if K > 1:
-        steady_ms = dom_ms - step1_ms
-        result["phases"] = {"step1_ms": round(step1_ms, 3),
-                            "steady_ms_per_step": round(steady_ms / (K - 1), 4),
-                            "steady_GBps": round((dom_bytes - step1_bytes) / (steady_ms * 1e-3) / 1e9, 1)}
+    if r["phases"]:
+        result["phases"] = r["phases"]
+    if args.config == 4 and not args.only:
+        # the single-layer 8B-shaped workloads, same step counts
+        others = {}
+        for idx in (1, 2, 3):
+            wo = CONFIGS[idx]
+            ro = run_decode(wo, K, W, se, dev)
+            torch.cuda.empty_cache()
+            e = {"config": config_fields(wo), "value": round(ro["value"], 1), "unit": "per-layer tokens/s",
+                 "ms_per_step": round(ro["ms_per_step"], 4), "roofline": ro["roofline"]}
+            if ro["phases"]:
+                e["phases"] = ro["phases"]
+            others[wo.name] = e
+            print(f"{wo.name}: {ro['value']:.0f} per-layer tokens/s, {ro['roofline']['frac']:.3f} of HBM peak",
+                  file=sys.stderr, flush=True)
+        result["other_configs"] = others
     if args.copy_calibration:
         n = 4 << 30
         a = torch.empty(n, dtype=torch.uint8, device=dev)
