@@ -567,37 +567,40 @@ struct Lanes {
   static constexpr int HP = D / 2;        // lanes per row set (two columns each)
   int r8, j8, own_row, own_head, col, rs;
   bool owns;
+  uint32_t koff;  // bytes from a page's start to the lane's K piece of row r8
+  uint32_t voff;  // bytes from a page's V block to the lane's column pair of row rs * RPL
 };
 
 // Loads of one page: K rows r8 and r8+8 (QK layout) and the V column pair
-// (PV layout).  Rows past the page's resident rows repeat its last row, whose
-// weight is zero.
+// (PV layout) of every row the lane owns.  The page base is wave-uniform
+// (scalar registers) and each row is a constant offset from the lane's offset,
+// so no load needs per-lane address arithmetic.  Rows past the page's resident
+// rows are read too (they lie inside the page): their logits are masked and
+// their value columns cleared before the PV update (pv_page).
+template <int D>
+__device__ __forceinline__ const char* page_base(const AttendParams& p, const PageRef& pr) {
+  return reinterpret_cast<const char*>(p.kv) + (size_t)pr.phys * (2 * kPage * D * 2);
+}
+
 template <int D>
 __device__ __forceinline__ void load_k(const AttendParams& p, const Lanes<D>& ln, const PageRef& pr,
                                        uint4 (&kb)[2 * Lanes<D>::K4]) {
-  constexpr int QC = Lanes<D>::QC, K4 = Lanes<D>::K4;
-  const uint16_t* kpage = p.kv + (size_t)pr.phys * (2 * kPage * D);
-  const int last = pr.nrows - 1;
+  constexpr int K4 = Lanes<D>::K4;
+  const char* kpage = page_base<D>(p, pr) + ln.koff;
 #pragma unroll
-  for (int pass = 0; pass < 2; ++pass) {
-    const int rk = min(ln.r8 + 8 * pass, last);
+  for (int pass = 0; pass < 2; ++pass)
 #pragma unroll
     for (int i = 0; i < K4; ++i)
-      kb[pass * K4 + i] = reinterpret_cast<const uint4*>(kpage + rk * D + ln.j8 * QC)[i];
-  }
+      kb[pass * K4 + i] = *reinterpret_cast<const uint4*>(kpage + pass * 8 * D * 2 + i * 16);
 }
 
 template <int D>
 __device__ __forceinline__ void load_v(const AttendParams& p, const Lanes<D>& ln, const PageRef& pr,
                                        uint32_t (&vb)[Lanes<D>::RPL]) {
   constexpr int RPL = Lanes<D>::RPL;
-  const uint16_t* vpage = p.kv + (size_t)pr.phys * (2 * kPage * D) + kPage * D;
-  const int last = pr.nrows - 1;
+  const char* vpage = page_base<D>(p, pr) + kPage * D * 2 + ln.voff;
 #pragma unroll
-  for (int i = 0; i < RPL; ++i) {
-    const int rv = min(ln.rs * RPL + i, last);
-    vb[i] = *reinterpret_cast<const uint32_t*>(vpage + rv * D + ln.col);
-  }
+  for (int i = 0; i < RPL; ++i) vb[i] = *reinterpret_cast<const uint32_t*>(vpage + i * D * 2);
 }
 
 // Reduce-scatter of the 8 lanes that share two K rows: on entry a[h] / b[h]
@@ -726,14 +729,19 @@ __device__ __forceinline__ float softmax_page(const AttendParams& p, const Lanes
 
 // o += P V for one page, the weights read back from LDS.
 template <int D, int G>
-__device__ __forceinline__ void pv_page(const Lanes<D>& ln, const uint32_t (&vb)[Lanes<D>::RPL],
+__device__ __forceinline__ void pv_page(const Lanes<D>& ln, const uint32_t (&vb)[Lanes<D>::RPL], int nrows,
                                         WaveSoftmax<G>& ws, const float* lds_pw) {
   constexpr int RPL = Lanes<D>::RPL;
+  // bf16 -> fp32 by byte permutes whose selectors are per row (scalar for
+  // D = 128): rows past the resident ones become zeros, since a zero weight
+  // times arbitrary bits (Inf, NaN) would not stay zero
+  constexpr uint32_t kLo = 0x01000c0cu, kHi = 0x03020c0cu, kZero = 0x0c0c0c0cu;
 #pragma unroll
   for (int i = 0; i < RPL; ++i) {
     const int rr = ln.rs * RPL + i;
-    const float v0 = bf16lo(vb[i]);
-    const float v1 = bf16hi(vb[i]);
+    const bool ok = rr < nrows;
+    const float v0 = __uint_as_float(__builtin_amdgcn_perm(0u, vb[i], ok ? kLo : kZero));
+    const float v1 = __uint_as_float(__builtin_amdgcn_perm(0u, vb[i], ok ? kHi : kZero));
 #pragma unroll
     for (int h = 0; h < G; ++h) {
       const float ph = lds_pw[rr * G + h];
@@ -800,6 +808,8 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   ln.owns = ln.own_head < G;
   ln.col = 2 * (lane % HP);
   ln.rs = lane / HP;
+  ln.koff = (uint32_t)(ln.r8 * D + ln.j8 * QC) * 2u;
+  ln.voff = (uint32_t)(ln.rs * RPL * D + ln.col) * 2u;
   const int j8 = ln.j8;
   const int col = ln.col;
 
@@ -968,7 +978,7 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
     pr.vp = __builtin_amdgcn_readfirstlane(lds_vp[gi]);
     pr.lp = __builtin_amdgcn_readfirstlane(lds_lp[gi]);
     pr.phys = __builtin_amdgcn_readfirstlane(lds_phys[gi]);
-    pr.nrows = min(kPage, Lp - pr.lp * kPage);
+    pr.nrows = __builtin_amdgcn_readfirstlane(min(kPage, Lp - pr.lp * kPage));
     pr.rn = -1;
     return pr;
   };
@@ -982,11 +992,7 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   uint4 kbA[2 * K4], kbB[2 * K4];
   uint32_t vb[RPL];
   if (n_my > 0) {
-    auto ref_or_tail = [&](int i) -> PageRef {
-      PageRef r = page_ref(i < n_my ? i : n_my - 1);
-      if (i >= n_my) r.nrows = 1;
-      return r;
-    };
+    auto ref_or_tail = [&](int i) -> PageRef { return page_ref(i < n_my ? i : n_my - 1); };
     PageRef cur = ref_or_tail(0);
     PageRef nx1 = ref_or_tail(1);
     load_k<D>(p, ln, cur, kbA);
@@ -1000,7 +1006,7 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
         const float z = qk_page<D, G>(ln, kbA, lds_q);
         load_k<D>(p, ln, nx2, kbA);
         softmax_page<D, G>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p, lds_w, lds_mr, wcap);
-        pv_page<D, G>(ln, vb, ws, lds_p[wave]);
+        pv_page<D, G>(ln, vb, cur.nrows, ws, lds_p[wave]);
         load_v<D>(p, ln, nx1, vb);
         cur = nx1;
         nx1 = nx2;
@@ -1011,7 +1017,7 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
         const float z = qk_page<D, G>(ln, kbB, lds_q);
         load_k<D>(p, ln, nx2, kbB);
         softmax_page<D, G>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p, lds_w, lds_mr, wcap);
-        pv_page<D, G>(ln, vb, ws, lds_p[wave]);
+        pv_page<D, G>(ln, vb, cur.nrows, ws, lds_p[wave]);
         load_v<D>(p, ln, nx1, vb);
         cur = nx1;
         nx1 = nx2;
