@@ -31,6 +31,7 @@
 // avoids a device-scope release/acquire (an L2 writeback and invalidate) in
 // every work-group.
 #include <mutex>
+#include <type_traits>
 
 #include "evict_core.h"
 #include "quest_core.h"
@@ -139,35 +140,54 @@ __device__ __forceinline__ float slot_weight(const AttendParams& p, size_t ubase
   return a;
 }
 
-// When one work-group holds a whole unit of at most kWeightPages<G> pages, the
-// per-slot weights and per-page reference maxima of the score update stay in
-// LDS instead of going through the workspace; the buffer is the eviction
-// scratch's holes array, which only the general eviction uses, after the scores
-// are written.
-constexpr int kWeightCap = 9216;  // floats (>= kMaxBudget ints for the holes)
+// When one work-group holds a whole unit, the per-slot weights (fp16: each
+// is rounded by at most 2^-11 relative before the fp32 score update) and the
+// per-page reference maxima (fp32) of its first kWeightPages<G> visit pages
+// stay in LDS instead of going through the workspace, which would add an HBM
+// write and read of 16 B per slot to the step; the buffer is the eviction
+// scratch's holes array, which only the general eviction uses, after the
+// scores are written.
+constexpr int kWeightCap = 9216;  // 32-bit words (>= kMaxBudget ints for the holes)
 constexpr int kSelectMaxPages = kWeightCap / 2;  // fused Quest selection: block-table row + scores
-template <int G>
-constexpr int kWeightPages = kWeightCap / (kPage * G);
+constexpr int kWeightMrCap = 2 * kWeightCap / kPage;  // reference maxima: one per (visit page, head)
+template <int G, typename W>
+constexpr int kWeightPages =
+    (kWeightCap * 4 / (int)sizeof(W) / (kPage * G)) < 1024 ? kWeightCap * 4 / (int)sizeof(W) / (kPage * G) : 1024;
 static_assert(kWeightCap >= kMaxBudget, "the weight buffer doubles as the holes array");
+static_assert(kWeightPages<4, _Float16> * 4 <= kWeightMrCap && kWeightPages<1, _Float16> <= kWeightMrCap,
+              "reference maxima");
+// The weight format of a kernel instantiation: fp32 where the units it takes
+// fit the buffer that way (the 512-thread per-wavefront steady variant, at most
+// wave_rows_pages pages), fp16 elsewhere (twice the pages).
+template <int NT, bool kWaveRows>
+using WeightT = typename std::conditional<kWaveRows && NT == 512, float, _Float16>::type;
 
 // Where the score update finds the weights: visit pages below `cap` in the
 // work-group's LDS buffer, the others in the workspace rows (global).
+template <typename W>
 struct WeightSrc {
-  const float* lw;   // LDS [visit page][16][G]
-  const float* lmr;  // LDS [visit page][G]
+  const W* lw;         // LDS [visit page][16][G]
+  const float* lfac;  // LDS [visit page][G]: exp2(m_ref - m) / l, the page's factor per head
   const float* gw;   // workspace, same layout
   const float* gmr;
   int cap;
 };
 
-template <int G>
-__device__ __forceinline__ float slot_weight_from(const WeightSrc& src, int vp, int rr, const float* fin_m,
+// A slot's weight summed over the group when its page's weights are in LDS.
+template <int G, typename W>
+__device__ __forceinline__ float slot_weight_lds(const WeightSrc<W>& src, int vp, int rr) {
+  float a = 0.f;
+#pragma unroll
+  for (int h = 0; h < G; ++h) a += (float)src.lw[(vp * kPage + rr) * G + h] * src.lfac[vp * G + h];
+  return a;
+}
+
+template <int G, typename W>
+__device__ __forceinline__ float slot_weight_from(const WeightSrc<W>& src, int vp, int rr, const float* fin_m,
                                                   const float* fin_il) {
   float a = 0.f;
   if (vp < src.cap) {
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-      a += src.lw[(vp * kPage + rr) * G + h] * fast_exp2(src.lmr[vp * G + h] - fin_m[h]) * fin_il[h];
+    a = slot_weight_lds<G, W>(src, vp, rr);
   } else {
 #pragma unroll
     for (int h = 0; h < G; ++h)
@@ -217,10 +237,10 @@ __device__ __forceinline__ void evict_in_epilogue(const AttendParams& p, const U
 // The staged table is the unit's page table (staged index = logical page).
 constexpr int kSteadyRows = 5;  // pages per wavefront up to 4 * kSteadyRows
 
-template <int NT, int G, int D>
+template <int NT, int G, int D, typename W>
 __device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitGeom& g, const float* fin_m,
                                               const float* fin_il, const int* lds_phys, const int* lds_vp,
-                                              const WeightSrc& wsrc, int32_t (&pos)[kSteadyRows],
+                                              const WeightSrc<W>& wsrc, int32_t (&pos)[kSteadyRows],
                                               float (&unew)[kSteadyRows], int rbeg, int wr, int n_my,
                                               const EvictScratch<NT>& sc) {
   constexpr int KW = kSteadyRows;
@@ -231,12 +251,6 @@ __device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitG
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int r = lane & (kPage - 1);
-  float fm[G], fil[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    fm[h] = fin_m[h];
-    fil[h] = fin_il[h];
-  }
   // slot of row j of this lane, or -1
   auto slot_of = [&](int j) -> int {
     const int i = (lane >> 4) + 4 * j;
@@ -252,7 +266,7 @@ __device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitG
     if (s >= 0) {
       live |= 1u << j;
       const int gi = s >> 4;
-      unew[j] += slot_weight_from<G>(wsrc, lds_vp[gi], r, fm, fil);
+      unew[j] += slot_weight_lds<G, W>(wsrc, lds_vp[gi], r);  // every page is in LDS here
       p.score_pool[(size_t)lds_phys[gi] * kPage + r] = unew[j];
     }
   }
@@ -326,9 +340,9 @@ __device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitG
 // The same for units too long for finish_steady's per-wavefront rows: thread
 // t handles slots t + k * NT, loaded here (branch-free, in groups).  lds_bt:
 // the unit's page table staged in LDS, in page order.
-template <int NT, int G, int D>
+template <int NT, int G, int D, typename W>
 __device__ __forceinline__ void finish_steady_strided(const AttendParams& p, const UnitGeom& g, const float* fin_m,
-                                              const float* fin_il, const int* lds_bt, const WeightSrc& wsrc,
+                                              const float* fin_il, const int* lds_bt, const WeightSrc<W>& wsrc,
                                               const EvictScratch<NT>& sc) {
   constexpr int KMAX = kMaxBudget / NT;  // slots per thread kept in registers
   int* const red_i = sc.red_i;
@@ -356,7 +370,7 @@ __device__ __forceinline__ void finish_steady_strided(const AttendParams& p, con
     for (int j = 0; j < RG; ++j) {
       const int s = min(tid + (k0 + j) * NT, g.Lp - 1);
       phys[k0 + j] = lds_bt[s >> 4];
-      a[j] = slot_weight_from<G>(wsrc, s >> 4, s & (kPage - 1), fin_m, fin_il);
+      a[j] = slot_weight_from<G, W>(wsrc, s >> 4, s & (kPage - 1), fin_m, fin_il);
     }
 #pragma unroll
     for (int j = 0; j < RG; ++j) {
@@ -448,9 +462,9 @@ __device__ __forceinline__ void finish_steady_strided(const AttendParams& p, con
 
 // The score update of every visited slot, BATCH slots per thread at a time with
 // all of a batch's loads issued before its stores.
-template <int NT, int G>
+template <int NT, int G, typename W>
 __device__ __forceinline__ void accumulate_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
-                                                const float* fin_il, const WeightSrc& wsrc) {
+                                                const float* fin_il, const WeightSrc<W>& wsrc) {
   constexpr int BATCH = 8;
   const size_t ubase_p = (size_t)g.unit * p.n_visit_max;
   const int32_t* bt = p.block_table + (size_t)g.unit * p.max_pages;
@@ -477,7 +491,7 @@ __device__ __forceinline__ void accumulate_unit(const AttendParams& p, const Uni
       }
       ok = ok && lp * kPage + rr < g.Lp;
       ph[j] = ok ? bt[lp] : -1;
-      a[j] = ok ? slot_weight_from<G>(wsrc, vp, rr, fm, fil) : 0.f;
+      a[j] = ok ? slot_weight_from<G, W>(wsrc, vp, rr, fm, fil) : 0.f;
     }
     float u[BATCH];
 #pragma unroll
@@ -502,14 +516,14 @@ __device__ __forceinline__ void accumulate_unit(const AttendParams& p, const Uni
 // unit, after its final (m, 1/l) per head are in fin_m / fin_il.  The weights
 // of visit pages below wcap come from the work-group's LDS buffer (lds_w,
 // lds_mr), the others from the workspace.
-template <int NT, int G, int D, bool kCanEvict>
+template <int NT, int G, int D, bool kCanEvict, typename W>
 __device__ __forceinline__ void finish_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
-                            const float* fin_il, const float* lds_w, const float* lds_mr, int wcap,
+                            const float* fin_il, const W* lds_w, const float* lds_mr, int wcap,
                             const EvictScratch<NT>* scp) {
   const int tid = threadIdx.x;
   const size_t ubase_p = (size_t)g.unit * p.n_visit_max;
-  const WeightSrc wsrc{lds_w, lds_mr, p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G, wcap};
-  if (p.accumulate) accumulate_unit<NT, G>(p, g, fin_m, fin_il, wsrc);
+  const WeightSrc<W> wsrc{lds_w, lds_mr, p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G, wcap};
+  if (p.accumulate) accumulate_unit<NT, G, W>(p, g, fin_m, fin_il, wsrc);
   if constexpr (kCanEvict) {
     if (p.evict && !g.quest && g.Lp > p.budget) {
       evict_in_epilogue<NT, D>(p, g, *scp);  // sets the length and the freed pages
@@ -683,11 +697,11 @@ __device__ __forceinline__ float qk_page(const Lanes<D>& ln, const uint4 (&kb)[2
 
 // Reference update, weight of the lane's pair, its workspace copy, and the
 // weights' broadcast through LDS (the page's PV follows).
-template <int D, int G>
+template <int D, int G, typename W>
 __device__ __forceinline__ float softmax_page(const AttendParams& p, const Lanes<D>& ln,
                                               const PageRef& pr, float z, WaveSoftmax<G>& ws,
                                               float* lds_pw, int lane, int unit, size_t ubase_p,
-                                              float* lds_w, float* lds_mr, int wcap) {
+                                              W* lds_w, float* lds_mr, int wcap) {
   constexpr float kBump = 8.0f;  // rescale only when a logit beats the reference by 2^8
   const bool valid = ln.owns && ln.own_row < pr.nrows;
   const float z2 = valid ? z * p.scale_log2 : -INFINITY;
@@ -716,7 +730,7 @@ __device__ __forceinline__ float softmax_page(const AttendParams& p, const Lanes
   const float pj = valid ? fast_exp2(z2 - ws.m_own) : 0.f;
   ws.l_own += pj;
   if (pr.vp < wcap) {
-    if (ln.owns) lds_w[(pr.vp * kPage + ln.own_row) * G + ln.own_head] = pj;
+    if (ln.owns) lds_w[(pr.vp * kPage + ln.own_row) * G + ln.own_head] = (W)pj;
     if (lane < G) lds_mr[pr.vp * G + lane] = ws.m_own;
   } else if (p.accumulate) {
     if (ln.owns) p.pbuf[((ubase_p + pr.vp) * kPage + ln.own_row) * G + ln.own_head] = pj;
@@ -774,7 +788,9 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   __shared__ int lds_vp[kMaxGroupPages];
   __shared__ uint32_t lds_q[G][D / 2];  // the unit's G query rows (bf16 pairs)
   __shared__ float lds_w[kWeightCap];    // per-slot weights, then the eviction's holes
-  __shared__ float lds_mr[kWeightCap / kPage];
+  __shared__ float lds_mr[kWeightMrCap];
+  using W = WeightT<NT, kWaveRows>;
+  W* const lds_wh = reinterpret_cast<W*>(lds_w);
   SE_EVICT_SCRATCH_WITH_HOLES(NT, esc, reinterpret_cast<int*>(lds_w));
   __shared__ int lds_scan[NT / kWave + 1];
 
@@ -793,7 +809,7 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   const size_t ubase_p = (size_t)unit * p.n_visit_max;  // page-indexed workspace rows
   // the score update's weights of visit pages below wcap stay in LDS (this
   // work-group holds the whole unit); the rest go to the workspace
-  const int wcap = (p.accumulate && p.n_split == 1) ? kWeightPages<G> : 0;
+  const int wcap = (p.accumulate && p.n_split == 1) ? kWeightPages<G, W> : 0;
 
   // QK layout: lane = 8*r8 + j8 reads columns [j8*QC, (j8+1)*QC) of rows r8
   // (pass A) and r8 + 8 (pass B).  After the 8-lane reduction, lane j8 < 4
@@ -1005,7 +1021,7 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
         const PageRef nx2 = ref_or_tail(i + 2);
         const float z = qk_page<D, G>(ln, kbA, lds_q);
         load_k<D>(p, ln, nx2, kbA);
-        softmax_page<D, G>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p, lds_w, lds_mr, wcap);
+        softmax_page<D, G, W>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p, lds_wh, lds_mr, wcap);
         pv_page<D, G>(ln, vb, cur.nrows, ws, lds_p[wave]);
         load_v<D>(p, ln, nx1, vb);
         cur = nx1;
@@ -1016,7 +1032,7 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
         const PageRef nx2 = ref_or_tail(i + 3);
         const float z = qk_page<D, G>(ln, kbB, lds_q);
         load_k<D>(p, ln, nx2, kbB);
-        softmax_page<D, G>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p, lds_w, lds_mr, wcap);
+        softmax_page<D, G, W>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p, lds_wh, lds_mr, wcap);
         pv_page<D, G>(ln, vb, cur.nrows, ws, lds_p[wave]);
         load_v<D>(p, ln, nx1, vb);
         cur = nx1;
@@ -1110,15 +1126,26 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
     if (tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_LENGTH);
     return;
   }
+  if (wcap > 0) {
+    // each LDS page's reference maximum becomes the factor its weights take in
+    // the score update, exp2(m_ref - m) / l per head: one exp2 per page and head
+    // instead of per slot and head
+    const int nl = min(g.n_visit, wcap) * G;
+    for (int i = tid; i < nl; i += NT) {
+      const int h = i % G;
+      lds_mr[i] = fast_exp2(lds_mr[i] - fin_m[h]) * fin_il[h];
+    }
+    __syncthreads();
+  }
   if (kWaveRows && steady) {
-    const WeightSrc wsrc{lds_w, lds_mr, p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G, wcap};
-    finish_steady<NT, G, D>(p, g, fin_m, fin_il, lds_phys, lds_vp, wsrc, spos, su, rbeg, wr, n_my,
+    const WeightSrc<W> wsrc{lds_wh, lds_mr, p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G, wcap};
+    finish_steady<NT, G, D, W>(p, g, fin_m, fin_il, lds_phys, lds_vp, wsrc, spos, su, rbeg, wr, n_my,
                                         esc);
   } else if (!kWaveRows && steady_any) {
-    const WeightSrc wsrc{lds_w, lds_mr, p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G, wcap};
-    finish_steady_strided<NT, G, D>(p, g, fin_m, fin_il, lds_phys, wsrc, esc);
+    const WeightSrc<W> wsrc{lds_wh, lds_mr, p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G, wcap};
+    finish_steady_strided<NT, G, D, W>(p, g, fin_m, fin_il, lds_phys, wsrc, esc);
   } else {
-    finish_unit<NT, G, D, true>(p, g, fin_m, fin_il, lds_w, lds_mr, wcap, &esc);
+    finish_unit<NT, G, D, true, W>(p, g, fin_m, fin_il, lds_wh, lds_mr, wcap, &esc);
   }
 }
 
@@ -1196,7 +1223,7 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(const A
     }
   }
   __syncthreads();
-  finish_unit<kCombineThreads, G, D, false>(p, g, fin_m, fin_il, nullptr, nullptr, 0, nullptr);
+  finish_unit<kCombineThreads, G, D, false, float>(p, g, fin_m, fin_il, nullptr, nullptr, 0, nullptr);
 }
 
 // With a split, the combine pass updates the scores and publishes the appended
@@ -1209,6 +1236,10 @@ template <int NT>
 constexpr int wave_rows_pages() {
   return (4 * 4 * kSteadyRows * 100 - 50) / RankWeights<NT / kWave / 4>::w[0];
 }
+// finish_steady reads every page's weights from LDS
+static_assert(wave_rows_pages<kAttendThreads>() <= kWeightPages<4, WeightT<kAttendThreads, true>> &&
+                  wave_rows_pages<kAttendThreadsWide>() <= kWeightPages<4, WeightT<kAttendThreadsWide, true>>,
+              "the per-wavefront steady eviction needs every weight in LDS");
 
 // Launches with at most one work-group per compute unit take 1024 threads.
 inline bool attend_wide(int num_units, int n_visit) {
