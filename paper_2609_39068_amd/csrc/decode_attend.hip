@@ -206,6 +206,9 @@ __device__ __forceinline__ uint32_t pos_order(int32_t pos) { return (uint32_t)po
 // token's slot (the last one) moves into it.  Anything else is left to the
 // general eviction kernel that se_decode_step_h2o launches next.
 // The general eviction of a unit in the epilogue (after its scores are written).
+// The kernel calls it from one place, as an unlikely branch at the end of the
+// epilogue, so that its code (a radix selection) sits after the hot path:
+// instruction-cache misses cost a memory latency each in every work-group.
 template <int NT, int D>
 __device__ __forceinline__ void evict_in_epilogue(const AttendParams& p, const UnitGeom& g, const EvictScratch<NT>& sc) {
   __syncthreads();
@@ -237,8 +240,35 @@ __device__ __forceinline__ void evict_in_epilogue(const AttendParams& p, const U
 // The staged table is the unit's page table (staged index = logical page).
 constexpr int kSteadyRows = 5;  // pages per wavefront up to 4 * kSteadyRows
 
+// The steady eviction's one move: the newest slot (mover) into the victim's
+// slot, with its key and value rows, position and score.  When the step
+// appended, the newest slot's rows are the step's k_new / v_new, read from
+// there rather than from the pool the append wrote, so nothing waits for the
+// append's stores.
+template <int D>
+__device__ __forceinline__ void move_newest(const AttendParams& p, const UnitGeom& g, int pv, int victim, int pm,
+                                            int mover, int32_t mpos, float mu) {
+  if (victim == mover) return;
+  const int tid = threadIdx.x;
+  constexpr int R4 = D / 8;  // 16-byte chunks per row
+  uint4* dst = reinterpret_cast<uint4*>(const_cast<uint16_t*>(p.kv) + (size_t)pv * (2 * kPage * D) + (victim & 15) * D);
+  if (tid < 2 * R4) {
+    const int part = tid / R4, c = tid - part * R4;  // part 0: key row, 1: value row
+    const uint4* src;
+    if (g.append && mover == g.L)
+      src = reinterpret_cast<const uint4*>((part ? p.v_new : p.k_new) + ((size_t)g.req * p.hkv + g.kvh) * D);
+    else
+      src = reinterpret_cast<const uint4*>(p.kv + (size_t)pm * (2 * kPage * D) + (mover & 15) * D) + part * kPage * R4;
+    dst[part * kPage * R4 + c] = src[c];
+  }
+  if (tid == 0) {
+    p.pos_pool[(size_t)pv * kPage + (victim & 15)] = mpos;
+    p.score_pool[(size_t)pv * kPage + (victim & 15)] = mu;
+  }
+}
+
 template <int NT, int G, int D, typename W>
-__device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitGeom& g, const float* fin_m,
+__device__ __forceinline__ bool finish_steady(const AttendParams& p, const UnitGeom& g, const float* fin_m,
                                               const float* fin_il, const int* lds_phys, const int* lds_vp,
                                               const WeightSrc<W>& wsrc, int32_t (&pos)[kSteadyRows],
                                               float (&unew)[kSteadyRows], int rbeg, int wr, int n_my,
@@ -258,7 +288,10 @@ __device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitG
     const int s = (rbeg + wr + 4 * i) * kPage + r;
     return s < g.Lp ? s : -1;
   };
-  // pos / unew hold the fetched positions and old scores; the scores become the new ones
+  // pos / unew hold the fetched positions and old scores; the scores become the
+  // new ones.  They are stored only after the block reductions: a barrier waits
+  // for the work-group's outstanding stores, which under a full memory system
+  // take tens of microseconds.
   uint32_t live = 0;
 #pragma unroll
   for (int j = 0; j < KW; ++j) {
@@ -267,9 +300,15 @@ __device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitG
       live |= 1u << j;
       const int gi = s >> 4;
       unew[j] += slot_weight_lds<G, W>(wsrc, lds_vp[gi], r);  // every page is in LDS here
-      p.score_pool[(size_t)lds_phys[gi] * kPage + r] = unew[j];
     }
   }
+  auto store_scores = [&](int skip) {
+#pragma unroll
+    for (int j = 0; j < KW; ++j) {
+      const int s = slot_of(j);
+      if (((live >> j) & 1) && s != skip) p.score_pool[(size_t)lds_phys[s >> 4] * kPage + r] = unew[j];
+    }
+  };
   const int w = min(p.recent, p.budget);
   int32_t pmax = INT32_MIN;
 #pragma unroll
@@ -281,9 +320,9 @@ __device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitG
 #pragma unroll
   for (int j = 0; j < KW; ++j) cnt += (((live >> j) & 1) && (int64_t)pos[j] > lo) ? 1 : 0;
   cnt = block_reduce<NT>(cnt, red_i, [](int x, int y) { return x + y; });
-  if (cnt != w) {  // scores are updated; the general path evicts
-    evict_in_epilogue<NT, D>(p, g, sc);
-    return;
+  if (cnt != w) {  // the general eviction runs from the updated scores
+    store_scores(-1);
+    return true;
   }
   unsigned long long best = ~0ull;
 #pragma unroll
@@ -313,21 +352,10 @@ __device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitG
   }
   __syncthreads();
   const int victim = bc[0];
-  if (victim != mover) {
-    const int pv = lds_phys[victim >> 4], pm = lds_phys[mover >> 4];
-    constexpr int R4 = D / 8;  // 16-byte chunks per row
-    const uint4* src = reinterpret_cast<const uint4*>(p.kv + (size_t)pm * (2 * kPage * D) + (mover & 15) * D);
-    uint4* dst = reinterpret_cast<uint4*>(const_cast<uint16_t*>(p.kv) + (size_t)pv * (2 * kPage * D) +
-                                          (victim & 15) * D);
-    if (tid < 2 * R4) {
-      const int part = tid / R4, c = tid - part * R4;  // part 0: key row, 1: value row
-      dst[part * kPage * R4 + c] = src[part * kPage * R4 + c];
-    }
-    if (tid == 0) {
-      p.pos_pool[(size_t)pv * kPage + (victim & 15)] = bc[1];
-      p.score_pool[(size_t)pv * kPage + (victim & 15)] = bc_u;
-    }
-  }
+  // every store after the last barrier: the scores (the victim's slot takes the
+  // mover's), the mover's row, position and score in the victim's slot
+  store_scores(victim);
+  move_newest<D>(p, g, lds_phys[victim >> 4], victim, lds_phys[mover >> 4], mover, bc[1], bc_u);
   if (tid == 0) {
     p.lengths[g.unit] = p.budget;
     const int f0 = (p.budget + kPage - 1) / kPage;
@@ -335,13 +363,14 @@ __device__ __forceinline__ void finish_steady(const AttendParams& p, const UnitG
     if (p.freed_pages != nullptr && nf > 0) p.freed_pages[(size_t)g.unit * p.freed_stride] = lds_phys[f0];
     if (p.freed_count != nullptr) p.freed_count[g.unit] = nf;
   }
+  return false;
 }
 
 // The same for units too long for finish_steady's per-wavefront rows: thread
 // t handles slots t + k * NT, loaded here (branch-free, in groups).  lds_bt:
 // the unit's page table staged in LDS, in page order.
 template <int NT, int G, int D, typename W>
-__device__ __forceinline__ void finish_steady_strided(const AttendParams& p, const UnitGeom& g, const float* fin_m,
+__device__ __forceinline__ bool finish_steady_strided(const AttendParams& p, const UnitGeom& g, const float* fin_m,
                                               const float* fin_il, const int* lds_bt, const WeightSrc<W>& wsrc,
                                               const EvictScratch<NT>& sc) {
   constexpr int KMAX = kMaxBudget / NT;  // slots per thread kept in registers
@@ -351,47 +380,45 @@ __device__ __forceinline__ void finish_steady_strided(const AttendParams& p, con
   __shared__ float bc_u;
   const int tid = threadIdx.x;
   const size_t ubase_p = (size_t)g.unit * p.n_visit_max;
-  const int32_t* bt = p.block_table + (size_t)g.unit * p.max_pages;
-  // Rows are loaded branch-free (rows past the end re-read the last slot, a bad
-  // page reads page 0 and is discarded) in groups of RG, whose loads are all in
-  // flight together; the stores come after every load, since a store between
-  // two rows' loads would keep the later loads from being issued early.
-  constexpr int RG = 4;
-  static_assert(KMAX % RG == 0, "row groups");
+  // Every row's position and old score is loaded first, all in flight together
+  // (one memory latency for the epilogue; rows past the end re-read the last
+  // slot, a bad page reads page 0 and is discarded), then the weights are added;
+  // the stores come after every load.
   float unew[KMAX];
   int32_t pos[KMAX];
-  int phys[KMAX];
+  uint32_t live = 0;  // rows k that hold a resident slot of a valid page
   int badp = 0;
   const int32_t pos_new = g.append ? p.new_pos[g.req] : 0;
 #pragma unroll
-  for (int k0 = 0; k0 < KMAX; k0 += RG) {
-    float a[RG];
-#pragma unroll
-    for (int j = 0; j < RG; ++j) {
-      const int s = min(tid + (k0 + j) * NT, g.Lp - 1);
-      phys[k0 + j] = lds_bt[s >> 4];
-      a[j] = slot_weight_from<G, W>(wsrc, s >> 4, s & (kPage - 1), fin_m, fin_il);
-    }
-#pragma unroll
-    for (int j = 0; j < RG; ++j) {
-      const int k = k0 + j;
-      const int s = tid + k * NT;
-      const bool ok = phys[k] >= 0 && (int64_t)phys[k] < p.num_pages;
-      badp |= (s < g.Lp && !ok) ? 1 : 0;
-      const size_t a_ = (size_t)(ok ? phys[k] : 0) * kPage + (min(s, g.Lp - 1) & (kPage - 1));
-      const float u_old = p.score_pool[a_];
-      const int32_t q_old = p.pos_pool[a_];
-      const bool live = s < g.Lp && ok;
-      const bool is_new = g.append && s == g.L;
-      unew[k] = live ? (is_new ? 0.f : u_old) + a[j] : 0.f;
-      pos[k] = live ? (is_new ? pos_new : q_old) : INT32_MIN;
-      if (!live) phys[k] = -1;
-    }
-    __builtin_amdgcn_sched_barrier(0);
+  for (int k = 0; k < KMAX; ++k) {
+    const int s = min(tid + k * NT, g.Lp - 1);
+    const int ph = lds_bt[s >> 4];
+    const bool ok = ph >= 0 && (int64_t)ph < p.num_pages;
+    if (ok && tid + k * NT < g.Lp) live |= 1u << k;
+    badp |= (tid + k * NT < g.Lp && !ok) ? 1 : 0;
+    const size_t a_ = (size_t)(ok ? ph : 0) * kPage + (s & (kPage - 1));
+    unew[k] = p.score_pool[a_];
+    pos[k] = p.pos_pool[a_];
   }
 #pragma unroll
-  for (int k = 0; k < KMAX; ++k)
-    if (phys[k] >= 0) p.score_pool[(size_t)phys[k] * kPage + ((tid + k * NT) & (kPage - 1))] = unew[k];
+  for (int k = 0; k < KMAX; ++k) {
+    const int s = tid + k * NT;
+    const int sc_ = min(s, g.Lp - 1);
+    const float a = slot_weight_from<G, W>(wsrc, sc_ >> 4, sc_ & (kPage - 1), fin_m, fin_il);
+    const bool lv = (live >> k) & 1;
+    const bool is_new = g.append && s == g.L;
+    unew[k] = lv ? (is_new ? 0.f : unew[k]) + a : 0.f;
+    pos[k] = lv ? (is_new ? pos_new : pos[k]) : INT32_MIN;
+  }
+  // the new scores are stored after the last barrier (a barrier waits for the
+  // work-group's outstanding stores), except when the general path evicts
+  auto store_scores = [&](int skip) {
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+      const int s = tid + k * NT;
+      if (((live >> k) & 1) && s != skip) p.score_pool[(size_t)lds_bt[s >> 4] * kPage + (s & (kPage - 1))] = unew[k];
+    }
+  };
   badp = block_reduce<NT>(badp, red_i, [](int x, int y) { return x | y; });
   const int w = min(p.recent, p.budget);
   int32_t pmax = INT32_MIN;
@@ -403,9 +430,9 @@ __device__ __forceinline__ void finish_steady_strided(const AttendParams& p, con
 #pragma unroll
   for (int k = 0; k < KMAX; ++k) cnt += (tid + k * NT < g.Lp && (int64_t)pos[k] > lo) ? 1 : 0;
   cnt = block_reduce<NT>(cnt, red_i, [](int x, int y) { return x + y; });
-  if (badp || cnt != w) {  // scores are updated; the general path evicts
-    evict_in_epilogue<NT, D>(p, g, sc);
-    return;
+  if (badp || cnt != w) {  // the general eviction runs from the updated scores
+    store_scores(-1);
+    return true;
   }
   unsigned long long best = ~0ull;
 #pragma unroll
@@ -435,28 +462,16 @@ __device__ __forceinline__ void finish_steady_strided(const AttendParams& p, con
   }
   __syncthreads();
   const int victim = bc[0];
-  if (victim != mover) {
-    const int pv = bt[victim >> 4], pm = bt[mover >> 4];
-    constexpr int R4 = D / 8;  // 16-byte chunks per row
-    const uint4* src = reinterpret_cast<const uint4*>(p.kv + (size_t)pm * (2 * kPage * D) + (mover & 15) * D);
-    uint4* dst = reinterpret_cast<uint4*>(const_cast<uint16_t*>(p.kv) + (size_t)pv * (2 * kPage * D) +
-                                          (victim & 15) * D);
-    if (tid < 2 * R4) {
-      const int part = tid / R4, c = tid - part * R4;  // part 0: key row, 1: value row
-      dst[part * kPage * R4 + c] = src[part * kPage * R4 + c];
-    }
-    if (tid == 0) {
-      p.pos_pool[(size_t)pv * kPage + (victim & 15)] = bc[1];
-      p.score_pool[(size_t)pv * kPage + (victim & 15)] = bc_u;
-    }
-  }
+  store_scores(victim);
+  move_newest<D>(p, g, lds_bt[victim >> 4], victim, lds_bt[mover >> 4], mover, bc[1], bc_u);
   if (tid == 0) {
     p.lengths[g.unit] = p.budget;
     const int f0 = (p.budget + kPage - 1) / kPage;
     const int nf = (g.Lp + kPage - 1) / kPage - f0;
-    if (p.freed_pages != nullptr && nf > 0) p.freed_pages[(size_t)g.unit * p.freed_stride] = bt[f0];
+    if (p.freed_pages != nullptr && nf > 0) p.freed_pages[(size_t)g.unit * p.freed_stride] = lds_bt[f0];
     if (p.freed_count != nullptr) p.freed_count[g.unit] = nf;
   }
+  return false;
 }
 
 
@@ -516,24 +531,23 @@ __device__ __forceinline__ void accumulate_unit(const AttendParams& p, const Uni
 // unit, after its final (m, 1/l) per head are in fin_m / fin_il.  The weights
 // of visit pages below wcap come from the work-group's LDS buffer (lds_w,
 // lds_mr), the others from the workspace.
-template <int NT, int G, int D, bool kCanEvict, typename W>
-__device__ __forceinline__ void finish_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
-                            const float* fin_il, const W* lds_w, const float* lds_mr, int wcap,
-                            const EvictScratch<NT>* scp) {
+// Returns true when the unit still needs the general eviction (which then sets
+// its length and freed pages).
+template <int NT, int G, bool kCanEvict, typename W>
+__device__ __forceinline__ bool finish_unit(const AttendParams& p, const UnitGeom& g, const float* fin_m,
+                                            const float* fin_il, const W* lds_w, const float* lds_mr, int wcap) {
   const int tid = threadIdx.x;
   const size_t ubase_p = (size_t)g.unit * p.n_visit_max;
   const WeightSrc<W> wsrc{lds_w, lds_mr, p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G, wcap};
   if (p.accumulate) accumulate_unit<NT, G, W>(p, g, fin_m, fin_il, wsrc);
   if constexpr (kCanEvict) {
-    if (p.evict && !g.quest && g.Lp > p.budget) {
-      evict_in_epilogue<NT, D>(p, g, *scp);  // sets the length and the freed pages
-      return;
-    }
+    if (p.evict && !g.quest && g.Lp > p.budget) return true;
   }
   if (tid == 0) {
     if (g.append) p.lengths[g.unit] = g.Lp;
     if (kCanEvict && p.evict && p.freed_count != nullptr) p.freed_count[g.unit] = 0;
   }
+  return false;
 }
 
 // Per-page coordinates a wavefront needs before it loads the page.
@@ -591,6 +605,15 @@ struct Lanes {
 // so no load needs per-lane address arithmetic.  Rows past the page's resident
 // rows are read too (they lie inside the page): their logits are masked and
 // their value columns cleared before the PV update (pv_page).
+// K/V page data is read once per step: nontemporal loads (streaming cache
+// policy), so the stream does not push the block tables, positions, scores and
+// the kernel's code out of the L2.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 stream_load16(const char* ptr) {
+  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(ptr));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 template <int D>
 __device__ __forceinline__ const char* page_base(const AttendParams& p, const PageRef& pr) {
   return reinterpret_cast<const char*>(p.kv) + (size_t)pr.phys * (2 * kPage * D * 2);
@@ -605,7 +628,7 @@ __device__ __forceinline__ void load_k(const AttendParams& p, const Lanes<D>& ln
   for (int pass = 0; pass < 2; ++pass)
 #pragma unroll
     for (int i = 0; i < K4; ++i)
-      kb[pass * K4 + i] = *reinterpret_cast<const uint4*>(kpage + pass * 8 * D * 2 + i * 16);
+      kb[pass * K4 + i] = stream_load16(kpage + pass * 8 * D * 2 + i * 16);
 }
 
 template <int D>
@@ -614,7 +637,7 @@ __device__ __forceinline__ void load_v(const AttendParams& p, const Lanes<D>& ln
   constexpr int RPL = Lanes<D>::RPL;
   const char* vpage = page_base<D>(p, pr) + kPage * D * 2 + ln.voff;
 #pragma unroll
-  for (int i = 0; i < RPL; ++i) vb[i] = *reinterpret_cast<const uint32_t*>(vpage + i * D * 2);
+  for (int i = 0; i < RPL; ++i) vb[i] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(vpage + i * D * 2));
 }
 
 // Reduce-scatter of the 8 lanes that share two K rows: on entry a[h] / b[h]
@@ -766,12 +789,43 @@ __device__ __forceinline__ void pv_page(const Lanes<D>& ln, const uint32_t (&vb)
   wave_lds_sync();
 }
 
+// se_decode_step_quest's selection inside the attention kernel (one work-group
+// per unit): the candidates' block-table row and page scores live in the
+// weight buffer, unused by Quest; the selection goes to sel and is read back by
+// the page staging.
+template <int NT, int D, int G>
+__device__ __forceinline__ void fused_quest_select(const AttendParams& p, int unit, int req, int kvh, int L,
+                                                             bool bad, float* lds_w, const EvictScratch<NT>& esc,
+                                                             int* lds_scan) {
+  const int tid = threadIdx.x;
+  const int Hq = p.hkv * G;
+  int32_t* sel_out = const_cast<int32_t*>(p.sel) + (size_t)unit * p.top_k;
+  const int n_cand = bad ? 0 : L / kPage;  // complete pages before the current one
+  int* const sbt = reinterpret_cast<int*>(lds_w);
+  float* const ssc = lds_w + kSelectMaxPages;
+  int badc = 0;
+  for (int i = tid; i < n_cand; i += NT) {
+    int ph = p.block_table[(size_t)unit * p.max_pages + i];
+    if (ph < 0 || (int64_t)ph >= p.num_pages) {
+      badc = 1;
+      ph = -1;
+    }
+    sbt[i] = ph;
+  }
+  if (badc) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
+  __syncthreads();
+  unit_bounds<NT, D, G>(p.meta, p.q + ((size_t)req * Hq + (size_t)kvh * G) * D, p.scale, n_cand, sbt, ssc, nullptr);
+  __syncthreads();
+  unit_topk<NT>(n_cand, p.top_k, ssc, sel_out, nullptr, esc.hist, lds_scan, esc.bcast);
+  __syncthreads();
+}
+
 // kWaveRows: the fused steady eviction keeps each wavefront's own slots
 // (finish_steady; units of at most kWaveRowsPages pages), else thread-strided
 // slots (finish_steady_strided).  Two instantiations, chosen on the host from
 // the step's length bound, since carrying both paths costs the shorter one
 // registers.
-template <int D, int G, int NT, bool kWaveRows>
+template <int D, int G, int NT, bool kWaveRows, bool kQuest>
 __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams p) {
   constexpr int NW = NT / kWave;  // wavefronts per work-group
   using LN = Lanes<D>;
@@ -802,7 +856,8 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   const int split = blockIdx.x - uslot * p.n_split;
   const UnitGeom g = unit_geom(p, unit);
   const int req = g.req, kvh = g.kvh, L = g.L, Lp = g.Lp, cur_page = g.cur_page;
-  const bool append = g.append, quest = g.quest, bad = g.bad;
+  const bool append = g.append, bad = g.bad;
+  constexpr bool quest = kQuest;  // a selection is given (sel != nullptr) exactly in the kQuest instantiations
   const int Hq = p.hkv * G;
   const int vbeg = split * p.pps;
   const int vend = min(vbeg + p.pps, g.n_visit);
@@ -850,27 +905,8 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   // ---- fused Quest selection (se_decode_step_quest; one work-group per unit):
   // the candidates' block-table row and page scores live in the weight buffer,
   // unused by Quest; the selection goes to sel and is read back below
-  if (p.select) {
-    int32_t* sel_out = const_cast<int32_t*>(p.sel) + (size_t)unit * p.top_k;
-    const int n_cand = bad ? 0 : L / kPage;  // complete pages before the current one
-    int* const sbt = reinterpret_cast<int*>(lds_w);
-    float* const ssc = lds_w + kSelectMaxPages;
-    int badc = 0;
-    for (int i = tid; i < n_cand; i += NT) {
-      int ph = p.block_table[(size_t)unit * p.max_pages + i];
-      if (ph < 0 || (int64_t)ph >= p.num_pages) {
-        badc = 1;
-        ph = -1;
-      }
-      sbt[i] = ph;
-    }
-    if (badc) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
-    __syncthreads();
-    unit_bounds<NT, D, G>(p.meta, p.q + ((size_t)req * Hq + (size_t)kvh * G) * D, p.scale, n_cand, sbt, ssc,
-                          nullptr);
-    __syncthreads();
-    unit_topk<NT>(n_cand, p.top_k, ssc, sel_out, nullptr, esc.hist, lds_scan, esc.bcast);
-    __syncthreads();
+  if constexpr (kQuest) {
+    if (p.select) fused_quest_select<NT, D, G>(p, unit, req, kvh, L, bad, lds_w, esc, lds_scan);
   }
 
   // ---- this work-group's pages: visit index, logical and physical ids of the
@@ -984,6 +1020,9 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
         if (p.score_pool != nullptr) p.score_pool[(size_t)ph * kPage + rn] = 0.f;
       }
       __builtin_amdgcn_s_waitcnt(0);  // the stores are done before this wavefront reads the page
+      // and no load of the page may be scheduled above them: the stream reads the
+      // pool through other pointer types than the append writes it
+      asm volatile("" ::: "memory");
     }
   }
 
@@ -1085,9 +1124,16 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   }
   __syncthreads();
 
-  // ---- work-group partial (fixed wavefront order)
+  // ---- work-group partial (fixed wavefront order).  A unit's output and lse
+  // are stored at the very end of the kernel: a barrier waits for the
+  // work-group's outstanding stores, which under a full memory system take tens
+  // of microseconds.
   const bool single = p.n_split == 1;
   float* part_u = p.part + (size_t)unit * p.n_split * G * (D + 2);
+  constexpr int OPT = (G * D + NT - 1) / NT;  // outputs per thread
+  float out_v[OPT], lse_v[OPT];
+#pragma unroll
+  for (int k = 0; k < OPT; ++k) out_v[k] = lse_v[k] = 0.f;
   for (int idx = tid; idx < G * D; idx += NT) {
     const int h = idx / D;
     const int c = idx - h * D;
@@ -1103,9 +1149,9 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
     }
     if (single) {
       if (!bad) {
-        p.out[((size_t)req * Hq + kvh * G + h) * D + c] = o / l;
+        out_v[(idx - tid) / NT] = o / l;
         if (c == 0) {
-          if (p.lse != nullptr) p.lse[(size_t)req * Hq + kvh * G + h] = (ms + __log2f(l)) * kLn2;
+          lse_v[(idx - tid) / NT] = (ms + __log2f(l)) * kLn2;
           fin_m[h] = ms;
           fin_il[h] = 1.f / l;
         }
@@ -1137,15 +1183,28 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
     }
     __syncthreads();
   }
+  bool general;
   if (kWaveRows && steady) {
     const WeightSrc<W> wsrc{lds_wh, lds_mr, p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G, wcap};
-    finish_steady<NT, G, D, W>(p, g, fin_m, fin_il, lds_phys, lds_vp, wsrc, spos, su, rbeg, wr, n_my,
-                                        esc);
+    general = finish_steady<NT, G, D, W>(p, g, fin_m, fin_il, lds_phys, lds_vp, wsrc, spos, su, rbeg, wr, n_my,
+                                         esc);
   } else if (!kWaveRows && steady_any) {
     const WeightSrc<W> wsrc{lds_wh, lds_mr, p.pbuf + ubase_p * kPage * G, p.mref + ubase_p * G, wcap};
-    finish_steady_strided<NT, G, D, W>(p, g, fin_m, fin_il, lds_phys, wsrc, esc);
+    general = finish_steady_strided<NT, G, D, W>(p, g, fin_m, fin_il, lds_phys, wsrc, esc);
   } else {
-    finish_unit<NT, G, D, true, W>(p, g, fin_m, fin_il, lds_wh, lds_mr, wcap, &esc);
+    general = finish_unit<NT, G, !kQuest, W>(p, g, fin_m, fin_il, lds_wh, lds_mr, wcap);
+  }
+  if constexpr (!kQuest) {
+    if (__builtin_expect(general, false)) evict_in_epilogue<NT, D>(p, g, esc);
+  }
+#pragma unroll
+  for (int k = 0; k < OPT; ++k) {
+    const int idx = tid + k * NT;
+    if (idx < G * D) {
+      const int h = idx / D, c = idx - h * D;
+      p.out[((size_t)req * Hq + kvh * G + h) * D + c] = out_v[k];
+      if (c == 0 && p.lse != nullptr) p.lse[(size_t)req * Hq + kvh * G + h] = lse_v[k];
+    }
   }
 }
 
@@ -1223,7 +1282,7 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(const A
     }
   }
   __syncthreads();
-  finish_unit<kCombineThreads, G, D, false, float>(p, g, fin_m, fin_il, nullptr, nullptr, 0, nullptr);
+  finish_unit<kCombineThreads, G, false, float>(p, g, fin_m, fin_il, nullptr, nullptr, 0);
 }
 
 // With a split, the combine pass updates the scores and publishes the appended
@@ -1248,10 +1307,12 @@ inline bool attend_wide(int num_units, int n_visit) {
 
 template <int D, int G, int NT>
 static void launch_attend_nt(const AttendParams& prm, int grid, hipStream_t stream) {
-  if (prm.n_visit_max <= wave_rows_pages<NT>())
-    hipLaunchKernelGGL((decode_attend_kernel<D, G, NT, true>), dim3(grid), dim3(NT), 0, stream, prm);
+  if (prm.sel != nullptr)  // Quest: no eviction code, per-wavefront rows are not used
+    hipLaunchKernelGGL((decode_attend_kernel<D, G, NT, false, true>), dim3(grid), dim3(NT), 0, stream, prm);
+  else if (prm.n_visit_max <= wave_rows_pages<NT>())
+    hipLaunchKernelGGL((decode_attend_kernel<D, G, NT, true, false>), dim3(grid), dim3(NT), 0, stream, prm);
   else
-    hipLaunchKernelGGL((decode_attend_kernel<D, G, NT, false>), dim3(grid), dim3(NT), 0, stream, prm);
+    hipLaunchKernelGGL((decode_attend_kernel<D, G, NT, false, false>), dim3(grid), dim3(NT), 0, stream, prm);
 }
 
 template <int D, int G>
