@@ -43,7 +43,8 @@
  *           int32 word *dev_err (atomic OR) and the affected unit is left unchanged;
  *           read and clear the word with se_read_device_errors.
  *  Numbers. K/V/q are bf16; logits, softmax and accumulation are fp32; outputs fp32.
- *  Limits.  page_size must be 16; head_dim 64 or 128; q_per_kv 1, 2 or 4.
+ *  Limits.  page_size must be 16; head_dim 64 or 128; q_per_kv 1, 2, 4 or 8
+ *           (se_accumulate_scores and se_omnikv_select: 1 .. 8).
  */
 #ifndef SPARSE_ENGINE_H
 #define SPARSE_ENGINE_H

@@ -55,8 +55,8 @@ struct AttendParams {
   const int32_t* sel;
   int32_t top_k;
   // se_decode_step_quest: the kernel selects the pages itself (Quest bound +
-  // top-k over the unit's candidate pages, which must number at most
-  // kSelectMaxPages) and writes the selection to sel before attending
+  // top-k over the unit's candidate pages; candidates plus top_k must not
+  // exceed kSelectMaxPages), attends over the selection and writes it to sel
   int32_t select;
   const uint16_t* meta;
   float scale;
@@ -148,19 +148,20 @@ __device__ __forceinline__ float slot_weight(const AttendParams& p, size_t ubase
 // scratch's holes array, which only the general eviction uses, after the
 // scores are written.
 constexpr int kWeightCap = 9216;  // 32-bit words (>= kMaxBudget ints for the holes)
-constexpr int kSelectMaxPages = kWeightCap / 2;  // fused Quest selection: block-table row + scores
+constexpr int kSelectMaxPages = kWeightCap / 2;  // fused Quest selection: block-table row + selection, scores
 constexpr int kWeightMrCap = 2 * kWeightCap / kPage;  // reference maxima: one per (visit page, head)
 template <int G, typename W>
 constexpr int kWeightPages =
     (kWeightCap * 4 / (int)sizeof(W) / (kPage * G)) < 1024 ? kWeightCap * 4 / (int)sizeof(W) / (kPage * G) : 1024;
 static_assert(kWeightCap >= kMaxBudget, "the weight buffer doubles as the holes array");
-static_assert(kWeightPages<4, _Float16> * 4 <= kWeightMrCap && kWeightPages<1, _Float16> <= kWeightMrCap,
+static_assert(kWeightPages<8, _Float16> * 8 <= kWeightMrCap && kWeightPages<4, _Float16> * 4 <= kWeightMrCap &&
+                  kWeightPages<1, _Float16> <= kWeightMrCap,
               "reference maxima");
 // The weight format of a kernel instantiation: fp32 where the units it takes
 // fit the buffer that way (the 512-thread per-wavefront steady variant, at most
-// wave_rows_pages pages), fp16 elsewhere (twice the pages).
-template <int NT, bool kWaveRows>
-using WeightT = typename std::conditional<kWaveRows && NT == 512, float, _Float16>::type;
+// wave_rows_pages pages, groups of up to 4), fp16 elsewhere (twice the pages).
+template <int NT, bool kWaveRows, int G>
+using WeightT = typename std::conditional<kWaveRows && NT == 512 && G <= 4, float, _Float16>::type;
 
 // Where the score update finds the weights: visit pages below `cap` in the
 // work-group's LDS buffer, the others in the workspace rows (global).
@@ -584,6 +585,14 @@ struct PageRef {
   int rn;      // row of the appended token in this page, or -1
 };
 
+// (row, head) pairs a lane keeps per page: heads own_head + 4k, k < kPairs.
+// Groups of 8 take two passes of the 4-head reduction over the same K
+// registers.
+template <int G>
+constexpr int kPairs = G > 4 ? G / 4 : 1;
+template <int G>
+constexpr int kPassHeads = G < 4 ? G : 4;  // heads per pass
+
 // Lane coordinates of the two layouts (see the kernel).
 template <int D>
 struct Lanes {
@@ -670,7 +679,7 @@ __device__ __forceinline__ float row_reduce_scatter(const float (&a)[G], const f
     const float kk = b0 ? t1 : t0, ss = b0 ? t0 : t1;
     return kk + dpp_f<kQuadXor1>(ss);
   } else {
-    static_assert(G == 1, "groups of 1, 2 or 4 query heads");
+    static_assert(G == 1, "passes of 1, 2 or 4 query heads");
     const float t = k[0] + dpp_f<kQuadXor2>(k[0]);
     return t + dpp_f<kQuadXor1>(t);
   }
@@ -683,85 +692,107 @@ template <int G>
 struct WaveSoftmax {
   float m_ref[G];
   float o_acc[G][2];
-  float l_own;
-  float m_own;  // m_ref of the lane's own head
+  float l_own[kPairs<G>];
+  float m_own[kPairs<G>];  // m_ref of the lane's heads
 };
 
-// Logits of the lane's (row, head) pair for one page.  The query rows are read
-// from LDS (one copy per work-group) instead of being held in registers, which
-// leaves room for a second page in flight.
+// Logits of the lane's (row, head) pairs for one page, one pass of up to four
+// heads at a time over the K registers.  The query rows are read from LDS (one
+// copy per work-group) instead of being held in registers, which leaves room
+// for a second page in flight.
 template <int D, int G>
-__device__ __forceinline__ float qk_page(const Lanes<D>& ln, const uint4 (&kb)[2 * Lanes<D>::K4],
-                                         const uint32_t (*lds_q)[D / 2]) {
-  constexpr int K4 = Lanes<D>::K4, QW = Lanes<D>::QW;
-  float accA[G], accB[G];
+__device__ __forceinline__ void qk_page(const Lanes<D>& ln, const uint4 (&kb)[2 * Lanes<D>::K4],
+                                        const uint32_t (*lds_q)[D / 2], float (&z)[kPairs<G>]) {
+  constexpr int K4 = Lanes<D>::K4, QW = Lanes<D>::QW, GH = kPassHeads<G>;
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
-    accA[h] = 0.f;
-    accB[h] = 0.f;
-  }
+  for (int k = 0; k < kPairs<G>; ++k) {
+    float accA[GH], accB[GH];
 #pragma unroll
-  for (int i = 0; i < K4; ++i) {
-    const uint32_t ka[4] = {kb[i].x, kb[i].y, kb[i].z, kb[i].w};
-    const uint32_t kc[4] = {kb[K4 + i].x, kb[K4 + i].y, kb[K4 + i].z, kb[K4 + i].w};
+    for (int h = 0; h < GH; ++h) {
+      accA[h] = 0.f;
+      accB[h] = 0.f;
+    }
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const uint4 qv = reinterpret_cast<const uint4*>(&lds_q[h][ln.j8 * QW])[i];
-      const uint32_t qw[4] = {qv.x, qv.y, qv.z, qv.w};
+    for (int i = 0; i < K4; ++i) {
+      const uint32_t ka[4] = {kb[i].x, kb[i].y, kb[i].z, kb[i].w};
+      const uint32_t kc[4] = {kb[K4 + i].x, kb[K4 + i].y, kb[K4 + i].z, kb[K4 + i].w};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        accA[h] = dot2bf16(qw[e], ka[e], accA[h]);
-        accB[h] = dot2bf16(qw[e], kc[e], accB[h]);
+      for (int h = 0; h < GH; ++h) {
+        const uint4 qv = reinterpret_cast<const uint4*>(&lds_q[4 * k + h][ln.j8 * QW])[i];
+        const uint32_t qw[4] = {qv.x, qv.y, qv.z, qv.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          accA[h] = dot2bf16(qw[e], ka[e], accA[h]);
+          accB[h] = dot2bf16(qw[e], kc[e], accB[h]);
+        }
       }
     }
+    z[k] = row_reduce_scatter<GH>(accA, accB, ln.j8);
   }
-  return row_reduce_scatter<G>(accA, accB, ln.j8);
 }
 
 // Reference update, weight of the lane's pair, its workspace copy, and the
 // weights' broadcast through LDS (the page's PV follows).
 template <int D, int G, typename W>
-__device__ __forceinline__ float softmax_page(const AttendParams& p, const Lanes<D>& ln,
-                                              const PageRef& pr, float z, WaveSoftmax<G>& ws,
-                                              float* lds_pw, int lane, int unit, size_t ubase_p,
-                                              W* lds_w, float* lds_mr, int wcap) {
+__device__ __forceinline__ void softmax_page(const AttendParams& p, const Lanes<D>& ln,
+                                             const PageRef& pr, const float (&z)[kPairs<G>], WaveSoftmax<G>& ws,
+                                             float* lds_pw, int lane, int unit, size_t ubase_p,
+                                             W* lds_w, float* lds_mr, int wcap) {
+  constexpr int NP = kPairs<G>, GH = kPassHeads<G>;
   constexpr float kBump = 8.0f;  // rescale only when a logit beats the reference by 2^8
   const bool valid = ln.owns && ln.own_row < pr.nrows;
-  const float z2 = valid ? z * p.scale_log2 : -INFINITY;
-  if (p.logits != nullptr && valid)
-    p.logits[((size_t)unit * G + ln.own_head) * p.logits_stride + pr.lp * kPage + ln.own_row] = z * p.scale;
-  const bool need = valid && (z2 > ws.m_own + kBump);
-  if (__ballot(need) != 0) {
-    float mx = z2;  // lanes of one head differ in lane bits 2..5
-    mx = fmaxf(mx, shfl_xor_f(mx, 4));
-    mx = fmaxf(mx, shfl_xor_f(mx, 8));
-    mx = fmaxf(mx, shfl_xor_f(mx, 16));
-    mx = fmaxf(mx, shfl_xor_f(mx, 32));
-    // lane h (< G) is row 0 of head h, so it holds head h's page maximum
+  float z2[NP];
+  bool need = false;
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float mh = fmaxf(ws.m_ref[h], __shfl(mx, h, kWave));
-      const float f = fast_exp2(ws.m_ref[h] - mh);
-      ws.o_acc[h][0] *= f;
-      ws.o_acc[h][1] *= f;
-      ws.m_ref[h] = mh;
+  for (int k = 0; k < NP; ++k) {
+    z2[k] = valid ? z[k] * p.scale_log2 : -INFINITY;
+    if (p.logits != nullptr && valid)
+      p.logits[((size_t)unit * G + ln.own_head + 4 * k) * p.logits_stride + pr.lp * kPage + ln.own_row] =
+          z[k] * p.scale;
+    need = need || (valid && (z2[k] > ws.m_own[k] + kBump));
+  }
+  if (__ballot(need) != 0) {
+#pragma unroll
+    for (int k = 0; k < NP; ++k) {
+      float mx = z2[k];  // lanes of one head differ in lane bits 2..5
+      mx = fmaxf(mx, shfl_xor_f(mx, 4));
+      mx = fmaxf(mx, shfl_xor_f(mx, 8));
+      mx = fmaxf(mx, shfl_xor_f(mx, 16));
+      mx = fmaxf(mx, shfl_xor_f(mx, 32));
+      // lane h (< GH) is row 0 of head 4k + h, so it holds that head's page maximum
+#pragma unroll
+      for (int h = 0; h < GH; ++h) {
+        const int hh = 4 * k + h;
+        const float mh = fmaxf(ws.m_ref[hh], __shfl(mx, h, kWave));
+        const float f = fast_exp2(ws.m_ref[hh] - mh);
+        ws.o_acc[hh][0] *= f;
+        ws.o_acc[hh][1] *= f;
+        ws.m_ref[hh] = mh;
+      }
+      const float m_new = fmaxf(ws.m_own[k], mx);
+      ws.l_own[k] *= fast_exp2(ws.m_own[k] - m_new);
+      ws.m_own[k] = m_new;
     }
-    const float m_new = fmaxf(ws.m_own, mx);
-    ws.l_own *= fast_exp2(ws.m_own - m_new);
-    ws.m_own = m_new;
   }
-  const float pj = valid ? fast_exp2(z2 - ws.m_own) : 0.f;
-  ws.l_own += pj;
-  if (pr.vp < wcap) {
-    if (ln.owns) lds_w[(pr.vp * kPage + ln.own_row) * G + ln.own_head] = (W)pj;
-    if (lane < G) lds_mr[pr.vp * G + lane] = ws.m_own;
-  } else if (p.accumulate) {
-    if (ln.owns) p.pbuf[((ubase_p + pr.vp) * kPage + ln.own_row) * G + ln.own_head] = pj;
-    if (lane < G) p.mref[(ubase_p + pr.vp) * G + lane] = ws.m_own;
+  float pj[NP];
+#pragma unroll
+  for (int k = 0; k < NP; ++k) {
+    pj[k] = valid ? fast_exp2(z2[k] - ws.m_own[k]) : 0.f;
+    ws.l_own[k] += pj[k];
   }
-  if (ln.owns) lds_pw[ln.own_row * G + ln.own_head] = pj;
+#pragma unroll
+  for (int k = 0; k < NP; ++k) {
+    const int hh = ln.own_head + 4 * k;
+    if (pr.vp < wcap) {
+      if (ln.owns) lds_w[(pr.vp * kPage + ln.own_row) * G + hh] = (W)pj[k];
+      if (lane < GH) lds_mr[pr.vp * G + lane + 4 * k] = ws.m_own[k];
+    } else if (p.accumulate) {
+      if (ln.owns) p.pbuf[((ubase_p + pr.vp) * kPage + ln.own_row) * G + hh] = pj[k];
+      if (lane < GH) p.mref[(ubase_p + pr.vp) * G + lane + 4 * k] = ws.m_own[k];
+    }
+    if (ln.owns) lds_pw[ln.own_row * G + hh] = pj[k];
+  }
   wave_lds_sync();
-  return pj;
 }
 
 // o += P V for one page, the weights read back from LDS.
@@ -790,18 +821,20 @@ __device__ __forceinline__ void pv_page(const Lanes<D>& ln, const uint32_t (&vb)
 }
 
 // se_decode_step_quest's selection inside the attention kernel (one work-group
-// per unit): the candidates' block-table row and page scores live in the
-// weight buffer, unused by Quest; the selection goes to sel and is read back by
-// the page staging.
+// per unit): the candidates' block-table row, the selection after it and the
+// page scores live in the weight buffer, unused by Quest.  The page staging
+// reads the selection and the selected pages' physical ids from there, and
+// the selection goes to sel at the end of the kernel (a store before a
+// barrier would hold the barrier until it completes).  Returns the selection
+// in LDS.
 template <int NT, int D, int G>
-__device__ __forceinline__ void fused_quest_select(const AttendParams& p, int unit, int req, int kvh, int L,
-                                                             bool bad, float* lds_w, const EvictScratch<NT>& esc,
-                                                             int* lds_scan) {
+__device__ __forceinline__ const int* fused_quest_select(const AttendParams& p, int unit, int req, int kvh,
+                                                         int n_cand, float* lds_w, const EvictScratch<NT>& esc,
+                                                         int* lds_scan) {
   const int tid = threadIdx.x;
   const int Hq = p.hkv * G;
-  int32_t* sel_out = const_cast<int32_t*>(p.sel) + (size_t)unit * p.top_k;
-  const int n_cand = bad ? 0 : L / kPage;  // complete pages before the current one
   int* const sbt = reinterpret_cast<int*>(lds_w);
+  int* const ssel = sbt + n_cand;  // n_cand + top_k <= kSelectMaxPages
   float* const ssc = lds_w + kSelectMaxPages;
   int badc = 0;
   for (int i = tid; i < n_cand; i += NT) {
@@ -816,8 +849,9 @@ __device__ __forceinline__ void fused_quest_select(const AttendParams& p, int un
   __syncthreads();
   unit_bounds<NT, D, G>(p.meta, p.q + ((size_t)req * Hq + (size_t)kvh * G) * D, p.scale, n_cand, sbt, ssc, nullptr);
   __syncthreads();
-  unit_topk<NT>(n_cand, p.top_k, ssc, sel_out, nullptr, esc.hist, lds_scan, esc.bcast);
+  unit_topk<NT>(n_cand, p.top_k, ssc, nullptr, ssel, esc.hist, lds_scan, esc.bcast);
   __syncthreads();
+  return ssel;
 }
 
 // kWaveRows: the fused steady eviction keeps each wavefront's own slots
@@ -831,10 +865,15 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   using LN = Lanes<D>;
   constexpr int QC = LN::QC, QW = LN::QW, K4 = LN::K4, RS = LN::RS, RPL = LN::RPL, HP = LN::HP;
 
+  constexpr int NP = kPairs<G>, GH = kPassHeads<G>;
+  // the wavefronts' partial outputs go through LDS up to four heads at a time
+  // (groups of 8 take two rounds), which keeps the work-group's LDS within two
+  // work-groups per compute unit
+  constexpr int GO = GH, NRND = G / GO;
   __shared__ float lds_p[NW][kPage * G];
   __shared__ float lds_m[NW][G];
   __shared__ float lds_l[NW][G];
-  __shared__ float lds_o[NW][G][D];
+  __shared__ float lds_o[NW][GO][D];
   __shared__ float fin_m[G];
   __shared__ float fin_il[G];
   __shared__ int lds_phys[kMaxGroupPages];
@@ -843,7 +882,7 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   __shared__ uint32_t lds_q[G][D / 2];  // the unit's G query rows (bf16 pairs)
   __shared__ float lds_w[kWeightCap];    // per-slot weights, then the eviction's holes
   __shared__ float lds_mr[kWeightMrCap];
-  using W = WeightT<NT, kWaveRows>;
+  using W = WeightT<NT, kWaveRows, G>;
   W* const lds_wh = reinterpret_cast<W*>(lds_w);
   SE_EVICT_SCRATCH_WITH_HOLES(NT, esc, reinterpret_cast<int*>(lds_w));
   __shared__ int lds_scan[NT / kWave + 1];
@@ -863,14 +902,16 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   const int vend = min(vbeg + p.pps, g.n_visit);
   const size_t ubase_p = (size_t)unit * p.n_visit_max;  // page-indexed workspace rows
   // the score update's weights of visit pages below wcap stay in LDS (this
-  // work-group holds the whole unit); the rest go to the workspace
-  const int wcap = (p.accumulate && p.n_split == 1) ? kWeightPages<G, W> : 0;
+  // work-group holds the whole unit); the rest go to the workspace.  The fused
+  // Quest selection keeps its results in the same buffer (and never accumulates).
+  const bool select = kQuest && p.select;
+  const int wcap = (p.accumulate && p.n_split == 1 && !select) ? kWeightPages<G, W> : 0;
 
   // QK layout: lane = 8*r8 + j8 reads columns [j8*QC, (j8+1)*QC) of rows r8
   // (pass A) and r8 + 8 (pass B).  After the 8-lane reduction, lane j8 < 4
   // keeps head j8 of row r8 and lane j8 >= 4 head j8-4 of row r8+8: each lane
-  // owns one (row, head) pair of the page.  PV layout: two adjacent columns,
-  // RPL rows.
+  // owns one (row, head) pair of the page per pass of four heads.  PV layout:
+  // two adjacent columns, RPL rows.
   LN ln;
   ln.r8 = lane >> 3;
   ln.j8 = lane & 7;
@@ -896,18 +937,33 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
     ws.o_acc[h][0] = 0.f;
     ws.o_acc[h][1] = 0.f;
   }
-  ws.l_own = 0.f;
-  ws.m_own = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < NP; ++k) {
+    ws.l_own[k] = 0.f;
+    ws.m_own[k] = -INFINITY;
+  }
 
   const uint16_t* knew_row = append ? p.k_new + ((size_t)req * p.hkv + kvh) * D : nullptr;
   const uint16_t* vnew_row = append ? p.v_new + ((size_t)req * p.hkv + kvh) * D : nullptr;
 
-  // ---- fused Quest selection (se_decode_step_quest; one work-group per unit):
-  // the candidates' block-table row and page scores live in the weight buffer,
-  // unused by Quest; the selection goes to sel and is read back below
+  // ---- fused Quest selection (se_decode_step_quest; one work-group per unit).
+  // The current page's physical id is fetched first: its load overlaps the
+  // selection.
+  const int n_cand = select && !bad ? L / kPage : 0;  // complete pages before the current one
+  const int* lds_sel = nullptr;
+  int ph_cur = -1;
   if constexpr (kQuest) {
-    if (p.select) fused_quest_select<NT, D, G>(p, unit, req, kvh, L, bad, lds_w, esc, lds_scan);
+    if (select) {
+      if (!bad) ph_cur = p.block_table[(size_t)unit * p.max_pages + cur_page];
+      lds_sel = fused_quest_select<NT, D, G>(p, unit, req, kvh, n_cand, lds_w, esc, lds_scan);
+    }
   }
+  auto store_sel = [&]() {
+    if constexpr (kQuest) {
+      if (select)
+        for (int i = tid; i < p.top_k; i += NT) const_cast<int32_t*>(p.sel)[(size_t)unit * p.top_k + i] = lds_sel[i];
+    }
+  };
 
   // ---- this work-group's pages: visit index, logical and physical ids of the
   // pages it must read, compacted and staged in LDS once, so the page stream
@@ -923,7 +979,7 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
     if (i < n_range) {
       bool ok = true;
       if (quest) {
-        lp = vp < p.top_k ? p.sel[(size_t)unit * p.top_k + vp] : cur_page;
+        lp = vp < p.top_k ? (select ? lds_sel[vp] : p.sel[(size_t)unit * p.top_k + vp]) : cur_page;
         if (lp < 0) ok = false;
         if (lp >= 0 && vp < p.top_k && lp >= cur_page) {
           bad_sel = true;
@@ -931,7 +987,10 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
         }
       }
       if (ok) {
-        ph = p.block_table[(size_t)unit * p.max_pages + lp];
+        if (select)  // the selected pages' ids are in the staged block-table row
+          ph = lp < n_cand ? reinterpret_cast<const int*>(lds_w)[lp] : ph_cur;
+        else
+          ph = p.block_table[(size_t)unit * p.max_pages + lp];
         if (ph < 0 || (int64_t)ph >= p.num_pages) {
           bad_page = true;
           ph = -1;
@@ -1058,7 +1117,8 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
     for (int i = 0; i < n_my; i += 2) {
       {
         const PageRef nx2 = ref_or_tail(i + 2);
-        const float z = qk_page<D, G>(ln, kbA, lds_q);
+        float z[NP];
+        qk_page<D, G>(ln, kbA, lds_q, z);
         load_k<D>(p, ln, nx2, kbA);
         softmax_page<D, G, W>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p, lds_wh, lds_mr, wcap);
         pv_page<D, G>(ln, vb, cur.nrows, ws, lds_p[wave]);
@@ -1069,7 +1129,8 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
       if (i + 1 >= n_my) break;
       {
         const PageRef nx2 = ref_or_tail(i + 3);
-        const float z = qk_page<D, G>(ln, kbB, lds_q);
+        float z[NP];
+        qk_page<D, G>(ln, kbB, lds_q, z);
         load_k<D>(p, ln, nx2, kbB);
         softmax_page<D, G, W>(p, ln, cur, z, ws, lds_p[wave], lane, unit, ubase_p, lds_wh, lds_mr, wcap);
         pv_page<D, G>(ln, vb, cur.nrows, ws, lds_p[wave]);
@@ -1085,7 +1146,8 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   // re-read a valid slot), while other wavefronts may still be streaming
   const bool steady_any = p.evict && p.accumulate && !quest && !bad && p.n_split == 1 && Lp == p.budget + 1 &&
                           Lp <= kMaxBudget && n_grp == g.n_visit;
-  const bool steady = kWaveRows && steady_any && (max_rcnt + 3) / 4 <= 4 * kSteadyRows;
+  const bool steady = kWaveRows && steady_any && (max_rcnt + 3) / 4 <= 4 * kSteadyRows &&
+                      g.n_visit <= kWeightPages<G, W>;
   int32_t spos[kSteadyRows];
   float su[kSteadyRows];
   if (kWaveRows && steady && n_my > 0) {
@@ -1099,11 +1161,15 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   }
 
   // ---- per-wavefront totals into LDS
-  float lsum = ws.l_own;  // lanes of one head differ in lane bits 2..5
-  lsum += shfl_xor_f(lsum, 4);
-  lsum += shfl_xor_f(lsum, 8);
-  lsum += shfl_xor_f(lsum, 16);
-  lsum += shfl_xor_f(lsum, 32);
+  float lsum[NP];
+#pragma unroll
+  for (int k = 0; k < NP; ++k) {
+    lsum[k] = ws.l_own[k];  // lanes of one head differ in lane bits 2..5
+    lsum[k] += shfl_xor_f(lsum[k], 4);
+    lsum[k] += shfl_xor_f(lsum[k], 8);
+    lsum[k] += shfl_xor_f(lsum[k], 16);
+    lsum[k] += shfl_xor_f(lsum[k], 32);
+  }
   if (RS == 2) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
@@ -1111,58 +1177,67 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
       ws.o_acc[h][1] += shfl_xor_f(ws.o_acc[h][1], 32);
     }
   }
-  if (lane < G) {
-    lds_m[wave][lane] = ws.m_own;
-    lds_l[wave][lane] = lsum;
-  }
-  if (lane < HP) {
+  if (lane < GH) {
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      lds_o[wave][h][col] = ws.o_acc[h][0];
-      lds_o[wave][h][col + 1] = ws.o_acc[h][1];
+    for (int k = 0; k < NP; ++k) {
+      lds_m[wave][lane + 4 * k] = ws.m_own[k];
+      lds_l[wave][lane + 4 * k] = lsum[k];
     }
   }
-  __syncthreads();
 
-  // ---- work-group partial (fixed wavefront order).  A unit's output and lse
-  // are stored at the very end of the kernel: a barrier waits for the
-  // work-group's outstanding stores, which under a full memory system take tens
-  // of microseconds.
+  // ---- work-group partial (fixed wavefront order), GO heads per round.  A
+  // unit's output and lse are stored at the very end of the kernel: a barrier
+  // waits for the work-group's outstanding stores, which under a full memory
+  // system take tens of microseconds.
   const bool single = p.n_split == 1;
   float* part_u = p.part + (size_t)unit * p.n_split * G * (D + 2);
-  constexpr int OPT = (G * D + NT - 1) / NT;  // outputs per thread
+  constexpr int OPR = (GO * D + NT - 1) / NT;  // outputs per thread and round
+  constexpr int OPT = NRND * OPR;
   float out_v[OPT], lse_v[OPT];
 #pragma unroll
   for (int k = 0; k < OPT; ++k) out_v[k] = lse_v[k] = 0.f;
-  for (int idx = tid; idx < G * D; idx += NT) {
-    const int h = idx / D;
-    const int c = idx - h * D;
-    float ms = lds_m[0][h];
 #pragma unroll
-    for (int w = 1; w < NW; ++w) ms = fmaxf(ms, lds_m[w][h]);
-    float o = 0.f, l = 0.f;
+  for (int rnd = 0; rnd < NRND; ++rnd) {
+    if (rnd > 0) __syncthreads();  // the previous round's reads of lds_o
+    if (lane < HP) {
 #pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      const float f = lds_m[w][h] == -INFINITY ? 0.f : fast_exp2(lds_m[w][h] - ms);
-      o += lds_o[w][h][c] * f;
-      l += lds_l[w][h] * f;
+      for (int h = 0; h < GO; ++h) {
+        lds_o[wave][h][col] = ws.o_acc[rnd * GO + h][0];
+        lds_o[wave][h][col + 1] = ws.o_acc[rnd * GO + h][1];
+      }
     }
-    if (single) {
-      if (!bad) {
-        out_v[(idx - tid) / NT] = o / l;
-        if (c == 0) {
-          lse_v[(idx - tid) / NT] = (ms + __log2f(l)) * kLn2;
-          fin_m[h] = ms;
-          fin_il[h] = 1.f / l;
+    __syncthreads();
+    for (int idx = tid; idx < GO * D; idx += NT) {
+      const int ho = idx / D;
+      const int h = rnd * GO + ho;
+      const int c = idx - ho * D;
+      float ms = lds_m[0][h];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) ms = fmaxf(ms, lds_m[w][h]);
+      float o = 0.f, l = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        const float f = lds_m[w][h] == -INFINITY ? 0.f : fast_exp2(lds_m[w][h] - ms);
+        o += lds_o[w][ho][c] * f;
+        l += lds_l[w][h] * f;
+      }
+      if (single) {
+        if (!bad) {
+          out_v[rnd * OPR + (idx - tid) / NT] = o / l;
+          if (c == 0) {
+            lse_v[rnd * OPR + (idx - tid) / NT] = (ms + __log2f(l)) * kLn2;
+            fin_m[h] = ms;
+            fin_il[h] = 1.f / l;
+          }
         }
+      } else {
+        float* rec = part_u + ((size_t)split * G + h) * (D + 2);
+        if (c == 0) {
+          rec[0] = ms;
+          rec[1] = l;
+        }
+        rec[2 + c] = o;
       }
-    } else {
-      float* rec = part_u + ((size_t)split * G + h) * (D + 2);
-      if (c == 0) {
-        rec[0] = ms;
-        rec[1] = l;
-      }
-      rec[2 + c] = o;
     }
   }
 
@@ -1170,6 +1245,7 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   __syncthreads();
   if (bad) {
     if (tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_LENGTH);
+    store_sel();
     return;
   }
   if (wcap > 0) {
@@ -1198,14 +1274,19 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
     if (__builtin_expect(general, false)) evict_in_epilogue<NT, D>(p, g, esc);
   }
 #pragma unroll
-  for (int k = 0; k < OPT; ++k) {
-    const int idx = tid + k * NT;
-    if (idx < G * D) {
-      const int h = idx / D, c = idx - h * D;
-      p.out[((size_t)req * Hq + kvh * G + h) * D + c] = out_v[k];
-      if (c == 0 && p.lse != nullptr) p.lse[(size_t)req * Hq + kvh * G + h] = lse_v[k];
+  for (int rnd = 0; rnd < NRND; ++rnd) {
+#pragma unroll
+    for (int k = 0; k < OPR; ++k) {
+      const int idx = tid + k * NT;
+      if (idx < GO * D) {
+        const int ho = idx / D, c = idx - ho * D;
+        const int h = rnd * GO + ho;
+        p.out[((size_t)req * Hq + kvh * G + h) * D + c] = out_v[rnd * OPR + k];
+        if (c == 0 && p.lse != nullptr) p.lse[(size_t)req * Hq + kvh * G + h] = lse_v[rnd * OPR + k];
+      }
     }
   }
+  store_sel();
 }
 
 // Launch order of the units when they take more than one round of work-groups:
@@ -1290,15 +1371,18 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(const A
 // 1024-thread work-groups hold a whole long unit in registers.
 // Units of at most this many pages take the per-wavefront steady eviction: the
 // largest slot rank's share of them, over four wavefronts, fits kSteadyRows
-// rows of four pages.
-template <int NT>
+// rows of four pages, and (finish_steady reads every page's weights from LDS)
+// every page's weights fit the LDS buffer.
+template <int NT, int G>
 constexpr int wave_rows_pages() {
-  return (4 * 4 * kSteadyRows * 100 - 50) / RankWeights<NT / kWave / 4>::w[0];
+  constexpr int rows = (4 * 4 * kSteadyRows * 100 - 50) / RankWeights<NT / kWave / 4>::w[0];
+  constexpr int lds = kWeightPages<G, WeightT<NT, true, G>>;
+  return rows < lds ? rows : lds;
 }
-// finish_steady reads every page's weights from LDS
-static_assert(wave_rows_pages<kAttendThreads>() <= kWeightPages<4, WeightT<kAttendThreads, true>> &&
-                  wave_rows_pages<kAttendThreadsWide>() <= kWeightPages<4, WeightT<kAttendThreadsWide, true>>,
-              "the per-wavefront steady eviction needs every weight in LDS");
+// groups of up to 4 are limited by the registers alone
+static_assert(wave_rows_pages<kAttendThreads, 4>() == (4 * 4 * kSteadyRows * 100 - 50) / RankWeights<2>::w[0] &&
+                  wave_rows_pages<kAttendThreadsWide, 4>() == (4 * 4 * kSteadyRows * 100 - 50) / RankWeights<4>::w[0],
+              "per-wavefront steady eviction bounds");
 
 // Launches with at most one work-group per compute unit take 1024 threads.
 inline bool attend_wide(int num_units, int n_visit) {
@@ -1309,7 +1393,7 @@ template <int D, int G, int NT>
 static void launch_attend_nt(const AttendParams& prm, int grid, hipStream_t stream) {
   if (prm.sel != nullptr)  // Quest: no eviction code, per-wavefront rows are not used
     hipLaunchKernelGGL((decode_attend_kernel<D, G, NT, false, true>), dim3(grid), dim3(NT), 0, stream, prm);
-  else if (prm.n_visit_max <= wave_rows_pages<NT>())
+  else if (prm.n_visit_max <= wave_rows_pages<NT, G>())
     hipLaunchKernelGGL((decode_attend_kernel<D, G, NT, true, false>), dim3(grid), dim3(NT), 0, stream, prm);
   else
     hipLaunchKernelGGL((decode_attend_kernel<D, G, NT, false, false>), dim3(grid), dim3(NT), 0, stream, prm);
@@ -1374,7 +1458,7 @@ static se_status attend_launch(const se_kv_view* kv, int32_t q_per_kv, const voi
                                hipStream_t stream, const AttendParams* fused_evict) {
   se_status st = check_view(kv);
   if (st != SE_OK) return st;
-  if (q_per_kv != 1 && q_per_kv != 2 && q_per_kv != 4) return SE_ERR_UNSUPPORTED;
+  if (q_per_kv != 1 && q_per_kv != 2 && q_per_kv != 4 && q_per_kv != 8) return SE_ERR_UNSUPPORTED;
   if (q == nullptr || out == nullptr || dev_err == nullptr || kv->kv_pool == nullptr)
     return SE_ERR_INVALID_ARGUMENT;
   if ((k_new == nullptr) != (v_new == nullptr)) return SE_ERR_INVALID_ARGUMENT;
@@ -1446,11 +1530,13 @@ static se_status attend_launch(const se_kv_view* kv, int32_t q_per_kv, const voi
   const int64_t grid = (int64_t)kv->num_units * s.n_split;
   if (grid > INT32_MAX) return SE_ERR_UNSUPPORTED;
   if (D == 128) {
-    if (q_per_kv == 4) launch_attend<128, 4>(prm, (int)grid, wide, stream);
+    if (q_per_kv == 8) launch_attend<128, 8>(prm, (int)grid, wide, stream);
+    else if (q_per_kv == 4) launch_attend<128, 4>(prm, (int)grid, wide, stream);
     else if (q_per_kv == 2) launch_attend<128, 2>(prm, (int)grid, wide, stream);
     else launch_attend<128, 1>(prm, (int)grid, wide, stream);
   } else {
-    if (q_per_kv == 4) launch_attend<64, 4>(prm, (int)grid, wide, stream);
+    if (q_per_kv == 8) launch_attend<64, 8>(prm, (int)grid, wide, stream);
+    else if (q_per_kv == 4) launch_attend<64, 4>(prm, (int)grid, wide, stream);
     else if (q_per_kv == 2) launch_attend<64, 2>(prm, (int)grid, wide, stream);
     else launch_attend<64, 1>(prm, (int)grid, wide, stream);
   }
@@ -1566,7 +1652,7 @@ extern "C" se_status se_decode_step_quest(const se_kv_view* kv, int32_t q_per_kv
   const SplitShape s = split_shape(kv->num_units, n_visit, wide ? 256 : 512);
   int64_t ml = max_len;
   if (ml > (int64_t)kv->max_pages * kPage) ml = (int64_t)kv->max_pages * kPage;
-  if (s.n_split == 1 && ml / kPage <= kSelectMaxPages) {
+  if (s.n_split == 1 && ml / kPage + top_k <= kSelectMaxPages) {
     AttendParams ex = {};
     ex.select = 1;
     ex.meta = static_cast<const uint16_t*>(kv->meta_pool);

@@ -5,12 +5,13 @@
 // min/max over the page's resident rows (exact on bf16 values).
 //
 // se_quest_select, two kernels:
-//   * bound: 8 lanes share one page, each owning D/8 channels of the page's
-//     min and max rows (16-byte loads).  max(q*m, q*M) = q+ * M + q- * m with
-//     q+ = max(q, 0) and q- = min(q, 0) (one of the two products is an exact
-//     zero), so the bound is two bf16 pair dot products per channel pair and
-//     needs no per-channel branch.  A 3-step lane reduction gives the page's
-//     bound per query row; the page score is the maximum over the G rows.
+//   * bound: 8 lanes share one page (16 for groups of 8 at D = 128), each
+//     owning D/8 (D/16) channels of the page's min and max rows (16-byte
+//     loads).  max(q*m, q*M) = q+ * M + q- * m with q+ = max(q, 0) and
+//     q- = min(q, 0) (one of the two products is an exact zero), so the bound
+//     is two bf16 pair dot products per channel pair and needs no per-channel
+//     branch.  A 3-step (4-step) lane reduction gives the page's bound per
+//     query row; the page score is the maximum over the G rows.
 //   * top-k: one work-group per unit, radix selection on order-preserving
 //     integer keys of the scores; equal scores keep the lower page index; the
 //     selected pages are written in ascending order by a block scan.
@@ -88,12 +89,11 @@ constexpr int kBoundPagesPerGroup = 256;
 
 template <int D, int G>
 __global__ __launch_bounds__(256) void quest_bound_kernel(const QuestParams p) {
-  constexpr int CH = D / 8;   // channels per lane
-  constexpr int CW = CH / 2;  // bf16 pairs per lane
-  constexpr int C4 = CW / 4;  // 16-byte loads per lane per row
+  using BL = BoundLanes<D, G>;
+  constexpr int CH = BL::CH, CW = BL::CW, C4 = BL::C4, LPP = BL::LPP;
+  constexpr int PPI = 256 / LPP;  // pages per iteration of the work-group
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int g = lane & 7;
+  const int g = lane & (LPP - 1);
   const int unit = blockIdx.x / p.blocks_per_unit;
   const int chunk = blockIdx.x - unit * p.blocks_per_unit;
   const int req = unit / p.hkv;
@@ -106,27 +106,10 @@ __global__ __launch_bounds__(256) void quest_bound_kernel(const QuestParams p) {
   const int b1 = min(b0 + kBoundPagesPerGroup, n_cand);
 
   uint32_t qp[G][CW], qn[G][CW];
-  {
-    const uint16_t* qb = p.q + ((size_t)req * p.hkv * G + (size_t)kvh * G) * D + g * CH;
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const uint4* src = reinterpret_cast<const uint4*>(qb + (size_t)h * D);
-#pragma unroll
-      for (int i = 0; i < C4; ++i) {
-        const uint4 t = src[i];
-        const uint32_t v[4] = {t.x, t.y, t.z, t.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          qp[h][4 * i + e] = pos_part(v[e]);
-          qn[h][4 * i + e] = neg_part(v[e]);
-        }
-      }
-    }
-  }
+  bound_query<D, G>(p.q + ((size_t)req * p.hkv * G + (size_t)kvh * G) * D, g, qp, qn);
 
-  for (int b = b0 + wave * 8 + (lane >> 3); b < b0 + kBoundPagesPerGroup; b += 32) {
+  for (int b = b0 + (int)threadIdx.x / LPP; b < b0 + kBoundPagesPerGroup; b += PPI) {
     const bool valid = b < b1;
-    float best = -INFINITY;
     if (__ballot(valid) == 0) break;
     int phys = 0;
     if (valid) {
@@ -137,37 +120,15 @@ __global__ __launch_bounds__(256) void quest_bound_kernel(const QuestParams p) {
       }
     }
     const bool load = valid && phys >= 0;
-    float acc[G];
+    // pages outside the pool read page 0's summaries (their score is -inf)
+    const uint16_t* meta = p.meta_pool + (size_t)(load ? phys : 0) * 2 * D + g * CH;
+    uint4 mn[C4], mx[C4];
 #pragma unroll
-    for (int h = 0; h < G; ++h) acc[h] = 0.f;
-    if (load) {
-      const uint16_t* meta = p.meta_pool + (size_t)phys * 2 * D + g * CH;
-      uint4 mn[C4], mx[C4];
-#pragma unroll
-      for (int i = 0; i < C4; ++i) {
-        mn[i] = reinterpret_cast<const uint4*>(meta)[i];
-        mx[i] = reinterpret_cast<const uint4*>(meta + D)[i];
-      }
-#pragma unroll
-      for (int i = 0; i < C4; ++i) {
-        const uint32_t lo[4] = {mn[i].x, mn[i].y, mn[i].z, mn[i].w};
-        const uint32_t hi[4] = {mx[i].x, mx[i].y, mx[i].z, mx[i].w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-#pragma unroll
-          for (int h = 0; h < G; ++h) {
-            acc[h] = dot2bf16(qp[h][4 * i + e], hi[e], acc[h]);
-            acc[h] = dot2bf16(qn[h][4 * i + e], lo[e], acc[h]);
-          }
-        }
-      }
+    for (int i = 0; i < C4; ++i) {
+      mn[i] = reinterpret_cast<const uint4*>(meta)[i];
+      mx[i] = reinterpret_cast<const uint4*>(meta + D)[i];
     }
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      float a = quad_sum(acc[h]);
-      a += shfl_xor_f(a, 4);
-      best = fmaxf(best, a);
-    }
+    const float best = page_bound<D, G>(qp, qn, mn, mx);
     if (valid && g == 0) p.scores[(size_t)unit * p.scores_stride + b] = load ? best * p.scale : -INFINITY;
   }
 }
@@ -308,7 +269,7 @@ extern "C" se_status se_quest_select(const se_kv_view* kv, int32_t q_per_kv, con
   if (page_scores != nullptr && scores_stride < kv->max_pages) return SE_ERR_INVALID_ARGUMENT;
   if (!given) {
     if (q == nullptr || kv->meta_pool == nullptr) return SE_ERR_INVALID_ARGUMENT;
-    if (q_per_kv != 1 && q_per_kv != 2 && q_per_kv != 4) return SE_ERR_UNSUPPORTED;
+    if (q_per_kv != 1 && q_per_kv != 2 && q_per_kv != 4 && q_per_kv != 8) return SE_ERR_UNSUPPORTED;
     if (!(scale > 0.f)) return SE_ERR_INVALID_ARGUMENT;
   }
   QuestParams prm = {};
@@ -342,11 +303,13 @@ extern "C" se_status se_quest_select(const se_kv_view* kv, int32_t q_per_kv, con
       const int D = kv->head_dim;
       const dim3 grid(kv->num_units), block(kFusedThreads);
       if (D == 128) {
-        if (q_per_kv == 4) hipLaunchKernelGGL((quest_select_fused_kernel<128, 4>), grid, block, 0, stream, prm);
+        if (q_per_kv == 8) hipLaunchKernelGGL((quest_select_fused_kernel<128, 8>), grid, block, 0, stream, prm);
+        else if (q_per_kv == 4) hipLaunchKernelGGL((quest_select_fused_kernel<128, 4>), grid, block, 0, stream, prm);
         else if (q_per_kv == 2) hipLaunchKernelGGL((quest_select_fused_kernel<128, 2>), grid, block, 0, stream, prm);
         else hipLaunchKernelGGL((quest_select_fused_kernel<128, 1>), grid, block, 0, stream, prm);
       } else {
-        if (q_per_kv == 4) hipLaunchKernelGGL((quest_select_fused_kernel<64, 4>), grid, block, 0, stream, prm);
+        if (q_per_kv == 8) hipLaunchKernelGGL((quest_select_fused_kernel<64, 8>), grid, block, 0, stream, prm);
+        else if (q_per_kv == 4) hipLaunchKernelGGL((quest_select_fused_kernel<64, 4>), grid, block, 0, stream, prm);
         else if (q_per_kv == 2) hipLaunchKernelGGL((quest_select_fused_kernel<64, 2>), grid, block, 0, stream, prm);
         else hipLaunchKernelGGL((quest_select_fused_kernel<64, 1>), grid, block, 0, stream, prm);
       }
@@ -357,11 +320,13 @@ extern "C" se_status se_quest_select(const se_kv_view* kv, int32_t q_per_kv, con
     if (grid > INT32_MAX) return SE_ERR_UNSUPPORTED;
     const int D = kv->head_dim;
     if (D == 128) {
-      if (q_per_kv == 4) hipLaunchKernelGGL((quest_bound_kernel<128, 4>), dim3((int)grid), dim3(256), 0, stream, prm);
+      if (q_per_kv == 8) hipLaunchKernelGGL((quest_bound_kernel<128, 8>), dim3((int)grid), dim3(256), 0, stream, prm);
+      else if (q_per_kv == 4) hipLaunchKernelGGL((quest_bound_kernel<128, 4>), dim3((int)grid), dim3(256), 0, stream, prm);
       else if (q_per_kv == 2) hipLaunchKernelGGL((quest_bound_kernel<128, 2>), dim3((int)grid), dim3(256), 0, stream, prm);
       else hipLaunchKernelGGL((quest_bound_kernel<128, 1>), dim3((int)grid), dim3(256), 0, stream, prm);
     } else {
-      if (q_per_kv == 4) hipLaunchKernelGGL((quest_bound_kernel<64, 4>), dim3((int)grid), dim3(256), 0, stream, prm);
+      if (q_per_kv == 8) hipLaunchKernelGGL((quest_bound_kernel<64, 8>), dim3((int)grid), dim3(256), 0, stream, prm);
+      else if (q_per_kv == 4) hipLaunchKernelGGL((quest_bound_kernel<64, 4>), dim3((int)grid), dim3(256), 0, stream, prm);
       else if (q_per_kv == 2) hipLaunchKernelGGL((quest_bound_kernel<64, 2>), dim3((int)grid), dim3(256), 0, stream, prm);
       else hipLaunchKernelGGL((quest_bound_kernel<64, 1>), dim3((int)grid), dim3(256), 0, stream, prm);
     }

@@ -24,39 +24,92 @@ __device__ __forceinline__ uint32_t neg_part(uint32_t x) {
   return lo | hi;
 }
 
-// Page bounds (eq. background-quest-score) of one unit's candidate pages [0, n)
-// by NT threads, 8 lanes per page, into lds_sc (and scores_out when not null).
-// q_unit: the unit's G query rows; lds_bt: its block-table row (-1 for an entry
-// outside the pool).  Every iteration's loads are issued before the previous
-// page is reduced.
-template <int NT, int D, int G>
-__device__ __forceinline__ void unit_bounds(const uint16_t* meta_pool, const uint16_t* q_unit, float scale, int n,
-                                            const int* lds_bt, float* lds_sc, float* scores_out) {
-  constexpr int CH = D / 8;   // channels per lane
-  constexpr int CW = CH / 2;  // bf16 pairs per lane
-  constexpr int C4 = CW / 4;  // 16-byte loads per lane per row
-  constexpr int SLOTS = NT / 8;
-  const int lane = threadIdx.x & 63;
-  const int g = lane & 7;
-  const int slot = threadIdx.x >> 3;
-  uint32_t qp[G][CW], qn[G][CW];
-  {
-    const uint16_t* qb = q_unit + g * CH;
+// Lane layout of the page bound: LPP lanes share one page, each with D / LPP
+// channels of its minimum and maximum rows (16-byte loads) and of the G query
+// rows' positive and negative halves, which take G * D / LPP registers: 8 lanes
+// per page, 16 when that would exceed 64 registers (G = 8 at D = 128).
+template <int D, int G>
+struct BoundLanes {
+  static constexpr int LPP = G * D > 512 ? 16 : 8;
+  static constexpr int CH = D / LPP;  // channels per lane
+  static constexpr int CW = CH / 2;   // bf16 pairs per lane
+  static constexpr int C4 = CW / 4;   // 16-byte loads per lane per row
+  static_assert(C4 >= 1 && G * CW * 2 <= 64, "bound lane layout");
+};
+
+// The lane's channels of the G query rows, split into q+ and q- halves.
+template <int D, int G>
+__device__ __forceinline__ void bound_query(const uint16_t* q_unit, int g, uint32_t (&qp)[G][BoundLanes<D, G>::CW],
+                                            uint32_t (&qn)[G][BoundLanes<D, G>::CW]) {
+  using BL = BoundLanes<D, G>;
+  const uint16_t* qb = q_unit + g * BL::CH;
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const uint4* src = reinterpret_cast<const uint4*>(qb + (size_t)h * D);
+  for (int h = 0; h < G; ++h) {
+    const uint4* src = reinterpret_cast<const uint4*>(qb + (size_t)h * D);
 #pragma unroll
-      for (int i = 0; i < C4; ++i) {
-        const uint4 t = src[i];
-        const uint32_t v[4] = {t.x, t.y, t.z, t.w};
+    for (int i = 0; i < BL::C4; ++i) {
+      const uint4 t = src[i];
+      const uint32_t v[4] = {t.x, t.y, t.z, t.w};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          qp[h][4 * i + e] = pos_part(v[e]);
-          qn[h][4 * i + e] = neg_part(v[e]);
-        }
+      for (int e = 0; e < 4; ++e) {
+        qp[h][4 * i + e] = pos_part(v[e]);
+        qn[h][4 * i + e] = neg_part(v[e]);
       }
     }
   }
+}
+
+// One page's bound (before the scale), the maximum over the G rows of
+// q+ . M + q- . m, reduced over the page's LPP lanes (every lane gets it).
+template <int D, int G>
+__device__ __forceinline__ float page_bound(const uint32_t (&qp)[G][BoundLanes<D, G>::CW],
+                                            const uint32_t (&qn)[G][BoundLanes<D, G>::CW],
+                                            const uint4 (&mn)[BoundLanes<D, G>::C4],
+                                            const uint4 (&mx)[BoundLanes<D, G>::C4]) {
+  using BL = BoundLanes<D, G>;
+  float acc[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) acc[h] = 0.f;
+#pragma unroll
+  for (int i = 0; i < BL::C4; ++i) {
+    const uint32_t lo[4] = {mn[i].x, mn[i].y, mn[i].z, mn[i].w};
+    const uint32_t hi[4] = {mx[i].x, mx[i].y, mx[i].z, mx[i].w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        acc[h] = dot2bf16(qp[h][4 * i + e], hi[e], acc[h]);
+        acc[h] = dot2bf16(qn[h][4 * i + e], lo[e], acc[h]);
+      }
+    }
+  }
+  float best = -INFINITY;
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    float a = quad_sum(acc[h]);
+    a += shfl_xor_f(a, 4);
+    if constexpr (BL::LPP == 16) a += shfl_xor_f(a, 8);
+    best = fmaxf(best, a);
+  }
+  return best;
+}
+
+// Page bounds (eq. background-quest-score) of one unit's candidate pages [0, n)
+// by NT threads, LPP lanes per page, into lds_sc (and scores_out when not
+// null).  q_unit: the unit's G query rows; lds_bt: its block-table row (-1 for
+// an entry outside the pool).  Every iteration's loads are issued before the
+// previous page is reduced.
+template <int NT, int D, int G>
+__device__ __forceinline__ void unit_bounds(const uint16_t* meta_pool, const uint16_t* q_unit, float scale, int n,
+                                            const int* lds_bt, float* lds_sc, float* scores_out) {
+  using BL = BoundLanes<D, G>;
+  constexpr int CH = BL::CH, CW = BL::CW, C4 = BL::C4, LPP = BL::LPP;
+  constexpr int SLOTS = NT / LPP;
+  const int lane = threadIdx.x & 63;
+  const int g = lane & (LPP - 1);
+  const int slot = threadIdx.x / LPP;
+  uint32_t qp[G][CW], qn[G][CW];
+  bound_query<D, G>(q_unit, g, qp, qn);
   auto load = [&](int b, uint4 (&mn)[C4], uint4 (&mx)[C4]) {
     const int ph = lds_bt[min(b, n - 1)];
     const uint16_t* meta = meta_pool + (size_t)(ph < 0 ? 0 : ph) * 2 * D + g * CH;
@@ -67,29 +120,7 @@ __device__ __forceinline__ void unit_bounds(const uint16_t* meta_pool, const uin
     }
   };
   auto bound = [&](int b, const uint4 (&mn)[C4], const uint4 (&mx)[C4]) {
-    float acc[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) acc[h] = 0.f;
-#pragma unroll
-    for (int i = 0; i < C4; ++i) {
-      const uint32_t lo[4] = {mn[i].x, mn[i].y, mn[i].z, mn[i].w};
-      const uint32_t hi[4] = {mx[i].x, mx[i].y, mx[i].z, mx[i].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-          acc[h] = dot2bf16(qp[h][4 * i + e], hi[e], acc[h]);
-          acc[h] = dot2bf16(qn[h][4 * i + e], lo[e], acc[h]);
-        }
-      }
-    }
-    float best = -INFINITY;
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      float a = quad_sum(acc[h]);
-      a += shfl_xor_f(a, 4);
-      best = fmaxf(best, a);
-    }
+    const float best = page_bound<D, G>(qp, qn, mn, mx);
     if (b < n && g == 0) {
       const float sc = lds_bt[b] >= 0 ? best * scale : -INFINITY;
       lds_sc[b] = sc;

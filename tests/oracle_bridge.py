@@ -20,6 +20,11 @@ U_RTOL = 1e-3            # accumulated scores, relative ...
 U_ATOL = 1e-7            # ... with this floor for scores below 1e-4
 QUEST_RTOL = 1e-3        # Quest page scores, relative to max(1, |score|)
 NEAR_TIE = 1e-4          # a selection may differ only between scores this close (relative)
+# The H2O step keeps its per-slot weights as fp16 while they wait for the score
+# update (each weight rounded by at most 2^-11 relative, so each new score by
+# at most 2^-11 of itself): a float64 retention may swap slots whose scores lie
+# within twice the score tolerance of each other.
+H2O_NEAR_TIE = 2 * U_RTOL
 
 
 def f64(t: torch.Tensor) -> np.ndarray:
@@ -49,9 +54,11 @@ def assert_scores_close(got, want, what=""):
     assert not bad.any(), f"{what}: {int(bad.sum())} scores off, worst {np.abs(got - want)[bad].max():.3e}"
 
 
-def h2o_near_tie(oracle_u_by_pos: dict, kept_gpu: set, kept_oracle: set) -> bool:
+def h2o_near_tie(oracle_u_by_pos: dict, kept_gpu: set, kept_oracle: set, tol: float = NEAR_TIE) -> bool:
     """True when the two retained sets differ only by swaps of entries whose
-    oracle scores agree to NEAR_TIE (a valid TopK up to float32 rounding)."""
+    oracle scores agree to tol, relative (a valid TopK up to the rounding of
+    the scores: NEAR_TIE for fp32 arithmetic, H2O_NEAR_TIE for decode-step
+    scores)."""
     only_g = kept_gpu - kept_oracle
     only_o = kept_oracle - kept_gpu
     if len(only_g) != len(only_o):
@@ -59,7 +66,7 @@ def h2o_near_tie(oracle_u_by_pos: dict, kept_gpu: set, kept_oracle: set) -> bool
     for x in only_g:
         for y in only_o:
             ux, uy = oracle_u_by_pos[x], oracle_u_by_pos[y]
-            if uy - ux > NEAR_TIE * max(abs(ux), abs(uy)):
+            if uy - ux > tol * max(abs(ux), abs(uy)):
                 return False
     return True
 

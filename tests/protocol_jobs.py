@@ -13,7 +13,7 @@ import numpy as np
 from oracle import h2o, quest
 from oracle.attention import selected_attention
 from oracle.state import new_unit
-from tests.oracle_bridge import (LSE_ATOL, OUT_ATOL, QUEST_RTOL, assert_scores_close, h2o_near_tie,
+from tests.oracle_bridge import (H2O_NEAR_TIE, LSE_ATOL, OUT_ATOL, QUEST_RTOL, assert_scores_close, h2o_near_tie,
                                  quest_near_tie)
 
 
@@ -57,7 +57,7 @@ def h2o_unit_job(job):
     if not np.array_equal(keep64, keep):
         p = res["pos_after_append"]
         ou = dict(zip(p.tolist(), res["u_after_accumulate"].tolist()))
-        assert h2o_near_tie(ou, set(p[keep].tolist()), set(p[keep64].tolist())), \
+        assert h2o_near_tie(ou, set(p[keep].tolist()), set(p[keep64].tolist()), H2O_NEAR_TIE), \
             f"{where}: float64 retention differs beyond a near tie"
         near = 1
     return holes, movers, freed, st2.pos, st2.u.astype(np.float32), near

@@ -63,6 +63,8 @@ def test_view_checks(kw, status):
 def test_attend_argument_checks():
     v = _view()
     assert _attend(v, G=3) == b.SE_ERR_UNSUPPORTED
+    assert _attend(v, G=16) == b.SE_ERR_UNSUPPORTED
+    assert _attend(v, G=8, q=None) == b.SE_ERR_INVALID_ARGUMENT      # groups of 8 are supported
     assert _attend(v, q=None) == b.SE_ERR_INVALID_ARGUMENT
     assert _attend(v, k=0x100) == b.SE_ERR_INVALID_ARGUMENT           # k without v
     assert _attend(v, k=0x100, v=0x200) == b.SE_ERR_INVALID_ARGUMENT  # append without new_pos

@@ -69,10 +69,21 @@ def test_trajectory_small_window_long_run(se):
     assert _run_h2o(se, w, 40) == 40 * w.units_per_layer
 
 
-@pytest.mark.parametrize("G,d", [(1, 128), (2, 64), (4, 64)])
+@pytest.mark.parametrize("G,d", [(1, 128), (2, 64), (4, 64), (8, 128), (8, 64)])
 def test_head_group_and_dim_variants(se, G, d):
     w = scaled(TINY_H2O, num_req=2, hq=2 * G, hkv=2, head_dim=d, ctx=300, budget=64, recent=16, steps=3)
     assert _run_h2o(se, w, 3) == 3 * w.units_per_layer
+
+
+@pytest.mark.parametrize("num_req,ctx,budget,recent", [(4, 3000, 2048, 256), (64, 2000, 1024, 128)])
+def test_group_of_8_trajectory(se, num_req, ctx, budget, recent):
+    # Groups of 8 query heads per KV head (two passes of the four-head
+    # reduction): 32 units split over work-groups with a combine pass, and 512
+    # units streamed whole with the fused eviction; the first step evicts down
+    # to the budget, the rest are steady.
+    w = scaled(LAYER_H2O, num_req=num_req, hq=64, hkv=8, ctx=ctx, budget=budget, recent=recent, steps=4)
+    assert w.q_per_kv == 8
+    assert _run_h2o(se, w, 4) == 4 * w.units_per_layer
 
 
 def test_budget_covers_context_is_dense(se):

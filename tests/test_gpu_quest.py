@@ -56,6 +56,16 @@ def test_quest_variants(se):
     assert _run_quest(se, w, 12) == 12 * w.units_per_layer
 
 
+@pytest.mark.parametrize("num_req,d", [(2, 128), (2, 64), (32, 128), (32, 64)])
+def test_quest_group_of_8(se, num_req, d):
+    # Groups of 8 query heads per KV head: the page bound takes 16 lanes per
+    # page at d = 128 (8 at d = 64); 16 units take the bound + top-k kernels,
+    # 256 units the selection inside the attention kernel.
+    w = scaled(LAYER_QUEST, num_req=num_req, hq=64, hkv=8, head_dim=d, ctx=2000, top_k=16, steps=6)
+    assert w.q_per_kv == 8
+    assert _run_quest(se, w, 6) == 6 * w.units_per_layer
+
+
 def test_largest_top_k(se):
     # top_k = 4096 of 4200 candidate pages: the attention reads 4097 pages per
     # unit, more than one work-group holds, so it is split and combined.
@@ -126,12 +136,13 @@ def test_select_from_given_scores_bitexact(se, n_pages, top_k, levels):
         assert (got[len(want):] == -1).all()
 
 
-def test_fused_select_matches_two_pass(se):
+@pytest.mark.parametrize("G,d", [(4, 128), (8, 128), (8, 64)])
+def test_fused_select_matches_two_pass(se, G, d):
     # 256 units take the one-kernel selection (bounds and top-k in one work-group
     # per unit); the first 16 units alone take the bound + top-k kernels.  Page
     # scores and selections agree bit for bit, and the fused selection equals
     # the top-k kernel's selection from the fused scores.
-    w = scaled(LAYER_QUEST, ctx=3001, steps=1)
+    w = scaled(LAYER_QUEST, ctx=3001, steps=1, hq=8 * G, hkv=8, head_dim=d, num_req=256 // 8)
     host = build_state(w, "cpu")
     steps = build_steps(w, host, "cpu", steps=1)
     gs = to_device(host, DEV)
@@ -166,20 +177,21 @@ def test_fused_select_matches_two_pass(se):
     assert (sel_f >= 0).all()
 
 
-@pytest.mark.parametrize("num_req", [32, 2])
-def test_step_quest_equals_select_then_attend(se, num_req):
+@pytest.mark.parametrize("num_req,G", [(32, 4), (2, 4), (32, 8), (2, 8)])
+def test_step_quest_equals_select_then_attend(se, num_req, G):
     # se_decode_step_quest against se_quest_select + se_decode_attend on copies of
     # one state, three steps: with 256 units the selection runs inside the
     # attention kernel, with 16 the call falls back to the two kernels.  The
     # selections, outputs, lse and the pools (append, Quest summaries) agree bit
     # for bit.
     from workloads import clone_state
-    w = scaled(LAYER_QUEST, num_req=num_req, ctx=3001, steps=3)
+    w = scaled(LAYER_QUEST, num_req=num_req, ctx=3001, steps=3, hq=8 * G, hkv=8)
     host = build_state(w, "cpu")
     steps = build_steps(w, host, "cpu", steps=3)
     a = to_device(host, DEV)
     b = clone_state(a)
-    U, G, P = w.units_per_layer, w.q_per_kv, host.max_pages
+    U, P = w.units_per_layer, host.max_pages
+    assert w.q_per_kv == G
     max_len = P * 16
     da = se.QuestDecoder(_view(se, a), G, w.scale, w.top_k, max_len, DEV)
     db = se.QuestDecoder(_view(se, b), G, w.scale, w.top_k, max_len, DEV)

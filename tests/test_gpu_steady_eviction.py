@@ -21,6 +21,11 @@ depends on the launch:
    512  2048   256      512     general retention in the epilogue: recent
         (gapped positions)      positions that are not one contiguous run
 
+Groups of 8 query heads per KV head repeat four of them: 512 x 2048 takes
+finish_steady with fp16 weights, 512 x 4096 the strided one, 16 x 2048 the
+1024-thread finish_steady (its 129 pages fit the fp16 weight buffer), 256 x
+8192 the general retention.
+
 Ties: six slots of one page, all outside the recent window for the whole run,
 get the same key (zero), the same value row and the same score (zero); every
 other slot starts at 0.5 or more.  Their accumulated scores stay bit-equal (one
@@ -39,7 +44,7 @@ from workloads import StepInputs, isolated_units, scaled, to_device
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda:0"
-G, D, HKV = 4, 128, 8
+D, HKV = 128, 8
 N_STEPS = 4
 N_TIE = 6
 
@@ -81,7 +86,7 @@ def _tied_state(units, budget, recent, mode, seed):
     return host, tie_pos
 
 
-def _steps(num_req, start_pos, seed):
+def _steps(num_req, start_pos, seed, G):
     g = torch.Generator().manual_seed(seed)
     q = torch.randn((N_STEPS, 1, num_req, HKV * G, D), generator=g).to(torch.bfloat16)
     k = torch.randn((N_STEPS, 1, num_req, HKV, D), generator=g).to(torch.bfloat16)
@@ -91,30 +96,35 @@ def _steps(num_req, start_pos, seed):
 
 
 CASES = [
-    # units, budget, window, positions
-    (512, 128, 16, "permuted"),
-    (16, 128, 16, "permuted"),
-    (256, 2048, 256, "permuted"),
-    (512, 2048, 256, "permuted"),
-    (512, 4096, 512, "permuted"),
-    (256, 4096, 512, "permuted"),
-    (256, 8192, 512, "permuted"),
-    (512, 2048, 256, "gapped"),
+    # units, budget, window, positions, query heads per KV head
+    (512, 128, 16, "permuted", 4),
+    (16, 128, 16, "permuted", 4),
+    (256, 2048, 256, "permuted", 4),
+    (512, 2048, 256, "permuted", 4),
+    (512, 4096, 512, "permuted", 4),
+    (256, 4096, 512, "permuted", 4),
+    (256, 8192, 512, "permuted", 4),
+    (512, 2048, 256, "gapped", 4),
+    # groups of 8: per-wavefront rows (fp16 weights), strided, wide, general
+    (512, 2048, 256, "permuted", 8),
+    (512, 4096, 512, "permuted", 8),
+    (16, 2048, 256, "permuted", 8),
+    (256, 8192, 512, "permuted", 8),
 ]
 
 
 @pytest.mark.timeout(300)
-@pytest.mark.parametrize("units,budget,recent,mode", CASES)
-def test_steady_step_with_ties(se, units, budget, recent, mode):
-    seed = units + budget + recent + len(mode)
-    print(f"case units={units} B={budget} w={recent} {mode}", flush=True)
+@pytest.mark.parametrize("units,budget,recent,mode,G", CASES)
+def test_steady_step_with_ties(se, units, budget, recent, mode, G):
+    seed = units + budget + recent + len(mode) + (G - 4)
+    print(f"case units={units} B={budget} w={recent} {mode} G={G}", flush=True)
     host, tie_pos = _tied_state(units, budget, recent, mode, seed)
     gs = to_device(host, DEV)
     gs.w = scaled(gs.w, hq=HKV * G, hkv=HKV, num_req=units // HKV)
     num_req = units // HKV
     # new positions continue above every resident one (per request: its units share them)
     top = host.pos_pool.max().item() + 1
-    steps = _steps(num_req, [top] * num_req, seed + 2)
+    steps = _steps(num_req, [top] * num_req, seed + 2, G)
     bounds = [budget + 1] * N_STEPS  # the benchmark's steady bound
     checked, near = h2o_trajectory(se, gs, steps, N_STEPS, {0: range(units)}, q_per_kv=G, scale=float(np.float32(D ** -0.5)),
                                    budget=budget, recent=recent, bounds=bounds, device=DEV)
