@@ -846,10 +846,12 @@ __device__ __forceinline__ const int* fused_quest_select(const AttendParams& p, 
     sbt[i] = ph;
   }
   if (badc) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
+  if (tid < 256) esc.hist[tid] = 0;
   __syncthreads();
-  unit_bounds<NT, D, G>(p.meta, p.q + ((size_t)req * Hq + (size_t)kvh * G) * D, p.scale, n_cand, sbt, ssc, nullptr);
+  unit_bounds<NT, D, G>(p.meta, p.q + ((size_t)req * Hq + (size_t)kvh * G) * D, p.scale, n_cand, sbt, ssc, nullptr,
+                        esc.hist);
   __syncthreads();
-  unit_topk<NT>(n_cand, p.top_k, ssc, nullptr, ssel, esc.hist, lds_scan, esc.bcast);
+  unit_topk<NT>(n_cand, p.top_k, ssc, nullptr, ssel, esc.hist, lds_scan, esc.bcast, true);
   __syncthreads();
   return ssel;
 }

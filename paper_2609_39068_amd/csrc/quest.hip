@@ -208,12 +208,13 @@ __global__ __launch_bounds__(kFusedThreads) void quest_select_fused_kernel(const
     lds_bt[i] = ph;
   }
   if (bad) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
+  if (tid < 256) hist[tid] = 0;
   __syncthreads();
   const int req = unit / p.hkv, kvh = unit - req * p.hkv;
   unit_bounds<NT, D, G>(p.meta_pool, p.q + ((size_t)req * p.hkv * G + (size_t)kvh * G) * D, p.scale, n, lds_bt,
-                        lds_sc, p.write_scores ? p.scores + (size_t)unit * p.scores_stride : nullptr);
+                        lds_sc, p.write_scores ? p.scores + (size_t)unit * p.scores_stride : nullptr, hist);
   __syncthreads();
-  unit_topk<NT>(n, p.top_k, lds_sc, out, nullptr, hist, scan_scratch, bcast);
+  unit_topk<NT>(n, p.top_k, lds_sc, out, nullptr, hist, scan_scratch, bcast, true);
 }
 
 }  // namespace se

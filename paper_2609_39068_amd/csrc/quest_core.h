@@ -94,14 +94,33 @@ __device__ __forceinline__ float page_bound(const uint32_t (&qp)[G][BoundLanes<D
   return best;
 }
 
+// Adds one digit per lane (kNoDigit: none) to an LDS histogram.  When every
+// lane with a digit has the same one (the common case in a radix selection's
+// first passes, whose digits are sign and exponent bits) one lane adds the
+// count, instead of 64 atomics on one LDS word.  All 64 lanes must be active.
+constexpr uint32_t kNoDigit = 0xFFFFFFFFu;
+__device__ __forceinline__ void hist_add_wave(unsigned* hist, uint32_t dg) {
+  const uint64_t valid = __ballot(dg != kNoDigit);
+  if (valid == 0) return;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int fl = __builtin_ctzll(valid);
+  const uint32_t d0 = __builtin_amdgcn_readlane(dg, fl);
+  if (__ballot(dg == d0) == valid) {
+    if (lane == fl) atomicAdd(&hist[d0], (unsigned)__popcll(valid));
+  } else if (dg != kNoDigit) {
+    atomicAdd(&hist[dg], 1u);
+  }
+}
+
 // Page bounds (eq. background-quest-score) of one unit's candidate pages [0, n)
 // by NT threads, LPP lanes per page, into lds_sc (and scores_out when not
 // null).  q_unit: the unit's G query rows; lds_bt: its block-table row (-1 for
 // an entry outside the pool).  Every iteration's loads are issued before the
-// previous page is reduced.
+// previous page is reduced.  With hist0 (256 zeroed bins), the scores' first
+// radix digits (unit_topk's first pass) are counted on the way.
 template <int NT, int D, int G>
 __device__ __forceinline__ void unit_bounds(const uint16_t* meta_pool, const uint16_t* q_unit, float scale, int n,
-                                            const int* lds_bt, float* lds_sc, float* scores_out) {
+                                            const int* lds_bt, float* lds_sc, float* scores_out, unsigned* hist0) {
   using BL = BoundLanes<D, G>;
   constexpr int CH = BL::CH, CW = BL::CW, C4 = BL::C4, LPP = BL::LPP;
   constexpr int SLOTS = NT / LPP;
@@ -121,11 +140,14 @@ __device__ __forceinline__ void unit_bounds(const uint16_t* meta_pool, const uin
   };
   auto bound = [&](int b, const uint4 (&mn)[C4], const uint4 (&mx)[C4]) {
     const float best = page_bound<D, G>(qp, qn, mn, mx);
+    uint32_t dg = kNoDigit;
     if (b < n && g == 0) {
       const float sc = lds_bt[b] >= 0 ? best * scale : -INFINITY;
       lds_sc[b] = sc;
       if (scores_out != nullptr) scores_out[b] = sc;
+      dg = float_key(sc) >> 24;
     }
+    if (hist0 != nullptr) hist_add_wave(hist0, dg);
   };
   const int iters = (n + SLOTS - 1) / SLOTS;
   uint4 mnA[C4], mxA[C4], mnB[C4], mxB[C4];
@@ -142,18 +164,26 @@ __device__ __forceinline__ void unit_bounds(const uint16_t* meta_pool, const uin
 // The top_k pages of one unit by score (ties: lower page index), ascending, from
 // the n scores in lds_sc, by NT threads; written to out_g and out_l (either may
 // be null), -1 past the selection.  Radix selection (8-bit digits, most
-// significant first) on order-preserving keys: every thread adds its keys to
-// an LDS histogram, then wavefront 0 alone scans the 256 bins and picks the
-// digit (three barriers per pass).  Wavefront 0 then writes the selected
-// indices in ascending order with ballots: keys above the threshold, and the
-// lowest-indexed ones equal to it until top_k are taken.
+// significant first) on order-preserving keys: every wavefront adds its keys
+// to an LDS histogram (hist_add_wave), then wavefront 0 alone scans the 256
+// bins, picks the digit and clears the bins (two barriers per pass).  With
+// counted, the first pass's histogram is already in hist (unit_bounds counts
+// it); else hist is cleared here.  Then every wavefront
+// takes a contiguous range of indices: it counts its keys above the threshold
+// and its keys equal to it, the counts of the ranges before it give its output
+// offset, and it writes its selected indices in ascending order (keys above
+// the threshold, and the lowest-indexed ones equal to it until top_k are
+// taken).
 template <int NT>
 __device__ __forceinline__ void unit_topk(int n, int top_k, const float* lds_sc, int32_t* out_g, int32_t* out_l,
-                                          unsigned* hist, int* scan_scratch, int* bcast) {
+                                          unsigned* hist, int* scan_scratch, int* bcast, bool counted) {
   (void)scan_scratch;
+  constexpr int NW = NT / kWave;
   static_assert(NT >= 256 && NT % kWave == 0, "threads 0..255 clear one bin each");
+  static_assert(2 * NW <= 256, "per-wavefront counts live in the histogram");
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
   const bool w0 = tid < kWave;
   if (n <= top_k) {
     for (int i = tid; i < top_k; i += NT) {
@@ -165,12 +195,21 @@ __device__ __forceinline__ void unit_topk(int n, int top_k, const float* lds_sc,
   }
   uint32_t prefix = 0, mask = 0;
   int k = top_k;
-  for (int shift = 24; shift >= 0; shift -= 8) {
+  if (!counted) {
     if (tid < 256) hist[tid] = 0;
     __syncthreads();
-    for (int i = tid; i < n; i += NT) {
-      const uint32_t key = float_key(lds_sc[i]);
-      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+  }
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    if (shift < 24 || !counted) {
+      for (int i0 = wave * kWave; i0 < n; i0 += NT) {  // wave-uniform trip count
+        const int i = i0 + lane;
+        uint32_t dg = kNoDigit;
+        if (i < n) {
+          const uint32_t key = float_key(lds_sc[i]);
+          if ((key & mask) == prefix) dg = (key >> shift) & 255u;
+        }
+        hist_add_wave(hist, dg);
+      }
     }
     __syncthreads();
     if (w0) {
@@ -196,6 +235,7 @@ __device__ __forceinline__ void unit_topk(int n, int top_k, const float* lds_sc,
           bcast[2] = c[j];
         }
         run += c[j];
+        hist[255 - 4 * lane - j] = 0;  // cleared for the next pass
       }
     }
     __syncthreads();
@@ -206,25 +246,46 @@ __device__ __forceinline__ void unit_topk(int n, int top_k, const float* lds_sc,
     mask |= 0xFFu << shift;
     if (cnt == k) break;
   }
-  // k keys equal to the threshold class (under mask) are taken, lowest index first
-  if (w0) {
-    int taken = 0, eq_seen = 0;
-    for (int b0 = 0; b0 < n; b0 += kWave) {
-      const int b = b0 + lane;
-      const uint32_t km = b < n ? (float_key(lds_sc[b]) & mask) : 0u;
-      const bool above = b < n && km > prefix;
-      const bool eq = b < n && km == prefix;
-      const uint64_t eqm = __ballot(eq);
-      const bool take = above || (eq && eq_seen + lane_prefix_count(eqm) < k);
-      const uint64_t tm = __ballot(take);
-      if (take) {
-        const int r = taken + lane_prefix_count(tm);
-        if (out_g != nullptr) out_g[r] = b;
-        if (out_l != nullptr) out_l[r] = b;
-      }
-      taken += __popcll(tm);
-      eq_seen += __popcll(eqm);
+  // k keys equal to the threshold class (under mask) are taken, lowest index
+  // first.  Wavefront w owns indices [w * span, (w + 1) * span).
+  const int span = (n + NW * kWave - 1) / (NW * kWave) * kWave;
+  const int beg = wave * span, end = min(n, beg + span);
+  auto classify = [&](int b, bool& above, bool& eq) {
+    const uint32_t km = b < end ? (float_key(lds_sc[b]) & mask) : 0u;
+    above = b < end && km > prefix;
+    eq = b < end && km == prefix;
+  };
+  int n_above = 0, n_eq = 0;
+  for (int b0 = beg; b0 < end; b0 += kWave) {
+    bool above, eq;
+    classify(b0 + lane, above, eq);
+    n_above += __popcll(__ballot(above));
+    n_eq += __popcll(__ballot(eq));
+  }
+  if (lane == 0) {
+    hist[wave] = (unsigned)n_above;  // the histogram is free after the last pass's barrier
+    hist[NW + wave] = (unsigned)n_eq;
+  }
+  __syncthreads();
+  int taken_above = 0, eq_seen = 0;  // in the ranges before this wavefront's
+  for (int v = 0; v < wave; ++v) {
+    taken_above += (int)hist[v];
+    eq_seen += (int)hist[NW + v];
+  }
+  for (int b0 = beg; b0 < end; b0 += kWave) {
+    const int b = b0 + lane;
+    bool above, eq;
+    classify(b, above, eq);
+    const uint64_t am = __ballot(above), eqm = __ballot(eq);
+    const int eq_rank = eq_seen + lane_prefix_count(eqm);
+    if (above || (eq && eq_rank < k)) {
+      // output rank: the kept keys at lower indices
+      const int r = taken_above + lane_prefix_count(am) + min(eq_rank, k);
+      if (out_g != nullptr) out_g[r] = b;
+      if (out_l != nullptr) out_l[r] = b;
     }
+    taken_above += __popcll(am);
+    eq_seen += __popcll(eqm);
   }
 }
 
