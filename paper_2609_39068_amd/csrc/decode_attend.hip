@@ -583,6 +583,7 @@ struct PageRef {
   int phys;    // physical page, or -1 when the page is skipped
   int nrows;   // resident rows of the page
   int rn;      // row of the appended token in this page, or -1
+  bool tail;   // a prefetch past the wavefront's last page (its loads are not used)
 };
 
 // (row, head) pairs a lane keeps per page: heads own_head + 4k, k < kPairs.
@@ -613,7 +614,10 @@ struct Lanes {
 // (scalar registers) and each row is a constant offset from the lane's offset,
 // so no load needs per-lane address arithmetic.  Rows past the page's resident
 // rows are read too (they lie inside the page): their logits are masked and
-// their value columns cleared before the PV update (pv_page).
+// their value columns cleared before the PV update (pv_page).  A tail
+// prefetch (past the wavefront's last page) reads the last page again with
+// every lane at the page's first bytes: a few cache lines instead of the
+// page, which the streaming loads have already let go from the L2.
 // K/V page data is read once per step: nontemporal loads (streaming cache
 // policy), so the stream does not push the block tables, positions, scores and
 // the kernel's code out of the L2.
@@ -632,7 +636,7 @@ template <int D>
 __device__ __forceinline__ void load_k(const AttendParams& p, const Lanes<D>& ln, const PageRef& pr,
                                        uint4 (&kb)[2 * Lanes<D>::K4]) {
   constexpr int K4 = Lanes<D>::K4;
-  const char* kpage = page_base<D>(p, pr) + ln.koff;
+  const char* kpage = page_base<D>(p, pr) + (pr.tail ? 0u : ln.koff);
 #pragma unroll
   for (int pass = 0; pass < 2; ++pass)
 #pragma unroll
@@ -644,7 +648,7 @@ template <int D>
 __device__ __forceinline__ void load_v(const AttendParams& p, const Lanes<D>& ln, const PageRef& pr,
                                        uint32_t (&vb)[Lanes<D>::RPL]) {
   constexpr int RPL = Lanes<D>::RPL;
-  const char* vpage = page_base<D>(p, pr) + kPage * D * 2 + ln.voff;
+  const char* vpage = page_base<D>(p, pr) + kPage * D * 2 + (pr.tail ? 0u : ln.voff);
 #pragma unroll
   for (int i = 0; i < RPL; ++i) vb[i] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(vpage + i * D * 2));
 }
@@ -1096,6 +1100,7 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
     pr.phys = __builtin_amdgcn_readfirstlane(lds_phys[gi]);
     pr.nrows = __builtin_amdgcn_readfirstlane(min(kPage, Lp - pr.lp * kPage));
     pr.rn = -1;
+    pr.tail = false;
     return pr;
   };
 
@@ -1108,7 +1113,11 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   uint4 kbA[2 * K4], kbB[2 * K4];
   uint32_t vb[RPL];
   if (n_my > 0) {
-    auto ref_or_tail = [&](int i) -> PageRef { return page_ref(i < n_my ? i : n_my - 1); };
+    auto ref_or_tail = [&](int i) -> PageRef {
+      PageRef r = page_ref(i < n_my ? i : n_my - 1);
+      r.tail = i >= n_my;
+      return r;
+    };
     PageRef cur = ref_or_tail(0);
     PageRef nx1 = ref_or_tail(1);
     load_k<D>(p, ln, cur, kbA);
