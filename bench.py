@@ -54,7 +54,7 @@ METRIC = "decode attn+eviction tokens/s/GPU; achieved HBM GB/s vs MI355X peak"
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_step_h2o_llama3-8b-layer-h2o_traffic.txt")
 SNAPKV_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "snapkv_compact_llama3-8b-prompt-snapkv_traffic.txt")
-DECODE_SOURCES = ("decode_attend.hip", "evict_compact.hip", "evict_core.h", "se_common.h")
+DECODE_SOURCES = ("decode_attend.hip", "evict_compact.hip", "evict_core.h", "quest_core.h", "se_common.h")
 SNAPKV_SOURCES = ("snapkv.hip", "evict_compact.hip", "evict_core.h", "se_common.h")
 PRUNE_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "prune_interval_llama3-8b-32-layer-prune-interval_traffic.txt")
 PRUNE_SOURCES = ("prune.hip", "se_common.h")
@@ -72,10 +72,12 @@ def parse():
     ap.add_argument("--config", type=int, default=4, help="decode workload index 0..4 (default 4, the headline)")
     ap.add_argument("--only", action="store_true",
                     help="with --config 4: skip the single-layer workloads 1-3 reported under other_configs")
-    ap.add_argument("--workload", choices=["decode", "snapkv", "omnikv", "h2o_prefill", "prune"], default="decode",
+    ap.add_argument("--workload", choices=["decode", "snapkv", "omnikv", "h2o_prefill", "prune", "read_ceiling"],
+                    default="decode",
                     help="decode (the --config workload), snapkv (prompt compaction), omnikv "
                          "(32-layer decode with OmniKV selection reuse), h2o_prefill (chunk-wise "
-                         "prefill eviction) or prune (interval prefix-cache pruning)")
+                         "prefill eviction), prune (interval prefix-cache pruning) or read_ceiling (the "
+                         "plain read rate of the decode page gathers, se_probe_read_pages)")
     ap.add_argument("--cpu-baseline", choices=["auto", "skip"], default="auto")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 4 GiB device copy (counter calibration under rocprofv3)")
@@ -570,6 +572,63 @@ def _oracle_prune_run(i):
         t0 = time.perf_counter()
         prune.prune(st, lo, hi, prune.budget_selection(st, lo, hi, w.budget))
         return time.perf_counter() - t0
+
+
+# Page gathers of the read-rate probe: (name, pages read, from a pool of, random order, work-groups).
+# 526,336 pages = one 32-layer-workload layer-step (2048 units x 257 pages); 66,048 = one steady step of
+# the 8B layer (512 units x 129 pages).
+READ_CASES = [
+    ("gather_4.3GB_random_of_17GB", 526336, 2097152, True, 2048),
+    ("gather_0.54GB_random_of_17GB", 66048, 2097152, True, 512),
+    ("stream_4.3GB", 526336, 2097152, False, 2048),
+    ("gather_17GB_random", 2097152, 2097152, True, 8192),
+]
+
+
+def main_read_ceiling(args):
+    """The plain read rate of the decode kernels' page gathers: se_probe_read_pages
+    reads 8 KiB pages (a 16-slot page at d = 128) listed in a seeded random
+    order from a 16 GiB pool with the decode stream's loads, K timed calls per
+    case between HIP events.  `value` is the first case (one layer-step of the
+    32-layer workload, 4.3 GB)."""
+    import torch
+    import paper_2609_39068_amd as se
+
+    K = int(args.steps if args.steps is not None else 20)
+    W = int(args.warmup if args.warmup is not None else 3)
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    dev = torch.device("cuda:0")
+    PB = 8192
+    pool_pages = max(c[2] for c in READ_CASES)
+    pool = torch.empty(pool_pages * PB, dtype=torch.uint8, device=dev)
+    sink = torch.empty(max(c[4] for c in READ_CASES) * 512, dtype=torch.int32, device=dev)
+    g = torch.Generator().manual_seed(7)
+    cases = {}
+    for name, n, of, rnd, grid in READ_CASES:
+        pages = (torch.randperm(of, generator=g)[:n] if rnd else torch.arange(n)).to(torch.int32).to(dev)
+        for _ in range(W):
+            se.se_probe_read_pages(pool, pool_pages, pages, n, PB, grid, sink)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ev[0].record()
+        for _ in range(K):
+            se.se_probe_read_pages(pool, pool_pages, pages, n, PB, grid, sink)
+        ev[1].record()
+        torch.cuda.synchronize()
+        us = 1e3 * ev[0].elapsed_time(ev[1]) / K
+        cases[name] = {"pages": n, "bytes": n * PB, "pool_bytes": of * PB, "random": rnd, "work_groups": grid,
+                       "us_per_call": round(us, 2), "GBps": round(n * PB / (us * 1e-6) / 1e9, 1)}
+        print(f"{name}: {us:.1f} us, {cases[name]['GBps']} GB/s", file=sys.stderr, flush=True)
+    head = cases[READ_CASES[0][0]]
+    line = {"metric": "hbm_read_GBps", "value": head["GBps"], "unit": "GB/s", "n_gpus": 1, "steps": K, "warmup": W,
+            "ms_per_step": round(head["us_per_call"] / 1e3, 4), "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "u8", "data": "synthetic",
+            "config": {"workload": "read_ceiling", "page_bytes": PB, "parallelism": "none (1 GPU)"},
+            "roofline": {"bound": "hbm", "kernel": "probe_read_kernel", "achieved": head["GBps"],
+                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(head["GBps"] / HBM_PEAK_GBS, 4),
+                         "traffic": None},
+            "cases": cases}
+    print(json.dumps(line))
 
 
 def main_prune(args):
@@ -1111,6 +1170,9 @@ def main():
         return
     if args.workload == "prune":
         main_prune(args)
+        return
+    if args.workload == "read_ceiling":
+        main_read_ceiling(args)
         return
     from workloads import CONFIGS
     w = CONFIGS[args.config]

@@ -412,6 +412,19 @@ const char* se_status_string(se_status status);
 /* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
 int32_t se_version(void);
 
+/* se_probe_read_pages — a measurement aid, not a step of the method (no passage of
+ * the paper defines it): the plain read rate of a page gather, which bounds what an
+ * HBM-bound kernel reading the same pages can reach.  Reads all page_bytes bytes of
+ * each page pages[0 .. n_pages) of `pool` (pool_pages pages of page_bytes bytes;
+ * entries outside [0, pool_pages) read page 0) with the decode stream's 16-byte
+ * nontemporal loads, on `grid` work-groups of 512 threads, and stores one XOR fold
+ * per thread in sink (uint32 [grid * 512], written, never read).  The call's time
+ * over n_pages * page_bytes is the read rate.
+ *  page_bytes must be 8192 (a 16-slot page at d = 128); grid >= 1; n_pages >= 1.
+ *  Errors: null pointers or other sizes -> SE_ERR_INVALID_ARGUMENT. */
+se_status se_probe_read_pages(const void* pool, int64_t pool_pages, const int32_t* pages, int64_t n_pages,
+                              int32_t page_bytes, int32_t grid, uint32_t* sink, hipStream_t stream);
+
 /*
  * se_prune_interval — sparsity-based prefix-cache pruning of a history interval
  * (Section 3.2, "Sparsity-Based Prefix-Cache Pruning", eq. prefix-pruning; Appendix C.2,

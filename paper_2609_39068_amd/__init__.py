@@ -9,7 +9,7 @@ from ._binding import (  # noqa: F401
     se_decode_step_quest, se_snapkv_compact, se_omnikv_select, se_attend_slots,
     se_h2o_prefill_chunk, se_prune_interval,
     se_evict_compact, se_quest_select, se_quest_summarize, se_read_device_errors,
-    se_version, se_workspace_bytes, status_string,
+    se_version, se_workspace_bytes, status_string, se_probe_read_pages,
     SE_ATTEND_ACCUMULATE, SE_QUEST_SCORES_GIVEN, SE_OP_DECODE_ATTEND, SE_OP_QUEST_SELECT,
     SE_OP_QUEST_STEP, SE_OP_SNAPKV, SE_SNAPKV_SCORE_ONLY, SE_OP_OMNIKV_SELECT, SE_OP_H2O_PREFILL,
     SE_DEVERR_BAD_PAGE, SE_DEVERR_CAPACITY, SE_DEVERR_BAD_LENGTH, SE_DEVERR_BAD_SELECTION,

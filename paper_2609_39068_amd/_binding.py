@@ -43,7 +43,7 @@ EXPORTED = (
     "se_decode_attend", "se_decode_step_h2o", "se_decode_step_quest", "se_accumulate_scores", "se_evict_compact", "se_quest_summarize",
     "se_quest_select", "se_workspace_bytes", "se_read_device_errors", "se_status_string",
     "se_version", "se_snapkv_compact", "se_omnikv_select", "se_attend_slots", "se_h2o_prefill_chunk",
-    "se_prune_interval", "se_decode_step_h2o_noalloc", "se_static_scratch_bytes",
+    "se_prune_interval", "se_decode_step_h2o_noalloc", "se_static_scratch_bytes", "se_probe_read_pages",
 )
 
 
@@ -97,6 +97,7 @@ def _load():
         "se_read_device_errors": (I32, [P, P, P]),
         "se_status_string": (ctypes.c_char_p, [I32]),
         "se_version": (I32, []),
+        "se_probe_read_pages": (I32, [P, ctypes.c_int64, P, ctypes.c_int64, I32, I32, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -316,6 +317,17 @@ def se_read_device_errors(dev_err, stream=None) -> int:
 
 def se_version() -> int:
     return int(_lib.se_version())
+
+
+def se_probe_read_pages(pool, pool_pages, pages, n_pages, page_bytes, grid, sink, stream=None):
+    """Measurement aid: reads the listed pages of `pool` (the read-rate ceiling of a page gather)."""
+    _need(pool, int(pool_pages) * int(page_bytes) // pool.element_size(), "pool")
+    _need(pages, int(n_pages), "pages")
+    _need(sink, int(grid) * 512, "sink")
+    st = _lib.se_probe_read_pages(_ptr(pool, None, "pool"), int(pool_pages), _ptr(pages, torch.int32, "pages"),
+                                  int(n_pages), int(page_bytes), int(grid), _ptr(sink, torch.int32, "sink"),
+                                  _stream(stream))
+    _check("se_probe_read_pages", st)
 
 
 def raw_library():

@@ -19,7 +19,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 18, names
+    assert len(names) == 19, names
     lib = b.raw_library()
     for n in names:
         assert hasattr(lib, n), f"{n} is declared in sparse_engine.h but not exported"
@@ -248,3 +248,18 @@ def test_workspace_sizes():
     assert b.se_workspace_bytes(b.SE_OP_H2O_PREFILL, 10, 1000, 63, 4, 128, 128) == 10 * 4 * 1024 * 4 + 10 * moves
     assert b.se_workspace_bytes(b.SE_OP_H2O_PREFILL, 10, 1000, 63, 4, 128, 32) == 10 * 1 * 1024 * 4 + 10 * moves
     assert b.se_workspace_bytes(99, 1, 1, 1, 1, 64, 0) == 0
+
+
+def test_probe_read_argument_checks():
+    lib = b.raw_library()
+
+    def call(pool=0x1000, pool_pages=64, pages=0x2000, n=8, page_bytes=8192, grid=4, sink=0x3000):
+        return lib.se_probe_read_pages(pool, pool_pages, pages, n, page_bytes, grid, sink, None)
+
+    assert call(pool=None) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(pages=None) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(sink=None) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(page_bytes=4096) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(grid=0) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(n=0) == b.SE_ERR_INVALID_ARGUMENT
+    assert call(pool_pages=0) == b.SE_ERR_INVALID_ARGUMENT
