@@ -192,15 +192,20 @@ def quest_step_bytes(L_pre, G, D, top_k):
     return int(n_cand.sum()) * (2 * D * 2) + int(visited.sum()) * (2 * D * 2) + L.shape[0] * per_unit
 
 
-def attend_kernel_name(units, n_visit, G, D):
+def attend_kernel_name(units, n_visit, G, D, quest=False):
     """The decode_attend_kernel instantiation a launch of these sizes runs (the
     library's rule: 1024 threads when the units fit one work-group per compute
     unit, else 512; per-wavefront rows for the fused steady eviction when the
-    largest wavefront slot's share of the pages fits them)."""
+    largest wavefront slot's share of the pages fits them and every page's
+    weights fit the LDS buffer; a Quest step's selection has its own)."""
     wide = units * -(-n_visit // 1024) <= 256
     nt = 1024 if wide else 512
+    if quest:
+        return f"decode_attend_kernel<{D},{G},{nt},false,true>"
     rows = (4 * 4 * 5 * 100 - 50) // (34 if wide else 58)
-    return f"decode_attend_kernel<{D},{G},{nt},{'true' if n_visit <= rows else 'false'}>"
+    wbytes = 4 if (nt == 512 and G <= 4) else 2  # fp32 or fp16 weights
+    rows = min(rows, 1024, 9216 * 4 // wbytes // (16 * G))
+    return f"decode_attend_kernel<{D},{G},{nt},{'true' if n_visit <= rows else 'false'},false>"
 
 
 def snapkv_bytes(L, w, G, D, budget):
@@ -1104,7 +1109,7 @@ def run_decode(w, K, W, se, dev):
 
     def kernels(ml):
         nv = n_visit_of(ml)
-        name = attend_kernel_name(U, nv, G, D)
+        name = attend_kernel_name(U, nv, G, D, quest=w.method == "quest")
         if w.method == "quest":
             return name + " (page bounds, top-k and attention)"
         ns = split_count(U, nv)
@@ -1131,7 +1136,7 @@ def run_decode(w, K, W, se, dev):
     else:
         dom_ms, dom_bytes, dom_launches, dom_ml = region_ms, sum(step_bytes), K * calls, bounds[0]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
-    roof = {"bound": "hbm", "kernel": attend_kernel_name(U, n_visit_of(dom_ml), G, D),
+    roof = {"bound": "hbm", "kernel": attend_kernel_name(U, n_visit_of(dom_ml), G, D, quest=w.method == "quest"),
             "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": None if traffic is None else traffic.get("hbm_bytes_steady"),
