@@ -346,7 +346,9 @@ se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, const void* 
  *  score_window 1 .. chunk_len, score_window * q_per_kv <= 1024; a unit with L <
  *               chunk_len sets SE_DEVERR_BAD_LENGTH and its scores are not updated
  *               (the eviction still applies to it)
- *  scale, budget, recent, max_len, freed_* as for se_evict_compact; max_len <= 131072
+ *  scale, budget, recent, max_len, freed_* as for se_evict_compact; max_len <= 131072;
+ *               a budget of at least max_len may exceed se_evict_compact's 8192: no unit
+ *               evicts, so the call only scores the chunk
  *  ws           se_workspace_bytes(SE_OP_H2O_PREFILL, num_units, max_len, max_pages,
  *               q_per_kv, head_dim, score_window) bytes (no zero-fill needed)
  */

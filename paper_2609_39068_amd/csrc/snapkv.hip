@@ -813,7 +813,8 @@ extern "C" se_status se_h2o_prefill_chunk(const se_kv_view* kv, int32_t q_per_kv
   if (!(scale > 0.f) || !(scale < INFINITY)) return SE_ERR_INVALID_ARGUMENT;
   if (freed_pages != nullptr && freed_stride < kv->max_pages) return SE_ERR_INVALID_ARGUMENT;
   if ((int64_t)score_window * q_per_kv > 8 * kSnapMaxRows) return SE_ERR_UNSUPPORTED;
-  if (budget > kMaxBudget || max_len > kSnapMaxPages * kPage) return SE_ERR_UNSUPPORTED;
+  // a budget of at least max_len evicts nothing, so it needs no eviction capacity
+  if ((budget > kMaxBudget && budget < max_len) || max_len > kSnapMaxPages * kPage) return SE_ERR_UNSUPPORTED;
   if (ws == nullptr || ws_bytes < se_h2o_prefill_workspace_bytes(kv->num_units, max_len, q_per_kv, score_window))
     return SE_ERR_WORKSPACE;
 

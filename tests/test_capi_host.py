@@ -200,7 +200,8 @@ def test_h2o_prefill_argument_checks():
     assert call(recent=-1) == b.SE_ERR_INVALID_ARGUMENT
     assert call(scale=0.0) == b.SE_ERR_INVALID_ARGUMENT
     assert call(G=8, sw=129, chunk=200) == b.SE_ERR_UNSUPPORTED   # 1032 scoring rows
-    assert call(budget=9000) == b.SE_ERR_UNSUPPORTED
+    assert call(budget=9000, max_len=16384) == b.SE_ERR_UNSUPPORTED
+    assert call(budget=9000, max_len=9000, ws=None) == b.SE_ERR_WORKSPACE  # scores only: accepted
     assert call(max_len=131073) == b.SE_ERR_UNSUPPORTED
     assert call(ws=None) == b.SE_ERR_WORKSPACE
     assert call(ws_bytes=8) == b.SE_ERR_WORKSPACE

@@ -2,17 +2,28 @@
 se_h2o_prefill_chunk (the chunk's scores from its last queries, then H2O's
 retention and compaction), one chunk and sequences of chunks.
 
-Every input comes from the seeded generators in workloads/; the oracle reads
-them before any library call touches them.  The test writes each chunk's keys,
-values and positions into the pools, as the prefill does before calling.
+Every chunk is checked by the same protocol as the decode steps: the oracle
+starts from the GPU's state before the chunk; a copy of that state takes the
+chunk with a budget no unit reaches (the call then only scores), which exposes
+the GPU's fp32 scores before the retention; the oracle's scores must agree
+with them (1e-3 relative), and the oracle's retention and compaction fed those
+fp32 scores must give the real call's retained set, slot layout, K/V bits,
+positions, scores and freed pages exactly.  The oracle's float64 retention may
+differ from that only by swaps of near-tied slots.  No unit is dropped.
+
+Every input comes from the seeded generators in workloads/.  The test writes
+each chunk's keys, values and positions into the pools, as the prefill does
+before calling.
 """
 import numpy as np
 import pytest
 import torch
 
 from oracle import h2o
+from oracle.state import new_unit
 from tests.oracle_bridge import assert_scores_close, f64, gpu_unit, h2o_near_tie, oracle_unit
-from workloads import H2O_PREFILL, build_observation, build_state, isolated_units, observation_queries, to_device
+from workloads import (H2O_PREFILL, build_observation, build_state, clone_state, isolated_units, observation_queries,
+                       to_device)
 
 pytestmark = pytest.mark.gpu
 
@@ -42,73 +53,90 @@ def _write_chunk(st, u, L0, K, V, pos):
     st.lengths[u] = L0 + K.shape[0]
 
 
-def _run(se, lengths0, hkv, G, d, chunks, sw, budget, recent, seed, max_diverged=0):
-    """Runs the chunks (lengths) through every unit on both sides and compares
-    after each.  Returns the number of units that ended on a near-tie."""
+def _scored_copy(se, gs, hkv, G, qs, sw, C, scale, recent, max_len, ws, err):
+    """A copy of the state after the chunk's scoring alone: with a budget of
+    max_len no unit evicts, so its scores are the GPU's fp32 scores before the
+    retention (the scoring does not depend on the budget)."""
+    cs = clone_state(gs)
+    se.se_h2o_prefill_chunk(_view(se, cs, hkv), G, qs, sw, C, scale, max_len, recent, max_len, None, 0, None, ws, err)
+    return cs
+
+
+def _check_chunk(where, r, c, g, budget, recent, fc, fp, bt_row):
+    """One unit after one chunk.  r: the oracle's chunk from the GPU's
+    pre-chunk state; c: the GPU unit after scoring only; g: after the real
+    call; fc / fp / bt_row: its freed count, freed pages and block-table row.
+    Returns 1 when the float64 retention differs from the fp32 one by near
+    ties."""
+    np.testing.assert_array_equal(c["pos"], r["pos_after_append"], err_msg=f"{where}: positions")
+    assert_scores_close(c["u"], r["u_after_accumulate"], where)
+    keep = h2o.retain(c["pos"], c["u"], budget, recent)
+    st = new_unit(c["K"].copy(), c["V"].copy(), c["pos"].copy(), c["u"].copy())
+    _, _, freed = h2o.compact(st, keep, budget)
+    np.testing.assert_array_equal(g["pos"], st.pos, err_msg=f"{where}: retained positions")
+    np.testing.assert_array_equal(g["K"], st.K, err_msg=f"{where}: keys")
+    np.testing.assert_array_equal(g["V"], st.V, err_msg=f"{where}: values")
+    np.testing.assert_array_equal(g["u"], st.u, err_msg=f"{where}: scores")
+    assert fc == len(freed), f"{where}: freed count"
+    np.testing.assert_array_equal(fp[:len(freed)], bt_row[freed], err_msg=f"{where}: freed pages")
+    if np.array_equal(keep, r["keep"]):
+        return 0
+    by_pos = dict(zip(r["pos_after_append"].tolist(), r["u_after_accumulate"].tolist()))
+    pos = c["pos"]
+    assert h2o_near_tie(by_pos, set(pos[keep].tolist()), set(pos[r["keep"]].tolist())), \
+        f"{where}: float64 retention differs beyond a near tie"
+    return 1
+
+
+def _run(se, lengths0, hkv, G, d, chunks, sw, budget, recent, seed):
+    """Runs the chunks through every unit, each checked after every chunk by
+    the protocol above.  Returns the number of near-tie differences."""
     U = len(lengths0)
     nreq = U // hkv
     cap = max(lengths0) + sum(chunks) + 16
     host = isolated_units(lengths0, -(-cap // 16), d, seed, num_kv_heads=hkv, position_mode="gapped")
     scale = float(np.float32(1 / np.sqrt(d)))
-    ost = {u: oracle_unit(host, u) for u in range(U)}
     gs = to_device(host, DEV)
-    view = _view(se, gs, hkv)
     max_len = cap
     ws = torch.empty(se.se_workspace_bytes(se.SE_OP_H2O_PREFILL, U, max_len, host.max_pages, G, d, sw),
                      dtype=torch.uint8, device=DEV)
     freed = torch.full((U, host.max_pages), -7, dtype=torch.int32, device=DEV)
     fcount = torch.zeros(U, dtype=torch.int32, device=DEV)
     err = torch.zeros(1, dtype=torch.int32, device=DEV)
-    diverged = set()
+    near = 0
     for ci, C in enumerate(chunks):
         kc = observation_queries(nreq, C, hkv, d, seed + 10 * ci + 1)
         vc = observation_queries(nreq, C, hkv, d, seed + 10 * ci + 2)
         qs = observation_queries(nreq, sw, hkv * G, d, seed + 10 * ci + 3)
-        # the device state gathered to the host, the chunk written, and back
+        # the device state gathered to the host (the oracle starts from it), the
+        # chunk written, and back
         hs = type(host)(**{**host.__dict__, "kv_pool": gs.kv_pool.cpu(), "pos_pool": gs.pos_pool.cpu(),
                            "score_pool": gs.score_pool.cpu(), "lengths": gs.lengths.cpu(),
                            "block_table": gs.block_table.cpu()})
-        res = {}
+        ost, cpos = {}, {}
         for u in range(U):
             req, h = divmod(u, hkv)
             L0 = int(hs.lengths[u])
+            ost[u] = oracle_unit(hs, u)
             base = int(max(ost[u].pos.max() + 1, 0)) if ost[u].length else 0
-            pos = base + 3 * np.arange(C)
-            if u not in diverged:
-                res[u] = h2o.prefill_chunk(ost[u], f64(kc[req, :, h]), f64(vc[req, :, h]), pos,
-                                           f64(qs[req, :, h * G:(h + 1) * G]), scale, budget, recent)
-            _write_chunk(hs, u, L0, kc[req, :, h], vc[req, :, h], pos)
+            cpos[u] = base + 3 * np.arange(C)
+            _write_chunk(hs, u, L0, kc[req, :, h], vc[req, :, h], cpos[u])
         gs = to_device(hs, DEV)
-        view = _view(se, gs, hkv)
         print(f"chunk {ci}: C={C} sw={sw} G={G} d={d} B={budget} w={recent}", flush=True)
-        se.se_h2o_prefill_chunk(view, G, qs.to(DEV), sw, C, scale, budget, recent, max_len, freed, host.max_pages,
-                                fcount, ws, err)
+        cs = _scored_copy(se, gs, hkv, G, qs.to(DEV), sw, C, scale, recent, max_len, ws, err)
+        se.se_h2o_prefill_chunk(_view(se, gs, hkv), G, qs.to(DEV), sw, C, scale, budget, recent, max_len, freed,
+                                host.max_pages, fcount, ws, err)
         torch.cuda.synchronize()
         assert se.se_read_device_errors(err) == 0
         fc, fp = fcount.cpu().numpy(), freed.cpu().numpy()
         bt = hs.block_table.numpy()
-        for u, r in res.items():
-            st = ost[u]
-            g = gpu_unit(gs, u)
-            if len(r["keep"]) <= budget:      # nothing evicted: every score compared
-                np.testing.assert_array_equal(g["pos"], st.pos)
-                assert_scores_close(g["u"], st.u, f"chunk {ci} unit {u}")
-                continue
-            kept_g, kept_o = set(g["pos"].tolist()), set(st.pos.tolist())
-            if kept_g != kept_o:
-                by_pos = dict(zip(r["pos_after_append"].tolist(), r["u_after_accumulate"].tolist()))
-                assert h2o_near_tie(by_pos, kept_g, kept_o), f"chunk {ci} unit {u}: retained sets differ"
-                diverged.add(u)
-                continue
-            np.testing.assert_array_equal(g["pos"], st.pos)
-            np.testing.assert_array_equal(g["K"], st.K)
-            np.testing.assert_array_equal(g["V"], st.V)
-            assert_scores_close(g["u"], st.u, f"chunk {ci} unit {u} after compaction")
-            n = len(r["freed"])
-            assert fc[u] == n
-            np.testing.assert_array_equal(fp[u, :n], bt[u, r["freed"]])
-    assert len(diverged) <= max_diverged, diverged
-    return len(diverged)
+        for u in range(U):
+            req, h = divmod(u, hkv)
+            r = h2o.prefill_chunk(ost[u], f64(kc[req, :, h]), f64(vc[req, :, h]), cpos[u],
+                                  f64(qs[req, :, h * G:(h + 1) * G]), scale, budget, recent)
+            near += _check_chunk(f"chunk {ci} unit {u}", r, gpu_unit(cs, u), gpu_unit(gs, u), budget, recent,
+                                 fc[u], fp[u], bt[u])
+    return near
 
 
 @pytest.mark.parametrize("G,d,sw", [(4, 128, 32), (4, 128, 64), (2, 64, 100), (1, 128, 7), (8, 64, 16)])
@@ -117,7 +145,7 @@ def test_chunk_sequence(se, G, d, sw):
     # 257 and 400 tokens, budget 512 with a 256-token window (ratio 0.5);
     # sw * G from 7 to 200 rows (two row blocks for 64 x 4 and 100 x 2)
     lengths0 = [0, 0, 100, 100, 511, 511, 700, 700]
-    _run(se, lengths0, 2, G, d, [300, 257, 400], sw, 512, 256, seed=G * 100 + sw, max_diverged=2)
+    _run(se, lengths0, 2, G, d, [300, 257, 400], sw, 512, 256, seed=G * 100 + sw)
 
 
 def test_whole_chunk_scoring_without_eviction(se):
@@ -128,7 +156,7 @@ def test_whole_chunk_scoring_without_eviction(se):
 
 def test_short_chunk_behind_a_long_state(se):
     # a 16-token chunk after 3000 retained slots: one page of window keys
-    _run(se, [3000, 3000], 2, 4, 128, [16, 33], 16, 2048, 1024, seed=8, max_diverged=1)
+    _run(se, [3000, 3000], 2, 4, 128, [16, 33], 16, 2048, 1024, seed=8)
 
 
 def test_length_below_chunk_is_reported(se):
@@ -168,6 +196,7 @@ def test_full_workload_sampled_units(se):
     fcount = torch.zeros(U, dtype=torch.int32, device=DEV)
     err = torch.zeros(1, dtype=torch.int32, device=DEV)
     print(f"full prefill workload: U={U} L={int(gs.lengths[0])} C={C} sw={sw}", flush=True)
+    cs = _scored_copy(se, gs, w.hkv, G, qs, sw, C, w.scale, w.recent, max_len, ws, err)
     se.se_h2o_prefill_chunk(_view(se, gs, w.hkv), G, qs, sw, C, w.scale, w.budget, w.recent, max_len, freed,
                             gs.max_pages, fcount, ws, err)
     torch.cuda.synchronize()
@@ -178,19 +207,7 @@ def test_full_workload_sampled_units(se):
     for u in sample:
         req, h = divmod(u, w.hkv)
         r = h2o.chunk_eviction(ost[u], C, f64(q[req, :, h * G:(h + 1) * G]), w.scale, w.budget, w.recent)
-        st, g = ost[u], gpu_unit(gs, u)
-        kept_g, kept_o = set(g["pos"].tolist()), set(st.pos.tolist())
-        if kept_g != kept_o:
-            by_pos = dict(zip(r["pos_after_append"].tolist(), r["u_after_accumulate"].tolist()))
-            assert h2o_near_tie(by_pos, kept_g, kept_o), f"unit {u}: retained sets differ"
-            continue
-        np.testing.assert_array_equal(g["pos"], st.pos)
-        np.testing.assert_array_equal(g["K"], st.K)
-        np.testing.assert_array_equal(g["V"], st.V)
-        assert_scores_close(g["u"], st.u, f"unit {u}")
-        n = len(r["freed"])
-        assert fc[u] == n
-        np.testing.assert_array_equal(fp[u, :n], bt[u, r["freed"]])
+        _check_chunk(f"unit {u}", r, gpu_unit(cs, u), gpu_unit(gs, u), w.budget, w.recent, fc[u], fp[u], bt[u])
 
 
 def test_maximum_length(se):
@@ -210,22 +227,13 @@ def test_maximum_length(se):
     fcount = torch.zeros(1, dtype=torch.int32, device=DEV)
     err = torch.zeros(1, dtype=torch.int32, device=DEV)
     print(f"maximum length: L={L} C={C} sw={sw}", flush=True)
+    cs = _scored_copy(se, gs, 1, G, qs.to(DEV), sw, C, scale, recent, L, ws, err)
     se.se_h2o_prefill_chunk(_view(se, gs, 1), G, qs.to(DEV), sw, C, scale, budget, recent, L, freed, 8192, fcount,
                             ws, err)
     torch.cuda.synchronize()
     assert se.se_read_device_errors(err) == 0
     assert int(gs.lengths[0]) == budget
     r = h2o.chunk_eviction(st, C, f64(qs[0]), scale, budget, recent)
-    g = gpu_unit(gs, 0)
-    kept_g, kept_o = set(g["pos"].tolist()), set(st.pos.tolist())
-    if kept_g != kept_o:
-        by_pos = dict(zip(r["pos_after_append"].tolist(), r["u_after_accumulate"].tolist()))
-        assert h2o_near_tie(by_pos, kept_g, kept_o), "retained sets differ"
-        return
-    np.testing.assert_array_equal(g["pos"], st.pos)
-    np.testing.assert_array_equal(g["K"], st.K)
-    np.testing.assert_array_equal(g["V"], st.V)
-    assert_scores_close(g["u"], st.u, "maximum length")
-    n = len(r["freed"])
-    assert int(fcount[0]) == n
-    np.testing.assert_array_equal(freed[0, :n].cpu().numpy(), host.block_table.numpy()[0, r["freed"]])
+    _check_chunk("maximum length", r, gpu_unit(cs, 0), gpu_unit(gs, 0), budget, recent, int(fcount[0]),
+                 freed[0].cpu().numpy(), host.block_table[0].numpy())
+
