@@ -52,6 +52,14 @@ sys.path.insert(0, ROOT)
 
 METRIC = "decode attn+eviction tokens/s/GPU; achieved HBM GB/s vs MI355X peak"
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+# Vector ALU: 256 compute units x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3e12 lane-slots/s
+# (one full-rate VALU operation per lane per slot; packed fp32, which would double
+# fma and add, is not used by this build); v_exp_f32 takes two slots (measured on
+# one MI355X: fma 3.99e13 lane-ops/s, exp2 alone 1.68e13/s, exp2 followed by two
+# fma 1.06e13/s).
+VALU_PEAK_TSLOTS = 256 * 4 * 16 * 2.4e9 / 1e12
+VALU_SLOTS_PER_LOGIT = 2 * (2 + 1 + 1)
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_step_h2o_llama3-8b-layer-h2o_traffic.txt")
 SNAPKV_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "snapkv_compact_llama3-8b-prompt-snapkv_traffic.txt")
 DECODE_SOURCES = ("decode_attend.hip", "evict_compact.hip", "evict_core.h", "quest_core.h", "se_common.h")
@@ -490,8 +498,16 @@ def main_h2o_prefill(args):
     elapsed = float(np.sum(walls))
     nbytes, flops = prefill_work(lengths0, C, sw, G, D, w.budget)
     achieved = nbytes / (ms * 1e-3) / 1e9
+    # the binding resource: the vector ALU.  Every logit is exponentiated in both
+    # passes (the row normaliser, then the weights), each time with one scale-and-
+    # shift and one accumulation: 2 x (2 + 1 + 1) lane-slots, exp2 running at half
+    # the full rate (at the peaks the ALU work takes 68 us, the HBM bytes 62 us and
+    # the logit MFMAs 34 us)
+    logits = flops // (2 * D)
+    valu_slots = logits * VALU_SLOTS_PER_LOGIT
+    alu_achieved = valu_slots / (ms * 1e-3) / 1e12
     result = {
-        "metric": "H2O chunked-prefill eviction prompt-tokens/s/GPU; achieved HBM GB/s vs MI355X peak",
+        "metric": "H2O chunked-prefill eviction prompt-tokens/s/GPU; achieved vector-ALU rate vs MI355X peak",
         "value": round(w.num_req * C * K / elapsed, 1),
         "unit": "prompt tokens/s",
         "n_gpus": 1, "steps": K, "warmup": W,
@@ -502,13 +518,17 @@ def main_h2o_prefill(args):
                    "head_dim": D, "page_size": w.page_size, "prompt": w.ctx, "chunk": C,
                    "retained_before": w.initial_resident - C, "scoring_window": sw, "budget": w.budget,
                    "recent": w.recent, "accumulate": "f32", "parallelism": "none (1 GPU)"},
-        "roofline": {"bound": "hbm", "kernel": "se_h2o_prefill_chunk", "achieved": round(achieved, 1),
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "roofline": {"bound": "alu", "kernel": "se_h2o_prefill_chunk (snapkv_score_kernel, accumulate mode)",
+                     "achieved": round(alu_achieved, 2), "peak": VALU_PEAK_TSLOTS,
+                     "unit": "T VALU lane-slots/s", "frac": round(alu_achieved / VALU_PEAK_TSLOTS, 4),
                      "traffic": read_traffic(PREFILL_TRAFFIC_SUMMARY, SNAPKV_SOURCES),
                      "avg_launch_us": round(1e3 * ms, 3),
+                     "algorithmic_valu_slots_per_launch": valu_slots,
                      "algorithmic_bytes_per_launch": nbytes,
                      "algorithmic_flops_per_launch": flops,
-                     "mfma_TFLOPs": round(flops / (ms * 1e-3) / 1e12, 1)},
+                     "hbm": {"achieved_GBps": round(achieved, 1), "frac": round(achieved / HBM_PEAK_GBS, 4)},
+                     "mfma": {"achieved_TFLOPs": round(flops / (ms * 1e-3) / 1e12, 1),
+                              "frac": round(flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)}},
         "cpu_baseline": cpu,
     }
     if args.copy_calibration:
