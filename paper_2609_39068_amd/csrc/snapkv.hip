@@ -46,7 +46,10 @@
 //
 // H2O chunk scoring (se_h2o_prefill_chunk) runs the same kernel over every key
 // with the causal mask in both passes, one row block of up to 128 scoring rows
-// per work-group (grid.y), one work-group per CU.  There the stages made only
+// per work-group (grid.y), one work-group per CU; a block of 128 rows sits in
+// two row groups of 64 (four row tiles per wavefront, each stage's four pages
+// split over the four wavefronts of a row group), so each key piece read from
+// LDS feeds four MFMA row tiles instead of two.  There the stages made only
 // of pages below the window run pipelined: stage j's MFMAs are issued in the
 // same branch-free block as the exponentials of stage j - 1's logits (the two
 // stages' logits alternate between two register sets), and four stages of
@@ -63,14 +66,12 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kSnapThreads = 512;
 constexpr int kSnapWaves = kSnapThreads / kWave;
-constexpr int kSnapRowGroups = 4;       // 32 rows each
-constexpr int kSnapHalves = kSnapWaves / kSnapRowGroups;  // key halves of a stage
+constexpr int kSnapRowGroups = 4;       // of up to 32 rows (SnapKV); H2O chunk scoring: 2 of 64
 constexpr int kSnapMaxRows = 128;
 constexpr int kPrefillBlockRows = 128;  // rows of a work-group in H2O chunk scoring
 constexpr int kSnapMaxHalf = 15;        // kappa <= 31
 constexpr int kSnapMaxPages = 8192;     // pages per unit (131072 slots)
 constexpr int kSnapStagePages = 4;      // pages per ring stage
-constexpr int kSnapHalfPages = kSnapStagePages / kSnapHalves;
 constexpr int kSnapBatches = 2;         // stages in flight per thread
 constexpr int kSnapPoolChunk = 2048;    // slots pooled per LDS round
 constexpr int kSnapHalo = kSnapMaxHalf + 1;
@@ -278,19 +279,23 @@ __device__ __forceinline__ void snapkv_pool(const SnapParams& p, const int32_t* 
 // the work-group's row block blockIdx.y).  kAccum: H2O chunk scoring -- u over
 // every key (the window keys with their causal mask) into the row block's
 // partial row of the workspace, no pooling; otherwise SnapKV.
-template <int D, int RTW, bool kAccum, bool kPipe, int kOcc>
+template <int D, int RTW, bool kAccum, bool kPipe, int kOcc, int NRG>
 __global__ __launch_bounds__(kSnapThreads, kOcc) void snapkv_score_kernel(const SnapParams p) {
+  // NRG row groups of 16 * RTW rows; the wavefronts of one row group split
+  // each stage's pages (NKH key parts of H pages)
+  constexpr int NKH = kSnapWaves / NRG;
+  static_assert(NKH * NRG == kSnapWaves && kSnapStagePages % NKH == 0, "wavefront layout");
   // stages in flight per thread: four when one work-group holds the CU
   constexpr int kNB = kOcc <= 2 ? 2 * kSnapBatches : kSnapBatches;
   constexpr int KS = D / 32;
   constexpr int S = kSnapStagePages;
-  constexpr int H = kSnapHalfPages;
+  constexpr int H = kSnapStagePages / NKH;
   constexpr int PB = 32 * D;
   constexpr int kRingBytes = 2 * S * 32 * 128;  // sized for head_dim 128
   static_assert(kRingBytes >= (kSnapPoolChunk + 2 * kSnapHalo) * 8, "the pool chunk reuses the ring");
   __shared__ __attribute__((aligned(16))) uint8_t s_ring[kRingBytes];
-  __shared__ float s_up[2][S][kSnapRowGroups][kPage];     // [stage parity][page][row group][key]
-  __shared__ float s_norm[kSnapHalves][2][kSnapMaxRows];   // [key half][ref, sum][row]
+  __shared__ float s_up[2][S][NRG][kPage];     // [stage parity][page][row group][key]
+  __shared__ float s_norm[NKH][2][kSnapMaxRows];   // [key part][ref, sum][row]
   __shared__ int s_red[kSnapWaves];
 
   const int tid = threadIdx.x;
@@ -298,8 +303,8 @@ __global__ __launch_bounds__(kSnapThreads, kOcc) void snapkv_score_kernel(const 
   const int grp = lane >> 4;
   const int col = lane & 15;
   const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);
-  const int rg = wv % kSnapRowGroups;
-  const int kh = wv / kSnapRowGroups;
+  const int rg = wv % NRG;
+  const int kh = wv / NRG;
   const int unit = blockIdx.x;
   const int L = p.lengths[unit];
   if ((!kAccum || p.snap_wide) && L <= p.budget) return;  // the prompt already fits: nothing to score or evict
@@ -501,7 +506,7 @@ __global__ __launch_bounds__(kSnapThreads, kOcc) void snapkv_score_kernel(const 
       const int row = row0 + 16 * T + 4 * grp + r;  // within the block
       float m = s_norm[0][0][row], sm = s_norm[0][1][row];
 #pragma unroll
-      for (int h = 1; h < kSnapHalves; ++h) merge_norm(m, sm, s_norm[h][0][row], s_norm[h][1][row]);
+      for (int h = 1; h < NKH; ++h) merge_norm(m, sm, s_norm[h][0][row], s_norm[h][1][row]);
       bias[T][r] = rbase + row < R ? m + __log2f(sm) : INFINITY;
     }
 
@@ -519,7 +524,7 @@ __global__ __launch_bounds__(kSnapThreads, kOcc) void snapkv_score_kernel(const 
       const float* up = &s_up[j & 1][wv][0][lane];
       float v = 0.f;
 #pragma unroll
-      for (int g = 0; g < kSnapRowGroups; ++g) v += up[g * kPage];
+      for (int g = 0; g < NRG; ++g) v += up[g * kPage];
       const int key = (j * S + wv) * kPage + lane;
       if (key < n_lim) u[key] = v;
     }
@@ -605,10 +610,17 @@ void launch_snapkv_d(const SnapParams& p, int num_units, int rows, hipStream_t s
   // which the pipelined form would not fit the registers
   constexpr int occ = kAccum ? 2 : 4;
   constexpr bool pipe = kAccum;
-  if (rows <= 64)
-    hipLaunchKernelGGL((snapkv_score_kernel<D, 1, kAccum, pipe, occ>), grid, dim3(kSnapThreads), 0, stream, p);
-  else
-    hipLaunchKernelGGL((snapkv_score_kernel<D, 2, kAccum, pipe, occ>), grid, dim3(kSnapThreads), 0, stream, p);
+  if (rows <= 64) {
+    hipLaunchKernelGGL((snapkv_score_kernel<D, 1, kAccum, pipe, occ, kSnapRowGroups>), grid, dim3(kSnapThreads), 0,
+                       stream, p);
+  } else if constexpr (kAccum) {
+    // 128 rows as two groups of 64: each key piece a wavefront reads from LDS
+    // feeds four row tiles, which halves the LDS reads of a stage
+    hipLaunchKernelGGL((snapkv_score_kernel<D, 4, kAccum, pipe, occ, 2>), grid, dim3(kSnapThreads), 0, stream, p);
+  } else {
+    hipLaunchKernelGGL((snapkv_score_kernel<D, 2, kAccum, pipe, occ, kSnapRowGroups>), grid, dim3(kSnapThreads), 0,
+                       stream, p);
+  }
 }
 
 // SnapKV with more than 128 scoring rows: the scoring kernel ran in its
