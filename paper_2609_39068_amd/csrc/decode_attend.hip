@@ -826,20 +826,27 @@ __device__ __forceinline__ void pv_page(const Lanes<D>& ln, const uint32_t (&vb)
 
 // se_decode_step_quest's selection inside the attention kernel (one work-group
 // per unit): the candidates' block-table row, the selection after it and the
-// page scores live in the weight buffer, unused by Quest.  The page staging
-// reads the selection and the selected pages' physical ids from there, and
-// the selection goes to sel at the end of the kernel (a store before a
-// barrier would hold the barrier until it completes).  Returns the selection
-// in LDS.
+// page scores live in the weight buffer, unused by Quest.  The selection goes
+// to sel at the end of the kernel (a store before a barrier would hold the
+// barrier until it completes).  Returns the selection in LDS.  When every
+// candidate page is in the pool and there are at least top_k of them (and the
+// current page is in the pool), the selection's output step also writes the
+// staged page list (lds_phys / lds_lp / lds_vp: the selected pages in rank
+// order, then the current page) and *n_staged is top_k + 1; else *n_staged is
+// -1 and the kernel stages the pages from the selection, skipping bad ones.
 template <int NT, int D, int G>
 __device__ __forceinline__ const int* fused_quest_select(const AttendParams& p, int unit, int req, int kvh,
-                                                         int n_cand, float* lds_w, const EvictScratch<NT>& esc,
-                                                         int* lds_scan) {
+                                                         int n_cand, int cur_page, int ph_cur, float* lds_w,
+                                                         int* lds_phys, int* lds_lp, int* lds_vp,
+                                                         const EvictScratch<NT>& esc, int* n_staged) {
+  __shared__ unsigned s_hist2[256];
+  __shared__ int s_badc;
   const int tid = threadIdx.x;
   const int Hq = p.hkv * G;
   int* const sbt = reinterpret_cast<int*>(lds_w);
   int* const ssel = sbt + n_cand;  // n_cand + top_k <= kSelectMaxPages
   float* const ssc = lds_w + kSelectMaxPages;
+  if (tid == 0) s_badc = 0;  // set below only after the next barrier
   int badc = 0;
   for (int i = tid; i < n_cand; i += NT) {
     int ph = p.block_table[(size_t)unit * p.max_pages + i];
@@ -850,13 +857,39 @@ __device__ __forceinline__ const int* fused_quest_select(const AttendParams& p, 
     sbt[i] = ph;
   }
   if (badc) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
-  if (tid < 256) esc.hist[tid] = 0;
+  if (tid < 256) {
+    esc.hist[tid] = 0;
+    s_hist2[tid] = 0;
+  }
   __syncthreads();
+  if (badc) s_badc = 1;
   unit_bounds<NT, D, G>(p.meta, p.q + ((size_t)req * Hq + (size_t)kvh * G) * D, p.scale, n_cand, sbt, ssc, nullptr,
-                        esc.hist);
+                        esc.hist, s_hist2);
   __syncthreads();
-  unit_topk<NT>(n_cand, p.top_k, ssc, nullptr, ssel, esc.hist, lds_scan, esc.bcast, true);
+  const int top_k = p.top_k;
+  // (every candidate lies before the current page unless the step does not
+  // append and the length ends a page; the staging loop checks that case)
+  const bool direct = __builtin_amdgcn_readfirstlane((int)(s_badc == 0 && n_cand >= top_k && n_cand <= cur_page &&
+                                                           p.n_split == 1 && top_k < kMaxGroupPages && ph_cur >= 0 &&
+                                                           (int64_t)ph_cur < p.num_pages)) != 0;
+  unit_topk<NT>(
+      n_cand, top_k, ssc,
+      [&](int r, int b) {
+        ssel[r] = b;
+        if (direct) {  // b >= 0: n_cand >= top_k
+          lds_phys[r] = sbt[b];
+          lds_lp[r] = b;
+          lds_vp[r] = r;
+        }
+      },
+      esc.hist, s_hist2, esc.bcast, true);
+  if (direct && tid == 0) {
+    lds_phys[top_k] = ph_cur;
+    lds_lp[top_k] = cur_page;
+    lds_vp[top_k] = top_k;
+  }
   __syncthreads();
+  *n_staged = direct ? top_k + 1 : -1;
   return ssel;
 }
 
@@ -958,10 +991,12 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   const int n_cand = select && !bad ? L / kPage : 0;  // complete pages before the current one
   const int* lds_sel = nullptr;
   int ph_cur = -1;
+  int n_staged = -1;  // >= 0: the selection staged the pages itself
   if constexpr (kQuest) {
     if (select) {
       if (!bad) ph_cur = p.block_table[(size_t)unit * p.max_pages + cur_page];
-      lds_sel = fused_quest_select<NT, D, G>(p, unit, req, kvh, n_cand, lds_w, esc, lds_scan);
+      lds_sel = fused_quest_select<NT, D, G>(p, unit, req, kvh, n_cand, cur_page, ph_cur, lds_w, lds_phys, lds_lp,
+                                             lds_vp, esc, &n_staged);
     }
   }
   auto store_sel = [&]() {
@@ -974,9 +1009,9 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   // ---- this work-group's pages: visit index, logical and physical ids of the
   // pages it must read, compacted and staged in LDS once, so the page stream
   // below never waits on a dependent table load or branches around a page
-  const int n_range = max(0, vend - vbeg);
+  const int n_range = n_staged >= 0 ? 0 : max(0, vend - vbeg);
   bool bad_sel = false, bad_page = false;
-  int n_grp = 0;
+  int n_grp = n_staged >= 0 ? n_staged : 0;
   for (int i0 = 0; i0 < n_range; i0 += NT) {
     const int i = i0 + tid;
     const int vp = vbeg + i;
@@ -1015,7 +1050,7 @@ __global__ __launch_bounds__(NT, 4) void decode_attend_kernel(const AttendParams
   if (bad_sel) set_error(p.dev_err, SE_DEVERR_BAD_SELECTION);
   if (bad_page) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
 
-  __syncthreads();  // the staged tables
+  if (n_staged < 0) __syncthreads();  // the staged tables (else the selection's last barrier)
 
   // Pages of this wavefront: the staged entries of its slot rank (a contiguous
   // share of the list, sized by kRankWeight), interleaved over the rank's four

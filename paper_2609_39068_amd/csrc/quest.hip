@@ -186,7 +186,7 @@ __global__ __launch_bounds__(kFusedThreads) void quest_select_fused_kernel(const
   __shared__ int lds_bt[kFusedMaxPages];
   __shared__ float lds_sc[kFusedMaxPages];
   __shared__ unsigned hist[256];
-  __shared__ int scan_scratch[NT / kWave + 1];
+  __shared__ unsigned hist2[256];
   __shared__ int bcast[4];
   const int tid = threadIdx.x;
   const int unit = blockIdx.x;
@@ -208,13 +208,16 @@ __global__ __launch_bounds__(kFusedThreads) void quest_select_fused_kernel(const
     lds_bt[i] = ph;
   }
   if (bad) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
-  if (tid < 256) hist[tid] = 0;
+  if (tid < 256) {
+    hist[tid] = 0;
+    hist2[tid] = 0;
+  }
   __syncthreads();
   const int req = unit / p.hkv, kvh = unit - req * p.hkv;
   unit_bounds<NT, D, G>(p.meta_pool, p.q + ((size_t)req * p.hkv * G + (size_t)kvh * G) * D, p.scale, n, lds_bt,
-                        lds_sc, p.write_scores ? p.scores + (size_t)unit * p.scores_stride : nullptr, hist);
+                        lds_sc, p.write_scores ? p.scores + (size_t)unit * p.scores_stride : nullptr, hist, hist2);
   __syncthreads();
-  unit_topk<NT>(n, p.top_k, lds_sc, out, nullptr, hist, scan_scratch, bcast, true);
+  unit_topk<NT>(n, p.top_k, lds_sc, [&](int r, int b) { out[r] = b; }, hist, hist2, bcast, true);
 }
 
 }  // namespace se

@@ -117,10 +117,14 @@ __device__ __forceinline__ void hist_add_wave(unsigned* hist, uint32_t dg) {
 // null).  q_unit: the unit's G query rows; lds_bt: its block-table row (-1 for
 // an entry outside the pool).  Every iteration's loads are issued before the
 // previous page is reduced.  With hist0 (256 zeroed bins), the scores' first
-// radix digits (unit_topk's first pass) are counted on the way.
+// radix digits (unit_topk's first pass) are counted on the way; with hist1
+// (256 zeroed bins), their second digits too, over every score (unit_topk's
+// second pass when every score shares the first digit, as page bounds of one
+// unit usually do: they lie within a factor of two of each other).
 template <int NT, int D, int G>
 __device__ __forceinline__ void unit_bounds(const uint16_t* meta_pool, const uint16_t* q_unit, float scale, int n,
-                                            const int* lds_bt, float* lds_sc, float* scores_out, unsigned* hist0) {
+                                            const int* lds_bt, float* lds_sc, float* scores_out, unsigned* hist0,
+                                            unsigned* hist1) {
   using BL = BoundLanes<D, G>;
   constexpr int CH = BL::CH, CW = BL::CW, C4 = BL::C4, LPP = BL::LPP;
   constexpr int SLOTS = NT / LPP;
@@ -140,14 +144,16 @@ __device__ __forceinline__ void unit_bounds(const uint16_t* meta_pool, const uin
   };
   auto bound = [&](int b, const uint4 (&mn)[C4], const uint4 (&mx)[C4]) {
     const float best = page_bound<D, G>(qp, qn, mn, mx);
-    uint32_t dg = kNoDigit;
+    uint32_t dg = kNoDigit, dg1 = kNoDigit;
     if (b < n && g == 0) {
       const float sc = lds_bt[b] >= 0 ? best * scale : -INFINITY;
       lds_sc[b] = sc;
       if (scores_out != nullptr) scores_out[b] = sc;
       dg = float_key(sc) >> 24;
+      dg1 = (float_key(sc) >> 16) & 255u;
     }
     if (hist0 != nullptr) hist_add_wave(hist0, dg);
+    if (hist1 != nullptr) hist_add_wave(hist1, dg1);
   };
   const int iters = (n + SLOTS - 1) / SLOTS;
   uint4 mnA[C4], mxA[C4], mnB[C4], mxB[C4];
@@ -162,22 +168,23 @@ __device__ __forceinline__ void unit_bounds(const uint16_t* meta_pool, const uin
 }
 
 // The top_k pages of one unit by score (ties: lower page index), ascending, from
-// the n scores in lds_sc, by NT threads; written to out_g and out_l (either may
-// be null), -1 past the selection.  Radix selection (8-bit digits, most
-// significant first) on order-preserving keys: every wavefront adds its keys
-// to an LDS histogram (hist_add_wave), then wavefront 0 alone scans the 256
-// bins, picks the digit and clears the bins (two barriers per pass).  With
-// counted, the first pass's histogram is already in hist (unit_bounds counts
-// it); else hist is cleared here.  Then every wavefront
-// takes a contiguous range of indices: it counts its keys above the threshold
-// and its keys equal to it, the counts of the ranges before it give its output
-// offset, and it writes its selected indices in ascending order (keys above
-// the threshold, and the lowest-indexed ones equal to it until top_k are
-// taken).
-template <int NT>
-__device__ __forceinline__ void unit_topk(int n, int top_k, const float* lds_sc, int32_t* out_g, int32_t* out_l,
-                                          unsigned* hist, int* scan_scratch, int* bcast, bool counted) {
-  (void)scan_scratch;
+// the n scores in lds_sc, by NT threads; emit(r, b) is called for each rank r
+// < top_k with the page index b of that rank (-1 past the selection).  Radix
+// selection (8-bit digits, most significant first) on order-preserving keys:
+// every wavefront adds its keys to an LDS histogram (hist_add_wave), then
+// wavefront 0 alone scans the 256 bins, picks the digit and clears the bins.
+// With counted, the first pass's histogram is already in hist (unit_bounds
+// counts it, and the caller has synchronised); else hist is cleared here.
+// pre2 (or null): the second digits of all n keys, counted the same way; it
+// is the second pass's histogram when every key has the first pass's digit.
+// Then every wavefront takes a contiguous range of indices: it counts its keys
+// above the threshold and its keys equal to it, the counts of the ranges
+// before it give its output offset, and it emits its selected indices in
+// ascending order (keys above the threshold, and the lowest-indexed ones equal
+// to it until top_k are taken).
+template <int NT, typename Emit>
+__device__ __forceinline__ void unit_topk(int n, int top_k, const float* lds_sc, Emit emit, unsigned* hist,
+                                          unsigned* pre2, int* bcast, bool counted) {
   constexpr int NW = NT / kWave;
   static_assert(NT >= 256 && NT % kWave == 0, "threads 0..255 clear one bin each");
   static_assert(2 * NW <= 256, "per-wavefront counts live in the histogram");
@@ -186,11 +193,7 @@ __device__ __forceinline__ void unit_topk(int n, int top_k, const float* lds_sc,
   const int wave = tid / kWave;
   const bool w0 = tid < kWave;
   if (n <= top_k) {
-    for (int i = tid; i < top_k; i += NT) {
-      const int v = i < n ? i : -1;
-      if (out_g != nullptr) out_g[i] = v;
-      if (out_l != nullptr) out_l[i] = v;
-    }
+    for (int i = tid; i < top_k; i += NT) emit(i, i < n ? i : -1);
     return;
   }
   uint32_t prefix = 0, mask = 0;
@@ -199,8 +202,10 @@ __device__ __forceinline__ void unit_topk(int n, int top_k, const float* lds_sc,
     if (tid < 256) hist[tid] = 0;
     __syncthreads();
   }
+  bool have2 = false;  // pre2 is the second pass's histogram
   for (int shift = 24; shift >= 0; shift -= 8) {
-    if (shift < 24 || !counted) {
+    unsigned* const h = have2 && shift == 16 ? pre2 : hist;
+    if ((shift < 24 || !counted) && h == hist) {
       for (int i0 = wave * kWave; i0 < n; i0 += NT) {  // wave-uniform trip count
         const int i = i0 + lane;
         uint32_t dg = kNoDigit;
@@ -210,14 +215,14 @@ __device__ __forceinline__ void unit_topk(int n, int top_k, const float* lds_sc,
         }
         hist_add_wave(hist, dg);
       }
+      __syncthreads();
     }
-    __syncthreads();
     if (w0) {
       // lane l holds digits 255-4l .. 252-4l (descending); inclusive prefix over lanes
       int c[4], s4 = 0;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        c[j] = (int)hist[255 - 4 * lane - j];
+        c[j] = (int)h[255 - 4 * lane - j];
         s4 += c[j];
       }
       int incl = s4;
@@ -235,7 +240,7 @@ __device__ __forceinline__ void unit_topk(int n, int top_k, const float* lds_sc,
           bcast[2] = c[j];
         }
         run += c[j];
-        hist[255 - 4 * lane - j] = 0;  // cleared for the next pass
+        h[255 - 4 * lane - j] = 0;  // cleared for a later pass
       }
     }
     __syncthreads();
@@ -245,6 +250,8 @@ __device__ __forceinline__ void unit_topk(int n, int top_k, const float* lds_sc,
     prefix |= (uint32_t)d << shift;
     mask |= 0xFFu << shift;
     if (cnt == k) break;
+    // every key has the first digit: the precounted second digits are exact
+    have2 = shift == 24 && pre2 != nullptr && cnt == n;
   }
   // k keys equal to the threshold class (under mask) are taken, lowest index
   // first.  Wavefront w owns indices [w * span, (w + 1) * span).
@@ -280,9 +287,7 @@ __device__ __forceinline__ void unit_topk(int n, int top_k, const float* lds_sc,
     const int eq_rank = eq_seen + lane_prefix_count(eqm);
     if (above || (eq && eq_rank < k)) {
       // output rank: the kept keys at lower indices
-      const int r = taken_above + lane_prefix_count(am) + min(eq_rank, k);
-      if (out_g != nullptr) out_g[r] = b;
-      if (out_l != nullptr) out_l[r] = b;
+      emit(taken_above + lane_prefix_count(am) + min(eq_rank, k), b);
     }
     taken_above += __popcll(am);
     eq_seen += __popcll(eqm);
