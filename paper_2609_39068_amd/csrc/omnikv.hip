@@ -38,8 +38,8 @@ constexpr int kOmniTopkThreads = 1024;
 constexpr int kOmniLdsScores = 32768 + 4096;            // scores kept in LDS (144 KB)
 constexpr int kOmniHistCopies = 8;                      // radix histogram copies (8 KB of LDS)
 constexpr int kOmniRowBatch = 8;                        // logit rows in flight per thread
-constexpr int kGatherThreads = 512;
-constexpr int kGatherWaves = kGatherThreads / kWave;
+constexpr int kGatherThreads = 512;       // two work-groups per compute unit
+constexpr int kGatherThreadsWide = 1024;  // at most one work-group per compute unit: twice the rows in flight
 constexpr int kGatherMaxSel = 8192;                     // selected slots per request
 constexpr uint32_t kNewRow = 0xFFFFFFFFu;               // the appended token (read from k_new / v_new)
 
@@ -278,8 +278,9 @@ struct GatherRow {
   static constexpr int VW = D / 64;  // value columns per lane
 };
 
-template <int D, int G>
-__global__ __launch_bounds__(kGatherThreads, (G >= 4 ? 2 : 4)) void gather_attend_kernel(const GatherParams p) {
+template <int D, int G, int NT>
+__global__ __launch_bounds__(NT, (G >= 4 ? 2 : 4) * kGatherThreads / NT) void gather_attend_kernel(const GatherParams p) {
+  constexpr int kGatherWaves = NT / kWave;
   constexpr int QW = GatherRow<D>::QW;
   constexpr int VC = GatherRow<D>::VW;
   __shared__ uint32_t s_row[kGatherMaxSel];
@@ -323,7 +324,7 @@ __global__ __launch_bounds__(kGatherThreads, (G >= 4 ? 2 : 4)) void gather_atten
   }
   if (fail) {
     if (tid == 0) set_error(p.dev_err, fail);
-    for (int i = tid; i < G * D; i += kGatherThreads) o_out[i] = 0.f;
+    for (int i = tid; i < G * D; i += NT) o_out[i] = 0.f;
     if (p.lse != nullptr && tid < G) p.lse[(size_t)req * Hq + kvh * G + tid] = -INFINITY;
     return;
   }
@@ -331,7 +332,7 @@ __global__ __launch_bounds__(kGatherThreads, (G >= 4 ? 2 : 4)) void gather_atten
   // ---- the selected rows (entries < 0 skipped; at or past L reported and skipped)
   int n_sel = 0, bad_sel = 0, bad_page = 0;
   const int32_t* sel = p.sel + (size_t)req * p.count;
-  for (int c0 = 0; c0 < p.count; c0 += kGatherThreads) {
+  for (int c0 = 0; c0 < p.count; c0 += NT) {
     const int i = c0 + tid;
     const int s = i < p.count ? sel[i] : -1;
     uint32_t row = 0;
@@ -351,13 +352,13 @@ __global__ __launch_bounds__(kGatherThreads, (G >= 4 ? 2 : 4)) void gather_atten
       }
     }
     int tot;
-    const int at = block_exclusive_scan<kGatherThreads>(ok ? 1 : 0, s_scan, &tot);
+    const int at = block_exclusive_scan<NT>(ok ? 1 : 0, s_scan, &tot);
     if (ok && n_sel + at < kGatherMaxSel) s_row[n_sel + at] = row;
     n_sel += tot;
   }
   if (tid == 0 && bad_sel) set_error(p.dev_err, SE_DEVERR_BAD_SELECTION);
   {
-    const int bp = block_reduce<kGatherThreads>(bad_page, s_red, [](int a, int c) { return a | c; });
+    const int bp = block_reduce<NT>(bad_page, s_red, [](int a, int c) { return a | c; });
     if (bp && tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
   }
   n_sel = min(n_sel, kGatherMaxSel);
@@ -503,7 +504,7 @@ __global__ __launch_bounds__(kGatherThreads, (G >= 4 ? 2 : 4)) void gather_atten
     for (int c = 0; c < VC; ++c) s_o[wv][g][lane * VC + c] = acc[g][c];
   }
   __syncthreads();
-  for (int i = tid; i < G * D; i += kGatherThreads) {
+  for (int i = tid; i < G * D; i += NT) {
     const int g = i / D, col = i % D;
     float M = -INFINITY;
 #pragma unroll
@@ -523,13 +524,26 @@ __global__ __launch_bounds__(kGatherThreads, (G >= 4 ? 2 : 4)) void gather_atten
   }
 }
 
+// 1024 threads when the units take at most one work-group per compute unit
+// (groups of up to 4 query heads: a group of 8 would not fit 128 registers)
 template <int D>
 void launch_gather_d(const GatherParams& p, int units, int G, hipStream_t s) {
+  constexpr int NW = kGatherThreadsWide, N = kGatherThreads;
+  const bool wide = units <= 256;
   switch (G) {
-    case 1: hipLaunchKernelGGL((gather_attend_kernel<D, 1>), dim3(units), dim3(kGatherThreads), 0, s, p); break;
-    case 2: hipLaunchKernelGGL((gather_attend_kernel<D, 2>), dim3(units), dim3(kGatherThreads), 0, s, p); break;
-    case 4: hipLaunchKernelGGL((gather_attend_kernel<D, 4>), dim3(units), dim3(kGatherThreads), 0, s, p); break;
-    default: hipLaunchKernelGGL((gather_attend_kernel<D, 8>), dim3(units), dim3(kGatherThreads), 0, s, p); break;
+    case 1:
+      if (wide) hipLaunchKernelGGL((gather_attend_kernel<D, 1, NW>), dim3(units), dim3(NW), 0, s, p);
+      else hipLaunchKernelGGL((gather_attend_kernel<D, 1, N>), dim3(units), dim3(N), 0, s, p);
+      break;
+    case 2:
+      if (wide) hipLaunchKernelGGL((gather_attend_kernel<D, 2, NW>), dim3(units), dim3(NW), 0, s, p);
+      else hipLaunchKernelGGL((gather_attend_kernel<D, 2, N>), dim3(units), dim3(N), 0, s, p);
+      break;
+    case 4:
+      if (wide) hipLaunchKernelGGL((gather_attend_kernel<D, 4, NW>), dim3(units), dim3(NW), 0, s, p);
+      else hipLaunchKernelGGL((gather_attend_kernel<D, 4, N>), dim3(units), dim3(N), 0, s, p);
+      break;
+    default: hipLaunchKernelGGL((gather_attend_kernel<D, 8, N>), dim3(units), dim3(N), 0, s, p); break;
   }
 }
 

@@ -217,30 +217,33 @@ def test_attend_slots_edge_cases(se):
     assert se.se_read_device_errors(err) & se.SE_DEVERR_BAD_SELECTION
 
 
-@pytest.mark.parametrize("G,d", [(8, 128), (8, 64), (1, 128)])
-def test_attend_slots_group_sizes(se, G, d):
+@pytest.mark.parametrize("G,d,nreq", [
+    (8, 128, 2), (8, 64, 2), (1, 128, 2),
+    (4, 128, 130),   # 260 units: more than one work-group per compute unit (512 threads, not 1024)
+])
+def test_attend_slots_group_sizes(se, G, d, nreq):
     # a sparse layer over a fixed selection (every third slot and the new token)
     hkv, L = 2, 777
-    st = isolated_units([L] * 4, 50, d, 9 + G, num_kv_heads=hkv)
-    q, k, v = _inputs(2, hkv, G, d, 31 + G)
-    npos = torch.tensor([L, L], dtype=torch.int32)
+    st = isolated_units([L] * (nreq * hkv), 50, d, 9 + G, num_kv_heads=hkv)
+    q, k, v = _inputs(nreq, hkv, G, d, 31 + G)
+    npos = torch.full((nreq,), L, dtype=torch.int32)
     J = np.concatenate([np.arange(0, L, 3), [L]]).astype(np.int32)
-    sel = torch.from_numpy(np.stack([J, J]))
+    sel = torch.from_numpy(np.stack([J] * nreq))
     scale = float(np.float32(1 / np.sqrt(d)))
     want = []
-    for r in range(2):
+    for r in range(nreq):
         units = [oracle_unit(st, r * hkv + h) for h in range(hkv)]
         want.append(omnikv.sparse_step(units, f64(q[r]), f64(k[r]), f64(v[r]), L, scale, J))
     gs = to_device(st, DEV)
     view = _view(se, gs, hkv)
-    out = torch.empty((2, hkv * G, d), dtype=torch.float32, device=DEV)
-    lse = torch.empty((2, hkv * G), dtype=torch.float32, device=DEV)
+    out = torch.empty((nreq, hkv * G, d), dtype=torch.float32, device=DEV)
+    lse = torch.empty((nreq, hkv * G), dtype=torch.float32, device=DEV)
     err = torch.zeros(1, dtype=torch.int32, device=DEV)
     se.se_attend_slots(view, G, q.to(DEV), k.to(DEV), v.to(DEV), npos.to(DEV), sel.to(DEV), len(J), scale, L + 1,
                        out, lse, err)
     torch.cuda.synchronize()
     assert se.se_read_device_errors(err) == 0
-    for r in range(2):
+    for r in range(nreq):
         assert np.abs(out.cpu().double().numpy()[r] - want[r]["o"]).max() <= OUT_ATOL
         assert np.abs(lse.cpu().double().numpy()[r] - want[r]["lse"]).max() <= LSE_ATOL
 
