@@ -213,6 +213,43 @@ def test_step_quest_equals_select_then_attend(se, num_req, G):
     assert torch.equal(a.meta_pool, b.meta_pool)
 
 
+def test_step_quest_with_a_bad_page_matches_two_pass(se):
+    # One candidate page of one unit outside the pool: both paths report it, its
+    # bound is -inf so neither selects it, and the one-kernel step (which then
+    # stages the pages from its selection instead of writing the staged list
+    # from the top-k's output) agrees with the two calls bit for bit.
+    from workloads import clone_state
+    w = scaled(LAYER_QUEST, num_req=32, ctx=3001, steps=1)
+    host = build_state(w, "cpu")
+    steps = build_steps(w, host, "cpu", steps=1)
+    a = to_device(host, DEV)
+    b = clone_state(a)
+    G, P = w.q_per_kv, host.max_pages
+    max_len = P * 16
+    da = se.QuestDecoder(_view(se, a), G, w.scale, w.top_k, max_len, DEV)
+    db = se.QuestDecoder(_view(se, b), G, w.scale, w.top_k, max_len, DEV)
+    da.summarize()
+    db.summarize()
+    torch.cuda.synchronize()
+    bad_unit, bad_page = 3, 5
+    a.block_table[bad_unit, bad_page] = -1
+    b.block_table[bad_unit, bad_page] = -1
+    q, kn, vn, npos = (x.to(DEV) for x in (steps.q[0, 0], steps.k_new[0, 0], steps.v_new[0, 0], steps.new_pos[0]))
+    shape_o = (w.num_req, w.hq, w.head_dim)
+    oa, ob = torch.empty(shape_o, device=DEV), torch.empty(shape_o, device=DEV)
+    la, lb = torch.empty(shape_o[:2], device=DEV), torch.empty(shape_o[:2], device=DEV)
+    da.step(q, kn, vn, npos, oa, la, fused=False)
+    db.step(q, kn, vn, npos, ob, lb, fused=True)
+    torch.cuda.synchronize()
+    assert se.se_read_device_errors(da.dev_err) & se.SE_DEVERR_BAD_PAGE
+    assert se.se_read_device_errors(db.dev_err) & se.SE_DEVERR_BAD_PAGE
+    assert not (da.sel[bad_unit] == bad_page).any()
+    assert torch.equal(da.sel, db.sel)
+    assert torch.equal(oa, ob) and torch.equal(la, lb)
+    assert torch.equal(a.kv_pool, b.kv_pool) and torch.equal(a.pos_pool, b.pos_pool)
+    assert torch.equal(a.meta_pool, b.meta_pool)
+
+
 def test_fused_select_ties_match_topk_kernel(se):
     # Many exactly equal page scores (every even page of a unit carries the
     # summaries of its page 0): the one-kernel selection keeps the lowest page
