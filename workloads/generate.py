@@ -169,7 +169,12 @@ def build_state(w: Workload, device, generate_values: bool = True) -> PagedInput
     cap = max_pages * P
     num_pages = w.layers * U * max_pages
 
-    perm = torch.randperm(num_pages, generator=_gen(w, 3, device), device=device)
+    # each layer's pages in a region of its own (as a per-layer KV tensor),
+    # scattered within it by a seeded permutation
+    per_layer = U * max_pages
+    gp = _gen(w, 3, device)
+    perm = torch.cat([l * per_layer + torch.randperm(per_layer, generator=gp, device=device)
+                      for l in range(w.layers)])
     block_table = perm.to(torch.int32).view(w.layers * U, max_pages)
     kv_pool = torch.empty((num_pages, 2, P, d), dtype=torch.bfloat16, device=device)
     pos_pool = torch.full((num_pages, P), -1, dtype=torch.int32, device=device)
