@@ -177,15 +177,16 @@ def test_fused_select_matches_two_pass(se, G, d):
     assert (sel_f >= 0).all()
 
 
-@pytest.mark.parametrize("num_req,G", [(32, 4), (2, 4), (32, 8), (2, 8)])
-def test_step_quest_equals_select_then_attend(se, num_req, G):
+@pytest.mark.parametrize("num_req,G,d", [(32, 4, 128), (2, 4, 128), (32, 8, 128), (2, 8, 128), (32, 1, 128),
+                                          (32, 2, 64)])
+def test_step_quest_equals_select_then_attend(se, num_req, G, d):
     # se_decode_step_quest against se_quest_select + se_decode_attend on copies of
     # one state, three steps: with 256 units the selection runs inside the
     # attention kernel, with 16 the call falls back to the two kernels.  The
     # selections, outputs, lse and the pools (append, Quest summaries) agree bit
     # for bit.
     from workloads import clone_state
-    w = scaled(LAYER_QUEST, num_req=num_req, ctx=3001, steps=3, hq=8 * G, hkv=8)
+    w = scaled(LAYER_QUEST, num_req=num_req, ctx=3001, steps=3, hq=8 * G, hkv=8, head_dim=d)
     host = build_state(w, "cpu")
     steps = build_steps(w, host, "cpu", steps=3)
     a = to_device(host, DEV)
