@@ -36,8 +36,10 @@ the chunk's last 128 queries of every head and cut back to 2048 with a
 `--workload prune` measures interval prefix-cache pruning (se_prune_interval
 over 8 chains x 32 layers x 8 KV heads of 32768 resident slots: the interval
 [16384, 20480) cut to its 819 best-scored slots per unit and the later slots
-closed up; one step is one call from a fresh copy of the cache); `--gpus N`
-with N > 1 is refused (single-GPU build).
+closed up; one step is one call from a fresh copy of the cache);
+`--workload read_ceiling` measures a plain gather of random 8 KiB pages with
+the decode stream's loads (se_probe_read_pages: the read rate the decode calls
+are compared against); `--gpus N` with N > 1 is refused (single-GPU build).
 """
 
 import argparse
