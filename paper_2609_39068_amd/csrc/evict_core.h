@@ -630,8 +630,9 @@ __device__ __forceinline__ void evict_unit_wide(const EvictJob& p, const WideScr
         above += (fk[k] & smask) > sprefix ? 1 : 0;
         tied += (fk[k] & smask) == sprefix ? 1 : 0;
       }
-    above = block_reduce<NT>(above, sc.red_i, [](int a, int b) { return a + b; });
-    tied = block_reduce<NT>(tied, sc.red_i, [](int a, int b) { return a + b; });
+    // (work-group totals: taken as scalars, so the branches below stay uniform)
+    above = __builtin_amdgcn_readfirstlane(block_reduce<NT>(above, sc.red_i, [](int a, int b) { return a + b; }));
+    tied = __builtin_amdgcn_readfirstlane(block_reduce<NT>(tied, sc.red_i, [](int a, int b) { return a + b; }));
     const int take = need - above;  // from the threshold class
     uint32_t tprefix = 0, tmask = 0;
     const bool split_ties = take < tied;  // only when scores tie exactly at the threshold
@@ -640,10 +641,54 @@ __device__ __forceinline__ void evict_unit_wide(const EvictJob& p, const WideScr
         fail(SE_DEVERR_BAD_POSITIONS);
         return;
       }
-      radix_top_slots<NT, uint32_t>(
-          p, L, take, [](int32_t q, float) { return 0xFFFFFFFFu - pos_key(q); },
-          [&](int32_t q, float u) { return (w == 0 || pos_key(q) < wthr) && float_key(u) == sprefix; }, sc,
-          &tprefix, &tmask);
+      if (tied <= kWave) {
+        // A small class (SnapKV's max pooling makes runs of up to kappa equal
+        // scores, so its threshold class is nearly always one): its positions go
+        // to LDS (the holes list is not written yet) and one wavefront finds the
+        // take-th smallest, instead of radix passes over every slot's position
+        // and score in memory.  Same kept set: the take lowest positions.
+        int* const tpos = sc.holes;
+        if (tid == 0) {
+          sc.bcast[0] = 0;  // entries
+          sc.bcast[2] = 0;  // found
+        }
+        __syncthreads();
+        {
+          uint64_t tm = 0;  // this thread's rows in the class
+#pragma unroll
+          for (int k = 0; k < KPT; ++k)
+            if (k < nrow && !((win >> k) & 1) && fk[k] == sprefix) tm |= 1ull << k;
+          const int t = opaque_int(tid);
+          while (tm != 0) {  // a few rows in the whole work-group
+            const int k = __builtin_ctzll(tm);
+            tm &= tm - 1;
+            const int i = atomicAdd(&sc.bcast[0], 1);
+            tpos[i] = p.pos_pool[addr(k * NT + t)];
+          }
+        }
+        __syncthreads();
+        if (wave == 0) {
+          const int v = lane < tied ? tpos[lane] : INT_MAX;
+          int rank = 0;  // tied entries with a smaller position
+          for (int j = 0; j < tied; ++j) rank += __shfl(v, j, kWave) < v ? 1 : 0;
+          if (lane < tied && rank == take - 1) {
+            sc.bcast[1] = v;
+            sc.bcast[2] = 1;
+          }
+        }
+        __syncthreads();
+        if (sc.bcast[2] == 0) {  // no unique take-th position: repeated positions
+          fail(SE_DEVERR_BAD_POSITIONS);
+          return;
+        }
+        tprefix = 0xFFFFFFFFu - pos_key(sc.bcast[1]);  // keep iff pos <= the take-th smallest
+        tmask = 0xFFFFFFFFu;
+      } else {
+        radix_top_slots<NT, uint32_t>(
+            p, L, take, [](int32_t q, float) { return 0xFFFFFFFFu - pos_key(q); },
+            [&](int32_t q, float u) { return (w == 0 || pos_key(q) < wthr) && float_key(u) == sprefix; }, sc,
+            &tprefix, &tmask);
+      }
     }
     const int t = opaque_int(tid);
 #pragma unroll

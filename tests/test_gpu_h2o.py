@@ -141,6 +141,8 @@ CASES = [
     ([4097] * 6, 4096, 512, "contiguous", 1000),     # steady at the 8B budget, ties
     ([32769, 20000], 2048, 256, "contiguous", 0),    # first step of the 8B workload
     ([6000, 3000], 1024, 64, "contiguous", 3),       # exact score ties at the threshold
+    ([6000, 3000], 1024, 64, "shuffled", 1500),      # small tie classes (a few slots) at the threshold
+    ([2000, 1500], 512, 32, "gapped", 40),           # tie classes of up to about 60 slots
     ([36000], 2048, 256, "shuffled", 7),             # past the register-resident size
     ([8193, 12000], 8192, 512, "shuffled", 0),       # the largest budget
     ([3, 1, 2, 0], 1, 1, "gapped", 2),               # budget 1: only the newest position stays
