@@ -133,22 +133,22 @@ __device__ __forceinline__ int bt_entry(const int32_t* bt, int i) {
   return ((const_i32_ptr)bt)[__builtin_amdgcn_readfirstlane(i)];
 }
 
-template <int D, int NB, typename Body>
+template <int D, int NB, int NT = kSnapThreads, typename Body>
 __device__ __forceinline__ void stream_stages(const SnapParams& p, const int32_t* bt, uint8_t* ring, int pb, int pe,
                                               Body body) {
   constexpr int S = kSnapStagePages;
   constexpr int PB = 32 * D;                       // K bytes of a page
   constexpr int PC = D / 8;                        // 16-byte pieces per key
-  constexpr int PT = S * 2 * D / kSnapThreads;     // pieces per thread per stage
+  constexpr int PT = S * 2 * D / NT;               // pieces per thread per stage
   static_assert(NB % 2 == 0, "ring slots alternate within the unrolled loop");
-  static_assert(PT >= 1 && PT * kSnapThreads == S * 2 * D, "whole pages per stage");
+  static_assert(PT >= 1 && PT * NT == S * 2 * D, "whole pages per stage");
   const int n_st = ceil_div_dev(pe - pb, S);
   if (n_st <= 0) return;
-  // piece g = threadIdx.x + q * kSnapThreads of a stage: page g / (2D), piece g % (2D)
+  // piece g = threadIdx.x + q * NT of a stage: page g / (2D), piece g % (2D)
   int pg_of[PT], off_of[PT], lds_of[PT];
 #pragma unroll
   for (int q = 0; q < PT; ++q) {
-    const int g = (int)threadIdx.x + q * kSnapThreads;
+    const int g = (int)threadIdx.x + q * NT;
     const int pp = g / (2 * D);
     const int t = g % (2 * D);
     pg_of[q] = __builtin_amdgcn_readfirstlane(pp);  // 2D is a multiple of the wavefront
@@ -696,6 +696,286 @@ __global__ __launch_bounds__(kApplyThreads) void h2o_chunk_apply_kernel(const Sn
   }
 }
 
+
+// ---------------------------------------------------------------- key split
+// H2O chunk scoring with 257 .. 512 scoring rows (e.g. 128 queries x 4 heads):
+// one work-group holds every row (eight wavefronts of 64 rows, four row tiles
+// each) and a contiguous part of the unit's pages, and the unit's pages are
+// split over gridDim.y work-groups.  Every wavefront reads every page of a
+// stage from the ring (four pages, 64 MFMAs per wavefront between barriers,
+// against 16 when a work-group holds a block of 128 rows and every key), and
+// each page is staged once per unit instead of once per row block.  The row
+// normalisers need every key, so the two passes are two kernels: the first
+// leaves each part's (reference, sum) per row in the workspace, the second
+// merges the parts in part order, forms each key's u over all the rows (the
+// wavefronts' sums added in wavefront order) and writes the slot's new score
+// (0 for the chunk's slots, plus u) itself.
+constexpr int kSplitRows = 512;  // rows of a work-group
+constexpr int kSplitThreads = 1024;
+// row tiles of 16 rows per wavefront: 4 with 512 threads (two wavefronts per
+// SIMD, up to 256 registers each), 2 with 1024 (four per SIMD, 128 registers)
+template <int NT>
+constexpr int kSplitRTW = kSplitRows / 16 / (NT / kWave);
+
+// the pages [*pb, *pe) of part kp of nkp
+__device__ __forceinline__ void key_part(int n_pages, int kp, int nkp, int* pb, int* pe) {
+  *pb = (int)((int64_t)n_pages * kp / nkp);
+  *pe = (int)((int64_t)n_pages * (kp + 1) / nkp);
+}
+
+// Unit checks shared by both passes (length, block table); the first pass's
+// first part reports them.
+template <int NT>
+__device__ __forceinline__ bool split_unit_ok(const SnapParams& p, int unit, int L, bool report, int* s_red) {
+  const int tid = threadIdx.x;
+  if (L > p.max_len || L > p.max_pages * kPage || L > kSnapMaxPages * kPage || L < p.chunk) {
+    if (report && tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_LENGTH);
+    return false;
+  }
+  const int32_t* bt = p.block_table + (size_t)unit * p.max_pages;
+  const int n_pages = ceil_div_dev(L, kPage);
+  int bad = 0;
+  for (int i = tid; i < n_pages; i += NT) bad |= (bt[i] < 0 || (int64_t)bt[i] >= p.num_pages);
+  bad = block_reduce<NT>(bad, s_red, [](int a, int b) { return a | b; });
+  if (bad) {
+    if (report && tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
+    return false;
+  }
+  return true;
+}
+
+// This wavefront's 16 * RTW query rows as A operands (rows past R are zero).
+template <int D, int RTW>
+__device__ __forceinline__ void split_queries(const SnapParams& p, int unit, int row0, uint4 (&qa)[RTW][D / 32]) {
+  constexpr int KS = D / 32;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int grp = lane >> 4, col = lane & 15;
+  const int req = unit / p.num_kv_heads, kvh = unit % p.num_kv_heads;
+  const int G = p.q_per_kv, R = p.w * G, hq = p.num_kv_heads * G;
+#pragma unroll
+  for (int T = 0; T < RTW; ++T) {
+    const int row = row0 + 16 * T + col;
+    const int t = row / G, g = row - (row / G) * G;
+    const uint16_t* src = p.q + (((size_t)req * p.w + t) * hq + (size_t)kvh * G + g) * D + 8 * grp;
+#pragma unroll
+    for (int k = 0; k < KS; ++k) qa[T][k] = row < R ? *reinterpret_cast<const uint4*>(src + 32 * k) : uint4{0u, 0u, 0u, 0u};
+  }
+#pragma unroll
+  for (int T = 0; T < RTW; ++T)
+#pragma unroll
+    for (int k = 0; k < KS; ++k)
+      asm volatile("" : "+v"(qa[T][k].x), "+v"(qa[T][k].y), "+v"(qa[T][k].z), "+v"(qa[T][k].w));
+}
+
+// The causal mask of a page holding window keys: key j is seen by the rows of
+// window position t iff j <= L - w + t; padded rows see nothing.
+template <int RTW>
+__device__ __forceinline__ void split_mask(const SnapParams& p, f32x4_t (&a)[RTW], int pg, int L, int row0) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int grp = lane >> 4, col = lane & 15;
+  const int key = pg * kPage + col;
+  const int G = p.q_per_kv, R = p.w * G;
+#pragma unroll
+  for (int T = 0; T < RTW; ++T)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = row0 + 16 * T + 4 * grp + r;
+      const int lim = row < R ? L - p.w + row / G : -1;
+      if (key > lim) a[T][r] = -INFINITY;
+    }
+}
+
+// Pass 1: per row, a lazy reference and the sum of exp2(c*z - reference) over
+// this part's keys, merged over the 16 key lanes; norm[(unit * nkp + kp) *
+// kSplitRows + row] = (reference, sum).
+template <int D, int NT>
+__global__ __launch_bounds__(NT, 2 * NT / kSnapThreads) void prefill_norm_kernel(const SnapParams p, float2* norm) {
+  constexpr int RTW = kSplitRTW<NT>, S = kSnapStagePages, PB = 32 * D, NW = NT / kWave;
+  __shared__ __attribute__((aligned(16))) uint8_t s_ring[2 * S * 32 * 128];
+  __shared__ int s_red[NW];
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int grp = lane >> 4, col = lane & 15;
+  const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int unit = blockIdx.x, kp = blockIdx.y, nkp = gridDim.y;
+  const int L = p.lengths[unit];
+  if (!split_unit_ok<NT>(p, unit, L, kp == 0, s_red)) return;
+  const int32_t* bt = p.block_table + (size_t)unit * p.max_pages;
+  const int n_pages = ceil_div_dev(L, kPage);
+  int pb, pe;
+  key_part(n_pages, kp, nkp, &pb, &pe);
+  const int row0 = 16 * RTW * wv;
+  uint4 qa[RTW][D / 32];
+  split_queries<D, RTW>(p, unit, row0, qa);
+  const float c = p.c;
+  const int p_full = (L - p.w + 1) / kPage;  // pages below hold only keys every row sees
+  float ref[RTW][4], sum[RTW][4];
+#pragma unroll
+  for (int T = 0; T < RTW; ++T)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      ref[T][r] = kRefInit;
+      sum[T][r] = 0.f;
+    }
+  auto norm_page = [&](const f32x4_t(&a)[RTW]) {
+    float dmax = -INFINITY;
+    float d[RTW][4];
+#pragma unroll
+    for (int T = 0; T < RTW; ++T)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        d[T][r] = fmaf(a[T][r], c, -ref[T][r]);
+        dmax = fmaxf(dmax, d[T][r]);
+      }
+    if (__builtin_amdgcn_ballot_w64(dmax > kLazy) != 0) {
+#pragma unroll
+      for (int T = 0; T < RTW; ++T)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float zc = a[T][r] * c;
+          const float m = fmaxf(ref[T][r], zc);
+          sum[T][r] *= fast_exp2(ref[T][r] - m);
+          d[T][r] = zc - m;
+          ref[T][r] = m;
+        }
+    }
+#pragma unroll
+    for (int T = 0; T < RTW; ++T)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sum[T][r] += fast_exp2(d[T][r]);
+  };
+  stream_stages<D, 2 * kSnapBatches, NT>(p, bt, s_ring, pb, pe, [&](int j, int slot) {
+    // page i + 1's MFMAs are issued before page i's exponentials
+    f32x4_t acc[2][RTW];
+    page_logits<D, RTW>(qa, s_ring + (slot * S) * PB, acc[0]);
+#pragma unroll
+    for (int i = 0; i < S; ++i) {
+      if (i + 1 < S) page_logits<D, RTW>(qa, s_ring + (slot * S + i + 1) * PB, acc[(i + 1) & 1]);
+      const int pg = pb + j * S + i;
+      if (pg < pe) {
+        if (pg >= p_full) split_mask<RTW>(p, acc[i & 1], pg, L, row0);
+        norm_page(acc[i & 1]);
+      }
+    }
+  });
+  float2* out = norm + ((size_t)unit * nkp + kp) * kSplitRows;
+#pragma unroll
+  for (int T = 0; T < RTW; ++T)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+#pragma unroll
+      for (int m = 1; m < 16; m <<= 1)
+        merge_norm(ref[T][r], sum[T][r], shfl_xor_f(ref[T][r], m), shfl_xor_f(sum[T][r], m));
+      if (col == 0) out[row0 + 16 * T + 4 * grp + r] = make_float2(ref[T][r], sum[T][r]);
+    }
+}
+
+// Pass 2: bias = log2 of each row's softmax denominator (the parts merged in
+// part order); u(j) = sum over every row of exp2(c*z - bias) for this part's
+// keys; score(j) = (j in the chunk ? 0 : score(j)) + u(j).
+template <int D, int NT>
+__global__ __launch_bounds__(NT, 2 * NT / kSnapThreads) void prefill_score_kernel(const SnapParams p, const float2* norm) {
+  constexpr int RTW = kSplitRTW<NT>, S = kSnapStagePages, PB = 32 * D, NW = NT / kWave;
+  __shared__ __attribute__((aligned(16))) uint8_t s_ring[2 * S * 32 * 128];
+  __shared__ float s_up[2][S][NW][kPage];  // [stage parity][page][wavefront][key]
+  __shared__ int s_red[NW];
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int grp = lane >> 4, col = lane & 15;
+  const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int unit = blockIdx.x, kp = blockIdx.y, nkp = gridDim.y;
+  const int L = p.lengths[unit];
+  if (!split_unit_ok<NT>(p, unit, L, false, s_red)) return;
+  const int32_t* bt = p.block_table + (size_t)unit * p.max_pages;
+  const int n_pages = ceil_div_dev(L, kPage);
+  int pb, pe;
+  key_part(n_pages, kp, nkp, &pb, &pe);
+  const int row0 = 16 * RTW * wv;
+  const int R = p.w * p.q_per_kv;
+  uint4 qa[RTW][D / 32];
+  split_queries<D, RTW>(p, unit, row0, qa);
+  const float c = p.c;
+  const int p_full = (L - p.w + 1) / kPage;
+  float bias[RTW][4];
+  {
+    const float2* nu = norm + (size_t)unit * nkp * kSplitRows;
+#pragma unroll
+    for (int T = 0; T < RTW; ++T)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = row0 + 16 * T + 4 * grp + r;
+        float2 a = nu[row];
+        for (int k = 1; k < nkp; ++k) {
+          const float2 b = nu[(size_t)k * kSplitRows + row];
+          merge_norm(a.x, a.y, b.x, b.y);
+        }
+        bias[T][r] = row < R ? a.x + __log2f(a.y) : INFINITY;
+      }
+  }
+  // a page's weights summed over the lane's rows (a tree), then over the four
+  // lane groups (rows 4*(lane/16)..+3 of each tile) of key lane%16
+  auto page_sum = [&](const f32x4_t(&a)[RTW]) {
+    float e[RTW * 4];
+#pragma unroll
+    for (int T = 0; T < RTW; ++T)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) e[4 * T + r] = fast_exp2(fmaf(a[T][r], c, -bias[T][r]));
+#pragma unroll
+    for (int n = RTW * 4; n > 1; n >>= 1)
+#pragma unroll
+      for (int k = 0; k < n / 2; ++k) e[k] = e[2 * k] + e[2 * k + 1];
+    return lane_group_sum(e[0]);
+  };
+  // once stage j's barrier has passed, wavefront v < S adds the wavefronts'
+  // sums of page v in wavefront order and writes the scores of its keys
+  const int cs = L - p.chunk;  // the chunk's first slot
+  auto flush = [&](int j) {
+    if (wv < S && lane < kPage) {
+      const int pg = pb + j * S + wv;
+      float v = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) v += s_up[j & 1][wv][w][lane];
+      const int key = pg * kPage + lane;
+      if (pg < pe && key < L) {
+        float* sc = p.score_pool + (size_t)bt[pg] * kPage + lane;
+        *sc = (key >= cs ? 0.f : *sc) + v;
+      }
+    }
+  };
+  const int n_st = ceil_div_dev(pe - pb, S);
+  stream_stages<D, 2 * kSnapBatches, NT>(p, bt, s_ring, pb, pe, [&](int j, int slot) {
+    if (j >= 1) flush(j - 1);
+    f32x4_t acc[2][RTW];
+    page_logits<D, RTW>(qa, s_ring + (slot * S) * PB, acc[0]);
+#pragma unroll
+    for (int i = 0; i < S; ++i) {
+      if (i + 1 < S) page_logits<D, RTW>(qa, s_ring + (slot * S + i + 1) * PB, acc[(i + 1) & 1]);
+      const int pg = pb + j * S + i;
+      if (pg >= p_full) split_mask<RTW>(p, acc[i & 1], pg, L, row0);
+      const float us = page_sum(acc[i & 1]);
+      if (grp == 0) s_up[j & 1][i][wv][col] = us;  // pages past the part are never written out
+    }
+  });
+  if (n_st >= 1) {
+    __syncthreads();
+    flush(n_st - 1);
+  }
+}
+
+// The number of work-groups a unit's keys are split over: at least 256
+// work-groups in all when the units allow, each over at least 8 pages.
+static int prefill_key_parts(int32_t num_units, int32_t max_len) {
+  const int64_t pages = ceil_div((int64_t)max_len, kPage);
+  int64_t kp = ceil_div((int64_t)256, (int64_t)num_units);
+  kp = std::min<int64_t>(kp, std::max<int64_t>(1, pages / 8));
+  return (int)std::max<int64_t>(1, kp);
+}
+
+static bool prefill_key_split(int32_t q_per_kv, int32_t window) {
+  const int64_t R = (int64_t)window * q_per_kv;
+  return R > 2 * kPrefillBlockRows && R <= kSplitRows;
+}
+
 }  // namespace se
 
 using namespace se;
@@ -798,8 +1078,11 @@ extern "C" se_status se_snapkv_compact(const se_kv_view* kv, int32_t q_per_kv, c
   return launch_status();
 }
 
-// Workspace: the row blocks' partial sums, then the eviction's move lists.
+// Workspace: the row blocks' partial sums (or, with the keys split, each
+// part's row normalisers), then the eviction's move lists.
 static size_t prefill_sums_bytes(int32_t num_units, int32_t max_len, int32_t q_per_kv, int32_t window) {
+  if (prefill_key_split(q_per_kv, window))
+    return align_up((size_t)num_units * prefill_key_parts(num_units, max_len) * kSplitRows * sizeof(float2), 256);
   const size_t n_rb = (size_t)ceil_div((int64_t)window * q_per_kv, kPrefillBlockRows);
   return align_up((size_t)num_units * n_rb * align_up((size_t)max_len, 64) * sizeof(float), 256);
 }
@@ -853,13 +1136,28 @@ extern "C" se_status se_h2o_prefill_chunk(const se_kv_view* kv, int32_t q_per_kv
   p.vec4 = (reinterpret_cast<uintptr_t>(kv->score_pool) % 16 == 0 && reinterpret_cast<uintptr_t>(ws) % 16 == 0) ? 1 : 0;
   p.c = scale * kLog2e;
   p.dev_err = dev_err;
-  const int rows = std::min(score_window * q_per_kv, kPrefillBlockRows);
-  if (kv->head_dim == 128)
-    launch_snapkv_d<128, true>(p, kv->num_units, rows, stream);
-  else
-    launch_snapkv_d<64, true>(p, kv->num_units, rows, stream);
-  hipLaunchKernelGGL(h2o_chunk_apply_kernel, dim3((unsigned)ceil_div(max_len, kApplySlots), kv->num_units),
-                     dim3(kApplyThreads), 0, stream, p);
+  if (prefill_key_split(q_per_kv, score_window)) {
+    // every row in one work-group, the unit's pages split over several
+    const dim3 grid(kv->num_units, prefill_key_parts(kv->num_units, max_len));
+    float2* norm = static_cast<float2*>(ws);
+    // head_dim 128: 1024 threads (a stage is one 16-byte piece per thread);
+    // 64: 512
+    if (kv->head_dim == 128) {
+      hipLaunchKernelGGL((prefill_norm_kernel<128, kSplitThreads>), grid, dim3(kSplitThreads), 0, stream, p, norm);
+      hipLaunchKernelGGL((prefill_score_kernel<128, kSplitThreads>), grid, dim3(kSplitThreads), 0, stream, p, norm);
+    } else {
+      hipLaunchKernelGGL((prefill_norm_kernel<64, kSnapThreads>), grid, dim3(kSnapThreads), 0, stream, p, norm);
+      hipLaunchKernelGGL((prefill_score_kernel<64, kSnapThreads>), grid, dim3(kSnapThreads), 0, stream, p, norm);
+    }
+  } else {
+    const int rows = std::min(score_window * q_per_kv, kPrefillBlockRows);
+    if (kv->head_dim == 128)
+      launch_snapkv_d<128, true>(p, kv->num_units, rows, stream);
+    else
+      launch_snapkv_d<64, true>(p, kv->num_units, rows, stream);
+    hipLaunchKernelGGL(h2o_chunk_apply_kernel, dim3((unsigned)ceil_div(max_len, kApplySlots), kv->num_units),
+                       dim3(kApplyThreads), 0, stream, p);
+  }
   st = launch_status();
   if (st != SE_OK) return st;
 

@@ -139,11 +139,14 @@ def _run(se, lengths0, hkv, G, d, chunks, sw, budget, recent, seed):
     return near
 
 
-@pytest.mark.parametrize("G,d,sw", [(4, 128, 32), (4, 128, 64), (2, 64, 100), (1, 128, 7), (8, 64, 16)])
+@pytest.mark.parametrize("G,d,sw", [(4, 128, 32), (4, 128, 64), (2, 64, 100), (1, 128, 7), (8, 64, 16),
+                                    (4, 128, 100), (8, 64, 40), (2, 128, 256), (1, 64, 257)])
 def test_chunk_sequence(se, G, d, sw):
     # ragged retained states (an empty one among them), three chunks of 300,
     # 257 and 400 tokens, budget 512 with a 256-token window (ratio 0.5);
-    # sw * G from 7 to 200 rows (two row blocks for 64 x 4 and 100 x 2)
+    # sw * G from 7 to 200 rows (two row blocks for 64 x 4 and 100 x 2), and
+    # 257 to 512 rows, where one work-group holds every row and the unit's
+    # pages are split over several (some parts of the short units are empty)
     lengths0 = [0, 0, 100, 100, 511, 511, 700, 700]
     _run(se, lengths0, 2, G, d, [300, 257, 400], sw, 512, 256, seed=G * 100 + sw)
 
