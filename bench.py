@@ -520,7 +520,8 @@ def main_h2o_prefill(args):
                    "head_dim": D, "page_size": w.page_size, "prompt": w.ctx, "chunk": C,
                    "retained_before": w.initial_resident - C, "scoring_window": sw, "budget": w.budget,
                    "recent": w.recent, "accumulate": "f32", "parallelism": "none (1 GPU)"},
-        "roofline": {"bound": "alu", "kernel": "se_h2o_prefill_chunk (snapkv_score_kernel, accumulate mode)",
+        "roofline": {"bound": "alu",
+                     "kernel": "se_h2o_prefill_chunk (prefill_norm_kernel + prefill_score_kernel, then the eviction)",
                      "achieved": round(alu_achieved, 2), "peak": VALU_PEAK_TSLOTS,
                      "unit": "T VALU lane-slots/s", "frac": round(alu_achieved / VALU_PEAK_TSLOTS, 4),
                      "traffic": read_traffic(PREFILL_TRAFFIC_SUMMARY, SNAPKV_SOURCES),
