@@ -44,8 +44,10 @@
 // and snapkv_pool_kernel adds the blocks in block order and pools over the
 // candidates.
 //
-// H2O chunk scoring (se_h2o_prefill_chunk) runs the same kernel over every key
-// with the causal mask in both passes, one row block of up to 128 scoring rows
+// H2O chunk scoring (se_h2o_prefill_chunk) with 257 .. 512 scoring rows runs
+// the key-split kernels further below; with other row counts it runs the same
+// kernel over every key with the causal mask in both passes, one row block of
+// up to 128 scoring rows
 // per work-group (grid.y), one work-group per CU; a block of 128 rows sits in
 // two row groups of 64 (four row tiles per wavefront, each stage's four pages
 // split over the four wavefronts of a row group), so each key piece read from
