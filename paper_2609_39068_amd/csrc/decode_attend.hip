@@ -268,6 +268,49 @@ __device__ __forceinline__ void move_newest(const AttendParams& p, const UnitGeo
   }
 }
 
+// The steady epilogue's one barrier round: the work-group's count of window
+// slots (sum) and its least eviction key with the slot holding it (equal keys,
+// which only repeated positions give, resolve to the lower slot, so every thread
+// agrees).  A thread without a candidate passes key ~0 and slot INT_MAX.  The
+// scratch is free again only after the caller's next barrier.
+template <int NT>
+__device__ __forceinline__ void steady_fold(int& cnt, unsigned long long& key, int& slot, const EvictScratch<NT>& sc) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  auto take = [&](int c2, unsigned long long k2, int s2) {
+    cnt += c2;
+    if (k2 < key || (k2 == key && s2 < slot)) {
+      key = k2;
+      slot = s2;
+    }
+  };
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) take(__shfl_xor(cnt, o, kWave), __shfl_xor(key, o, kWave), __shfl_xor(slot, o, kWave));
+  if (lane == 0) {
+    sc.red_i[wave] = cnt;
+    sc.red_u64[wave] = key;
+    sc.scan[wave] = slot;
+  }
+  __syncthreads();
+  cnt = 0;
+  key = ~0ull;
+  slot = INT_MAX;
+#pragma unroll
+  for (int w = 0; w < NT / kWave; ++w) take(sc.red_i[w], sc.red_u64[w], sc.scan[w]);
+}
+
+// The lower bound of the recent window, lo: when exactly w resident positions
+// lie above lo, they are the w largest and every other slot is a candidate.
+// With an append, the new position (the largest in order) gives lo at once;
+// otherwise the largest resident position does, by one more reduction.
+template <int NT>
+__device__ __forceinline__ int64_t steady_window_lo(const AttendParams& p, const UnitGeom& g, int32_t pmax, int w,
+                                                    int* red_i) {
+  if (g.append) return (int64_t)p.new_pos[g.req] - w;
+  pmax = block_reduce<NT>(pmax, red_i, [](int x, int y) { return x > y ? x : y; });
+  return (int64_t)pmax - w;
+}
+
 template <int NT, int G, int D, typename W>
 __device__ __forceinline__ bool finish_steady(const AttendParams& p, const UnitGeom& g, const float* fin_m,
                                               const float* fin_il, const int* lds_phys, const int* lds_vp,
@@ -275,9 +318,7 @@ __device__ __forceinline__ bool finish_steady(const AttendParams& p, const UnitG
                                               float (&unew)[kSteadyRows], int rbeg, int wr, int n_my,
                                               const EvictScratch<NT>& sc) {
   constexpr int KW = kSteadyRows;
-  int* const red_i = sc.red_i;
-  unsigned long long* const red_k = sc.red_u64;
-  __shared__ int bc[2];
+  __shared__ int bc_pos;  // the mover's position and score
   __shared__ float bc_u;
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -290,7 +331,7 @@ __device__ __forceinline__ bool finish_steady(const AttendParams& p, const UnitG
     return s < g.Lp ? s : -1;
   };
   // pos / unew hold the fetched positions and old scores; the scores become the
-  // new ones.  They are stored only after the block reductions: a barrier waits
+  // new ones.  They are stored only after the last barrier: a barrier waits
   // for the work-group's outstanding stores, which under a full memory system
   // take tens of microseconds.
   uint32_t live = 0;
@@ -315,48 +356,40 @@ __device__ __forceinline__ bool finish_steady(const AttendParams& p, const UnitG
 #pragma unroll
   for (int j = 0; j < KW; ++j)
     if ((live >> j) & 1) pmax = max(pmax, pos[j]);
-  pmax = block_reduce<NT>(pmax, red_i, [](int x, int y) { return x > y ? x : y; });
-  const int64_t lo = (int64_t)pmax - w;  // the window is the positions above lo when contiguous
-  int cnt = 0;
-#pragma unroll
-  for (int j = 0; j < KW; ++j) cnt += (((live >> j) & 1) && (int64_t)pos[j] > lo) ? 1 : 0;
-  cnt = block_reduce<NT>(cnt, red_i, [](int x, int y) { return x + y; });
-  if (cnt != w) {  // the general eviction runs from the updated scores
-    store_scores(-1);
-    return true;
-  }
-  unsigned long long best = ~0ull;
-#pragma unroll
-  for (int j = 0; j < KW; ++j) {
-    if (((live >> j) & 1) && (int64_t)pos[j] <= lo) {
-      const unsigned long long key = ((unsigned long long)float_key(unew[j]) << 32) |
-                                     (unsigned long long)(0xFFFFFFFFu - pos_order(pos[j]));
-      best = key < best ? key : best;
-    }
-  }
-  const unsigned long long kmin =
-      block_reduce<NT>(best, red_k, [](unsigned long long x, unsigned long long y) { return x < y ? x : y; });
+  const int64_t lo = steady_window_lo<NT>(p, g, pmax, w, sc.red_i);
   const int mover = g.Lp - 1;
+  int cnt = 0;
+  unsigned long long best = ~0ull;
+  int victim = INT_MAX;
 #pragma unroll
   for (int j = 0; j < KW; ++j) {
     if (!((live >> j) & 1)) continue;
     const int s = slot_of(j);
-    if ((int64_t)pos[j] <= lo) {
+    if ((int64_t)pos[j] > lo) {
+      ++cnt;
+    } else {
       const unsigned long long key = ((unsigned long long)float_key(unew[j]) << 32) |
                                      (unsigned long long)(0xFFFFFFFFu - pos_order(pos[j]));
-      if (key == kmin) bc[0] = s;  // keys are distinct
+      if (key < best) {
+        best = key;
+        victim = s;
+      }
     }
     if (s == mover) {
-      bc[1] = pos[j];
+      bc_pos = pos[j];
       bc_u = unew[j];
     }
   }
-  __syncthreads();
-  const int victim = bc[0];
+  steady_fold<NT>(cnt, best, victim, sc);
+  if (cnt != w) {  // the general eviction runs from the updated scores
+    __syncthreads();
+    store_scores(-1);
+    return true;
+  }
   // every store after the last barrier: the scores (the victim's slot takes the
   // mover's), the mover's row, position and score in the victim's slot
   store_scores(victim);
-  move_newest<D>(p, g, lds_phys[victim >> 4], victim, lds_phys[mover >> 4], mover, bc[1], bc_u);
+  move_newest<D>(p, g, lds_phys[victim >> 4], victim, lds_phys[mover >> 4], mover, bc_pos, bc_u);
   if (tid == 0) {
     p.lengths[g.unit] = p.budget;
     const int f0 = (p.budget + kPage - 1) / kPage;

@@ -329,43 +329,9 @@ __global__ __launch_bounds__(NT, (G >= 4 ? 2 : 4) * kGatherThreads / NT) void ga
     return;
   }
 
-  // ---- the selected rows (entries < 0 skipped; at or past L reported and skipped)
-  int n_sel = 0, bad_sel = 0, bad_page = 0;
-  const int32_t* sel = p.sel + (size_t)req * p.count;
-  for (int c0 = 0; c0 < p.count; c0 += NT) {
-    const int i = c0 + tid;
-    const int s = i < p.count ? sel[i] : -1;
-    uint32_t row = 0;
-    bool ok = s >= 0 && s < L;
-    bad_sel |= (s >= L);
-    if (ok) {
-      if (append && s == L0) {
-        row = kNewRow;
-      } else {
-        const int ph = bt[s >> 4];
-        if (ph < 0 || (int64_t)ph >= p.num_pages) {
-          ok = false;
-          bad_page = 1;
-        } else {
-          row = (uint32_t)ph * 2 * kPage + (uint32_t)(s & (kPage - 1));
-        }
-      }
-    }
-    int tot;
-    const int at = block_exclusive_scan<NT>(ok ? 1 : 0, s_scan, &tot);
-    if (ok && n_sel + at < kGatherMaxSel) s_row[n_sel + at] = row;
-    n_sel += tot;
-  }
-  if (tid == 0 && bad_sel) set_error(p.dev_err, SE_DEVERR_BAD_SELECTION);
-  {
-    const int bp = block_reduce<NT>(bad_page, s_red, [](int a, int c) { return a | c; });
-    if (bp && tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
-  }
-  n_sel = min(n_sel, kGatherMaxSel);
-  __syncthreads();  // the row list and the appended row are complete
-  if (append && tid == 0) p.lengths[unit] = L;
-
-  // ---- queries: lane (row r8 = lane/8, c8 = lane%8) holds columns [c8*D/8, ...) of the G rows
+  // ---- queries (loaded first, so that their latency overlaps the row
+  // translation): lane (row r8 = lane/8, c8 = lane%8) holds columns [c8*D/8, ...)
+  // of the G rows
   const int c8 = lane & 7;
   const int r8 = lane >> 3;
   uint32_t qr[G][QW];
@@ -382,6 +348,60 @@ __global__ __launch_bounds__(NT, (G >= 4 ? 2 : 4) * kGatherThreads / NT) void ga
         qr[g][i + 3] = t.w;
       }
   }
+  // ---- the selected rows (entries < 0 skipped; at or past L reported and
+  // skipped), 2 * NT entries a round: a thread's two entries (c0 + tid and
+  // c0 + NT + tid) and their page-table entries are loaded together, and one
+  // block scan of both counts (16 bits each in one int; a count is at most NT)
+  // places the rows in selection order
+  int n_sel = 0, bad_sel = 0, bad_page = 0;
+  const int32_t* sel = p.sel + (size_t)req * p.count;
+  for (int c0 = 0; c0 < p.count; c0 += 2 * NT) {
+    int s2[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int i = c0 + k * NT + tid;
+      s2[k] = i < p.count ? sel[i] : -1;
+    }
+    int ph2[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) ph2[k] = (s2[k] >= 0 && s2[k] < L) ? bt[s2[k] >> 4] : 0;
+    uint32_t row2[2];
+    bool ok2[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int s_ = s2[k];
+      bool ok = s_ >= 0 && s_ < L;
+      bad_sel |= (s_ >= L);
+      row2[k] = 0;
+      if (ok) {
+        if (append && s_ == L0) {
+          row2[k] = kNewRow;
+        } else if (ph2[k] < 0 || (int64_t)ph2[k] >= p.num_pages) {
+          ok = false;
+          bad_page = 1;
+        } else {
+          row2[k] = (uint32_t)ph2[k] * 2 * kPage + (uint32_t)(s_ & (kPage - 1));
+        }
+      }
+      ok2[k] = ok;
+    }
+    int tot;
+    const int at = block_exclusive_scan<NT>((ok2[0] ? 1 : 0) | (ok2[1] ? 1 << 16 : 0), s_scan, &tot);
+    const int tot0 = tot & 0xFFFF;
+    const int at0 = n_sel + (at & 0xFFFF), at1 = n_sel + tot0 + (at >> 16);
+    if (ok2[0] && at0 < kGatherMaxSel) s_row[at0] = row2[0];
+    if (ok2[1] && at1 < kGatherMaxSel) s_row[at1] = row2[1];
+    n_sel += tot0 + (tot >> 16);
+  }
+  if (tid == 0 && bad_sel) set_error(p.dev_err, SE_DEVERR_BAD_SELECTION);
+  {
+    const int bp = block_reduce<NT>(bad_page, s_red, [](int a, int c) { return a | c; });
+    if (bp && tid == 0) set_error(p.dev_err, SE_DEVERR_BAD_PAGE);
+  }
+  n_sel = min(n_sel, kGatherMaxSel);
+  __syncthreads();  // the row list and the appended row are complete
+  if (append && tid == 0) p.lengths[unit] = L;
+
   const uint16_t* knew = append ? p.k_new + ((size_t)req * p.num_kv_heads + kvh) * D : nullptr;
   const uint16_t* vnew = append ? p.v_new + ((size_t)req * p.num_kv_heads + kvh) * D : nullptr;
 
