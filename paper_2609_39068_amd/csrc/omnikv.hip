@@ -272,6 +272,29 @@ struct GatherParams {
   int32_t* dev_err;
 };
 
+// Cross-lane steps of the gather pass, all in VALU (DPP and permlane swaps,
+// no LDS permutes).  row8_sum: the sum over each group of 8 lanes, in all 8
+// (quad sums, then each lane adds the mirror lane of its half-row, which
+// holds the other quad's sum: the pairs of an xor-1/2/4 butterfly, so the
+// same rounding).  lane8_max: the maximum over the 8 lanes of equal lane % 8
+// (bit 3 by a rotation of each 16-lane row by 8, bits 5 and 4 by permlane
+// swaps).
+constexpr int kRowHalfMirror = 0x141;  // DPP row_half_mirror: lane i of 8 reads lane 7 - i
+constexpr int kRowRor8 = 0x128;        // DPP row_ror:8: lane i of 16 reads lane (i + 8) % 16
+__device__ __forceinline__ float row8_sum(float v) {
+  v = quad_sum(v);
+  return v + dpp_f<kRowHalfMirror>(v);
+}
+__device__ __forceinline__ float lane8_max(float v) {
+  v = fmaxf(v, dpp_f<kRowRor8>(v));
+  const uint32_t b = __float_as_uint(v);
+  const auto h = __builtin_amdgcn_permlane32_swap(b, b, false, false);
+  const float y = fmaxf(__uint_as_float(h[0]), __uint_as_float(h[1]));
+  const uint32_t c = __float_as_uint(y);
+  const auto r = __builtin_amdgcn_permlane16_swap(c, c, false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 template <int D>
 struct GatherRow {
   static constexpr int QW = D / 16;  // 32-bit words of a key row per lane (8 lanes per row)
@@ -456,17 +479,13 @@ __global__ __launch_bounds__(NT, (G >= 4 ? 2 : 4) * kGatherThreads / NT) void ga
       float a = 0.f;
 #pragma unroll
       for (int i = 0; i < QW; ++i) a = dot2bf16(qr[g][i], cur.k[i], a);
-      a += shfl_xor_f(a, 1);
-      a += shfl_xor_f(a, 2);
-      a += shfl_xor_f(a, 4);
+      a = row8_sum(a);
       z[g] = rb + ps * 8 + r8 < re ? a * p.scale_log2 : -INFINITY;
     }
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       float mx = z[g];
-      mx = fmaxf(mx, shfl_xor_f(mx, 8));
-      mx = fmaxf(mx, shfl_xor_f(mx, 16));
-      mx = fmaxf(mx, shfl_xor_f(mx, 32));
+      mx = lane8_max(mx);
       const float mn = fmaxf(m[g], mx);
       const float corr = fast_exp2(m[g] - mn);  // m = -inf at first: 0
       m[g] = mn;
