@@ -285,6 +285,15 @@ __device__ __forceinline__ float row8_sum(float v) {
   v = quad_sum(v);
   return v + dpp_f<kRowHalfMirror>(v);
 }
+__device__ __forceinline__ float lane8_sum(float v) {
+  v += dpp_f<kRowRor8>(v);
+  const uint32_t b = __float_as_uint(v);
+  const auto h = __builtin_amdgcn_permlane32_swap(b, b, false, false);
+  const float y = __uint_as_float(h[0]) + __uint_as_float(h[1]);
+  const uint32_t c = __float_as_uint(y);
+  const auto r = __builtin_amdgcn_permlane16_swap(c, c, false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 __device__ __forceinline__ float lane8_max(float v) {
   v = fmaxf(v, dpp_f<kRowRor8>(v));
   const uint32_t b = __float_as_uint(v);
@@ -489,10 +498,11 @@ __global__ __launch_bounds__(NT, (G >= 4 ? 2 : 4) * kGatherThreads / NT) void ga
       const float mn = fmaxf(m[g], mx);
       const float corr = fast_exp2(m[g] - mn);  // m = -inf at first: 0
       m[g] = mn;
-      l[g] *= corr;
+      const float w = fast_exp2(z[g] - mn);
+      if (c8 == 0) s_w[wv][r8][g] = w;
+      l[g] = fmaf(l[g], corr, w);  // row r8's share (the row's 8 lanes hold the same)
 #pragma unroll
       for (int c = 0; c < VC; ++c) acc[g][c] *= corr;
-      if (c8 == 0) s_w[wv][r8][g] = fast_exp2(z[g] - mn);
     }
     wave_lds_sync();
 #pragma unroll
@@ -507,7 +517,6 @@ __global__ __launch_bounds__(NT, (G >= 4 ? 2 : 4) * kGatherThreads / NT) void ga
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         const float wgt = s_w[wv][r][g];
-        l[g] += wgt;
 #pragma unroll
         for (int c = 0; c < VC; ++c) acc[g][c] = fmaf(wgt, vf[c], acc[g][c]);
       }
@@ -532,9 +541,10 @@ __global__ __launch_bounds__(NT, (G >= 4 ? 2 : 4) * kGatherThreads / NT) void ga
       load(ps + 5, b2);
     }
   }
-  // ---- combine the wavefronts
+  // ---- combine the wavefronts (l: the sum of the 8 row lanes' shares)
 #pragma unroll
   for (int g = 0; g < G; ++g) {
+    l[g] = lane8_sum(l[g]);
     if (lane == 0) {
       s_m[wv][g] = m[g];
       s_l[wv][g] = l[g];
