@@ -246,7 +246,13 @@ def test_workspace_sizes():
     assert b.se_workspace_bytes(b.SE_OP_SNAPKV, 3, 1000, 63, 8, 128, 32) == 3 * 2 * 1024 * 4 + 3 * moves
     assert b.se_workspace_bytes(b.SE_OP_SNAPKV, 3, 1000, 63, 4, 128, 32) == 3 * 1024 * 4 + 3 * moves
     assert b.se_workspace_bytes(b.SE_OP_OMNIKV_SELECT, 32, 33000, 2063, 4, 128, 0) == 32 * 33024 * 4
-    assert b.se_workspace_bytes(b.SE_OP_H2O_PREFILL, 10, 1000, 63, 4, 128, 128) == 10 * 4 * 1024 * 4 + 10 * moves
+    # 257..512 scoring rows (window 128 x G 4 = 512): each unit's pages split into key parts, min(ceil(256 /
+    # units), max(1, pages / 8)) of them, each leaving a (reference, sum) float pair per row
+    assert b.se_workspace_bytes(b.SE_OP_H2O_PREFILL, 10, 1000, 63, 4, 128, 128) == 10 * 7 * 512 * 8 + 10 * moves
+    assert b.se_workspace_bytes(b.SE_OP_H2O_PREFILL, 300, 1000, 63, 4, 128, 128) == 300 * 1 * 512 * 8 + 300 * moves
+    assert b.se_workspace_bytes(b.SE_OP_H2O_PREFILL, 64, 10240, 640, 4, 128, 128) == 64 * 4 * 512 * 8 + 64 * moves
+    # 129..256 rows (window 64 x G 4): two row blocks of per-slot sums
+    assert b.se_workspace_bytes(b.SE_OP_H2O_PREFILL, 10, 1000, 63, 4, 128, 64) == 10 * 2 * 1024 * 4 + 10 * moves
     assert b.se_workspace_bytes(b.SE_OP_H2O_PREFILL, 10, 1000, 63, 4, 128, 32) == 10 * 1 * 1024 * 4 + 10 * moves
     assert b.se_workspace_bytes(99, 1, 1, 1, 1, 64, 0) == 0
 
