@@ -66,37 +66,61 @@ struct OmniSelectParams {
 // `hist` holds COPIES * 257 words.
 template <int NT, int COPIES, typename KeyT, typename KeyFn, typename CandFn>
 __device__ void radix_select_top_rep(int n, int k, KeyFn key_of, CandFn cand, KeyT* prefix_out, KeyT* mask_out,
-                                     int* k_rest_out, unsigned* hist, int* scan_scratch, int* bcast) {
-  static_assert(NT >= 256 && NT % kWave == 0, "threads 0..255 own one bin each");
+                                     int* k_rest_out, unsigned* hist, int* bcast) {
+  static_assert(NT % kWave == 0, "whole wavefronts");
   constexpr int kStride = 257;
   KeyT prefix = 0, mask = 0;
   const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
   unsigned* const my_hist = hist + (tid % COPIES) * kStride;
+  for (int i = tid; i < COPIES * kStride; i += NT) hist[i] = 0;
+  __syncthreads();
+  // two barriers a pass: the counts are in; then wavefront 0 alone sums the
+  // copies (clearing them for the next pass), scans the 256 digits and
+  // broadcasts the threshold digit
   for (int shift = (int)sizeof(KeyT) * 8 - 8; shift >= 0; shift -= 8) {
-    for (int i = tid; i < COPIES * kStride; i += NT) hist[i] = 0;
-    __syncthreads();
     for (int i = tid; i < n; i += NT) {
       if (!cand(i)) continue;
       const KeyT key = key_of(i);
       if ((key & mask) == prefix) atomicAdd(&my_hist[(unsigned)(key >> shift) & 255u], 1u);
     }
     __syncthreads();
-    int v = 0;  // thread t counts digit 255 - t over the copies
-    if (tid < 256)
+    if (tid < kWave) {
+      // lane l holds digits 255-4l .. 252-4l (descending); inclusive prefix over lanes
+      int c[4], s4 = 0;
 #pragma unroll
-      for (int c = 0; c < COPIES; ++c) v += (int)hist[c * kStride + 255 - tid];
-    int total;
-    const int excl = block_exclusive_scan<NT>(v, scan_scratch, &total);
-    if (v > 0 && excl < k && excl + v >= k) {
-      bcast[0] = 255 - tid;
-      bcast[1] = excl;
-      bcast[2] = v;
+      for (int j = 0; j < 4; ++j) {
+        int v = 0;
+#pragma unroll
+        for (int cp = 0; cp < COPIES; ++cp) {
+          unsigned* const w = hist + cp * kStride + 255 - 4 * lane - j;
+          v += (int)*w;
+          *w = 0u;
+        }
+        c[j] = v;
+        s4 += v;
+      }
+      int incl = s4;
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const int y = __shfl_up(incl, o, kWave);
+        if (lane >= o) incl += y;
+      }
+      int run = incl - s4;  // candidates in higher digits than this lane's first
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (c[j] > 0 && run < k && run + c[j] >= k) {
+          bcast[0] = 255 - 4 * lane - j;
+          bcast[1] = run;
+          bcast[2] = c[j];
+        }
+        run += c[j];
+      }
     }
     __syncthreads();
     const int d = bcast[0];
     k -= bcast[1];
     const int cnt = bcast[2];
-    __syncthreads();
     prefix |= (KeyT)d << shift;
     mask |= (KeyT)0xFF << shift;
     if (cnt == k) break;
@@ -179,7 +203,10 @@ __global__ __launch_bounds__(kOmniTopkThreads) void omnikv_topk_kernel(const Omn
   const float* gsc = p.scores + (size_t)req * p.ws_stride;
   const float* sc = gsc;
   if (L <= kOmniLdsScores) {
-    // eight loads in flight per thread (16-byte ones when the rows are aligned)
+    // eight loads in flight per thread (16-byte ones when the rows are aligned);
+    // the loads are unconditional (an index past the end re-reads the last
+    // element, which is not stored), so the values stay in registers and no
+    // load waits for the one before it
     constexpr int NB = 8;
     int done = 0;
     if (p.vec4) {
@@ -187,10 +214,8 @@ __global__ __launch_bounds__(kOmniTopkThreads) void omnikv_topk_kernel(const Omn
       for (int i = tid; i < n4; i += kOmniTopkThreads * NB) {
         float4 v[NB];
 #pragma unroll
-        for (int k = 0; k < NB; ++k) {
-          const int x = i + k * kOmniTopkThreads;
-          if (x < n4) v[k] = reinterpret_cast<const float4*>(gsc)[x];
-        }
+        for (int k = 0; k < NB; ++k)
+          v[k] = reinterpret_cast<const float4*>(gsc)[min(i + k * kOmniTopkThreads, n4 - 1)];
 #pragma unroll
         for (int k = 0; k < NB; ++k) {
           const int x = i + k * kOmniTopkThreads;
@@ -202,10 +227,7 @@ __global__ __launch_bounds__(kOmniTopkThreads) void omnikv_topk_kernel(const Omn
     for (int i = done + tid; i < L; i += kOmniTopkThreads * NB) {
       float v[NB];
 #pragma unroll
-      for (int k = 0; k < NB; ++k) {
-        const int x = i + k * kOmniTopkThreads;
-        if (x < L) v[k] = gsc[x];
-      }
+      for (int k = 0; k < NB; ++k) v[k] = gsc[min(i + k * kOmniTopkThreads, L - 1)];
 #pragma unroll
       for (int k = 0; k < NB; ++k) {
         const int x = i + k * kOmniTopkThreads;
@@ -219,14 +241,46 @@ __global__ __launch_bounds__(kOmniTopkThreads) void omnikv_topk_kernel(const Omn
   int k_rest;
   radix_select_top_rep<kOmniTopkThreads, kOmniHistCopies, uint32_t>(
       L, b, [&](int i) { return float_key(sc[i]); }, [](int) { return true; }, &prefix, &mask, &k_rest, s_hist,
-      s_scan, s_bcast);
+      s_bcast);
   // thread t owns slots [t*run, (t+1)*run): count the threshold ties, rank them
   // in slot order, then place the selected slots
   const int run = ceil_div_dev(L, kOmniTopkThreads);
   const int lo = min(L, tid * run), hi = min(L, lo + run);
+  int tot;
+  if (run <= 64) {
+    // one pass over the run builds two masks (bit j: slot lo + j above the
+    // threshold, equal to it), read in an order rotated by the thread so that
+    // a wavefront's lanes read different banks; the counts, the ties taken
+    // (the first k_rest - eq_before of the block's ties, in slot order) and
+    // the output offsets then come from the masks alone
+    const int n = hi - lo;
+    const int rot = (tid >> 1) % run;
+    uint64_t gt = 0, eq = 0;
+    for (int j = 0; j < run; ++j) {
+      const int jj = j + rot < run ? j + rot : j + rot - run;
+      if (jj < n) {
+        const uint32_t km = float_key(sc[lo + jj]) & mask;
+        gt |= (uint64_t)(km > prefix) << jj;
+        eq |= (uint64_t)(km == prefix) << jj;
+      }
+    }
+    const int n_eq = __popcll(eq);
+    const int eq_before = block_exclusive_scan<kOmniTopkThreads>(n_eq, s_scan, &tot);
+    uint64_t selm = gt;
+    for (int t = min(max(k_rest - eq_before, 0), n_eq); t > 0; --t) {
+      const uint64_t low = eq & (~eq + 1);  // the lowest remaining tie
+      selm |= low;
+      eq ^= low;
+    }
+    int o = block_exclusive_scan<kOmniTopkThreads>(__popcll(selm), s_scan, &tot);
+    while (selm != 0) {
+      out[o++] = lo + __builtin_ctzll(selm);
+      selm &= selm - 1;
+    }
+    return;
+  }
   int n_eq = 0;
   for (int i = lo; i < hi; ++i) n_eq += ((float_key(sc[i]) & mask) == prefix);
-  int tot;
   const int eq_before = block_exclusive_scan<kOmniTopkThreads>(n_eq, s_scan, &tot);
   int n_sel = 0, e = eq_before;
   for (int i = lo; i < hi; ++i) {

@@ -145,21 +145,25 @@ def test_long_context_selection_from_workspace(se):
     _run_step(se, [40000], 1, 4, 128, 2048, seed=4)
 
 
-@pytest.mark.parametrize("G,L,stride", [(4, 1000, 1024), (4, 1000, 1027), (3, 1001, 1024), (5, 999, 1000)])
-def test_select_from_given_logits_with_ties(se, G, L, stride):
+@pytest.mark.parametrize("G,L,stride,budget", [(4, 1000, 1024, 97), (4, 1000, 1027, 97), (3, 1001, 1024, 97),
+                                               (5, 999, 1000, 97), (4, 20000, 20000, 2048), (4, 36000, 36003, 2048),
+                                               (4, 40000, 40000, 2048), (2, 70000, 70000, 4096)])
+def test_select_from_given_logits_with_ties(se, G, L, stride, budget):
     # logits taken as given (integer levels, many exact ties): the selection is
     # bit-exact against the oracle's TopK over max-over-heads scores; rows in
     # 16-byte aligned strides (four slots per load, 8 / 6 / 10 rows per request)
-    # and an unaligned stride
-    hkv, nreq, budget = 2, 3, 97
+    # and unaligned strides; from 20000 slots on, every thread of the ranking
+    # owns a run of 20 to 69 slots (the tie classes span many runs), from
+    # 36865 on the scores are ranked from the workspace
+    hkv, nreq = 2, 3
     g = torch.Generator().manual_seed(5 + G + stride)
     logits = torch.randint(0, 7, (nreq * hkv * G, stride), generator=g).to(torch.float32)
-    st = isolated_units([L] * (nreq * hkv), 64, 64, 1, num_kv_heads=hkv)
+    st = isolated_units([L] * (nreq * hkv), (L + 15) // 16, 64, 1, num_kv_heads=hkv, with_scores=False)
     gs = to_device(st, DEV)
     view = _view(se, gs, hkv)
     sel = torch.empty((nreq, budget), dtype=torch.int32, device=DEV)
-    ws = torch.empty(se.se_workspace_bytes(se.SE_OP_OMNIKV_SELECT, nreq, L, 64, G, 64, 0), dtype=torch.uint8,
-                     device=DEV)
+    ws = torch.empty(se.se_workspace_bytes(se.SE_OP_OMNIKV_SELECT, nreq, L, (L + 15) // 16, G, 64, 0),
+                     dtype=torch.uint8, device=DEV)
     err = torch.zeros(1, dtype=torch.int32, device=DEV)
     se.se_omnikv_select(view, G, logits.to(DEV), stride, budget, L, sel, ws, err)
     torch.cuda.synchronize()
