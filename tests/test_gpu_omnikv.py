@@ -147,14 +147,16 @@ def test_long_context_selection_from_workspace(se):
 
 @pytest.mark.parametrize("G,L,stride,budget", [(4, 1000, 1024, 97), (4, 1000, 1027, 97), (3, 1001, 1024, 97),
                                                (5, 999, 1000, 97), (4, 20000, 20000, 2048), (4, 36000, 36003, 2048),
-                                               (4, 40000, 40000, 2048), (2, 70000, 70000, 4096)])
+                                               (4, 30001, 30004, 2048), (4, 40000, 40000, 2048),
+                                               (2, 70000, 70000, 4096)])
 def test_select_from_given_logits_with_ties(se, G, L, stride, budget):
     # logits taken as given (integer levels, many exact ties): the selection is
     # bit-exact against the oracle's TopK over max-over-heads scores; rows in
     # 16-byte aligned strides (four slots per load, 8 / 6 / 10 rows per request)
     # and unaligned strides; from 20000 slots on, every thread of the ranking
-    # owns a run of 20 to 69 slots (the tie classes span many runs), from
-    # 36865 on the scores are ranked from the workspace
+    # owns a run of 20 to 69 slots (the tie classes span many runs; at 30001 the
+    # last run holds one slot), from 36865 on the scores are ranked from the
+    # workspace
     hkv, nreq = 2, 3
     g = torch.Generator().manual_seed(5 + G + stride)
     logits = torch.randint(0, 7, (nreq * hkv * G, stride), generator=g).to(torch.float32)
