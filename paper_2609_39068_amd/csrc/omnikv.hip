@@ -358,6 +358,8 @@ __device__ __forceinline__ float lane8_max(float v) {
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
+typedef uint32_t gather_u32x4 __attribute__((ext_vector_type(4)));
+
 template <int D>
 struct GatherRow {
   static constexpr int QW = D / 16;  // 32-bit words of a key row per lane (8 lanes per row)
@@ -504,10 +506,11 @@ __global__ __launch_bounds__(NT, (G >= 4 ? 2 : 4) * kGatherThreads / NT) void ga
     const int e = min(rb + ps * 8 + r8, re - 1);
     const uint32_t row = s_row[max(e, 0)];
     const uint16_t* ksrc = row == kNewRow ? knew : p.kv + (size_t)row * D;
-    const uint4* k4 = reinterpret_cast<const uint4*>(ksrc + c8 * (D / 8));
+    // rows are read once: nontemporal loads (as the decode stream's)
+    const gather_u32x4* k4 = reinterpret_cast<const gather_u32x4*>(ksrc + c8 * (D / 8));
 #pragma unroll
     for (int i = 0; i < QW; i += 4) {
-      const uint4 t = k4[i / 4];
+      const gather_u32x4 t = __builtin_nontemporal_load(k4 + i / 4);
       bf.k[i] = t.x;
       bf.k[i + 1] = t.y;
       bf.k[i + 2] = t.z;
@@ -519,9 +522,9 @@ __global__ __launch_bounds__(NT, (G >= 4 ? 2 : 4) * kGatherThreads / NT) void ga
       const uint32_t vr = __builtin_amdgcn_readfirstlane(s_row[max(er, 0)]);  // one row per wavefront
       const uint16_t* vsrc = vr == kNewRow ? vnew : p.kv + ((size_t)vr + kPage) * D;
       if (VC == 2)
-        bf.v[r] = reinterpret_cast<const uint32_t*>(vsrc)[lane];
+        bf.v[r] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(vsrc) + lane);
       else
-        bf.v[r] = reinterpret_cast<const uint16_t*>(vsrc)[lane];
+        bf.v[r] = __builtin_nontemporal_load(reinterpret_cast<const uint16_t*>(vsrc) + lane);
     }
   };
 
