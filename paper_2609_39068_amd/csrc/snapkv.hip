@@ -161,7 +161,8 @@ __device__ __forceinline__ void stream_stages(const SnapParams& p, const int32_t
 #pragma unroll
     for (int q = 0; q < PT; ++q) {
       const int pg = min(pb + st * S + pg_of[q], pe - 1);  // the same in every lane of a wavefront
-      r[q] = *reinterpret_cast<const u32x4_t*>(p.kv + (size_t)bt_entry(bt, pg) * 2 * kPage * D + off_of[q]);
+      r[q] = __builtin_nontemporal_load(
+          reinterpret_cast<const u32x4_t*>(p.kv + (size_t)bt_entry(bt, pg) * 2 * kPage * D + off_of[q]));
     }
   };
   auto store = [&](const u32x4_t(&r)[PT], int slot) {
