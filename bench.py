@@ -57,7 +57,7 @@ HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 # Vector ALU: 256 compute units x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3e12 lane-slots/s
 # (one full-rate VALU operation per lane per slot; packed fp32, which would double
-# fma and add, is not used by this build); v_exp_f32 takes two slots (measured on
+# fma and add, is not used by the library's kernels); v_exp_f32 takes two slots (measured on
 # one MI355X: fma 3.99e13 lane-ops/s, exp2 alone 1.68e13/s, exp2 followed by two
 # fma 1.06e13/s).
 VALU_PEAK_TSLOTS = 256 * 4 * 16 * 2.4e9 / 1e12
