@@ -224,7 +224,7 @@ def test_attend_slots_edge_cases(se):
 
 
 @pytest.mark.parametrize("G,d,nreq", [
-    (8, 128, 2), (8, 64, 2), (1, 128, 2),
+    (8, 128, 2), (8, 64, 2), (1, 128, 2), (4, 64, 2), (2, 64, 3),
     (4, 128, 130),   # 260 units: more than one work-group per compute unit (512 threads, not 1024)
 ])
 def test_attend_slots_group_sizes(se, G, d, nreq):
